@@ -1,0 +1,221 @@
+/*
+ * dpa4c.h -- C ABI of the MI355X (gfx950) energy-and-force path of the DPA4C
+ * machine-learning potential (arXiv 2608.19041).
+ *
+ * The library evaluates, for N atoms with positions r_i, species a_i and a
+ * periodic orthorhombic cell, the neighbour graph of Methods Eq.
+ * (neighbor-set), the single message-passing layer of Eqs. (edge-geometry)
+ * .. (moments), the invariant readout and MLP of Eqs. (alignment) ..
+ * (fitting), and the forces of Eq. (forces), F_k = -dE/dr_k.  The compressed
+ * execution of Methods "Compressed inference" is used: the radial maps g(rho)
+ * and q(rho) come from a quintic Hermite table (Supplementary Note "Quintic
+ * Hermite interpolation of the radial table"), the ordered-pair modulation
+ * from a per-pair cache; everything else is analytic.
+ *
+ * Units: Angstrom, eV, fs, atomic mass units (u).
+ *
+ * Pointers marked "device" are HIP device pointers on the model's device;
+ * pointers marked "host" are ordinary host memory.  The caller owns every
+ * array passed in; the library owns only what hangs off a model handle
+ * (weights, tables, caches, a grow-only workspace) and a small per-device
+ * workspace of build_neighbors.  All device work is enqueued on ``stream``
+ * (a hipStream_t; NULL = the default stream) and runs asynchronously unless
+ * stated otherwise; inputs must stay valid until the stream reaches that
+ * point.
+ *
+ * Every function returns 0 on success or a negative DPA4C_ERR_* code; on
+ * failure dpa4c_last_error() describes the problem.  Nothing is written to
+ * caller outputs on failure, except where a function says so.
+ *
+ * Calls that share a model handle must not overlap (the handle's workspace
+ * is shared); different handles may be used concurrently.
+ */
+#ifndef DPA4C_H
+#define DPA4C_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DPA4C_OK 0
+#define DPA4C_ERR_INVALID_ARG (-1) /* bad pointer, size or value */
+#define DPA4C_ERR_UNSUPPORTED (-2) /* non-orthorhombic or non-periodic cell, profile not built */
+#define DPA4C_ERR_CAPACITY (-3)    /* neighbour capacity too small; *n_pairs holds the need */
+#define DPA4C_ERR_HIP (-4)         /* a HIP runtime call failed */
+#define DPA4C_ERR_NONFINITE (-5)   /* a non-finite position was found */
+#define DPA4C_ERR_SKIN (-6)        /* an atom moved more than half the skin, rebuild disabled */
+
+typedef struct dpa4c_model dpa4c_model;
+
+/*
+ * Weight blob (little endian).  A 64-byte header
+ *     char magic[8] = "DPA4CW01"; int32 version = 1;
+ *     int32 C0, L, R, n_rbf, F (MLP width), n_layers (Lambda), n_types (T);
+ *     float64 r_c, delta (radial-table spacing, Angstrom); zero padding,
+ * followed by float32 row-major arrays in this order (widths per Methods
+ * Eqs. (degree-channels), (probe-ranks), (dim-out); H = 8 ceil(C0/3),
+ * Hp = 8 ceil(2 C0/3), K1 = C2, K2 = 2):
+ *     type_embed [T+1][C0]      Eq. (init-features); row T is the zero padding type
+ *     omega      [n_rbf]        Eq. (bessel-basis)
+ *     W_in       [n_rbf][2H]    Eq. (radial-map); gate = first H columns
+ *     W_out      [H][C0]
+ *     W_mode     [H][R]         Eq. (radial-modes)
+ *     Wp_in      [2 C0][2 Hp]   Eq. (pairfilm); gate = first Hp columns
+ *     Wp_out     [Hp][C0 (2+R)] output split [s, t, w], w channel-major (C0, R)
+ *     W_align1   [C1][C1], W_align2 [C2][C2]   Eq. (alignment)
+ *     A1         [C1][K1]       Eq. (probes); only when K1 != C1
+ *     A2         [C2][K2]
+ *     Theta1 [D_out][F], b1 [F], then Theta_t [F][F], b_t [F] for t = 2..Lambda
+ *     w_head [F], b_head [1]    Eq. (fitting)
+ *     E_ref  [T+1]              Eq. (atomic-energy)
+ *     mu [D_out], sigma [D_out] Eq. (calibration)
+ * Supported profiles (C0, L, R): (32, 2, 0) and (128, 3, 4).
+ *
+ * Creates a model on ``device``: uploads the weights, tabulates [g, q] on
+ * knots rho_s = s*delta (values and first two derivatives evaluated in
+ * float64, quintic coefficients stored float32), evaluates the ordered-pair
+ * cache for all (T+1)^2 pairs, and builds the Gaunt coupling tensors of
+ * Eq. (gaunt).  Synchronous.  *out receives the handle.
+ */
+int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model** out);
+
+/* Frees the handle and everything it owns (synchronises its device). */
+void dpa4c_model_destroy(dpa4c_model* model);
+
+/*
+ * Integer widths of a model, written to ``info`` (host, 12 int64):
+ * C0, L, R, S (Eq. (moment-width)), D_out (Eq. (dim-out)), F, n_layers,
+ * n_types, table rows, C1, C2, K1.
+ */
+int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
+
+/*
+ * Neighbour list of Eq. (neighbor-set) at radius r_list (typically r_c plus
+ * a skin), for an orthorhombic fully periodic cell.
+ *
+ * Membership uses the exact fixed-point predicate
+ *     |Q(r_j) + n.Q(h) - Q(r_i)|^2 < Q(r_list)^2,  Q(x) = rint(x * 2^20)
+ * in 64-bit integers, so the list is a deterministic function of the float64
+ * positions.  Periodic images are distinct neighbours, only (j = i, n = 0)
+ * is excluded, both orientations are stored and there is no capacity per
+ * atom.  Rows are in canonical order: ascending (j, n_x, n_y, n_z).
+ * Positions need not lie inside the cell.
+ *
+ * pos       device float64 [N][3]
+ * cell      host float64 [9], rows are lattice vectors; must be diagonal
+ * pbc       host int [3]; must be {1, 1, 1}
+ * row_ptr   device int64 [N+1] out: CSR row offsets
+ * nbr_j     device int32 [cap] out: neighbour index j
+ * nbr_shift device int32 [cap] out: image n packed as
+ *           ((n_x+128) << 16) | ((n_y+128) << 8) | (n_z+128), |n_a| <= 127
+ * n_pairs   host out: number of edges; always set when the count succeeded.
+ * If the edge count exceeds cap, returns DPA4C_ERR_CAPACITY with *n_pairs
+ * set and row_ptr written, but nbr_j / nbr_shift untouched; call again with
+ * cap >= *n_pairs.  A non-finite position gives DPA4C_ERR_NONFINITE; a row
+ * longer than 1024 or an image index beyond +-127 gives
+ * DPA4C_ERR_UNSUPPORTED.  Synchronises ``stream`` twice (to read the count
+ * and the error flags).
+ */
+int build_neighbors(const double* pos, int64_t N, const double cell[9], const int pbc[3],
+                    double r_list, int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift,
+                    int64_t cap, int64_t* n_pairs, void* stream);
+
+/*
+ * Energy and forces for one configuration (Eqs. (energy-decomposition),
+ * (atomic-energy), (forces)).
+ *
+ * The neighbour list passed in is a skin list from build_neighbors at any
+ * radius r_list >= r_c built for positions from which no atom has moved by
+ * more than (r_list - r_c)/2 (integer norm); the library keeps the edges with
+ * the r_c predicate itself, in canonical order.  r_c must equal the model's.
+ * n_pairs is the number of edges of that list (row_ptr[N], as returned by
+ * build_neighbors); it sizes the library's edge workspace.
+ *
+ * pos      device float64 [N][3];  species device int32 [N], 0 <= a < T
+ * e_atom   device float64 [N] out: E_i
+ * forces   device float64 [N][3] out
+ * e_total  device float64 [1] out: sum of E_i (fixed-order two-pass sum)
+ * All reductions run in a fixed order without floating-point atomics, so
+ * repeated calls give bit-identical results.  Does not synchronise.
+ */
+int compute_energy_forces(const dpa4c_model* model, const double* pos, const int32_t* species,
+                          int64_t N, const double cell[9], const int pbc[3], double r_c,
+                          const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
+                          int64_t n_pairs, double* e_atom, double* forces, double* e_total,
+                          void* stream);
+
+/*
+ * ``nsteps`` velocity-Verlet NVE steps (Supplementary Note on the MD
+ * protocol: full neighbour list with a skin, checked every step):
+ *     v += dt/2 F/m;  r += dt v;  [rebuild];  F = F(r);  v += dt/2 F/m.
+ * The library keeps its own skin list (radius r_c + skin) in the model
+ * workspace.  It is rebuilt at the first step of a call, every
+ * ``rebuild_every`` steps when that is > 0, and whenever some atom has moved
+ * by more than skin/2 since the last build (checked on the device every
+ * step).  With rebuild_every < 0 no rebuild happens after the first step and
+ * a violation returns DPA4C_ERR_SKIN after the call.
+ *
+ * pos, vel         device float64 [N][3], in/out (A, A/fs)
+ * species          device int32 [N]
+ * mass_by_species  host float64 [T+1] (u)
+ * forces           device float64 [N][3]: in = forces at the input
+ *                  positions (from compute_energy_forces or a previous call);
+ *                  out = forces at the final positions
+ * e_pot, e_kin     device float64 [nsteps] out: potential and kinetic energy
+ *                  after each step (eV)
+ * n_rebuilds       host int64 out (may be NULL): rebuilds done in this call
+ * Synchronises ``stream`` twice: after the first neighbour build (to size
+ * the skin list; capacity is then 1.5x that count plus 64 per atom) and at
+ * the end (to read the device-side flags).  If a later rebuild would exceed
+ * the capacity, returns DPA4C_ERR_CAPACITY and the trajectory from that step
+ * on is not valid.
+ */
+int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_t* species,
+                const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+                double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
+                double* e_pot, double* e_kin, double* forces, int64_t* n_rebuilds, void* stream);
+
+/*
+ * Intermediate quantities of the last compute_energy_forces (or the last
+ * step of verlet_step) on this model, copied into caller device buffers,
+ * for stage-by-stage checks.  Any pointer may be NULL.
+ *   node_state  float32 [N][S+2]: [sum chi^2, sum chi^4, unnormalised
+ *               features Y (degree -> m -> channel)]   Eq. (payload)
+ *   descriptor  float32 [N][D_out]: calibrated D       Eq. (calibration)
+ *   edge_count  int32 [N]: edges within r_c per centre
+ * Synchronous on ``stream``.
+ */
+int dpa4c_debug_stages(const dpa4c_model* model, int64_t N, float* node_state,
+                       float* descriptor, int32_t* edge_count, void* stream);
+
+/*
+ * Per-stage timing.  When enabled, the library records HIP events around
+ * every kernel it launches on the caller's stream and accumulates their
+ * durations per stage.  dpa4c_get_timings writes up to ``n`` stage times
+ * (milliseconds, summed over calls since the last reset) to ``ms``, launch
+ * counts to ``count`` (either may be NULL) and returns the number of stages;
+ * dpa4c_stage_name gives their names.  Reading synchronises the device.
+ */
+int dpa4c_set_timing(dpa4c_model* model, int enable);
+int dpa4c_get_timings(dpa4c_model* model, double* ms, int64_t* count, int n);
+const char* dpa4c_stage_name(int stage);
+
+/*
+ * C = A B for row-major float32 A [M][K], B [K][N], C [M][N] (device), with
+ * K a multiple of 16 and N a multiple of 4: the fp32 matrix-core GEMM of the
+ * MLP stage, exported so that tests can check it against a reference.
+ */
+int dpa4c_debug_gemm(const float* A, const float* B, float* C, int M, int N, int K,
+                     void* stream);
+
+/* Thread-local description of the last error (library-owned string). */
+const char* dpa4c_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DPA4C_H */

@@ -1,0 +1,582 @@
+// C-ABI entry points of the DPA4C library (declared in include/dpa4c.h).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+
+#include "../../include/dpa4c.h"
+#include "launch.h"
+#include "model.h"
+
+namespace dpa4c {
+
+namespace {
+thread_local std::string g_last_error;
+
+// per-device scratch of build_neighbors
+std::mutex g_nb_lock;
+std::map<int, NeighborScratch*> g_nb_scratch;
+std::map<int, DevBuf*> g_nb_flags;
+
+constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8;
+
+int check_cell(const double* cell, const int* pbc) {
+  if (!cell || !pbc) {
+    set_error("cell and pbc must not be null");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (!pbc[0] || !pbc[1] || !pbc[2]) {
+    set_error("the GPU path needs a fully periodic cell");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  for (int a = 0; a < 3; ++a)
+    for (int b = 0; b < 3; ++b)
+      if (a != b && cell[3 * a + b] != 0.0) {
+        set_error("the GPU path needs an orthorhombic cell (diagonal lattice matrix)");
+        return DPA4C_ERR_UNSUPPORTED;
+      }
+  return 0;
+}
+
+int64_t qfix_host(double x) { return static_cast<int64_t>(std::rint(x * kQScale)); }
+
+int flags_to_error(int64_t f) {
+  if (f & kFlagNonFinite) {
+    set_error("non-finite (or |x| > 1e12) position");
+    return DPA4C_ERR_NONFINITE;
+  }
+  if (f & kFlagRowTooLong) {
+    set_error("a neighbour row is longer than 1024 entries");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  if (f & kFlagShift) {
+    set_error("an image index exceeds +-127 (atom far outside the cell)");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  if (f & kFlagCapacity) {
+    set_error("neighbour capacity exceeded");
+    return DPA4C_ERR_CAPACITY;
+  }
+  return 0;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    hipGetDevice(&prev);
+    if (prev != dev) hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur;
+    hipGetDevice(&cur);
+    if (prev >= 0 && cur != prev) hipSetDevice(prev);
+  }
+};
+
+// Stage timing with HIP events on the caller's stream.
+struct StageScope {
+  dpa4c_model* m;
+  hipStream_t st;
+  int stage;
+  size_t slot = SIZE_MAX;
+  StageScope(const dpa4c_model* mm, int s, hipStream_t stream)
+      : m(const_cast<dpa4c_model*>(mm)), st(stream), stage(s) {
+    if (!m || !m->timing.enabled) return;
+    Timing& t = m->timing;
+    if (t.used + 2 > t.pool.size()) {
+      size_t grow = t.pool.size() < 256 ? 256 : t.pool.size();
+      for (size_t k = 0; k < grow; ++k) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        t.pool.push_back(e);
+      }
+      t.ev_stage.resize(t.pool.size() / 2);
+    }
+    slot = t.used;
+    t.used += 2;
+    t.ev_stage[slot / 2] = stage;
+    hipEventRecord(t.pool[slot], st);
+  }
+  ~StageScope() {
+    if (slot != SIZE_MAX) hipEventRecord(m->timing.pool[slot + 1], st);
+  }
+};
+
+void collect_timing(dpa4c_model* m) {
+  Timing& t = m->timing;
+  if (!t.used) return;
+  hipDeviceSynchronize();
+  for (size_t s = 0; s + 1 < t.used; s += 2) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.pool[s], t.pool[s + 1]) == hipSuccess) {
+      t.ms[t.ev_stage[s / 2]] += ms;
+      t.count[t.ev_stage[s / 2]] += 1;
+    }
+  }
+  t.used = 0;
+}
+
+// Workspace sizing for N atoms and a skin list of ``cap`` edges.
+int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
+  Workspace& w = m->ws;
+  const int64_t nn = n < 1 ? 1 : n, cc = cap < 1 ? 1 : cap;
+  const int dstr = (m->D_out + 15) / 16 * 16;
+  if (w.ecount.ensure(4 * nn) || w.edge.ensure(16 * cc) || w.cidx.ensure(4 * cc) ||
+      w.sidx.ensure(4 * cc) || w.rev.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
+      w.skin_rev.ensure(4 * cc) || w.node.ensure(4 * nn * (m->S + 2)) ||
+      w.desc.ensure(4 * nn * dstr) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
+      w.flags.ensure(8 * 8) || w.ekin_atom.ensure(8 * nn) || w.eatom.ensure(8 * nn))
+    return DPA4C_ERR_HIP;
+  for (int t = 0; t < 3; ++t)
+    if (w.h[t].ensure(4 * nn * m->F) || w.ds[t].ensure(4 * nn * m->F)) return DPA4C_ERR_HIP;
+  return 0;
+}
+
+// Everything after the skin list: compaction, reverse index, forward,
+// MLP, backward, forces and the energy sum.
+int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
+              const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
+              const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
+              double* forces, double* e_total, hipStream_t st) {
+  dpa4c_model* m = const_cast<dpa4c_model*>(mc);
+  Workspace& w = m->ws;
+  const int64_t rcq = qfix_host(m->r_c);
+  int rc;
+  {
+    StageScope t(m, kStCompact, st);
+    rc = launch_compact_edges(pos, n, g, rcq, box, row_ptr, nbr_j, nbr_shift, cap,
+                              w.ecount.as<int32_t>(), w.edge.as<float4>(), w.cidx.as<int32_t>(),
+                              w.sidx.as<int32_t>(), st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStRev, st);
+    rc = launch_rev(row_ptr, w.ecount.as<int32_t>(), w.sidx.as<int32_t>(), skin_rev,
+                    w.cidx.as<int32_t>(), n, w.rev.as<int32_t>(), st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStForward, st);
+    rc = launch_forward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
+                        w.node.as<float>(), w.desc.as<float>(), st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStMlpForward, st);
+    rc = launch_mlp_forward(m, n, species, w.desc.as<float>(), w.h[0].as<float>(),
+                            w.h[1].as<float>(), w.h[2].as<float>(), w.ds[0].as<float>(),
+                            w.ds[1].as<float>(), w.ds[2].as<float>(), e_atom, st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStMlpBackward, st);
+    rc = launch_mlp_backward(m, n, w.desc.as<float>(), w.h[0].as<float>(), w.h[1].as<float>(),
+                             w.h[2].as<float>(), w.ds[0].as<float>(), w.ds[1].as<float>(),
+                             w.ds[2].as<float>(), st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStBackward, st);
+    rc = launch_backward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
+                         w.node.as<float>(), w.desc.as<float>(), w.grad.as<float4>(), st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStForces, st);
+    rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.grad.as<float4>(),
+                       w.rev.as<int32_t>(), forces, st);
+    if (rc) return rc;
+  }
+  {
+    StageScope t(m, kStEnergy, st);
+    rc = launch_energy(n, e_atom, w.epart.as<double>(), e_total, st);
+  }
+  m->last_n = n;
+  w.last_species = species;
+  w.skin_row_used = row_ptr;
+  return rc;
+}
+
+}  // namespace
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+
+}  // namespace dpa4c
+
+using namespace dpa4c;
+
+extern "C" {
+
+int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model** out) {
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
+    set_error("dpa4c_model_create: no such HIP device");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  DeviceGuard guard(device);
+  return create_model(blob, nbytes, device, out);
+}
+
+void dpa4c_model_destroy(dpa4c_model* m) {
+  if (!m) return;
+  DeviceGuard guard(m->device);
+  hipDeviceSynchronize();
+  m->params.release();
+  Workspace& w = m->ws;
+  DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
+                    &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
+                    &w.desc,     &w.epart,  &w.flags,      &w.ekin_atom, &w.inv_mass, &w.mass,
+                    &w.eatom,
+                    &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
+                    &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
+  for (DevBuf* b : bufs) b->release();
+  for (int t = 0; t < 3; ++t) {
+    w.h[t].release();
+    w.ds[t].release();
+  }
+  for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
+  if (w.host_flags) hipHostFree(w.host_flags);
+  delete m;
+}
+
+int dpa4c_model_info(const dpa4c_model* m, int64_t* info) {
+  if (!m || !info) {
+    set_error("dpa4c_model_info: null argument");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  int64_t v[12] = {m->C0, m->L, m->R, m->S, m->D_out, m->F, m->n_layers, m->n_types,
+                   m->n_rows, m->C[1], m->C[2], m->K[1]};
+  std::memcpy(info, v, sizeof(v));
+  return 0;
+}
+
+int build_neighbors(const double* pos, int64_t N, const double cell[9], const int pbc[3],
+                    double r_list, int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift,
+                    int64_t cap, int64_t* n_pairs, void* stream) {
+  if (!n_pairs || !row_ptr || N < 0 || cap < 0 || (N > 0 && !pos) || (cap > 0 && (!nbr_j || !nbr_shift))) {
+    set_error("build_neighbors: bad pointer or size");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (N >= (int64_t(1) << 31)) {
+    set_error("build_neighbors: at most 2^31 - 1 atoms");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  int rc = check_cell(cell, pbc);
+  if (rc) return rc;
+  if (!(r_list > 0.0) || !(r_list < 1000.0)) {
+    set_error("build_neighbors: r_list must be in (0, 1000) A");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  CellGrid g;
+  rc = make_grid(cell, qfix_host(r_list), &g);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  DPA4C_HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lock(g_nb_lock);
+  NeighborScratch*& nb = g_nb_scratch[dev];
+  if (!nb) nb = new NeighborScratch();
+  DevBuf*& fl = g_nb_flags[dev];
+  if (!fl) fl = new DevBuf();
+  if (fl->ensure(8 * 8)) return DPA4C_ERR_HIP;
+  if (!nb->host_flag.p) {
+    DPA4C_HIP_TRY(hipHostMalloc(&nb->host_flag.p, 64, hipHostMallocDefault));
+    nb->host_flag.bytes = 64;
+  }
+  int64_t* hflag = nb->host_flag.as<int64_t>();
+  if (N == 0) {
+    DPA4C_HIP_TRY(hipMemsetAsync(row_ptr, 0, sizeof(int64_t), st));
+    DPA4C_HIP_TRY(hipStreamSynchronize(st));
+    *n_pairs = 0;
+    return 0;
+  }
+  int64_t* flags = fl->as<int64_t>();
+  DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
+  rc = build_skin_list(*nb, pos, N, g, row_ptr, nullptr, nullptr, cap, nullptr, flags, false, st);
+  if (rc) return rc;
+  DPA4C_HIP_TRY(hipMemcpyAsync(hflag, row_ptr + N, 8, hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 1, flags, 8, hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
+  if (hflag[1] & kFlagNonFinite) return flags_to_error(hflag[1]);
+  *n_pairs = hflag[0];
+  if (hflag[0] > cap) {
+    set_error("build_neighbors: capacity " + std::to_string(cap) + " < " + std::to_string(hflag[0]) +
+              " edges");
+    return DPA4C_ERR_CAPACITY;
+  }
+  rc = fill_skin_list(*nb, N, g, row_ptr, nbr_j, nbr_shift, cap, flags, st);
+  if (rc) return rc;
+  DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 1, flags, 8, hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
+  return flags_to_error(hflag[1]);
+}
+
+int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t* species,
+                          int64_t N, const double cell[9], const int pbc[3], double r_c,
+                          const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
+                          int64_t n_pairs, double* e_atom, double* forces, double* e_total,
+                          void* stream) {
+  if (!m || N < 0 || n_pairs < 0 || !row_ptr || !e_total ||
+      (N > 0 && (!pos || !species || !e_atom || !forces)) ||
+      (n_pairs > 0 && (!nbr_j || !nbr_shift))) {
+    set_error("compute_energy_forces: bad pointer or size");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (N >= (int64_t(1) << 31) || n_pairs >= (int64_t(1) << 31)) {
+    set_error("compute_energy_forces: at most 2^31 - 1 atoms and edges");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (std::fabs(r_c - m->r_c) > 1e-12) {
+    set_error("compute_energy_forces: r_c differs from the model's cutoff");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  int rc = check_cell(cell, pbc);
+  if (rc) return rc;
+  DeviceGuard guard(m->device);
+  dpa4c_model* mm = const_cast<dpa4c_model*>(m);
+  std::lock_guard<std::mutex> lock(mm->mu_lock);
+  CellGrid g;
+  rc = make_grid(cell, qfix_host(m->r_c), &g);
+  if (rc) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  rc = ensure_workspace(mm, N, n_pairs);
+  if (rc) return rc;
+  double box[3] = {cell[0], cell[4], cell[8]};
+  if (N == 0) {
+    DPA4C_HIP_TRY(hipMemsetAsync(e_total, 0, sizeof(double), st));
+    return 0;
+  }
+  {
+    StageScope t(m, kStSkinRev, st);
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), nullptr, st);
+    if (rc) return rc;
+  }
+  return run_model(m, pos, species, N, g, box, row_ptr, nbr_j, nbr_shift, n_pairs,
+                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, st);
+}
+
+int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
+                const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+                double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
+                double* e_pot, double* e_kin, double* forces, int64_t* n_rebuilds, void* stream) {
+  if (!m || N <= 0 || nsteps < 0 || !pos || !vel || !species || !mass_by_species || !forces ||
+      (nsteps > 0 && (!e_pot || !e_kin))) {
+    set_error("verlet_step: bad pointer or size");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (N >= (int64_t(1) << 31)) {
+    set_error("verlet_step: at most 2^31 - 1 atoms");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (std::fabs(r_c - m->r_c) > 1e-12 || !(skin >= 0.0) || skin > 100.0 || !(dt_fs > 0.0) ||
+      !(dt_fs < 100.0)) {
+    set_error("verlet_step: r_c must equal the model's; skin in [0, 100] A; dt in (0, 100) fs");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  const int T1 = m->n_types + 1;
+  for (int t = 0; t < T1; ++t)
+    if (!(mass_by_species[t] > 0.0) || !std::isfinite(mass_by_species[t])) {
+      set_error("verlet_step: masses must be positive and finite");
+      return DPA4C_ERR_INVALID_ARG;
+    }
+  int rc = check_cell(cell, pbc);
+  if (rc) return rc;
+  DeviceGuard guard(m->device);
+  dpa4c_model* mm = const_cast<dpa4c_model*>(m);
+  std::lock_guard<std::mutex> lock(mm->mu_lock);
+  Workspace& w = mm->ws;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t rcq = qfix_host(m->r_c), skq = qfix_host(skin);
+  CellGrid g_list, g_cut;
+  rc = make_grid(cell, rcq + skq, &g_list);
+  if (rc) return rc;
+  rc = make_grid(cell, rcq, &g_cut);
+  if (rc) return rc;
+  const double box[3] = {cell[0], cell[4], cell[8]};
+
+  // masses on the device
+  if (w.inv_mass.ensure(8 * T1) || w.mass.ensure(8 * T1) || w.flags.ensure(64) ||
+      w.skin_row.ensure(8 * (N + 1)) || w.skin_row_new.ensure(8 * (N + 1)) ||
+      w.qbuild.ensure(8 * 3 * N))
+    return DPA4C_ERR_HIP;
+  if (!w.host_flags) DPA4C_HIP_TRY(hipHostMalloc((void**)&w.host_flags, 64, hipHostMallocDefault));
+  {
+    std::vector<double> im(T1);
+    for (int t = 0; t < T1; ++t) im[t] = 1.0 / (mass_by_species[t] * (1.66053906660e-17 / 1.602176634e-19));
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.inv_mass.p, im.data(), 8 * T1, hipMemcpyHostToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.mass.p, mass_by_species, 8 * T1, hipMemcpyHostToDevice, st));
+  }
+  int64_t* flags = w.flags.as<int64_t>();
+  DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
+
+  // the first build of the call sizes the skin list
+  auto initial_build = [&]() -> int {
+    int r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,
+                            nullptr, flags, false, st);
+    if (r) return r;
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, w.skin_row.as<int64_t>() + N, 8,
+                                 hipMemcpyDeviceToHost, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags + 1, flags, 8, hipMemcpyDeviceToHost, st));
+    DPA4C_HIP_TRY(hipStreamSynchronize(st));
+    if (w.host_flags[1]) return flags_to_error(w.host_flags[1]);
+    int64_t need = w.host_flags[0];
+    int64_t cap = need + need / 2 + 64 * N;
+    if (cap >= (int64_t(1) << 31)) cap = (int64_t(1) << 31) - 1;
+    if (cap < need) {
+      set_error("verlet_step: more than 2^31 - 1 neighbour pairs");
+      return DPA4C_ERR_CAPACITY;
+    }
+    if (cap > w.cap || !w.skin_j.p) {
+      if (w.skin_j.ensure(4 * cap) || w.skin_shift.ensure(4 * cap)) return DPA4C_ERR_HIP;
+      w.cap = cap;
+    }
+    r = ensure_workspace(mm, N, w.cap);
+    if (r) return r;
+    {
+      StageScope t(m, kStNeighborFill, st);
+      r = fill_skin_list(w.nb, N, g_list, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
+                         w.skin_shift.as<int32_t>(), w.cap, flags, st);
+      if (r) return r;
+    }
+    r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
+                        N, w.skin_rev.as<int32_t>(), nullptr, st);
+    if (r) return r;
+    return launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), nullptr, st);
+  };
+
+  int64_t rebuilds = 0;
+  for (int step = 0; step < nsteps; ++step) {
+    {
+      StageScope t(m, kStIntegrate, st);
+      rc = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs, 1,
+                             step == 0 ? nullptr : w.qbuild.as<int64_t>(), skq, flags, st);
+      if (rc) return rc;
+    }
+    if (step == 0) {
+      rc = initial_build();
+      if (rc) return rc;
+      ++rebuilds;
+    } else if (rebuild_every >= 0) {
+      const bool forced = rebuild_every > 0 && step % rebuild_every == 0;
+      if (forced) {
+        rc = launch_set_flag(flags, 1, 1, st);
+        if (rc) return rc;
+      }
+      const int64_t* active = flags + 1;
+      {
+        // the scan goes to a scratch row array; it replaces the live one only
+        // when the new list fits the capacity
+        StageScope t(m, kStNeighborCount, st);
+        rc = build_skin_list(w.nb, pos, N, g_list, w.skin_row_new.as<int64_t>(),
+                             w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap, active,
+                             flags, true, st);
+        if (rc) return rc;
+        rc = commit_rows(w.skin_row_new.as<int64_t>(), w.skin_row.as<int64_t>(), N, w.cap, flags,
+                         active, st);
+        if (rc) return rc;
+      }
+      rc = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
+                           w.skin_shift.as<int32_t>(), N, w.skin_rev.as<int32_t>(), active, st);
+      if (rc) return rc;
+      rc = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), active, st);
+      if (rc) return rc;
+      rc = launch_rebuild_done(flags, st);
+      if (rc) return rc;
+    }
+    rc = run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
+                   w.skin_shift.as<int32_t>(), w.cap, w.skin_rev.as<int32_t>(), w.eatom.as<double>(),
+                   forces, e_pot + step, st);
+    if (rc) return rc;
+    {
+      StageScope t(m, kStIntegrate, st);
+      rc = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs, 0, nullptr,
+                             0, flags, st);
+      if (rc) return rc;
+      rc = launch_kinetic(N, vel, species, w.mass.as<double>(), T1, w.ekin_atom.as<double>(),
+                          w.epart.as<double>(), e_kin + step, st);
+      if (rc) return rc;
+    }
+  }
+  DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
+  if (n_rebuilds) *n_rebuilds = rebuilds + w.host_flags[3];
+  rc = flags_to_error(w.host_flags[0]);
+  if (rc) return rc;
+  if (rebuild_every < 0 && w.host_flags[1]) {
+    set_error("verlet_step: an atom moved more than skin/2 and rebuilds are disabled");
+    return DPA4C_ERR_SKIN;
+  }
+  return 0;
+}
+
+int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float* descriptor,
+                       int32_t* edge_count, void* stream) {
+  if (!m || N < 0 || N != m->last_n || !m->ws.last_species) {
+    set_error("dpa4c_debug_stages: N must match the last evaluation on this model");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  DeviceGuard guard(m->device);
+  dpa4c_model* mm = const_cast<dpa4c_model*>(m);
+  std::lock_guard<std::mutex> lock(mm->mu_lock);
+  Workspace& w = mm->ws;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (N == 0) return 0;
+  // recompute node state and descriptor from the stored compacted edges
+  int rc = launch_forward(m, N, w.last_species, w.skin_row_used, w.ecount.as<int32_t>(),
+                          w.edge.as<float4>(), w.node.as<float>(), w.desc.as<float>(), st);
+  if (rc) return rc;
+  const int dstr = (m->D_out + 15) / 16 * 16;
+  if (node_state)
+    DPA4C_HIP_TRY(hipMemcpyAsync(node_state, w.node.p, 4 * N * (m->S + 2), hipMemcpyDeviceToDevice, st));
+  if (descriptor)
+    DPA4C_HIP_TRY(hipMemcpy2DAsync(descriptor, 4 * m->D_out, w.desc.p, 4 * dstr, 4 * m->D_out, N,
+                                   hipMemcpyDeviceToDevice, st));
+  if (edge_count)
+    DPA4C_HIP_TRY(hipMemcpyAsync(edge_count, w.ecount.p, 4 * N, hipMemcpyDeviceToDevice, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
+  return 0;
+}
+
+int dpa4c_set_timing(dpa4c_model* m, int enable) {
+  if (!m) {
+    set_error("dpa4c_set_timing: null model");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  DeviceGuard guard(m->device);
+  collect_timing(m);
+  m->timing.enabled = enable != 0;
+  return 0;
+}
+
+int dpa4c_get_timings(dpa4c_model* m, double* ms, int64_t* count, int n) {
+  if (!m || n < 0) {
+    set_error("dpa4c_get_timings: bad argument");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  DeviceGuard guard(m->device);
+  collect_timing(m);
+  for (int s = 0; s < n && s < kNumStages; ++s) {
+    if (ms) ms[s] = m->timing.ms[s];
+    if (count) count[s] = m->timing.count[s];
+    m->timing.ms[s] = 0;
+    m->timing.count[s] = 0;
+  }
+  return kNumStages;
+}
+
+const char* dpa4c_stage_name(int s) { return stage_name(s); }
+
+int dpa4c_debug_gemm(const float* A, const float* B, float* C, int M, int N, int K, void* stream) {
+  if (!A || !B || !C || M < 0 || N <= 0 || N % 4 || K <= 0 || K % 16) {
+    set_error("dpa4c_debug_gemm: need K % 16 == 0 and N % 4 == 0");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  return launch_gemm_test(A, B, C, M, N, K, static_cast<hipStream_t>(stream));
+}
+
+const char* dpa4c_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

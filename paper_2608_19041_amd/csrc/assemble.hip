@@ -1,0 +1,236 @@
+// Force assembly, energy reduction and velocity-Verlet kernels.
+//
+// Forces, Eq. (forces): F_k = sum_{j in N_k} dE/dr_kj - sum_{i: k in N_i} dE/dr_ik.
+// Every edge e = (k -> j, n) of row k has a reverse edge rev[e] = (j -> k, -n)
+// in row j, so F_k = sum over row k of (g_e - g_rev[e]): one reduction per
+// atom over its own row, in a fixed order, in float64, with no atomics.
+// The total energy is a fixed-order two-pass float64 sum.
+#include <hip/hip_runtime.h>
+
+#include "../../include/dpa4c.h"
+#include "launch.h"
+
+namespace dpa4c {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kLanesPerAtom = 16;
+constexpr int kRedBlock = 256;
+constexpr int kRedPer = 16;                 // elements per thread in the first pass
+
+__global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
+                                                        const int32_t* __restrict__ ecount,
+                                                        const float4* __restrict__ grad,
+                                                        const int32_t* __restrict__ rev,
+                                                        double* __restrict__ forces) {
+  const int sub = threadIdx.x % kLanesPerAtom;
+  const int64_t per_grid = int64_t(gridDim.x) * (kBlock / kLanesPerAtom);
+  for (int64_t k = blockIdx.x * int64_t(kBlock / kLanesPerAtom) + threadIdx.x / kLanesPerAtom; k < n;
+       k += per_grid) {
+    const int64_t b = row_ptr[k], e = b + ecount[k];
+    double fx = 0.0, fy = 0.0, fz = 0.0;
+    for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
+      const float4 g = grad[s];
+      const float4 r = grad[rev[s]];
+      fx += double(g.x) - double(r.x);
+      fy += double(g.y) - double(r.y);
+      fz += double(g.z) - double(r.z);
+    }
+    for (int off = 1; off < kLanesPerAtom; off <<= 1) {
+      fx += __shfl_xor(fx, off, kLanesPerAtom);
+      fy += __shfl_xor(fy, off, kLanesPerAtom);
+      fz += __shfl_xor(fz, off, kLanesPerAtom);
+    }
+    if (sub == 0) {
+      forces[3 * k] = fx;
+      forces[3 * k + 1] = fy;
+      forces[3 * k + 2] = fz;
+    }
+  }
+}
+
+// first pass: block b sums the fixed slice [b*T, (b+1)*T) of x (times w if
+// given), in a fixed tree order
+__device__ inline double block_sum(double v, double* sh) {
+  sh[threadIdx.x] = v;
+  __syncthreads();
+  for (int off = kRedBlock / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off) sh[threadIdx.x] += sh[threadIdx.x + off];
+    __syncthreads();
+  }
+  return sh[0];
+}
+
+__global__ void __launch_bounds__(kRedBlock) partial_sum_kernel(const double* __restrict__ x, int64_t n,
+                                                                double* __restrict__ partials) {
+  __shared__ double sh[kRedBlock];
+  const int64_t base = blockIdx.x * int64_t(kRedBlock * kRedPer) + threadIdx.x;
+  double s = 0.0;
+  for (int t = 0; t < kRedPer; ++t) {
+    int64_t i = base + int64_t(t) * kRedBlock;
+    if (i < n) s += x[i];
+  }
+  double tot = block_sum(s, sh);
+  if (threadIdx.x == 0) partials[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(kRedBlock) final_sum_kernel(const double* __restrict__ partials,
+                                                              int64_t np, double* __restrict__ out) {
+  __shared__ double sh[kRedBlock];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < np; i += kRedBlock) s += partials[i];
+  double tot = block_sum(s, sh);
+  if (threadIdx.x == 0) *out = tot;
+}
+
+int fixed_sum(const double* x, int64_t n, double* partials, double* out, hipStream_t st) {
+  int64_t np = (n + kRedBlock * kRedPer - 1) / (kRedBlock * kRedPer);
+  if (np < 1) np = 1;
+  hipLaunchKernelGGL(partial_sum_kernel, dim3(np), dim3(kRedBlock), 0, st, x, n, partials);
+  hipLaunchKernelGGL(final_sum_kernel, dim3(1), dim3(kRedBlock), 0, st, partials, np, out);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+__device__ inline int64_t qfix(double x) { return static_cast<int64_t>(__builtin_rint(x * kQScale)); }
+
+// v += dt/2 F/m; optionally r += dt v and flag a rebuild when some atom moved
+// by more than half the skin since the last build (fixed-point norm:
+// 4 |dq|^2 > skin_q^2).
+__global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__ pos, double* __restrict__ vel,
+                                                            const double* __restrict__ forces,
+                                                            const int32_t* __restrict__ species,
+                                                            const double* __restrict__ inv_mass,
+                                                            int n_types1, int64_t n, double half_dt,
+                                                            double dt,
+                                                            int drift, const int64_t* __restrict__ qbuild,
+                                                            int64_t skin_q, int64_t* __restrict__ flags) {
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i >= n) return;
+  int a0 = species[i];
+  a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
+  const double im = inv_mass[a0];
+  double v[3], x[3];
+  for (int a = 0; a < 3; ++a) {
+    v[a] = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
+    vel[3 * i + a] = v[a];
+  }
+  if (!drift) return;
+  bool bad = false;
+  int64_t d2 = 0;
+  bool far = false;
+  for (int a = 0; a < 3; ++a) {
+    x[a] = pos[3 * i + a] + dt * v[a];
+    pos[3 * i + a] = x[a];
+    if (!isfinite(x[a]) || fabs(x[a]) > 1.0e12) bad = true;
+    if (!bad && qbuild) {
+      int64_t dq = qfix(x[a]) - qbuild[3 * i + a];
+      if (dq > skin_q || dq < -skin_q) far = true;
+      else d2 += dq * dq;
+    }
+  }
+  if (bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), 8ull);
+  if (bad || far || 4 * d2 > skin_q * skin_q)
+    atomicOr(reinterpret_cast<unsigned long long*>(flags + 1), 1ull);
+}
+
+__global__ void __launch_bounds__(kBlock) kinetic_kernel(int64_t n, const double* __restrict__ vel,
+                                                         const int32_t* __restrict__ species,
+                                                         const double* __restrict__ mass,
+                                                         int n_types1, double* __restrict__ ek) {
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i >= n) return;
+  int a0 = species[i];
+  a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
+  const double m = mass[a0];
+  const double vx = vel[3 * i], vy = vel[3 * i + 1], vz = vel[3 * i + 2];
+  // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
+  ek[i] = 0.5 * m * (vx * vx + vy * vy + vz * vz) * (1.66053906660e-17 / 1.602176634e-19);
+}
+
+__global__ void __launch_bounds__(kBlock) snapshot_kernel(const double* __restrict__ pos, int64_t n,
+                                                          int64_t* __restrict__ qbuild,
+                                                          const int64_t* active) {
+  if (active && *active == 0) return;
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i >= 3 * n) return;
+  qbuild[i] = qfix(pos[i]);
+}
+
+__global__ void set_flag_kernel(int64_t* flags, int idx, int64_t value) {
+  if (threadIdx.x == 0) flags[idx] = value;
+}
+
+__global__ void rebuild_done_kernel(int64_t* flags) {
+  if (threadIdx.x == 0 && flags[1]) {
+    flags[1] = 0;
+    flags[3] += 1;
+  }
+}
+
+int blocks_for(int64_t n) {
+  int64_t b = (n + kBlock - 1) / kBlock;
+  return static_cast<int>(b < 1 ? 1 : b);
+}
+
+}  // namespace
+
+int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
+                  const int32_t* rev, double* forces, hipStream_t st) {
+  int64_t blocks = (n + (kBlock / kLanesPerAtom) - 1) / (kBlock / kLanesPerAtom);
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(forces_kernel, dim3(blocks), dim3(kBlock), 0, st, n, row_ptr, ecount, grad,
+                     rev, forces);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_energy(int64_t n, const double* e_atom, double* partials, double* out, hipStream_t st) {
+  return fixed_sum(e_atom, n, partials, out, st);
+}
+
+int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
+                      const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
+                      const int64_t* qbuild, int64_t skin_q, int64_t* flags, hipStream_t st) {
+  hipLaunchKernelGGL(kick_drift_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, pos, vel, forces,
+                     species, inv_mass, n_types1, n, 0.5 * dt, dt, drift, qbuild, skin_q, flags);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_kinetic(int64_t n, const double* vel, const int32_t* species, const double* mass,
+                   int n_types1, double* ekin_atom, double* partials, double* out, hipStream_t st) {
+  hipLaunchKernelGGL(kinetic_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, n, vel, species, mass,
+                     n_types1, ekin_atom);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return fixed_sum(ekin_atom, n, partials, out, st);
+}
+
+int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, const int64_t* active,
+                      hipStream_t st) {
+  hipLaunchKernelGGL(snapshot_kernel, dim3(blocks_for(3 * n)), dim3(kBlock), 0, st, pos, n, qbuild,
+                     active);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st) {
+  hipLaunchKernelGGL(set_flag_kernel, dim3(1), dim3(64), 0, st, flags, idx, value);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_rebuild_done(int64_t* flags, hipStream_t st) {
+  hipLaunchKernelGGL(rebuild_done_kernel, dim3(1), dim3(64), 0, st, flags);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int partial_count(int64_t n) {
+  int64_t np = (n + kRedBlock * kRedPer - 1) / (kRedBlock * kRedPer);
+  return static_cast<int>(np < 1 ? 1 : np);
+}
+
+}  // namespace dpa4c

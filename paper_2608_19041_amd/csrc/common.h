@@ -1,0 +1,120 @@
+// Internal definitions shared by the HIP sources of the DPA4C library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+namespace dpa4c {
+
+constexpr double kEps = 1.0e-7;          // Eq. (edge-geometry) regulariser
+constexpr double kQScale = 1048576.0;    // 2^20: fixed-point resolution of positions
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Compile-time profile (C0, L, R): every width of the model follows from it
+// (Eqs. (degree-channels), (probe-ranks), (moment-width), (dim-out)).
+// ---------------------------------------------------------------------------
+constexpr int ceil_log2(int x) { return x <= 1 ? 0 : 1 + ceil_log2((x + 1) / 2); }
+constexpr int imax(int a, int b) { return a > b ? a : b; }
+
+template <int C0_, int L_, int R_>
+struct Profile {
+  static constexpr int C0 = C0_, L = L_, R = R_;
+  static constexpr int C1 = imax(4, 1 << ((ceil_log2(C0) + 1) / 2));
+  static constexpr int C2 = imax(4, C1 / 2);
+  static constexpr int C3 = 1;
+  static constexpr int K1 = C2, K2 = 2, K3 = 1;
+  static constexpr bool kHasA1 = (K1 != C1);
+  static constexpr int S = C0 + 3 * C1 + 5 * C2 + (L >= 3 ? 7 * C3 : 0);
+  static constexpr int NS = S + 2;               // node state: [S0, S1, Y]
+  // offsets inside the node state (after the two normaliser sums)
+  static constexpr int Y0 = 2;
+  static constexpr int Y1 = Y0 + C0;              // [3][C1]
+  static constexpr int Y2 = Y1 + 3 * C1;          // [5][C2]
+  static constexpr int Y3 = Y2 + 5 * C2;          // [7]
+  // lane mapping of the edge kernels: LPE lanes per edge, lane k owns the
+  // channels c = k + LPE*j, j < CPL, so channel c < C1 sits in slot j = 0
+  static constexpr int LPE = C1;
+  static constexpr int CPL = C0 / LPE;
+  static constexpr int EPW = kWave / LPE;
+  static constexpr int PW = 2 + R;                // pair cache entries per channel
+  // descriptor layout, Eq. (descriptor)
+  static constexpr int nG1 = C1 * (C1 + 1) / 2, nG2 = C2 * (C2 + 1) / 2, nG3 = (L >= 3 ? 1 : 0);
+  static constexpr int n112 = K1 * (K1 + 1) / 2 * K2;
+  static constexpr int n123 = (L >= 3 ? K1 * K2 * K3 : 0);
+  static constexpr int n222 = K2 * (K2 + 1) * (K2 + 2) / 6;
+  static constexpr int n233 = (L >= 3 ? K2 : 0);
+  static constexpr int nPi = K2 * K1;
+  static constexpr int oX0 = 0, oX = C0, oM0 = 2 * C0, oM1 = 2 * C0 + 1;
+  static constexpr int oG1 = 2 * C0 + 2, oG2 = oG1 + nG1, oG3 = oG2 + nG2;
+  static constexpr int o112 = oG3 + nG3, o123 = o112 + n112, o222 = o123 + n123;
+  static constexpr int o233 = o222 + n222, oPi = o233 + n233;
+  static constexpr int DOUT = oPi + nPi;
+  static constexpr int DSTR = (DOUT + 15) / 16 * 16;   // row stride of descriptor arrays
+  static_assert(C0 % LPE == 0, "channel split");
+  static_assert(kWave % LPE == 0, "edge groups");
+};
+
+using SmallProfile = Profile<32, 2, 0>;
+using FullProfile = Profile<128, 3, 4>;
+static_assert(SmallProfile::DOUT == 144 && SmallProfile::S == 76, "Table S2 (32, 2)");
+static_assert(FullProfile::DOUT == 541 && FullProfile::S == 223, "Table S2 (128, 3)");
+
+// ---------------------------------------------------------------------------
+// Device-side view of a model, passed to kernels by value.
+// ---------------------------------------------------------------------------
+struct Sparse3 {            // nonzeros of one coupling tensor
+  int n;
+  const int* idx;           // [n][3] (m1, m2, m3)
+  const float* val;         // [n]
+};
+
+struct ModelDev {
+  // radial table: g rows [n_rows][CPL][LPE][6], q rows [n_rows][R][6]
+  const float* gtab;
+  const float* qtab;
+  int n_rows;
+  float inv_delta;
+  float r_c;
+  int n_types1;             // T + 1
+  const float* pair;        // [(T+1)^2][CPL][LPE][PW]
+  const float* type_embed;  // [T+1][C0]
+  const float* W1;          // [C1][C1] alignment, degree 1 (I + W applied in-kernel)
+  const float* W2;          // [C2][C2]
+  const float* A1;          // [C1][K1] or null (identity)
+  const float* A2;          // [C2][K2]
+  const float* mu;          // [D_out]
+  const float* inv_sigma;   // [D_out]
+  Sparse3 c123, c233;
+  const float* E_ref;       // [T+1]
+};
+
+// ---------------------------------------------------------------------------
+// Error handling
+// ---------------------------------------------------------------------------
+void set_error(const std::string& msg);
+
+#define DPA4C_HIP_TRY(expr)                                                      \
+  do {                                                                           \
+    hipError_t _e = (expr);                                                      \
+    if (_e != hipSuccess) {                                                      \
+      ::dpa4c::set_error(std::string(#expr) + ": " + hipGetErrorString(_e));     \
+      return DPA4C_ERR_HIP;                                                      \
+    }                                                                            \
+  } while (0)
+
+// packed image shift: ((nx+128) << 16) | ((ny+128) << 8) | (nz+128)
+__host__ __device__ inline int32_t pack_shift(int nx, int ny, int nz) {
+  return ((nx + 128) << 16) | ((ny + 128) << 8) | (nz + 128);
+}
+__host__ __device__ inline int unpack_x(int32_t s) { return ((s >> 16) & 0xFF) - 128; }
+__host__ __device__ inline int unpack_y(int32_t s) { return ((s >> 8) & 0xFF) - 128; }
+__host__ __device__ inline int unpack_z(int32_t s) { return (s & 0xFF) - 128; }
+// shift of the reverse edge: n -> -n
+__host__ __device__ inline int32_t negate_shift(int32_t s) {
+  return pack_shift(-unpack_x(s), -unpack_y(s), -unpack_z(s));
+}
+
+}  // namespace dpa4c

@@ -1,0 +1,125 @@
+// Device helpers shared by the forward and backward edge kernels:
+// edge geometry, envelope, harmonics and the quintic radial table.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace dpa4c {
+
+__device__ inline int lane_of() { return threadIdx.x & (kWave - 1); }
+
+__device__ inline void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// Eq. (edge-geometry) in float32
+struct EdgeGeom {
+  float rho, ux, uy, uz, inv_rho;
+};
+__device__ inline EdgeGeom edge_geom(float rx, float ry, float rz) {
+  EdgeGeom g;
+  float r2 = rx * rx + ry * ry + rz * rz + float(kEps * kEps);
+  g.rho = sqrtf(r2);
+  g.inv_rho = 1.0f / g.rho;
+  g.ux = rx * g.inv_rho;
+  g.uy = ry * g.inv_rho;
+  g.uz = rz * g.inv_rho;
+  return g;
+}
+
+// Eq. (envelope): chi = t^4 (1 + 4x + 10x^2 + 20x^3 + 35x^4), x = rho/r_c,
+// t = 1 - x, clipped; d chi / d rho = -280 x^4 t^3 / r_c.
+__device__ inline void envelope(float rho, float r_c, float* chi, float* dchi) {
+  float x = fminf(rho / r_c, 1.0f);
+  float t = 1.0f - x;
+  float t2 = t * t;
+  float p = 1.0f + x * (4.0f + x * (10.0f + x * (20.0f + x * 35.0f)));
+  *chi = t2 * t2 * p;
+  if (dchi) {
+    float x2 = x * x;
+    *dchi = -280.0f * x2 * x2 * t2 * t / r_c;
+  }
+}
+
+// Real Cartesian harmonics with |u|^2 set to one (Methods "Fidelity of the
+// compressed model"; the error is O(eps^2/rho^2)).
+__device__ inline void harm2(float x, float y, float z, float* b) {
+  const float r3 = 1.7320508075688772f;
+  b[0] = r3 * x * y;
+  b[1] = r3 * y * z;
+  b[2] = 0.5f * (3.0f * z * z - 1.0f);
+  b[3] = r3 * x * z;
+  b[4] = 0.5f * r3 * (x * x - y * y);
+}
+__device__ inline void harm3(float x, float y, float z, float* b) {
+  const float a = 0.7905694150420949f;   // sqrt(5/8)
+  const float r15 = 3.872983346207417f;  // sqrt(15)
+  const float c = 0.6123724356957945f;   // sqrt(3/8)
+  b[0] = a * y * (3.0f * x * x - y * y);
+  b[1] = r15 * x * y * z;
+  b[2] = c * y * (5.0f * z * z - 1.0f);
+  b[3] = 0.5f * z * (5.0f * z * z - 3.0f);
+  b[4] = c * x * (5.0f * z * z - 1.0f);
+  b[5] = 0.5f * r15 * z * (x * x - y * y);
+  b[6] = a * x * (x * x - 3.0f * y * y);
+}
+// gradients d B / d u (with |u|^2 = 1 held constant): g[m][3]
+__device__ inline void harm2_grad(float x, float y, float z, float (*g)[3]) {
+  const float r3 = 1.7320508075688772f;
+  g[0][0] = r3 * y; g[0][1] = r3 * x; g[0][2] = 0.0f;
+  g[1][0] = 0.0f;   g[1][1] = r3 * z; g[1][2] = r3 * y;
+  g[2][0] = 0.0f;   g[2][1] = 0.0f;   g[2][2] = 3.0f * z;
+  g[3][0] = r3 * z; g[3][1] = 0.0f;   g[3][2] = r3 * x;
+  g[4][0] = r3 * x; g[4][1] = -r3 * y; g[4][2] = 0.0f;
+}
+__device__ inline void harm3_grad(float x, float y, float z, float (*g)[3]) {
+  const float a = 0.7905694150420949f, r15 = 3.872983346207417f, c = 0.6123724356957945f;
+  const float d = 0.5f * r15;
+  g[0][0] = 6.0f * a * x * y;            g[0][1] = 3.0f * a * (x * x - y * y); g[0][2] = 0.0f;
+  g[1][0] = r15 * y * z;                 g[1][1] = r15 * x * z;                g[1][2] = r15 * x * y;
+  g[2][0] = 0.0f;                        g[2][1] = c * (5.0f * z * z - 1.0f);  g[2][2] = 10.0f * c * y * z;
+  g[3][0] = 0.0f;                        g[3][1] = 0.0f;                       g[3][2] = 7.5f * z * z - 1.5f;
+  g[4][0] = c * (5.0f * z * z - 1.0f);   g[4][1] = 0.0f;                       g[4][2] = 10.0f * c * x * z;
+  g[5][0] = 2.0f * d * x * z;            g[5][1] = -2.0f * d * y * z;          g[5][2] = d * (x * x - y * y);
+  g[6][0] = 3.0f * a * (x * x - y * y);  g[6][1] = -6.0f * a * x * y;          g[6][2] = 0.0f;
+}
+
+// Table interval and local coordinate tau in [0, 1) for rho.
+// The row index is clamped to the table (a NaN rho maps to row 0 and gives
+// a NaN tau, never an out-of-range read); beyond the last knot the last
+// polynomial is extrapolated, where the envelope is already zero.
+__device__ inline int table_row(float rho, float inv_delta, int n_rows, float* tau) {
+  float s = rho * inv_delta;
+  float sc = fminf(fmaxf(s, 0.0f), static_cast<float>(n_rows - 1));
+  int r = static_cast<int>(sc);
+  *tau = s - static_cast<float>(r);
+  return r;
+}
+
+// species index clamped into the type table (the padding type for bad input)
+__device__ inline int clamp_type(int a, int n_types1) {
+  return static_cast<unsigned>(a) < static_cast<unsigned>(n_types1) ? a : n_types1 - 1;
+}
+
+// quintic in normalised form: value (Horner)
+__device__ inline float quintic_val(const float* c, float t) {
+  return c[0] + t * (c[1] + t * (c[2] + t * (c[3] + t * (c[4] + t * c[5]))));
+}
+// value and d/dtau
+__device__ inline void quintic_val_der(const float* c, float t, float* v, float* d) {
+  *v = c[0] + t * (c[1] + t * (c[2] + t * (c[3] + t * (c[4] + t * c[5]))));
+  *d = c[1] + t * (2.0f * c[2] + t * (3.0f * c[3] + t * (4.0f * c[4] + t * (5.0f * c[5]))));
+}
+
+// load 6 floats from an 8-byte aligned address as three float2
+__device__ inline void load6(const float* __restrict__ p, float* c) {
+  const float2* q = reinterpret_cast<const float2*>(p);
+  float2 a = q[0], b = q[1], d = q[2];
+  c[0] = a.x; c[1] = a.y; c[2] = b.x; c[3] = b.y; c[4] = d.x; c[5] = d.y;
+}
+
+}  // namespace dpa4c

@@ -1,0 +1,138 @@
+// Host-side model object and workspace of the DPA4C library.
+#pragma once
+
+#include <mutex>
+#include <vector>
+
+#include "common.h"
+
+struct dpa4c_model;
+
+namespace dpa4c {
+
+enum Stage {
+  kStNeighborBin = 0,
+  kStNeighborCount,
+  kStNeighborScan,
+  kStNeighborFill,
+  kStSkinRev,
+  kStCompact,
+  kStRev,
+  kStForward,
+  kStMlpForward,
+  kStMlpBackward,
+  kStBackward,
+  kStForces,
+  kStEnergy,
+  kStIntegrate,
+  kNumStages
+};
+const char* stage_name(int s);
+
+// grow-only device buffer
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  int ensure(size_t want);   // returns 0 or DPA4C_ERR_HIP
+  void release();
+  template <class T> T* as() const { return static_cast<T*>(p); }
+};
+
+// Cell-list scratch used by neighbour builds.
+struct NeighborScratch {
+  DevBuf qpos;       // int64 [N][3] wrapped fixed-point positions
+  DevBuf wrap;       // int32 [N][3] lattice translations removed by wrapping
+  DevBuf cell_of;    // int32 [N]
+  DevBuf cell_cnt;   // int32 [ncell]
+  DevBuf cell_start; // int32 [ncell+1]
+  DevBuf cell_fill;  // int32 [ncell]
+  DevBuf cell_atoms; // int32 [N]
+  DevBuf counts;     // int64 [N]
+  DevBuf partials;   // int64 scan partials
+  DevBuf host_flag;  // pinned host int64 [4]
+};
+
+struct Workspace {
+  int64_t n_atoms = 0;
+  int64_t cap = 0;
+  // skin list owned by verlet_step
+  DevBuf skin_row;      // int64 [N+1]
+  DevBuf skin_row_new;  // int64 [N+1]: scan of a device-side rebuild before commit
+  DevBuf skin_j;        // int32 [cap]
+  DevBuf skin_shift;    // int32 [cap]
+  DevBuf skin_rev;      // int32 [cap]
+  DevBuf qbuild;        // int64 [N][3] fixed-point positions at the last build
+  // compacted (r < r_c) edges, stored in the rows of the skin list
+  DevBuf ecount;        // int32 [N]
+  DevBuf edge;          // float4 [cap]: r_ij (x, y, z) and j (bits)
+  DevBuf cidx;          // int32 [cap]: compact slot of each skin edge or -1
+  DevBuf sidx;          // int32 [cap]: skin edge of each compact slot
+  DevBuf rev;           // int32 [cap]
+  DevBuf grad;          // float4 [cap]: dE/dr_ij
+  // per-atom state
+  DevBuf node;          // float [N][NS]
+  DevBuf desc;          // float [N][D_out]  (D, then dE/dD)
+  DevBuf h[3];          // float [N][F]
+  DevBuf ds[3];         // float [N][F]  SiLU'(pre) then back-propagated grads
+  DevBuf epart;         // double partial sums
+  DevBuf flags;         // int64 [8] device flags
+  DevBuf ekin_atom;     // double [N]
+  DevBuf eatom;         // double [N] (per-atom energies inside verlet_step)
+  DevBuf inv_mass;      // double [T+1]: 1 / (m * 103.6427)  (A/fs^2 per eV/A)
+  DevBuf mass;          // double [T+1]
+  int64_t* host_flags = nullptr;          // pinned [8]
+  const int32_t* last_species = nullptr;  // inputs of the last evaluation
+  const int64_t* skin_row_used = nullptr;
+  NeighborScratch nb;
+};
+
+struct Timing {
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<int> ev_stage;      // stage of each recorded pair
+  size_t used = 0;
+  double ms[kNumStages] = {};
+  int64_t count[kNumStages] = {};
+};
+
+}  // namespace dpa4c
+
+struct dpa4c_model {
+  int device = 0;
+  int C0 = 0, L = 0, R = 0, n_rbf = 0, F = 0, n_layers = 0, n_types = 0;
+  double r_c = 0, delta = 0;
+  int C[5] = {}, K[5] = {};
+  int S = 0, D_out = 0, H = 0, Hp = 0, n_rows = 0;
+  // device parameter storage
+  dpa4c::DevBuf params;             // one allocation holding every array below
+  float* gtab = nullptr;
+  float* qtab = nullptr;
+  float* pair = nullptr;
+  float* type_embed = nullptr;
+  float* W1 = nullptr;
+  float* W2 = nullptr;
+  float* A1 = nullptr;
+  float* A2 = nullptr;
+  float* mu = nullptr;
+  float* inv_sigma = nullptr;
+  float* E_ref = nullptr;
+  float* theta[8] = {};             // Theta_t [in][F]
+  float* thetaT[8] = {};            // Theta_t^T [F][in]
+  float* bias[8] = {};
+  float* w_head = nullptr;
+  float b_head = 0;
+  int* c123_idx = nullptr;
+  float* c123_val = nullptr;
+  int c123_n = 0;
+  int* c233_idx = nullptr;
+  float* c233_val = nullptr;
+  int c233_n = 0;
+  // host copies kept for tests of the host logic
+  std::vector<double> gaunt[4];     // (1,1,2), (1,2,3), (2,2,2), (2,3,3) normalised couplings
+  dpa4c::Workspace ws;
+  dpa4c::Timing timing;
+  std::mutex mu_lock;
+  int64_t last_n = 0;
+
+  dpa4c::ModelDev dev() const;
+};

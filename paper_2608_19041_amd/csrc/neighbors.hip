@@ -1,0 +1,646 @@
+// Cell-list neighbour search and per-step edge compaction, Methods Eq.
+// (neighbor-set), integer arithmetic only.
+//
+// Positions are mapped to fixed point Q(x) = rint(x * 2^20) (int64) and the
+// membership test |Q(r_j) + n.Q(h) - Q(r_i)|^2 < Q(r)^2 is exact, so every
+// list built here is a deterministic function of the float64 positions.
+// Rows come out in canonical order (ascending j, then n_x, n_y, n_z).
+//
+// Work mapping: one 64-lane wavefront per centre atom, waves striding over
+// centres; candidate atoms of a stencil cell are spread over the lanes and
+// compacted with a wave ballot, which keeps their relative order.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "../../include/dpa4c.h"
+#include "launch.h"
+
+namespace dpa4c {
+
+namespace {
+
+constexpr int kBlock = 256;            // 4 waves
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kMaxRow = 1024;          // longest row the fill kernel sorts in LDS
+constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8,
+                  kFlagRev = 16;
+
+__device__ inline int64_t floor_div(int64_t a, int64_t b) {
+  int64_t q = a / b;
+  return (a % b != 0 && ((a < 0) != (b < 0))) ? q - 1 : q;
+}
+
+__device__ inline int64_t qfix(double x) { return static_cast<int64_t>(__builtin_rint(x * kQScale)); }
+
+__device__ inline int lane_id() { return threadIdx.x & (kWave - 1); }
+
+// exclusive prefix count of ``pred`` over the lanes below this one
+__device__ inline int ballot_prefix(bool pred, uint64_t* mask_out) {
+  uint64_t m = __ballot(pred);
+  *mask_out = m;
+  return __popcll(m & ((uint64_t(1) << lane_id()) - 1));
+}
+
+__device__ inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__device__ inline bool inactive(const int64_t* active) { return active && *active == 0; }
+
+struct GridDev {
+  int64_t Lq0, Lq1, Lq2;
+  int nc0, nc1, nc2;
+  int re0, re1, re2;
+  int64_t rq;
+};
+
+GridDev to_dev(const CellGrid& g) {
+  return {g.Lq[0], g.Lq[1], g.Lq[2], g.nc[0], g.nc[1], g.nc[2], g.reach[0], g.reach[1],
+          g.reach[2], g.rq};
+}
+
+// within (strictly) the fixed-point radius; no overflow: components are
+// rejected before squaring
+__device__ inline bool within(int64_t dx, int64_t dy, int64_t dz, int64_t rq) {
+  if (dx >= rq || dx <= -rq || dy >= rq || dy <= -rq || dz >= rq || dz <= -rq) return false;
+  return dx * dx + dy * dy + dz * dz < rq * rq;
+}
+
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kBlock) zero_i32_kernel(int32_t* __restrict__ p, int64_t n,
+                                                          const int64_t* active) {
+  if (inactive(active)) return;
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+__global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ pos, int64_t n,
+                                                     GridDev g, int64_t* __restrict__ qpos,
+                                                     int32_t* __restrict__ wrap,
+                                                     int32_t* __restrict__ cell_of,
+                                                     int32_t* __restrict__ cell_cnt,
+                                                     int64_t* __restrict__ flags,
+                                                     const int64_t* active) {
+  if (inactive(active)) return;
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i >= n) return;
+  const int64_t Lq[3] = {g.Lq0, g.Lq1, g.Lq2};
+  const int nc[3] = {g.nc0, g.nc1, g.nc2};
+  int c[3];
+  bool bad = false;
+  for (int a = 0; a < 3; ++a) {
+    double x = pos[3 * i + a];
+    if (!isfinite(x) || fabs(x) > 1.0e12) {
+      bad = true;
+      x = 0.0;
+    }
+    int64_t q = qfix(x);
+    int64_t m = floor_div(q, Lq[a]);
+    int64_t qw = q - m * Lq[a];
+    qpos[3 * i + a] = qw;
+    wrap[3 * i + a] = static_cast<int32_t>(m);
+    c[a] = static_cast<int>((qw * nc[a]) / Lq[a]);
+  }
+  if (bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagNonFinite);
+  int cid = (c[0] * nc[1] + c[1]) * nc[2] + c[2];
+  cell_of[i] = cid;
+  atomicAdd(&cell_cnt[cid], 1);
+}
+
+// exclusive scan of the (few thousand) cell counts in one block
+__global__ void __launch_bounds__(1024) cell_scan_kernel(const int32_t* __restrict__ cnt,
+                                                         int64_t ncell, int32_t* __restrict__ start,
+                                                         int32_t* __restrict__ fill,
+                                                         const int64_t* active) {
+  if (inactive(active)) return;
+  __shared__ int32_t part[1024];
+  int64_t per = (ncell + 1023) / 1024;
+  int64_t b = threadIdx.x * per, e = b + per < ncell ? b + per : ncell;
+  int32_t s = 0;
+  for (int64_t k = b; k < e; ++k) s += cnt[k];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t run = 0;
+    for (int t = 0; t < 1024; ++t) {
+      int32_t v = part[t];
+      part[t] = run;
+      run += v;
+    }
+    start[ncell] = run;
+  }
+  __syncthreads();
+  int32_t run = part[threadIdx.x];
+  for (int64_t k = b; k < e; ++k) {
+    start[k] = run;
+    fill[k] = 0;
+    run += cnt[k];
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) place_kernel(int64_t n, const int32_t* __restrict__ cell_of,
+                                                       const int32_t* __restrict__ start,
+                                                       int32_t* __restrict__ fill,
+                                                       int32_t* __restrict__ atoms,
+                                                       const int64_t* active) {
+  if (inactive(active)) return;
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i >= n) return;
+  int cid = cell_of[i];
+  int slot = atomicAdd(&fill[cid], 1);
+  atoms[start[cid] + slot] = static_cast<int32_t>(i);
+}
+
+// Visits every (cell, image) of the stencil of centre i and calls
+// f(j, nx, ny, nz, pred) on chunks of candidates (one per lane, pred false on
+// idle lanes).  Wave-uniform control flow.
+template <class Fn>
+__device__ inline void for_candidates(const GridDev& g, int64_t i, const int64_t* __restrict__ qpos,
+                                      const int32_t* __restrict__ wrap,
+                                      const int32_t* __restrict__ start,
+                                      const int32_t* __restrict__ atoms, Fn&& f) {
+  const int64_t qi0 = qpos[3 * i], qi1 = qpos[3 * i + 1], qi2 = qpos[3 * i + 2];
+  const int mi0 = wrap[3 * i], mi1 = wrap[3 * i + 1], mi2 = wrap[3 * i + 2];
+  const int ci0 = static_cast<int>((qi0 * g.nc0) / g.Lq0);
+  const int ci1 = static_cast<int>((qi1 * g.nc1) / g.Lq1);
+  const int ci2 = static_cast<int>((qi2 * g.nc2) / g.Lq2);
+  const int lane = lane_id();
+  for (int d0 = -g.re0; d0 <= g.re0; ++d0) {
+    int t0 = ci0 + d0;
+    int s0 = static_cast<int>(floor_div(t0, g.nc0));
+    int w0 = t0 - s0 * g.nc0;
+    for (int d1 = -g.re1; d1 <= g.re1; ++d1) {
+      int t1 = ci1 + d1;
+      int s1 = static_cast<int>(floor_div(t1, g.nc1));
+      int w1 = t1 - s1 * g.nc1;
+      for (int d2 = -g.re2; d2 <= g.re2; ++d2) {
+        int t2 = ci2 + d2;
+        int s2 = static_cast<int>(floor_div(t2, g.nc2));
+        int w2 = t2 - s2 * g.nc2;
+        int cid = (w0 * g.nc1 + w1) * g.nc2 + w2;
+        int cb = start[cid], ce = start[cid + 1];
+        for (int base = cb; base < ce; base += kWave) {
+          int idx = base + lane;
+          bool pred = false;
+          int32_t j = 0;
+          int nx = 0, ny = 0, nz = 0;
+          if (idx < ce) {
+            j = atoms[idx];
+            int64_t dx = qpos[3 * j] + s0 * g.Lq0 - qi0;
+            int64_t dy = qpos[3 * j + 1] + s1 * g.Lq1 - qi1;
+            int64_t dz = qpos[3 * j + 2] + s2 * g.Lq2 - qi2;
+            nx = s0 - wrap[3 * j] + mi0;
+            ny = s1 - wrap[3 * j + 1] + mi1;
+            nz = s2 - wrap[3 * j + 2] + mi2;
+            pred = within(dx, dy, dz, g.rq) && !(j == i && nx == 0 && ny == 0 && nz == 0);
+          }
+          f(j, nx, ny, nz, pred);
+        }
+      }
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) count_kernel(int64_t n, GridDev g,
+                                                       const int64_t* __restrict__ qpos,
+                                                       const int32_t* __restrict__ wrap,
+                                                       const int32_t* __restrict__ start,
+                                                       const int32_t* __restrict__ atoms,
+                                                       int64_t* __restrict__ counts,
+                                                       const int64_t* active) {
+  if (inactive(active)) return;
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+    int64_t total = 0;
+    for_candidates(g, i, qpos, wrap, start, atoms, [&](int32_t, int, int, int, bool pred) {
+      total += __popcll(__ballot(pred));
+    });
+    if (lane_id() == 0) counts[i] = total;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// int64 exclusive scan: out[0..n] with out[n] = total
+constexpr int kScanPer = 8;
+constexpr int kScanTile = kBlock * kScanPer;
+
+__device__ inline int64_t block_exclusive_scan(int64_t v, int64_t* sh, int64_t* total) {
+  int t = threadIdx.x;
+  sh[t] = v;
+  __syncthreads();
+  for (int off = 1; off < kBlock; off <<= 1) {
+    int64_t add = t >= off ? sh[t - off] : 0;
+    __syncthreads();
+    sh[t] += add;
+    __syncthreads();
+  }
+  int64_t incl = sh[t];
+  *total = sh[kBlock - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+__global__ void __launch_bounds__(kBlock) scan_partials_kernel(const int64_t* __restrict__ in,
+                                                               int64_t n,
+                                                               int64_t* __restrict__ partials,
+                                                               const int64_t* active) {
+  if (inactive(active)) return;
+  __shared__ int64_t sh[kBlock];
+  int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
+  int64_t s = 0;
+  for (int k = 0; k < kScanPer; ++k)
+    if (base + k < n) s += in[base + k];
+  int64_t tot;
+  block_exclusive_scan(s, sh, &tot);
+  if (threadIdx.x == 0) partials[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(kBlock) scan_top_kernel(int64_t* __restrict__ partials,
+                                                          int64_t nparts, const int64_t* active) {
+  if (inactive(active)) return;
+  __shared__ int64_t sh[kBlock];
+  int64_t carry = 0;
+  for (int64_t b = 0; b < nparts; b += kBlock) {
+    int64_t idx = b + threadIdx.x;
+    int64_t v = idx < nparts ? partials[idx] : 0;
+    int64_t tot;
+    int64_t ex = block_exclusive_scan(v, sh, &tot);
+    if (idx < nparts) partials[idx] = ex + carry;
+    carry += tot;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) scan_apply_kernel(const int64_t* __restrict__ in,
+                                                            int64_t n,
+                                                            const int64_t* __restrict__ partials,
+                                                            int64_t* __restrict__ out,
+                                                            const int64_t* active) {
+  if (inactive(active)) return;
+  __shared__ int64_t sh[kBlock];
+  int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
+  int64_t v[kScanPer];
+  int64_t s = 0;
+  for (int k = 0; k < kScanPer; ++k) {
+    v[k] = base + k < n ? in[base + k] : 0;
+    s += v[k];
+  }
+  int64_t tot;
+  int64_t run = block_exclusive_scan(s, sh, &tot) + partials[blockIdx.x];
+  for (int k = 0; k < kScanPer; ++k) {
+    if (base + k < n) out[base + k] = run;
+    run += v[k];
+  }
+  if (base <= n - 1 && n - 1 < base + kScanPer) out[n] = run;  // thread holding the last element
+}
+
+int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
+                   const int64_t* active, hipStream_t st) {
+  int64_t nb = (n + kScanTile - 1) / kScanTile;
+  if (nb == 0) nb = 1;
+  if (partials.ensure(sizeof(int64_t) * nb)) return DPA4C_ERR_HIP;
+  hipLaunchKernelGGL(scan_partials_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
+                     partials.as<int64_t>(), active);
+  hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kBlock), 0, st, partials.as<int64_t>(), nb,
+                     active);
+  hipLaunchKernelGGL(scan_apply_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
+                     partials.as<int64_t>(), out, active);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
+                                                      const int64_t* __restrict__ qpos,
+                                                      const int32_t* __restrict__ wrap,
+                                                      const int32_t* __restrict__ start,
+                                                      const int32_t* __restrict__ atoms,
+                                                      const int64_t* __restrict__ row_ptr,
+                                                      int32_t* __restrict__ nbr_j,
+                                                      int32_t* __restrict__ nbr_shift, int64_t cap,
+                                                      int64_t* __restrict__ flags,
+                                                      const int64_t* active) {
+  if (inactive(active)) return;
+  __shared__ int64_t keys_all[kWavesPerBlock][kMaxRow];
+  if (row_ptr[n] > cap) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagCapacity);
+      atomicMax(reinterpret_cast<unsigned long long*>(flags + 2), (unsigned long long)row_ptr[n]);
+    }
+    return;
+  }
+  int64_t* keys = keys_all[threadIdx.x / kWave];
+  const int lane = lane_id();
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+    const int64_t r0 = row_ptr[i];
+    const int len = static_cast<int>(row_ptr[i + 1] - r0);
+    if (len > kMaxRow) {
+      if (lane == 0)
+        atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagRowTooLong);
+      continue;
+    }
+    int fill = 0;
+    bool shift_bad = false;
+    for_candidates(g, i, qpos, wrap, start, atoms, [&](int32_t j, int nx, int ny, int nz, bool pred) {
+      uint64_t m;
+      int pre = ballot_prefix(pred, &m);
+      if (pred) {
+        if (nx < -127 || nx > 127 || ny < -127 || ny > 127 || nz < -127 || nz > 127) shift_bad = true;
+        int slot = fill + pre;
+        if (slot < kMaxRow)
+          keys[slot] = (int64_t(j) << 24) | int64_t(pack_shift(nx, ny, nz) & 0xFFFFFF);
+      }
+      fill += __popcll(m);
+    });
+    if (shift_bad)
+      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagShift);
+    int np = 1;
+    while (np < len) np <<= 1;
+    for (int t = len + lane; t < np; t += kWave) keys[t] = INT64_MAX;
+    wave_lds_sync();
+    // bitonic sort of keys[0, np)
+    for (int k = 2; k <= np; k <<= 1) {
+      for (int jj = k >> 1; jj > 0; jj >>= 1) {
+        for (int t = lane; t < np; t += kWave) {
+          int p = t ^ jj;
+          if (p > t) {
+            int64_t a = keys[t], b = keys[p];
+            bool up = (t & k) == 0;
+            if ((a > b) == up) {
+              keys[t] = b;
+              keys[p] = a;
+            }
+          }
+        }
+        wave_lds_sync();
+      }
+    }
+    for (int t = lane; t < len; t += kWave) {
+      int64_t key = keys[t];
+      nbr_j[r0 + t] = static_cast<int32_t>(key >> 24);
+      nbr_shift[r0 + t] = static_cast<int32_t>(key & 0xFFFFFF);
+    }
+    wave_lds_sync();
+  }
+}
+
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
+                                                          const int32_t* __restrict__ nbr_j,
+                                                          const int32_t* __restrict__ nbr_shift,
+                                                          int32_t* __restrict__ rev,
+                                                          const int64_t* active) {
+  if (inactive(active)) return;
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  const int lane = lane_id();
+  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+    int64_t b = row_ptr[i], e = row_ptr[i + 1];
+    for (int64_t s = b + lane; s < e; s += kWave) {
+      int32_t j = nbr_j[s];
+      int64_t want = (int64_t(i) << 24) | int64_t(negate_shift(nbr_shift[s]) & 0xFFFFFF);
+      if (j < 0 || j >= n) {
+        rev[s] = -1;
+        continue;
+      }
+      int64_t lo = row_ptr[j], hi = row_ptr[j + 1];   // search [lo, hi)
+      while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        int64_t key = (int64_t(nbr_j[mid]) << 24) | int64_t(nbr_shift[mid] & 0xFFFFFF);
+        if (key < want) lo = mid + 1;
+        else hi = mid;
+      }
+      bool found = lo < row_ptr[j + 1] &&
+                   ((int64_t(nbr_j[lo]) << 24) | int64_t(nbr_shift[lo] & 0xFFFFFF)) == want;
+      rev[s] = found ? static_cast<int32_t>(lo) : -1;
+    }
+  }
+}
+
+// Keep the skin edges inside r_c (same fixed-point predicate) and write the
+// edge record r_ij = (r_j + n.h) - r_i, computed in float64 and stored
+// float32, with j in the w lane.  Slots are the first ecount[i] entries of
+// the skin row of i, in canonical order.
+__global__ void __launch_bounds__(kBlock) compact_kernel(
+    const double* __restrict__ pos, int64_t n, int64_t Lq0, int64_t Lq1, int64_t Lq2, int64_t rcq,
+    double L0, double L1, double L2, int64_t cap, const int64_t* __restrict__ row_ptr,
+    const int32_t* __restrict__ nbr_j, const int32_t* __restrict__ nbr_shift,
+    int32_t* __restrict__ ecount, float4* __restrict__ edge, int32_t* __restrict__ cidx,
+    int32_t* __restrict__ sidx) {
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  const int lane = lane_id();
+  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+    const double xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
+    const int64_t qi0 = qfix(xi), qi1 = qfix(yi), qi2 = qfix(zi);
+    const int64_t b = row_ptr[i];
+    int64_t e = row_ptr[i + 1];
+    if (b < 0 || e > cap || e < b) e = b;   // malformed row: keep nothing
+    int kept = 0;
+    for (int64_t base = b; base < e; base += kWave) {
+      int64_t s = base + lane;
+      bool pred = false;
+      int32_t j = 0;
+      int nx = 0, ny = 0, nz = 0;
+      if (s < e) {
+        j = nbr_j[s];
+        int32_t sh = nbr_shift[s];
+        nx = unpack_x(sh); ny = unpack_y(sh); nz = unpack_z(sh);
+        if (j >= 0 && j < n) {
+          int64_t dx = qfix(pos[3 * j]) + nx * Lq0 - qi0;
+          int64_t dy = qfix(pos[3 * j + 1]) + ny * Lq1 - qi1;
+          int64_t dz = qfix(pos[3 * j + 2]) + nz * Lq2 - qi2;
+          pred = within(dx, dy, dz, rcq);
+        }
+      }
+      uint64_t m;
+      int pre = ballot_prefix(pred, &m);
+      if (s < e) {
+        if (pred) {
+          int64_t slot = b + kept + pre;
+          double rx = (pos[3 * j] + nx * L0) - xi;
+          double ry = (pos[3 * j + 1] + ny * L1) - yi;
+          double rz = (pos[3 * j + 2] + nz * L2) - zi;
+          edge[slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
+                                   static_cast<float>(rz), __int_as_float(j));
+          sidx[slot] = static_cast<int32_t>(s);
+          cidx[s] = static_cast<int32_t>(slot);
+        } else {
+          cidx[s] = -1;
+        }
+      }
+      kept += __popcll(m);
+    }
+    if (lane == 0) ecount[i] = kept;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
+                                                     const int32_t* __restrict__ ecount,
+                                                     const int32_t* __restrict__ sidx,
+                                                     const int32_t* __restrict__ skin_rev,
+                                                     const int32_t* __restrict__ cidx,
+                                                     int32_t* __restrict__ rev) {
+  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
+  const int lane = lane_id();
+  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+    int64_t b = row_ptr[i], e = b + ecount[i];
+    for (int64_t s = b + lane; s < e; s += kWave) {
+      const int32_t sr = skin_rev[sidx[s]];
+      const int32_t c = sr >= 0 ? cidx[sr] : -1;
+      rev[s] = c >= 0 ? c : static_cast<int32_t>(s);   // never happens for a valid list
+    }
+  }
+}
+
+// Copy a freshly scanned row_ptr over the live one when it fits the
+// capacity; otherwise keep the old (consistent) list and raise the flag.
+__global__ void __launch_bounds__(kBlock) commit_rows_kernel(const int64_t* __restrict__ fresh,
+                                                             int64_t* __restrict__ live, int64_t n,
+                                                             int64_t cap, int64_t* __restrict__ flags,
+                                                             const int64_t* active) {
+  if (inactive(active)) return;
+  const int64_t total = fresh[n];
+  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (total > cap) {
+    if (i == 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagCapacity);
+      atomicMax(reinterpret_cast<unsigned long long*>(flags + 2), (unsigned long long)total);
+    }
+    return;
+  }
+  if (i <= n) live[i] = fresh[i];
+}
+
+int waves_grid(int64_t n) {
+  int64_t blocks = (n + kWavesPerBlock - 1) / kWavesPerBlock;
+  if (blocks > 4096) blocks = 4096;
+  return static_cast<int>(blocks < 1 ? 1 : blocks);
+}
+
+}  // namespace
+
+int make_grid(const double cell[9], int64_t rq, CellGrid* g) {
+  for (int a = 0; a < 3; ++a)
+    for (int b = 0; b < 3; ++b)
+      if (a != b && cell[3 * a + b] != 0.0) {
+        set_error("only orthorhombic cells (diagonal lattice matrix) are supported on the GPU");
+        return DPA4C_ERR_UNSUPPORTED;
+      }
+  if (rq <= 0 || rq > int64_t(1000) * int64_t(kQScale)) {
+    set_error("bad neighbour radius");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  g->rq = rq;
+  g->ncell = 1;
+  for (int a = 0; a < 3; ++a) {
+    double L = cell[4 * a];
+    if (!(L > 0) || L > 1.0e6) {
+      set_error("cell lengths must be positive and below 1e6 A");
+      return DPA4C_ERR_INVALID_ARG;
+    }
+    g->Lq[a] = static_cast<int64_t>(std::rint(L * kQScale));
+    int64_t nc = g->Lq[a] / g->rq;
+    if (nc < 1) nc = 1;
+    if (nc > 1024) nc = 1024;
+    g->nc[a] = static_cast<int>(nc);
+    g->reach[a] = static_cast<int>((g->rq * nc + g->Lq[a] - 1) / g->Lq[a]);
+    g->ncell *= nc;
+  }
+  return 0;
+}
+
+int ensure_scratch(NeighborScratch& nb, int64_t n, const CellGrid& g) {
+  if (nb.qpos.ensure(sizeof(int64_t) * 3 * n) || nb.wrap.ensure(sizeof(int32_t) * 3 * n) ||
+      nb.cell_of.ensure(sizeof(int32_t) * n) || nb.cell_cnt.ensure(sizeof(int32_t) * g.ncell) ||
+      nb.cell_start.ensure(sizeof(int32_t) * (g.ncell + 1)) ||
+      nb.cell_fill.ensure(sizeof(int32_t) * g.ncell) || nb.cell_atoms.ensure(sizeof(int32_t) * n) ||
+      nb.counts.ensure(sizeof(int64_t) * n))
+    return DPA4C_ERR_HIP;
+  return 0;
+}
+
+int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const CellGrid& g,
+                    int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift, int64_t cap,
+                    const int64_t* active, int64_t* flags, bool fill, hipStream_t st) {
+  int rc = ensure_scratch(nb, n, g);
+  if (rc) return rc;
+  GridDev gd = to_dev(g);
+  int blocks = static_cast<int>((n + kBlock - 1) / kBlock);
+  int cblocks = static_cast<int>((g.ncell + kBlock - 1) / kBlock);
+  hipLaunchKernelGGL(zero_i32_kernel, dim3(cblocks), dim3(kBlock), 0, st,
+                     nb.cell_cnt.as<int32_t>(), g.ncell, active);
+  hipLaunchKernelGGL(bin_kernel, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
+                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                     nb.cell_cnt.as<int32_t>(), flags, active);
+  hipLaunchKernelGGL(cell_scan_kernel, dim3(1), dim3(1024), 0, st, nb.cell_cnt.as<int32_t>(),
+                     g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(), active);
+  hipLaunchKernelGGL(place_kernel, dim3(blocks), dim3(kBlock), 0, st, n, nb.cell_of.as<int32_t>(),
+                     nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(),
+                     nb.cell_atoms.as<int32_t>(), active);
+  hipLaunchKernelGGL(count_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
+                     nb.cell_atoms.as<int32_t>(), nb.counts.as<int64_t>(), active);
+  DPA4C_HIP_TRY(hipGetLastError());
+  rc = exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, active, st);
+  if (rc) return rc;
+  if (fill) {
+    hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
+                       nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags, active);
+    DPA4C_HIP_TRY(hipGetLastError());
+  }
+  return 0;
+}
+
+int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
+                   int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
+                   hipStream_t st) {
+  GridDev gd = to_dev(g);
+  hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
+                     nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags,
+                     (const int64_t*)nullptr);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int commit_rows(const int64_t* fresh, int64_t* live, int64_t n, int64_t cap, int64_t* flags,
+                const int64_t* active, hipStream_t st) {
+  int blocks = static_cast<int>((n + 1 + kBlock - 1) / kBlock);
+  hipLaunchKernelGGL(commit_rows_kernel, dim3(blocks), dim3(kBlock), 0, st, fresh, live, n, cap,
+                     flags, active);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
+                    int64_t n, int32_t* skin_rev, const int64_t* active, hipStream_t st) {
+  hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
+                     nbr_shift, skin_rev, active);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_compact_edges(const double* pos, int64_t n, const CellGrid& g, int64_t rcq,
+                         const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
+                         const int32_t* nbr_shift, int64_t cap, int32_t* ecount, float4* edge,
+                         int32_t* cidx, int32_t* sidx, hipStream_t st) {
+  hipLaunchKernelGGL(compact_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, pos, n, g.Lq[0],
+                     g.Lq[1], g.Lq[2], rcq, box[0], box[1], box[2], cap, row_ptr, nbr_j, nbr_shift,
+                     ecount, edge, cidx, sidx);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_rev(const int64_t* row_ptr, const int32_t* ecount, const int32_t* sidx,
+               const int32_t* skin_rev, const int32_t* cidx, int64_t n, int32_t* rev,
+               hipStream_t st) {
+  hipLaunchKernelGGL(rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, ecount,
+                     sidx, skin_rev, cidx, rev);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+}  // namespace dpa4c

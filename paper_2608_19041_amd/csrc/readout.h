@@ -1,0 +1,445 @@
+// Per-atom invariant readout (Methods "Nonlinear readout and atomic energy",
+// Eqs. (alignment) .. (calibration)) and its vector-Jacobian product, run by
+// one 64-lane wavefront per atom on a wave-private LDS block.
+//
+// Each stage spreads its outputs over the lanes (gather form: every output is
+// computed by one lane from values written by the previous stage), so the
+// results do not depend on scheduling.  The (1,1,2) and (2,2,2) bispectrum
+// blocks use the closed forms of Eq. (closed-forms); (1,2,3) and (2,3,3)
+// contract sparse coupling lists.
+#pragma once
+
+#include "common.h"
+#include "edge_math.h"
+
+namespace dpa4c {
+
+template <class P>
+struct ReadoutLds {
+  float y[P::NS];                 // [S0, S1, Y]
+  float xt1[3 * P::C1];           // aligned features, Eq. (alignment)
+  float xt2[5 * P::C2];
+  float xt3[8];
+  float z1[3 * P::K1];            // probes, Eq. (probes)
+  float z2[5 * P::K2];
+  float q[P::K2][9];              // STF matrices of the degree-two probes
+  float qv[P::K2][P::K1][3];      // Q_eta v_kappa
+  float d[P::DOUT];               // D~ (forward) or dE/dD~ (backward)
+  // backward only
+  float gxt1[3 * P::C1];
+  float gxt2[5 * P::C2];
+  float gxt3[8];
+  float gz1[3 * P::K1];
+  float gz2[5 * P::K2];
+  float gz3[8];
+  float gq[P::K2][9];
+  float gy[P::NS];
+  float red[4];
+};
+
+constexpr float kSqrt2 = 1.4142135623730951f;
+constexpr float kInvSqrt2 = 0.7071067811865476f;
+constexpr float kInvSqrt6 = 0.4082482904638631f;
+constexpr float kInvSqrt5 = 0.4472135954999579f;
+constexpr float kSqrt12_35 = 0.5855400437691199f;
+
+// vech index t -> (c, c') with c <= c', row-major over the upper triangle
+__device__ inline void vech_pair(int t, int C, int* c, int* cp) {
+  int r = 0;
+  while (t >= C - r) {
+    t -= C - r;
+    ++r;
+  }
+  *c = r;
+  *cp = r + t;
+}
+
+// STF(z) of Eq. (stf) in the basis order (xy, yz, z^2, xz, x^2 - y^2):
+// entry (a, b) of the symmetric trace-free matrix
+__device__ inline float stf_entry(const float* z, int stride, int a, int b) {
+  float z0 = z[0], z1 = z[stride], z2 = z[2 * stride], z3 = z[3 * stride], z4 = z[4 * stride];
+  if (a > b) { int t = a; a = b; b = t; }
+  if (a == 0 && b == 0) return -z2 * kInvSqrt6 + z4 * kInvSqrt2;
+  if (a == 1 && b == 1) return -z2 * kInvSqrt6 - z4 * kInvSqrt2;
+  if (a == 2 && b == 2) return 2.0f * z2 * kInvSqrt6;
+  if (a == 0 && b == 1) return z0 * kInvSqrt2;
+  if (a == 1 && b == 2) return z1 * kInvSqrt2;
+  return z3 * kInvSqrt2;   // (0, 2)
+}
+// adjoint: dE/dz_m = E_m : Qbar for a (not necessarily symmetric) 3x3 Qbar
+__device__ inline float stf_adjoint(const float* g, int m) {
+  switch (m) {
+    case 0: return (g[1] + g[3]) * kInvSqrt2;
+    case 1: return (g[5] + g[7]) * kInvSqrt2;
+    case 2: return (-g[0] - g[4] + 2.0f * g[8]) * kInvSqrt6;
+    case 3: return (g[2] + g[6]) * kInvSqrt2;
+    default: return (g[0] - g[4]) * kInvSqrt2;
+  }
+}
+
+// index of the (k1 <= k2) pair in row-major order over the upper triangle
+__device__ inline int tri_index(int k1, int k2, int K) { return k1 * K - k1 * (k1 - 1) / 2 + (k2 - k1); }
+
+// the four (2,2,2) entries for K2 = 2: (0,0,0) (0,0,1) (0,1,1) (1,1,1)
+__device__ inline void e222(int t, int* a, int* b, int* c, float* w) {
+  const float r3 = 1.7320508075688772f;
+  *a = t >= 3 ? 1 : 0;
+  *b = t >= 2 ? 1 : 0;
+  *c = t >= 1 ? 1 : 0;
+  *w = (t == 0 || t == 3) ? 1.0f : r3;
+}
+
+// Forward intermediates from s.y: M, aligned features, probes, Q, Qv.
+template <class P>
+__device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md, float* M0, float* M1) {
+  const int lane = lane_of();
+  const float m0 = sqrtf(0.25f + s.y[0]);
+  const float m1 = sqrtf(0.25f + s.y[1]);
+  *M0 = m0;
+  *M1 = m1;
+  const float i1 = 1.0f / m1;
+  constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
+  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+    if (o < n1) {
+      int m = o / P::C1, cp = o % P::C1;
+      const float* x = s.y + P::Y1 + m * P::C1;
+      float acc = x[cp];
+      for (int c = 0; c < P::C1; ++c) acc += x[c] * md.W1[c * P::C1 + cp];
+      s.xt1[o] = acc * i1;
+    } else if (o < n1 + n2) {
+      int t = o - n1, m = t / P::C2, cp = t % P::C2;
+      const float* x = s.y + P::Y2 + m * P::C2;
+      float acc = x[cp];
+      for (int c = 0; c < P::C2; ++c) acc += x[c] * md.W2[c * P::C2 + cp];
+      s.xt2[t] = acc * i1;
+    } else {
+      int m = o - n1 - n2;
+      s.xt3[m] = s.y[P::Y3 + m] * i1;
+    }
+  }
+  wave_sync();
+  for (int o = lane; o < 3 * P::K1 + 5 * P::K2; o += kWave) {
+    if (o < 3 * P::K1) {
+      int m = o / P::K1, k = o % P::K1;
+      float acc;
+      if constexpr (P::kHasA1) {
+        acc = 0.0f;
+        for (int c = 0; c < P::C1; ++c) acc += s.xt1[m * P::C1 + c] * md.A1[c * P::K1 + k];
+      } else {
+        acc = s.xt1[m * P::C1 + k];
+      }
+      s.z1[o] = acc;
+    } else {
+      int t = o - 3 * P::K1, m = t / P::K2, k = t % P::K2;
+      float acc = 0.0f;
+      for (int c = 0; c < P::C2; ++c) acc += s.xt2[m * P::C2 + c] * md.A2[c * P::K2 + k];
+      s.z2[t] = acc;
+    }
+  }
+  wave_sync();
+  if (lane < P::K2 * 9) {
+    int eta = lane / 9, ab = lane % 9;
+    s.q[eta][ab] = stf_entry(s.z2 + eta, P::K2, ab / 3, ab % 3);
+  }
+  wave_sync();
+  for (int o = lane; o < P::K2 * P::K1 * 3; o += kWave) {
+    int eta = o / (P::K1 * 3), k = (o / 3) % P::K1, a = o % 3;
+    float acc = 0.0f;
+    for (int b = 0; b < 3; ++b) acc += s.q[eta][a * 3 + b] * s.z1[b * P::K1 + k];
+    s.qv[eta][k][a] = acc;
+  }
+  wave_sync();
+}
+
+// Eqs. (gram) .. (calibration): writes the calibrated descriptor of atom
+// ``ai`` to ``dout`` (global memory).  s.y must hold the node state.
+template <class P>
+__device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
+                                float* __restrict__ dout) {
+  const int lane = lane_of();
+  float M0, M1;
+  readout_intermediates<P>(s, md, &M0, &M1);
+  const float i0 = 1.0f / M0;
+  for (int c = lane; c < P::C0; c += kWave) {
+    s.d[P::oX0 + c] = md.type_embed[ai * P::C0 + c];
+    s.d[P::oX + c] = s.y[P::Y0 + c] * i0;
+  }
+  if (lane == 0) {
+    s.d[P::oM0] = M0;
+    s.d[P::oM1] = M1;
+  }
+  // Gram blocks, Eq. (gram), vech with sqrt(2) off the diagonal
+  for (int o = lane; o < P::nG1 + P::nG2 + P::nG3; o += kWave) {
+    float acc = 0.0f;
+    if (o < P::nG1) {
+      int c, cp;
+      vech_pair(o, P::C1, &c, &cp);
+      for (int m = 0; m < 3; ++m) acc += s.xt1[m * P::C1 + c] * s.xt1[m * P::C1 + cp];
+      if (c != cp) acc *= kSqrt2;
+    } else if (o < P::nG1 + P::nG2) {
+      int c, cp;
+      vech_pair(o - P::nG1, P::C2, &c, &cp);
+      for (int m = 0; m < 5; ++m) acc += s.xt2[m * P::C2 + c] * s.xt2[m * P::C2 + cp];
+      if (c != cp) acc *= kSqrt2;
+    } else {
+      for (int m = 0; m < 7; ++m) acc += s.xt3[m] * s.xt3[m];
+    }
+    s.d[P::oG1 + o] = acc;
+  }
+  // (1,1,2): -(f/sqrt5) v_k1 . Q_eta v_k2, k1 <= k2
+  for (int o = lane; o < P::n112; o += kWave) {
+    int eta = o % P::K2, pr = o / P::K2, k1, k2;
+    vech_pair(pr, P::K1, &k1, &k2);
+    float acc = 0.0f;
+    for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];
+    s.d[P::o112 + o] = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc;
+  }
+  // (2,2,2): -sqrt(12/35) w tr(Q_a Q_b Q_c)
+  if (lane < P::n222) {
+    int a, b, c;
+    float w;
+    e222(lane, &a, &b, &c, &w);
+    float tr = 0.0f;
+    for (int r = 0; r < 3; ++r)
+      for (int t = 0; t < 3; ++t) {
+        float ab = 0.0f;
+        for (int u = 0; u < 3; ++u) ab += s.q[a][r * 3 + u] * s.q[b][u * 3 + t];
+        tr += ab * s.q[c][t * 3 + r];
+      }
+    s.d[P::o222 + lane] = -kSqrt12_35 * w * tr;
+  }
+  if constexpr (P::L >= 3) {
+    // (1,2,3) and (2,3,3) through the sparse couplings
+    for (int o = lane; o < P::n123 + P::n233; o += kWave) {
+      float acc = 0.0f;
+      if (o < P::n123) {
+        int k1 = o / P::K2, k2 = o % P::K2;
+        for (int e = 0; e < md.c123.n; ++e) {
+          const int* ix = md.c123.idx + 3 * e;
+          acc += md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] * s.z2[ix[1] * P::K2 + k2] * s.xt3[ix[2]];
+        }
+        s.d[P::o123 + o] = acc;
+      } else {
+        int eta = o - P::n123;
+        for (int e = 0; e < md.c233.n; ++e) {
+          const int* ix = md.c233.idx + 3 * e;
+          acc += md.c233.val[e] * s.z2[ix[0] * P::K2 + eta] * s.xt3[ix[1]] * s.xt3[ix[2]];
+        }
+        s.d[P::o233 + eta] = acc;
+      }
+    }
+  }
+  // projected quartic, Eq. (quartic), eta-major
+  for (int o = lane; o < P::nPi; o += kWave) {
+    int eta = o / P::K1, k = o % P::K1;
+    float acc = 0.0f;
+    for (int a = 0; a < 3; ++a) acc += s.qv[eta][k][a] * s.qv[eta][k][a];
+    s.d[P::oPi + o] = acc;
+  }
+  wave_sync();
+  for (int o = lane; o < P::DSTR; o += kWave)
+    dout[o] = o < P::DOUT ? (s.d[o] - md.mu[o]) * md.inv_sigma[o] : 0.0f;
+  wave_sync();
+}
+
+// fixed-order sum over the 64 lanes (butterfly; every lane gets the same bits)
+__device__ inline float wave_sum(float v) {
+  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Vector-Jacobian product of the readout: from dE/dD (global, calibrated
+// descriptor gradient) to dE/d(node state) in s.gy.  s.y must hold the
+// node state.
+template <class P>
+__device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
+                                 const float* __restrict__ dD) {
+  const int lane = lane_of();
+  float M0, M1;
+  readout_intermediates<P>(s, md, &M0, &M1);
+  for (int o = lane; o < P::DOUT; o += kWave) s.d[o] = dD[o] * md.inv_sigma[o];
+  wave_sync();
+  // --- dE/dQ_eta (3x3, not symmetrised) from (1,1,2), quartic and (2,2,2)
+  if (lane < P::K2 * 9) {
+    int eta = lane / 9, a = (lane % 9) / 3, b = lane % 3;
+    float acc = 0.0f;
+    for (int k1 = 0; k1 < P::K1; ++k1)
+      for (int k2 = k1; k2 < P::K1; ++k2) {
+        float jb = s.d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
+        float f = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2);
+        acc += jb * f * s.z1[a * P::K1 + k1] * s.z1[b * P::K1 + k2];
+      }
+    for (int k = 0; k < P::K1; ++k) {
+      float pb = s.d[P::oPi + eta * P::K1 + k];
+      acc += 2.0f * pb * s.qv[eta][k][a] * s.z1[b * P::K1 + k];
+    }
+    for (int t = 0; t < P::n222; ++t) {
+      int ia, ib, ic;
+      float w;
+      e222(t, &ia, &ib, &ic, &w);
+      float jb = s.d[P::o222 + t] * (-kSqrt12_35) * w;
+      // d tr(A B C) / dA = (B C)^T, / dB = (C A)^T, / dC = (A B)^T
+      if (ia == eta) {
+        float v = 0.0f;
+        for (int u = 0; u < 3; ++u) v += s.q[ib][b * 3 + u] * s.q[ic][u * 3 + a];
+        acc += jb * v;
+      }
+      if (ib == eta) {
+        float v = 0.0f;
+        for (int u = 0; u < 3; ++u) v += s.q[ic][b * 3 + u] * s.q[ia][u * 3 + a];
+        acc += jb * v;
+      }
+      if (ic == eta) {
+        float v = 0.0f;
+        for (int u = 0; u < 3; ++u) v += s.q[ia][b * 3 + u] * s.q[ib][u * 3 + a];
+        acc += jb * v;
+      }
+    }
+    s.gq[eta][a * 3 + b] = acc;
+  }
+  // --- dE/dv (probe gradients of degree one) from (1,1,2) and the quartic
+  for (int o = lane; o < 3 * P::K1; o += kWave) {
+    int m = o / P::K1, k = o % P::K1;
+    float acc = 0.0f;
+    for (int eta = 0; eta < P::K2; ++eta) {
+      for (int kp = 0; kp < P::K1; ++kp) {
+        int k1 = k < kp ? k : kp, k2 = k < kp ? kp : k;
+        float jb = s.d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
+        float f = -kInvSqrt5 * (k1 == k2 ? 2.0f : kSqrt2);
+        acc += jb * f * s.qv[eta][kp][m];
+      }
+      float pb = s.d[P::oPi + eta * P::K1 + k];
+      float v = 0.0f;
+      for (int b = 0; b < 3; ++b) v += s.q[eta][m * 3 + b] * s.qv[eta][k][b];
+      acc += 2.0f * pb * v;
+    }
+    if constexpr (P::L >= 3) {
+      for (int e = 0; e < md.c123.n; ++e) {
+        const int* ix = md.c123.idx + 3 * e;
+        if (ix[0] != m) continue;
+        for (int k2 = 0; k2 < P::K2; ++k2)
+          acc += s.d[P::o123 + k * P::K2 + k2] * md.c123.val[e] * s.z2[ix[1] * P::K2 + k2] *
+                 s.xt3[ix[2]];
+      }
+    }
+    s.gz1[o] = acc;
+  }
+  if constexpr (P::L >= 3) {
+    if (lane < 7) {
+      int m = lane;
+      float acc = 0.0f;
+      for (int e = 0; e < md.c123.n; ++e) {
+        const int* ix = md.c123.idx + 3 * e;
+        if (ix[2] != m) continue;
+        for (int k1 = 0; k1 < P::K1; ++k1)
+          for (int k2 = 0; k2 < P::K2; ++k2)
+            acc += s.d[P::o123 + k1 * P::K2 + k2] * md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] *
+                   s.z2[ix[1] * P::K2 + k2];
+      }
+      for (int e = 0; e < md.c233.n; ++e) {
+        const int* ix = md.c233.idx + 3 * e;
+        for (int eta = 0; eta < P::K2; ++eta) {
+          float base = s.d[P::o233 + eta] * md.c233.val[e] * s.z2[ix[0] * P::K2 + eta];
+          if (ix[1] == m) acc += base * s.xt3[ix[2]];
+          if (ix[2] == m) acc += base * s.xt3[ix[1]];
+        }
+      }
+      s.gz3[m] = acc;
+    }
+  }
+  wave_sync();
+  // --- dE/dz2 = E_m : dE/dQ + generic couplings
+  if (lane < 5 * P::K2) {
+    int m = lane / P::K2, eta = lane % P::K2;
+    float acc = stf_adjoint(s.gq[eta], m);
+    if constexpr (P::L >= 3) {
+      for (int e = 0; e < md.c123.n; ++e) {
+        const int* ix = md.c123.idx + 3 * e;
+        if (ix[1] != m) continue;
+        for (int k1 = 0; k1 < P::K1; ++k1)
+          acc += s.d[P::o123 + k1 * P::K2 + eta] * md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] *
+                 s.xt3[ix[2]];
+      }
+      for (int e = 0; e < md.c233.n; ++e) {
+        const int* ix = md.c233.idx + 3 * e;
+        if (ix[0] != m) continue;
+        acc += s.d[P::o233 + eta] * md.c233.val[e] * s.xt3[ix[1]] * s.xt3[ix[2]];
+      }
+    }
+    s.gz2[lane] = acc;
+  }
+  wave_sync();
+  // --- dE/dX~ from the Gram blocks and the probes
+  constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
+  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+    if (o < n1) {
+      int m = o / P::C1, c = o % P::C1;
+      float acc = 0.0f;
+      for (int cp = 0; cp < P::C1; ++cp) {
+        int a = c < cp ? c : cp, b = c < cp ? cp : c;
+        float gb = s.d[P::oG1 + tri_index(a, b, P::C1)];
+        acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt1[m * P::C1 + cp];
+      }
+      if constexpr (P::kHasA1) {
+        for (int k = 0; k < P::K1; ++k) acc += s.gz1[m * P::K1 + k] * md.A1[c * P::K1 + k];
+      } else {
+        acc += s.gz1[m * P::K1 + c];
+      }
+      s.gxt1[o] = acc;
+    } else if (o < n1 + n2) {
+      int t = o - n1, m = t / P::C2, c = t % P::C2;
+      float acc = 0.0f;
+      for (int cp = 0; cp < P::C2; ++cp) {
+        int a = c < cp ? c : cp, b = c < cp ? cp : c;
+        float gb = s.d[P::oG2 + tri_index(a, b, P::C2)];
+        acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt2[m * P::C2 + cp];
+      }
+      for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * md.A2[c * P::K2 + k];
+      s.gxt2[t] = acc;
+    } else {
+      int m = o - n1 - n2;
+      s.gxt3[m] = 2.0f * s.d[P::oG3] * s.xt3[m] + s.gz3[m];
+    }
+  }
+  wave_sync();
+  // --- through the alignment (I + W) and the normalisation X = Y / M
+  const float i0 = 1.0f / M0, i1 = 1.0f / M1;
+  float part0 = 0.0f, part1 = 0.0f;   // sum Xbar * Y per normaliser
+  for (int c = lane; c < P::C0; c += kWave) {
+    float xb = s.d[P::oX + c];
+    s.gy[P::Y0 + c] = xb * i0;
+    part0 += xb * s.y[P::Y0 + c];
+  }
+  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+    float xb;
+    int yi;
+    if (o < n1) {
+      int m = o / P::C1, c = o % P::C1;
+      xb = s.gxt1[o];
+      for (int cp = 0; cp < P::C1; ++cp) xb += s.gxt1[m * P::C1 + cp] * md.W1[c * P::C1 + cp];
+      yi = P::Y1 + o;
+    } else if (o < n1 + n2) {
+      int t = o - n1, m = t / P::C2, c = t % P::C2;
+      xb = s.gxt2[t];
+      for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * md.W2[c * P::C2 + cp];
+      yi = P::Y2 + t;
+    } else {
+      int m = o - n1 - n2;
+      xb = s.gxt3[m];
+      yi = P::Y3 + m;
+    }
+    s.gy[yi] = xb * i1;
+    part1 += xb * s.y[yi];
+  }
+  part0 = wave_sum(part0);
+  part1 = wave_sum(part1);
+  if (lane == 0) {
+    float mb0 = s.d[P::oM0] - part0 * i0 * i0;
+    float mb1 = s.d[P::oM1] - part1 * i1 * i1;
+    s.gy[0] = mb0 * 0.5f * i0;   // M0 = sqrt(1/4 + S0)
+    s.gy[1] = mb1 * 0.5f * i1;
+  }
+  wave_sync();
+}
+
+}  // namespace dpa4c

@@ -1,0 +1,216 @@
+"""GPU path versus the float64 oracle, through the C ABI.
+
+Tolerances are the stated targets: neighbour lists bit-identical, E_i within
+1e-5 eV and forces within 1e-4 eV/A (max abs) of the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import model as om
+from oracle import neighbors as onb
+
+pytestmark = pytest.mark.gpu
+
+E_TOL = 1e-5
+F_TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    return torch.device("cuda", 0)
+
+
+@pytest.fixture(scope="module")
+def dp():
+    import paper_2608_19041_amd as m
+    m.library()          # fails loudly if the library is missing
+    return m
+
+
+_models = {}
+
+
+def gpu_model(dp, name):
+    if name not in _models:
+        spec, w = synth.model_weights(name)
+        _models[name] = (dp.Model(synth.pack_blob(spec, w)), om.Oracle(spec, w), spec)
+    return _models[name]
+
+
+def on_dev(s, dev):
+    pos = torch.tensor(s.pos, dtype=torch.float64, device=dev)
+    species = torch.tensor(s.species, dtype=torch.int32, device=dev)
+    return pos, species
+
+
+def gpu_rows(row_ptr, nbr_j, nbr_shift, dp):
+    rp = row_ptr.cpu().numpy()
+    j = nbr_j.cpu().numpy().astype(np.int64)
+    n = dp.unpack_shift(nbr_shift.cpu().numpy())
+    i = np.repeat(np.arange(len(rp) - 1), np.diff(rp))
+    return i, j, n
+
+
+def assert_rows_equal(gpu, ref, centres=None):
+    gi, gj, gn = gpu
+    ri, rj, rn = ref
+    if centres is not None:
+        keep = np.isin(gi, centres)
+        gi, gj, gn = gi[keep], gj[keep], gn[keep]
+    assert len(gi) == len(ri)
+    assert np.array_equal(gi, ri)
+    assert np.array_equal(gj, rj)
+    assert np.array_equal(gn, rn)
+
+
+# -- fp32 matrix-core GEMM ----------------------------------------------------
+@pytest.mark.parametrize("M,N,K", [(1, 4, 16), (77, 384, 544), (200, 144, 192), (4000, 384, 384),
+                                   (130, 544, 384)])
+def test_gemm(dev, dp, M, N, K):
+    g = torch.Generator().manual_seed(M * 7 + N)
+    A = torch.randn(M, K, generator=g, dtype=torch.float32)
+    B = torch.randn(K, N, generator=g, dtype=torch.float32)
+    C = dp.debug_gemm(A.to(dev), B.to(dev)).cpu().double()
+    ref = A.double() @ B.double()
+    err = (C - ref).abs().max().item()
+    assert err < 2e-5 * K ** 0.5 * ref.abs().max().item() / 10 + 1e-5, err
+
+
+# -- neighbour lists -------------------------------------------------------------
+@pytest.mark.parametrize("case", range(6))
+def test_neighbors_small_cells(dev, dp, case):
+    rng = np.random.Generator(np.random.PCG64(case))
+    n = [1, 2, 3, 5, 7, 12][case]
+    box = rng.uniform(3.0, 9.0, size=3)
+    s = synth.random_periodic(n, seed=case, cell=np.diag(box), d_min=0.5)
+    # also atoms far outside the cell (unwrapped coordinates)
+    s.pos[0] += np.array([2, -1, 3]) * box
+    pos, _ = on_dev(s, dev)
+    r = 6.5
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, r)
+    ref = onb.neighbor_list(s.pos, s.cell, s.pbc, r)
+    assert e == len(ref[0])
+    assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref)
+
+
+@pytest.mark.parametrize("workload", ["fcc108_small", "fcc4000_full"])
+def test_neighbors_full_lists(dev, dp, workload):
+    s = synth.make_workload(workload)[0]
+    pos, _ = on_dev(s, dev)
+    for r in (6.0, 7.0):
+        rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, r)
+        ref = onb.neighbor_list(s.pos, s.cell, s.pbc, r)
+        assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref)
+
+
+@pytest.mark.parametrize("workload", ["bcc_hea31250_full", "water24000_full", "fcc1m_full"])
+def test_neighbors_large_sampled(dev, dp, workload):
+    s = synth.make_workload(workload)[0]
+    pos, _ = on_dev(s, dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 7.0)
+    rng = np.random.Generator(np.random.PCG64(5))
+    centres = np.sort(np.concatenate([[0, s.n - 1], rng.choice(s.n, 200, replace=False)]))
+    centres = np.unique(centres)
+    ref = onb.neighbor_list(s.pos, s.cell, s.pbc, 7.0, centres=centres)
+    assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref, centres=centres)
+    # row lengths of every atom against the symmetric pair count
+    counts = np.diff(rp.cpu().numpy())
+    assert counts.sum() == e
+
+
+# -- model stages, energies and forces --------------------------------------------
+def evaluate(dp, model, s, dev, skin=1.0):
+    pos, species = on_dev(s, dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 6.0 + skin)
+    ea, F, et = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
+    torch.cuda.synchronize()
+    return ea.cpu().numpy(), F.cpu().numpy(), et.item()
+
+
+def test_stages_small_model(dev, dp):
+    model, oracle, _ = gpu_model(dp, "small")
+    s = synth.make_workload("fcc108_small")[0]
+    evaluate(dp, model, s, dev)
+    node, desc, cnt = model.debug_stages(s.n)
+    ref = oracle.stages(s.pos, s.species, s.cell, s.pbc)
+    ei, _, _ = onb.neighbor_list(s.pos, s.cell, s.pbc, 6.0)
+    assert np.array_equal(cnt.cpu().numpy(), np.bincount(ei, minlength=s.n))
+    node = node.cpu().numpy().astype(np.float64)
+    assert np.allclose(node[:, 0], ref["S0"], rtol=1e-5, atol=1e-5)
+    assert np.allclose(node[:, 1], ref["S1"], rtol=1e-5, atol=1e-5)
+    C0 = oracle.C0
+    y_ref = ref["X_flat"].copy()
+    y_ref[:, :C0] *= ref["M0"][:, None]
+    y_ref[:, C0:] *= ref["M1"][:, None]
+    scale = np.abs(y_ref).max()
+    assert np.abs(node[:, 2:] - y_ref).max() < 2e-5 * scale
+    d = desc.cpu().numpy().astype(np.float64)
+    assert np.abs(d - ref["D"]).max() < 1e-4 * max(1.0, np.abs(ref["D"]).max())
+
+
+@pytest.mark.parametrize("name,structure", [
+    ("small", "fcc108"), ("small", "periodic24"), ("full", "fcc108"), ("full", "periodic24")])
+def test_energy_forces_small_systems(dev, dp, name, structure):
+    model, oracle, _ = gpu_model(dp, name)
+    if structure == "fcc108":
+        s = synth.fcc_copper(3, 0.08, seed=3)
+    else:
+        s = synth.random_periodic(24, seed=11, cell=np.diag([8.3, 8.9, 9.4]), d_min=1.6)
+    ea, F, et = evaluate(dp, model, s, dev)
+    ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc)
+    assert np.abs(ea - ref_e).max() < E_TOL
+    assert np.abs(F - ref_f).max() < F_TOL
+    assert abs(et - ref_e.sum()) < E_TOL * s.n
+    assert abs(F.sum(0)).max() < 1e-9
+
+
+def test_energy_forces_config2_sampled(dev, dp):
+    """4000-atom FCC with the full model: E_i of sampled centres and the forces
+    of sampled atoms (whose exact value needs the centres k and N(k))."""
+    model, oracle, _ = gpu_model(dp, "full")
+    s = synth.make_workload("fcc4000_full")[0]
+    ea, F, et = evaluate(dp, model, s, dev)
+    rng = np.random.Generator(np.random.PCG64(9))
+    ks = np.sort(rng.choice(s.n, 6, replace=False)).astype(np.int64)
+    _, ej, _ = onb.neighbor_list(s.pos, s.cell, s.pbc, 6.0, centres=ks)
+    centres = np.unique(np.concatenate([ks, ej]))
+    ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc, centres=centres)
+    assert np.abs(ea[centres] - ref_e).max() < E_TOL
+    assert np.abs(F[ks] - ref_f[ks]).max() < F_TOL
+
+
+def test_runs_are_bit_identical(dev, dp):
+    model, _, _ = gpu_model(dp, "full")
+    s = synth.make_workload("fcc4000_full")[0]
+    a = evaluate(dp, model, s, dev)
+    b = evaluate(dp, model, s, dev)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]) and a[2] == b[2]
+
+
+def test_verlet_matches_oracle_dynamics(dev, dp):
+    """Config 1: 20 velocity-Verlet steps on the GPU against the oracle's own
+    integrator, then energy conservation over 100 steps."""
+    from oracle import md
+    model, oracle, _ = gpu_model(dp, "small")
+    s = synth.make_workload("fcc108_small")[0]
+    v0 = synth.maxwell_boltzmann(s, 300.0)
+    pos, species = on_dev(s, dev)
+    vel = torch.tensor(v0, dtype=torch.float64, device=dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 7.0)
+    _, F, _ = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
+    ep, ek, nreb = model.verlet_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0, 1.0,
+                                     1.0, 20, 0, F)
+    torch.cuda.synchronize()
+    rep, rek, rpos, rvel = md.nve(oracle, s.pos, v0, s.species, s.cell, s.pbc,
+                                  s.mass_by_type[s.species], 1.0, 20)
+    assert np.abs(pos.cpu().numpy() - rpos).max() < 1e-6
+    assert np.abs(ep.cpu().numpy() - rep[1:]).max() < E_TOL * s.n
+    assert np.abs(ek.cpu().numpy() - rek[1:]).max() < E_TOL * s.n
+    ep2, ek2, _ = model.verlet_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0, 1.0,
+                                    1.0, 100, 0, F)
+    et = (ep2 + ek2).cpu().numpy()
+    assert abs(md.drift_ev_per_atom_ps(et, 1.0, s.n)) < 1e-5
