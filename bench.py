@@ -1,0 +1,224 @@
+"""MD throughput of the DPA4C energy-and-force path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one velocity-Verlet NVE step through the C ABI (verlet_step):
+half kick, drift, displacement check and (when due) cell-list rebuild,
+compaction of the skin list, fused forward edge kernel, MLP forward and
+backward on the matrix cores, fused backward edge kernel, force assembly,
+energy and kinetic sums.  Inputs are synthetic (seeded lattice, random-init
+weights) and resident in HBM before timing starts.
+
+Prints one JSON line.  The ``roofline`` entry reports the kernel that takes
+the most time, from HIP events recorded around every launch in the timed
+region; ``cpu_baseline`` times the float64 oracle on a bounded sample of the
+same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+if HERE not in sys.path:
+    sys.path.insert(0, HERE)
+
+METRIC = "MD throughput: atom-steps/s (E+F) and ns/day at 1 MI355X; HBM/MFMA % peak"
+PEAK_HBM_GBS = 8000.0
+PEAK_FP32_MFMA_TFLOPS = 157.3
+# 256 CUs x 4 SIMDs x 16 lanes x 2 flop (FMA) x 2.4 GHz, without packed fp32
+PEAK_FP32_VALU_TFLOPS = 78.6
+
+DESCRIPTIONS = {
+    "fcc108_small": "108-atom FCC Cu-like cell (3^3 cells, a=3.615 A, jitter 0.05 A), "
+                    "small model (C0=32, L=2, R=0, 8 radial functions, MLP 3x192), r_c=6 A, "
+                    "NVE 1 fs from 300 K, 1 A skin",
+    "fcc4000_full": "4000-atom FCC Cu-like crystal (10^3 cells, a=3.615 A, jitter 0.08 A), "
+                    "full-width model (C0=128, L=3, R=4, 16 radial functions, MLP 3x384), "
+                    "r_c=6 A, NVE 1 fs from 600 K, 1 A skin",
+    "bcc_hea31250_full": "31250-atom BCC 5-species alloy (25^3 cells, a=2.87 A), full-width "
+                         "model, NVE 1 fs from 1000 K, rebuild every 10 steps, 1 A skin",
+    "water24000_full": "24000-atom water-like liquid (8000 molecules, 1.0 g/cm^3), full-width "
+                       "model, NVE 0.5 fs from 300 K, 1 A skin",
+    "fcc1m_full": "1000188-atom FCC crystal (63^3 cells), full-width model, NVE 1 fs, "
+                  "rebuild every 20 steps, 1 A skin",
+}
+
+
+def stage_work(name, spec, n_atoms, n_edges, n_skin):
+    """Algorithmic work of one launch of a stage: (bound, amount, unit).
+
+    Per-edge and per-atom figures (full-width profile numbers in comments):
+      forward edge kernel  - VALU: per edge the quintic value of C0+R channels
+        (5 FMA each), psi (1+R FMA per channel), the S accumulations
+        (1 FMA each) -> 2*(5(C0+R) + (1+R)C0 + S) flop
+      backward edge kernel - VALU: quintic value and derivative (9 FMA per
+        channel), psi and psi' (2(1+R) FMA per channel), two channel
+        contractions per accumulated entry (2 FMA each) and the angular
+        gradient (3 FMA per entry of degree >= 1)
+      MLP                  - matrix cores: forward and input-gradient
+        products, 2 x 2 (D_out F + (L-1) F^2) flop per atom
+      forces               - HBM: per edge 16 B gradient + 16 B gathered
+        reverse gradient + 4 B reverse index, 24 B per atom out
+    """
+    C0, R, L = spec.C0, spec.R, spec.L
+    C1 = max(4, 1 << math.ceil(0.5 * math.log2(C0)))
+    C2 = max(4, C1 // 2)
+    S = C0 + 3 * C1 + 5 * C2 + (7 if L >= 3 else 0)
+    D = synth.descriptor_width(C0, L)
+    F, nl = spec.F, spec.n_layers
+    if name == "forward":
+        per_edge = 2 * (5 * (C0 + R) + (1 + R) * C0 + S)
+        return "alu", per_edge * n_edges, "flop"
+    if name == "backward":
+        per_edge = 2 * (9 * (C0 + R) + 2 * (1 + R) * C0 + 2 * S + 3 * (S - C0))
+        return "alu", per_edge * n_edges, "flop"
+    if name in ("mlp_forward", "mlp_backward"):
+        return "mfma", 2 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
+    if name == "forces":
+        return "hbm", 36 * n_edges + 24 * n_atoms, "byte"
+    if name == "compact":
+        return "hbm", 8 * n_skin + 16 * n_edges + 24 * n_atoms, "byte"
+    return None
+
+
+def cpu_baseline(spec, weights, system, budget_s=15.0):
+    """The float64 oracle on the host: E and F of a sample of centres."""
+    import torch
+    from oracle import model as om
+    from oracle import neighbors as onb
+    oracle = om.Oracle(spec, weights)
+    rng = np.random.Generator(np.random.PCG64(1))
+    n_s = min(64, system.n)
+    elapsed, done = 0.0, 0
+    t0 = time.perf_counter()
+    while elapsed < budget_s:
+        cs = np.sort(rng.choice(system.n, size=n_s, replace=False)).astype(np.int64)
+        edges = onb.neighbor_list(system.pos, system.cell, system.pbc, spec.r_c, centres=cs)
+        oracle.energy_forces(system.pos, system.species, system.cell, system.pbc, centres=cs,
+                             edges=edges)
+        done += len(cs)
+        elapsed = time.perf_counter() - t0
+    return {"value": done / elapsed, "unit": "atom-steps/s", "cores": torch.get_num_threads(),
+            "kind": "oracle",
+            "sample": f"float64 torch-CPU oracle: energies and forces of {done} sampled centres "
+                      f"(neighbour list, radial network per edge, readout, MLP, autograd) of "
+                      f"the {system.n}-atom workload, {elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="fcc4000_full", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(spatial decomposition is designed but not built); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_19041_amd as dp
+    global synth
+    import synth
+
+    dev = torch.device("cuda", 0)
+    system, model_name, temp, dt, _, rebuild_every = synth.make_workload(args.workload)
+    spec, weights = synth.model_weights(model_name)
+    model = dp.Model(synth.pack_blob(spec, weights))
+    pos = torch.tensor(system.pos, dtype=torch.float64, device=dev)
+    vel = torch.tensor(synth.maxwell_boltzmann(system, temp), dtype=torch.float64, device=dev)
+    species = torch.tensor(system.species, dtype=torch.int32, device=dev)
+    skin = 1.0
+    rp, nj, ns, npairs = dp.build_neighbors(pos, system.cell, system.pbc, spec.r_c + skin)
+    _, forces, _ = model.compute_energy_forces(pos, species, system.cell, system.pbc, spec.r_c,
+                                               rp, nj, ns, npairs)
+    n_edges = int(np.sum(model.debug_stages(system.n)[2].cpu().numpy()))
+    del rp, nj, ns
+    e_pot = torch.empty(max(args.steps, args.warmup, 1), dtype=torch.float64, device=dev)
+    e_kin = torch.empty_like(e_pot)
+    if args.warmup:
+        model.verlet_step(pos, vel, species, system.mass_by_type, system.cell, system.pbc, spec.r_c,
+                          skin, dt, args.warmup, rebuild_every, forces, e_pot, e_kin)
+    torch.cuda.synchronize()
+
+    # timed region, HIP events around every launch
+    model.set_timing(True)
+    model.timings()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ep, ek, nreb = model.verlet_step(pos, vel, species, system.mass_by_type, system.cell,
+                                     system.pbc, spec.r_c, skin, dt, args.steps, rebuild_every,
+                                     forces, e_pot, e_kin)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = model.timings()
+    model.set_timing(False)
+
+    wall = t1 - t0
+    steps_per_s = args.steps / wall
+    value = system.n * steps_per_s
+    et = (ep + ek).cpu().numpy()
+    tt = np.arange(len(et)) * dt * 1e-3
+    drift = float(np.polyfit(tt, et / system.n, 1)[0]) if len(et) > 2 else None
+
+    n_skin = None
+    stage_ms = {k: v[0] for k, v in stages.items() if v[1]}
+    stage_cnt = {k: v[1] for k, v in stages.items() if v[1]}
+    dominant = max(stage_ms, key=stage_ms.get)
+    roof = None
+    work = stage_work(dominant, spec, system.n, n_edges, n_skin or 0)
+    if work:
+        bound, amount, unit = work
+        avg_s = stage_ms[dominant] / stage_cnt[dominant] * 1e-3
+        if unit == "flop":
+            achieved = amount / avg_s / 1e12
+            peak = PEAK_FP32_MFMA_TFLOPS if bound == "mfma" else PEAK_FP32_VALU_TFLOPS
+            u = "TFLOP/s"
+        else:
+            achieved = amount / avg_s / 1e9
+            peak = PEAK_HBM_GBS
+            u = "GB/s"
+        roof = {"bound": bound, "kernel": dominant, "achieved": round(achieved, 3), "peak": peak,
+                "unit": u, "frac": round(achieved / peak, 4), "traffic": None,
+                "avg_launch_ms": round(avg_s * 1e3, 5),
+                "work_per_launch": amount}
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "atom-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
+                   "atoms": system.n, "edges_within_rc": n_edges, "dt_fs": dt,
+                   "rebuild_every": rebuild_every, "table_spacing_A": spec.delta},
+        "ns_per_day": round(steps_per_s * dt * 86400 * 1e-6, 4),
+        "nve_drift_ev_per_atom_ps": drift,
+        "neighbor_rebuilds": nreb,
+        "stage_ms_per_step": {k: round(v / args.steps, 5) for k, v in stage_ms.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, weights, system, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
