@@ -127,11 +127,10 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   if (w.ecount.ensure(4 * nn) || w.edge.ensure(16 * cc) || w.cidx.ensure(4 * cc) ||
       w.sidx.ensure(4 * cc) || w.rev.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
       w.skin_rev.ensure(4 * cc) || w.node.ensure(4 * nn * (m->S + 2)) ||
-      w.desc.ensure(4 * nn * dstr) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
+      w.node_grad.ensure(4 * nn * (m->S + 2)) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
       w.flags.ensure(8 * 8) || w.ekin_atom.ensure(8 * nn) || w.eatom.ensure(8 * nn))
     return DPA4C_ERR_HIP;
-  for (int t = 0; t < 3; ++t)
-    if (w.h[t].ensure(4 * nn * m->F) || w.ds[t].ensure(4 * nn * m->F)) return DPA4C_ERR_HIP;
+  (void)dstr;
   return 0;
 }
 
@@ -161,27 +160,19 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStForward, st);
     rc = launch_forward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                        w.node.as<float>(), w.desc.as<float>(), st);
+                        w.node.as<float>(), st);
     if (rc) return rc;
   }
   {
-    StageScope t(m, kStMlpForward, st);
-    rc = launch_mlp_forward(m, n, species, w.desc.as<float>(), w.h[0].as<float>(),
-                            w.h[1].as<float>(), w.h[2].as<float>(), w.ds[0].as<float>(),
-                            w.ds[1].as<float>(), w.ds[2].as<float>(), e_atom, st);
-    if (rc) return rc;
-  }
-  {
-    StageScope t(m, kStMlpBackward, st);
-    rc = launch_mlp_backward(m, n, w.desc.as<float>(), w.h[0].as<float>(), w.h[1].as<float>(),
-                             w.h[2].as<float>(), w.ds[0].as<float>(), w.ds[1].as<float>(),
-                             w.ds[2].as<float>(), st);
+    StageScope t(m, kStAtoms, st);
+    rc = launch_atoms(m, n, species, w.node.as<float>(), w.node_grad.as<float>(), e_atom, nullptr,
+                      st);
     if (rc) return rc;
   }
   {
     StageScope t(m, kStBackward, st);
     rc = launch_backward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                         w.node.as<float>(), w.desc.as<float>(), w.grad.as<float4>(), st);
+                         w.node_grad.as<float>(), w.grad.as<float4>(), st);
     if (rc) return rc;
   }
   {
@@ -228,15 +219,11 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   Workspace& w = m->ws;
   DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
                     &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
-                    &w.desc,     &w.epart,  &w.flags,      &w.ekin_atom, &w.inv_mass, &w.mass,
+                    &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.ekin_atom, &w.inv_mass, &w.mass,
                     &w.eatom,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
   for (DevBuf* b : bufs) b->release();
-  for (int t = 0; t < 3; ++t) {
-    w.h[t].release();
-    w.ds[t].release();
-  }
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
   if (w.host_flags) hipHostFree(w.host_flags);
   delete m;
@@ -526,14 +513,17 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   if (N == 0) return 0;
   // recompute node state and descriptor from the stored compacted edges
   int rc = launch_forward(m, N, w.last_species, w.skin_row_used, w.ecount.as<int32_t>(),
-                          w.edge.as<float4>(), w.node.as<float>(), w.desc.as<float>(), st);
+                          w.edge.as<float4>(), w.node.as<float>(), st);
   if (rc) return rc;
-  const int dstr = (m->D_out + 15) / 16 * 16;
+  if (w.desc.ensure(size_t(4) * N * m->D_out) || w.eatom.ensure(size_t(8) * N)) return DPA4C_ERR_HIP;
+  rc = launch_atoms(m, N, w.last_species, w.node.as<float>(), w.node_grad.as<float>(),
+                    w.eatom.as<double>(), w.desc.as<float>(), st);
+  if (rc) return rc;
   if (node_state)
     DPA4C_HIP_TRY(hipMemcpyAsync(node_state, w.node.p, 4 * N * (m->S + 2), hipMemcpyDeviceToDevice, st));
   if (descriptor)
-    DPA4C_HIP_TRY(hipMemcpy2DAsync(descriptor, 4 * m->D_out, w.desc.p, 4 * dstr, 4 * m->D_out, N,
-                                   hipMemcpyDeviceToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(descriptor, w.desc.p, size_t(4) * N * m->D_out,
+                                 hipMemcpyDeviceToDevice, st));
   if (edge_count)
     DPA4C_HIP_TRY(hipMemcpyAsync(edge_count, w.ecount.p, 4 * N, hipMemcpyDeviceToDevice, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));

@@ -2,181 +2,169 @@
 // the edge recomputation of Methods "Fused execution and backward
 // recomputation".
 //
-// For centre i the kernel first turns dE/dD_i into the node-state gradient
-// [dE/dS0, dE/dS1, dE/dY] (readout VJP), then revisits the edges of row i,
-// recomputes the tabulated radial maps (value and derivative), the pair
-// coefficients, the envelope and the harmonics, and writes
+// For centre i the workgroup reads the node-state gradient
+// [dE/dS0, dE/dS1, dE/dY] (from the per-atom kernel), revisits the edges of
+// row i, recomputes the tabulated radial maps (value and derivative), the
+// pair coefficients and the envelope, and writes
 //     dE/dr_ij = (dE/drho) u + (I - u u^T)(dE/du) / rho,
 // with  dE/drho = sum_lmc Ybar_lmc B_lm d(chi_l psi_c)/drho
 //               + Sbar0 d(chi^2)/drho + Sbar1 d(chi^4)/drho,
 //       dE/du   = sum_lmc Ybar_lmc chi_l psi_c dB_lm/du.
-// Each lane forms its partial sums over the channels it owns; the LPE lanes
-// of an edge group combine them with a fixed xor butterfly.
+//
+// Lane k of an edge group owns the channels c = k + LPE*j.  For the
+// non-scalar degrees the channel c = k contributes
+//     psi_k * Q_k(u),  Q_k(u) = sum_{l>=1, m} Ybar_lmk B_lm(u),
+// and Q_k is a fixed polynomial per centre: v.u (degree one), u.W u (degree
+// two, W symmetric) and a cubic (degree three).  Its coefficients are formed
+// once per centre, so per edge each lane evaluates one short polynomial and
+// its gradient instead of every harmonic.  The LPE partial sums of an edge
+// are combined with a fixed DPP butterfly.
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
 #include "edge_math.h"
 #include "launch.h"
-#include "readout.h"
 
 namespace dpa4c {
 
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWpb = kBlock / kWave;
+constexpr int kTeam = 256;
 
 template <class P>
-__global__ void __launch_bounds__(kBlock) backward_kernel(ModelDev md, int64_t n,
-                                                          const int32_t* __restrict__ species,
-                                                          const int64_t* __restrict__ row_ptr,
-                                                          const int32_t* __restrict__ ecount,
-                                                          const float4* __restrict__ edge,
-                                                          const float* __restrict__ node,
-                                                          const float* __restrict__ dD,
-                                                          float4* __restrict__ grad) {
-  __shared__ ReadoutLds<P> lds_all[kWpb];
-  ReadoutLds<P>& s = lds_all[threadIdx.x / kWave];
-  const int lane = lane_of();
-  const int grp = lane / P::LPE;
-  const int k = lane % P::LPE;
-  const int64_t nwaves = int64_t(gridDim.x) * kWpb;
+__global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
+                                                         const int32_t* __restrict__ species,
+                                                         const int64_t* __restrict__ row_ptr,
+                                                         const int32_t* __restrict__ ecount,
+                                                         const float4* __restrict__ edge,
+                                                         const float* __restrict__ node_grad,
+                                                         float4* __restrict__ grad) {
+  static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
+  constexpr int G = kTeam / P::LPE;
+  const int tid = threadIdx.x;
+  const int grp = tid / P::LPE;
+  const int k = tid % P::LPE;
   const int T1 = md.n_types1;
   const float inv_delta = md.inv_delta;
 
-  for (int64_t i = blockIdx.x * int64_t(kWpb) + threadIdx.x / kWave; i < n; i += nwaves) {
+  for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
     const int ai = clamp_type(species[i], T1);
-    const float* nrow = node + size_t(i) * P::NS;
-    for (int t = lane; t < P::NS; t += kWave) s.y[t] = nrow[t];
-    wave_sync();
-    readout_backward<P>(s, md, dD + size_t(i) * P::DSTR);
-    // node-state gradient into registers, in the lane's channel layout
+    const float* gyr = node_grad + size_t(i) * P::NS;
+    // per-centre coefficients in the lane's channel layout
     float gy0[P::CPL];
 #pragma unroll
-    for (int j = 0; j < P::CPL; ++j) gy0[j] = s.gy[P::Y0 + j * P::LPE + k];
-    float gy1[3], gy2[5], gy3[7];
+    for (int j = 0; j < P::CPL; ++j) gy0[j] = gyr[P::Y0 + j * P::LPE + k];
+    float v1[3];
 #pragma unroll
-    for (int m = 0; m < 3; ++m) gy1[m] = s.gy[P::Y1 + m * P::C1 + k];
+    for (int m = 0; m < 3; ++m) v1[m] = gyr[P::Y1 + m * P::C1 + k];
+    float M2[6];
+    {
+      float w[5];
 #pragma unroll
-    for (int m = 0; m < 5; ++m) gy2[m] = k < P::C2 ? s.gy[P::Y2 + m * P::C2 + k] : 0.0f;
+      for (int m = 0; m < 5; ++m) w[m] = k < P::C2 ? gyr[P::Y2 + m * P::C2 + k] : 0.0f;
+      quad_form2(w, M2);
+    }
+    float G3[3][6];
+    {
+      float w[7];
 #pragma unroll
-    for (int m = 0; m < 7; ++m) gy3[m] = (P::L >= 3 && k == 0) ? s.gy[P::Y3 + m] : 0.0f;
-    const float gs0 = s.gy[0], gs1 = s.gy[1];
-    wave_sync();
+      for (int m = 0; m < 7; ++m) w[m] = (P::L >= 3 && k == 0) ? gyr[P::Y3 + m] : 0.0f;
+      cubic_form3(w, G3);
+    }
+    const float gs0 = k == 0 ? gyr[0] : 0.0f;
+    const float gs1 = k == 0 ? gyr[1] : 0.0f;
 
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
     const float* pair_base = md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
-    for (int base = 0; base < cnt; base += P::EPW) {
+    for (int base = 0; base < cnt; base += G) {
       const int el = base + grp;
       const bool valid = el < cnt;
-      float drho = 0.0f, dux = 0.0f, duy = 0.0f, duz = 0.0f;
-      EdgeGeom g{1.0f, 0.0f, 0.0f, 1.0f, 1.0f};
-      if (valid) {
-        const float4 rec = edge[b + el];
-        const int j = __float_as_int(rec.w);
-        const int aj = clamp_type(species[j], T1);
-        g = edge_geom(rec.x, rec.y, rec.z);
-        float chi, dchi;
-        envelope(g.rho, md.r_c, &chi, &dchi);
-        float tau;
-        const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
-        float q[P::R > 0 ? P::R : 1], dq[P::R > 0 ? P::R : 1];
+      const float4 rec = edge[b + (valid ? el : 0)];
+      const int j = __float_as_int(rec.w);
+      const int aj = clamp_type(species[valid ? j : i], T1);
+      const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
+      float chi, dchi;
+      envelope(g.rho, md.r_c, &chi, &dchi);
+      float tau;
+      const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
+      const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;
+      const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
+      float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (P::R > 0) {
+        float c[6];
+        load6(md.qtab + (size_t(row) * P::R + (k < P::R ? k : 0)) * 6, c);
+        const float qk = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
+        const float dqk = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+#pragma unroll
+        for (int mu = 0; mu < 4; ++mu) {
+          q[mu] = __shfl(qk, mu, P::LPE);
+          dq[mu] = __shfl(dqk, mu, P::LPE);
+        }
+      }
+      const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
+      const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
+      float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < P::CPL; ++jj) {
+        float c[6];
+        load6(gt + (jj * P::LPE + k) * 6, c);
+        const float gv = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
+        const float gd = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+        const float* pp = pc + (jj * P::LPE + k) * P::PW;
+        const float2 gb = *reinterpret_cast<const float2*>(pp);
+        float psi = gb.x * gv + gb.y;
+        float dpsi = gb.x * gd;
         if constexpr (P::R > 0) {
-#pragma unroll
-          for (int mu = 0; mu < P::R; ++mu) {
-            float c[6], v, d;
-            load6(md.qtab + (size_t(row) * P::R + mu) * 6, c);
-            quintic_val_der(c, tau, &v, &d);
-            q[mu] = v;
-            dq[mu] = d * inv_delta;
-          }
+          const float2 u01 = *reinterpret_cast<const float2*>(pp + 2);
+          const float2 u23 = *reinterpret_cast<const float2*>(pp + 4);
+          psi += u01.x * q[0] + u01.y * q[1] + u23.x * q[2] + u23.y * q[3];
+          dpsi += u01.x * dq[0] + u01.y * dq[1] + u23.x * dq[2] + u23.y * dq[3];
         }
-        const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
-        const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
-        float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
-#pragma unroll
-        for (int jj = 0; jj < P::CPL; ++jj) {
-          float c[6], gv, gd;
-          load6(gt + (jj * P::LPE + k) * 6, c);
-          quintic_val_der(c, tau, &gv, &gd);
-          gd *= inv_delta;
-          const float* pp = pc + (jj * P::LPE + k) * P::PW;
-          float psi = pp[0] * gv + pp[1];
-          float dpsi = pp[0] * gd;
-          if constexpr (P::R > 0) {
-#pragma unroll
-            for (int mu = 0; mu < P::R; ++mu) {
-              psi += pp[2 + mu] * q[mu];
-              dpsi += pp[2 + mu] * dq[mu];
-            }
-          }
-          a0 += gy0[jj] * psi;
-          b0 += gy0[jj] * dpsi;
-          if (jj == 0) {
-            psi0 = psi;
-            dpsi0 = dpsi;
-          }
+        a0 += gy0[jj] * psi;
+        b0 += gy0[jj] * dpsi;
+        if (jj == 0) {
+          psi0 = psi;
+          dpsi0 = dpsi;
         }
-        // degree 0: weight chi
-        drho = dchi * a0 + chi * b0;
-        // degrees >= 1: weight chi^2, channel c = k
-        const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
-        {
-          const float u[3] = {g.ux, g.uy, g.uz};
-#pragma unroll
-          for (int m = 0; m < 3; ++m) {
-            const float a = gy1[m] * psi0, bb = gy1[m] * dpsi0;
-            drho += u[m] * (dchi2 * a + chi2 * bb);
-          }
-          dux += chi2 * gy1[0] * psi0;
-          duy += chi2 * gy1[1] * psi0;
-          duz += chi2 * gy1[2] * psi0;
-        }
-        if (k < P::C2) {
-          float b2[5], g2[5][3];
-          harm2(g.ux, g.uy, g.uz, b2);
-          harm2_grad(g.ux, g.uy, g.uz, g2);
-#pragma unroll
-          for (int m = 0; m < 5; ++m) {
-            const float a = gy2[m] * psi0, bb = gy2[m] * dpsi0;
-            drho += b2[m] * (dchi2 * a + chi2 * bb);
-            dux += chi2 * a * g2[m][0];
-            duy += chi2 * a * g2[m][1];
-            duz += chi2 * a * g2[m][2];
-          }
-        }
-        if constexpr (P::L >= 3) {
-          if (k == 0) {
-            float b3[7], g3[7][3];
-            harm3(g.ux, g.uy, g.uz, b3);
-            harm3_grad(g.ux, g.uy, g.uz, g3);
-#pragma unroll
-            for (int m = 0; m < 7; ++m) {
-              const float a = gy3[m] * psi0, bb = gy3[m] * dpsi0;
-              drho += b3[m] * (dchi2 * a + chi2 * bb);
-              dux += chi2 * a * g3[m][0];
-              duy += chi2 * a * g3[m][1];
-              duz += chi2 * a * g3[m][2];
-            }
-          }
-        }
-        if (k == 0) drho += gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2;   // d(chi^4) = 2 chi^2 d(chi^2)
       }
-      // combine the lanes of the edge group (fixed butterfly)
+      // Q_k(u) and its gradient
+      const float x = g.ux, y = g.uy, z = g.uz;
+      const float mono[6] = {x * x, x * y, x * z, y * y, y * z, z * z};
+      float gq[3];
+      gq[0] = M2[0] * x + M2[3] * y + M2[5] * z;
+      gq[1] = M2[3] * x + M2[1] * y + M2[4] * z;
+      gq[2] = M2[5] * x + M2[4] * y + M2[2] * z;
+      float c3[3] = {0.f, 0.f, 0.f};
+      if constexpr (P::L >= 3) {
 #pragma unroll
-      for (int off = 1; off < P::LPE; off <<= 1) {
-        drho += __shfl_xor(drho, off);
-        dux += __shfl_xor(dux, off);
-        duy += __shfl_xor(duy, off);
-        duz += __shfl_xor(duz, off);
+        for (int a = 0; a < 3; ++a) {
+#pragma unroll
+          for (int qq = 0; qq < 6; ++qq) c3[a] += G3[a][qq] * mono[qq];
+        }
       }
+      // Q = v.u + (1/2) u.M u + (1/3) u.grad P3 (Euler's relation per degree)
+      const float Q = (v1[0] * x + v1[1] * y + v1[2] * z) +
+                      0.5f * (gq[0] * x + gq[1] * y + gq[2] * z) +
+                      (1.0f / 3.0f) * (c3[0] * x + c3[1] * y + c3[2] * z);
+      const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
+      float drho = dchi * a0 + chi * b0 + Q * (dchi2 * psi0 + chi2 * dpsi0) +
+                   gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2;
+      const float wu = chi2 * psi0;
+      float dux = wu * (v1[0] + gq[0] + c3[0]);
+      float duy = wu * (v1[1] + gq[1] + c3[1]);
+      float duz = wu * (v1[2] + gq[2] + c3[2]);
+      if (!valid) drho = dux = duy = duz = 0.0f;
+      drho = group_sum<P::LPE>(drho);
+      dux = group_sum<P::LPE>(dux);
+      duy = group_sum<P::LPE>(duy);
+      duz = group_sum<P::LPE>(duz);
       if (valid && k == 0) {
-        const float udu = g.ux * dux + g.uy * duy + g.uz * duz;
-        const float gx = drho * g.ux + (dux - udu * g.ux) * g.inv_rho;
-        const float gyv = drho * g.uy + (duy - udu * g.uy) * g.inv_rho;
-        const float gz = drho * g.uz + (duz - udu * g.uz) * g.inv_rho;
-        grad[b + el] = make_float4(gx, gyv, gz, 0.0f);
+        const float udu = x * dux + y * duy + z * duz;
+        const float gx = drho * x + (dux - udu * x) * g.inv_rho;
+        const float gy_ = drho * y + (duy - udu * y) * g.inv_rho;
+        const float gz = drho * z + (duz - udu * z) * g.inv_rho;
+        grad[b + el] = make_float4(gx, gy_, gz, 0.0f);
       }
     }
   }
@@ -184,13 +172,12 @@ __global__ void __launch_bounds__(kBlock) backward_kernel(ModelDev md, int64_t n
 
 template <class P>
 int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_t* row_ptr,
-           const int32_t* ecount, const float4* edge, const float* node, const float* dD,
-           float4* grad, hipStream_t st) {
-  int64_t blocks = (n + kWpb - 1) / kWpb;
-  if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(backward_kernel<P>, dim3(blocks), dim3(kBlock), 0, st, m->dev(), n, species,
-                     row_ptr, ecount, edge, node, dD, grad);
+           const int32_t* ecount, const float4* edge, const float* node_grad, float4* grad,
+           hipStream_t st) {
+  int64_t blocks = n < 16384 ? n : 16384;
+  if (blocks < 1) return 0;
+  hipLaunchKernelGGL(backward_kernel<P>, dim3(blocks), dim3(kTeam), 0, st, m->dev(), n, species,
+                     row_ptr, ecount, edge, node_grad, grad);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -199,10 +186,10 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                    const float* node, const float* dD, float4* grad, hipStream_t st) {
+                    const float* node_grad, float4* grad, hipStream_t st) {
   if (m->C0 == 32)
-    return launch<SmallProfile>(m, n, species, row_ptr, ecount, edge, node, dD, grad, st);
-  return launch<FullProfile>(m, n, species, row_ptr, ecount, edge, node, dD, grad, st);
+    return launch<SmallProfile>(m, n, species, row_ptr, ecount, edge, node_grad, grad, st);
+  return launch<FullProfile>(m, n, species, row_ptr, ecount, edge, node_grad, grad, st);
 }
 
 }  // namespace dpa4c

@@ -54,6 +54,7 @@ struct Profile {
   static constexpr int DOUT = oPi + nPi;
   static constexpr int DSTR = (DOUT + 15) / 16 * 16;   // row stride of descriptor arrays
   static_assert(C0 % LPE == 0, "channel split");
+  static_assert(R == 0 || R == 4, "the edge kernels handle 0 or 4 radial modes");
   static_assert(kWave % LPE == 0, "edge groups");
 };
 
@@ -65,11 +66,9 @@ static_assert(FullProfile::DOUT == 541 && FullProfile::S == 223, "Table S2 (128,
 // ---------------------------------------------------------------------------
 // Device-side view of a model, passed to kernels by value.
 // ---------------------------------------------------------------------------
-struct Sparse3 {            // nonzeros of one coupling tensor
-  int n;
-  const int* idx;           // [n][3] (m1, m2, m3)
-  const float* val;         // [n]
-};
+constexpr int kC123 = 3 * 5 * 7;          // dense (1,2,3) coupling, [m1][m2][m3]
+constexpr int kC233 = 5 * 7 * 7;          // dense (2,3,3) coupling
+constexpr int kCouplings = kC123 + kC233;
 
 struct ModelDev {
   // radial table: g rows [n_rows][CPL][LPE][6], q rows [n_rows][R][6]
@@ -87,7 +86,7 @@ struct ModelDev {
   const float* A2;          // [C2][K2]
   const float* mu;          // [D_out]
   const float* inv_sigma;   // [D_out]
-  Sparse3 c123, c233;
+  const float* cpl;         // [kCouplings]: C123 then C233 (symmetric in m2, m3), or null
   const float* E_ref;       // [T+1]
 };
 

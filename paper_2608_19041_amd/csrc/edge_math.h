@@ -100,6 +100,84 @@ __device__ inline int table_row(float rho, float inv_delta, int n_rows, float* t
   return r;
 }
 
+// Sum over aligned groups of G = 8 or 16 lanes with DPP row permutations
+// (quad xor 1, quad xor 2, half-row mirror, row mirror).  Every lane of the
+// group ends with the same bits: each step adds a value and its partner, in
+// the same order on both sides of the pair.
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int G>
+__device__ inline float group_sum(float v) {
+  static_assert(G == 8 || G == 16, "group of 8 or 16 lanes");
+  v += dpp_f<0xB1>(v);
+  v += dpp_f<0x4E>(v);
+  v += dpp_f<0x141>(v);
+  if constexpr (G == 16) v += dpp_f<0x140>(v);
+  return v;
+}
+
+// Degree-two and degree-three harmonics as homogeneous polynomials of u
+// (|u|^2 kept as x^2 + y^2 + z^2), Eq. (harmonics) and the degree-three
+// block of the Supplementary Note.
+__device__ inline void harm2_h(float x, float y, float z, float* b) {
+  const float r3 = 1.7320508075688772f;
+  b[0] = r3 * x * y;
+  b[1] = r3 * y * z;
+  b[2] = z * z - 0.5f * (x * x + y * y);
+  b[3] = r3 * x * z;
+  b[4] = 0.5f * r3 * (x * x - y * y);
+}
+__device__ inline void harm3_h(float x, float y, float z, float* b) {
+  const float a = 0.7905694150420949f;   // sqrt(5/8)
+  const float r15 = 3.872983346207417f;  // sqrt(15)
+  const float c = 0.6123724356957945f;   // sqrt(3/8)
+  const float x2 = x * x, y2 = y * y, z2 = z * z;
+  b[0] = a * y * (3.0f * x2 - y2);
+  b[1] = r15 * x * y * z;
+  b[2] = c * y * (4.0f * z2 - x2 - y2);
+  b[3] = z * (z2 - 1.5f * (x2 + y2));
+  b[4] = c * x * (4.0f * z2 - x2 - y2);
+  b[5] = 0.5f * r15 * z * (x2 - y2);
+  b[6] = a * x * (x2 - 3.0f * y2);
+}
+
+// For weights w_m, sum_m w_m B_2m(u) = u.W u with the symmetric W below;
+// returns M = 2W as (xx, yy, zz, xy, yz, xz), so that grad = M u.
+__device__ inline void quad_form2(const float* w, float* M) {
+  const float h3 = 0.8660254037844386f;   // sqrt(3)/2
+  M[0] = 2.0f * (-0.5f * w[2] + h3 * w[4]);
+  M[1] = 2.0f * (-0.5f * w[2] - h3 * w[4]);
+  M[2] = 2.0f * w[2];
+  M[3] = 2.0f * h3 * w[0];
+  M[4] = 2.0f * h3 * w[1];
+  M[5] = 2.0f * h3 * w[3];
+}
+// For weights w_m, P(u) = sum_m w_m B_3m(u) is a cubic in (x, y, z); G holds
+// the coefficients of its gradient over the monomials (x^2, xy, xz, y^2, yz,
+// z^2): dP/du_a = sum_q G[a][q] mono_q.  P = u . grad P / 3.
+__device__ inline void cubic_form3(const float* w, float (*G)[6]) {
+  const float a = 0.7905694150420949f, b = 3.872983346207417f, c = 0.6123724356957945f;
+  const float d = 0.5f * b;
+  const float pxxx = -c * w[4] + a * w[6];
+  const float pxxy = 3.0f * a * w[0] - c * w[2];
+  const float pxxz = -1.5f * w[3] + d * w[5];
+  const float pxyy = -c * w[4] - 3.0f * a * w[6];
+  const float pxyz = b * w[1];
+  const float pxzz = 4.0f * c * w[4];
+  const float pyyy = -a * w[0] - c * w[2];
+  const float pyyz = -1.5f * w[3] - d * w[5];
+  const float pyzz = 4.0f * c * w[2];
+  const float pzzz = w[3];
+  G[0][0] = 3.0f * pxxx; G[0][1] = 2.0f * pxxy; G[0][2] = 2.0f * pxxz;
+  G[0][3] = pxyy;        G[0][4] = pxyz;        G[0][5] = pxzz;
+  G[1][0] = pxxy;        G[1][1] = 2.0f * pxyy; G[1][2] = pxyz;
+  G[1][3] = 3.0f * pyyy; G[1][4] = 2.0f * pyyz; G[1][5] = pyzz;
+  G[2][0] = pxxz;        G[2][1] = pxyz;        G[2][2] = 2.0f * pxzz;
+  G[2][3] = pyyz;        G[2][4] = 2.0f * pyzz; G[2][5] = 3.0f * pzzz;
+}
+
 // species index clamped into the type table (the padding type for bad input)
 __device__ inline int clamp_type(int a, int n_types1) {
   return static_cast<unsigned>(a) < static_cast<unsigned>(n_types1) ? a : n_types1 - 1;

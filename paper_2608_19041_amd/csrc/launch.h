@@ -44,15 +44,14 @@ int launch_rev(const int64_t* row_ptr, const int32_t* ecount, const int32_t* sid
 // model stages
 int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
                    const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                   float* node, float* desc, hipStream_t st);
-int launch_mlp_forward(const dpa4c_model* m, int64_t n, const int32_t* species, float* desc,
-                       float* h0, float* h1, float* h2, float* ds0, float* ds1, float* ds2,
-                       double* e_atom, hipStream_t st);
-int launch_mlp_backward(const dpa4c_model* m, int64_t n, float* desc, float* h0, float* h1,
-                        float* h2, float* ds0, float* ds1, float* ds2, hipStream_t st);
+                   float* node, hipStream_t st);
+// readout + MLP + head + MLP gradient + readout VJP on 16-atom tiles;
+// desc_out (float [N][D_out]) receives D when not null
+int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
+                 float* node_grad, double* e_atom, float* desc_out, hipStream_t st);
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                    const float* node, const float* dD, float4* grad, hipStream_t st);
+                    const float* node_grad, float4* grad, hipStream_t st);
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* rev, double* forces, hipStream_t st);
 int launch_energy(int64_t n, const double* e_atom, double* partials, double* out,

@@ -1,15 +1,7 @@
-// Atomic-energy MLP of Eqs. (atomic-energy) and (fitting) and its
-// vector-Jacobian product, on fp32 matrix cores (v_mfma_f32_16x16x4_f32).
-//
-// Forward, per hidden layer t:  pre = A Theta_t + b_t,
-//     h_t = SiLU(pre) (+ h_{t-1} when the widths agree),  ds_t = SiLU'(pre).
-// Head:  E_i = h_L . w + b + E_ref[a_i]  (accumulated into float64), and the
-// back-propagation seed p_L = w * ds_L.
-// Backward (weights fixed, input gradient only):
-//     hbar_{t-1} = [hbar_t] + p_t Theta_t^T,   p_{t-1} = hbar_{t-1} * ds_{t-1},
-//     dE/dD = p_1 Theta_1^T.
-// Bias, activation, residual and the SiLU' product are fused into the GEMM
-// epilogues, so every activation is written once.
+// Plain fp32 GEMM on the matrix cores (v_mfma_f32_16x16x4_f32) with an
+// optional fused epilogue (bias + SiLU + residual, or residual + product).
+// The energy path uses the per-atom kernel; this one backs the exported
+// dpa4c_debug_gemm entry used to check the MFMA operand layout.
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
@@ -139,97 +131,7 @@ int gemm(const float* A, int lda, const float* B, int ldb, float* C, int ldc, in
   return 0;
 }
 
-// E_i = h_i . w + b + E_ref[a_i] in float64 (fixed-order wave sum), and the
-// seed p = w * ds in place.  One wavefront per atom.
-__global__ void __launch_bounds__(256) head_kernel(int64_t n, int F, const float* __restrict__ h,
-                                                   const float* __restrict__ w, float b_head,
-                                                   const float* __restrict__ E_ref,
-                                                   const int32_t* __restrict__ species, int n_types1,
-                                                   float* __restrict__ ds, double* __restrict__ e_atom) {
-  const int lane = threadIdx.x & 63;
-  const int64_t nw = int64_t(gridDim.x) * 4;
-  for (int64_t i = blockIdx.x * int64_t(4) + (threadIdx.x >> 6); i < n; i += nw) {
-    const float* hr = h + size_t(i) * F;
-    float* dr = ds + size_t(i) * F;
-    float acc = 0.0f;
-    for (int c = lane; c < F; c += 64) {
-      acc += hr[c] * w[c];
-      dr[c] *= w[c];
-    }
-    for (int off = 1; off < 64; off <<= 1) acc += __shfl_xor(acc, off);
-    if (lane == 0) {
-      int a = species[i];
-      a = static_cast<unsigned>(a) < static_cast<unsigned>(n_types1) ? a : n_types1 - 1;
-      e_atom[i] = double(acc) + double(b_head) + double(E_ref[a]);
-    }
-  }
-}
-
 }  // namespace
-
-int launch_mlp_forward(const dpa4c_model* m, int64_t n, const int32_t* species, float* desc,
-                       float* h0, float* h1, float* h2, float* ds0, float* ds1, float* ds2,
-                       double* e_atom, hipStream_t st) {
-  const int F = m->F, Kp = (m->D_out + 15) / 16 * 16;
-  float* hs[3] = {h0, h1, h2};
-  float* dss[3] = {ds0, ds1, ds2};
-  if (m->n_layers != 3) {
-    set_error("the MLP launcher is built for three hidden layers");
-    return DPA4C_ERR_UNSUPPORTED;
-  }
-  const float* in = desc;
-  int ld_in = Kp, K = Kp;
-  for (int t = 0; t < 3; ++t) {
-    Epilogue ep{};
-    ep.mode = 0;
-    ep.bias = m->bias[t];
-    ep.aux = dss[t];
-    if (K == F) {            // identity residual where the widths agree
-      ep.res_mat = in;
-      ep.ldr = ld_in;
-    }
-    int rc = gemm(in, ld_in, m->theta[t], F, hs[t], F, static_cast<int>(n), F, K, ep, st);
-    if (rc) return rc;
-    in = hs[t];
-    ld_in = F;
-    K = F;
-  }
-  int64_t blocks = (n + 3) / 4;
-  if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(head_kernel, dim3(blocks), dim3(256), 0, st, n, F, h2, m->w_head, m->b_head,
-                     m->E_ref, species, m->n_types + 1, ds2, e_atom);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
-int launch_mlp_backward(const dpa4c_model* m, int64_t n, float* desc, float* h0, float* h1,
-                        float* h2, float* ds0, float* ds1, float* ds2, hipStream_t st) {
-  const int F = m->F, Kp = (m->D_out + 15) / 16 * 16;
-  const int M = static_cast<int>(n);
-  (void)h0;
-  (void)h1;
-  // hbar2 = w + p3 Theta3^T  (stored in h2),  p2 = hbar2 * ds1 (in place)
-  Epilogue e3{};
-  e3.mode = 1;
-  e3.res_vec = m->w_head;
-  e3.out_h = h2;
-  e3.mul = ds1;
-  int rc = gemm(ds2, F, m->thetaT[2], F, ds1, F, M, F, F, e3, st);
-  if (rc) return rc;
-  // hbar1 = hbar2 + p2 Theta2^T,  p1 = hbar1 * ds0 (in place)
-  Epilogue e2{};
-  e2.mode = 1;
-  e2.res_mat = h2;
-  e2.ldr = F;
-  e2.mul = ds0;
-  rc = gemm(ds1, F, m->thetaT[1], F, ds0, F, M, F, F, e2, st);
-  if (rc) return rc;
-  // dE/dD = p1 Theta1^T
-  Epilogue e1{};
-  e1.mode = 1;
-  return gemm(ds0, F, m->thetaT[0], Kp, desc, Kp, M, Kp, F, e1, st);
-}
 
 int launch_gemm_test(const float* A, const float* B, float* C, int M, int N, int K,
                      hipStream_t st) {

@@ -1,0 +1,291 @@
+// Per-atom kernel: readout, atomic-energy MLP, head, MLP input gradient and
+// readout vector-Jacobian product for a tile of 16 atoms in one workgroup
+// (Eqs. (alignment) .. (fitting)).  The descriptor D and dE/dD never leave
+// LDS: the node state Y comes in, E_i and dE/d(node state) go out.
+//
+//   h1 = SiLU(D Th1 + b1), h2 = SiLU(h1 Th2 + b2) + h1, h3 = SiLU(h2 Th3 + b3) + h2
+//   E  = h3 . w + b + E_ref[a]
+//   hb2 = w + (w * s3) Th3^T,  hb1 = hb2 + (hb2 * s2) Th2^T,  dE/dD = (hb1 * s1) Th1^T
+// with s_t = SiLU'(pre_t).  Every product runs on v_mfma_f32_16x16x4_f32.
+//
+// Layout: the 16-row activation tile (the A operand) lives in LDS; each of the
+// four waves owns a fixed set of 16-column output tiles, so the SiLU'
+// factors and the residual carry of every (row, column) stay in the same
+// lane's registers from the forward to the backward pass.  Weights are
+// stored in fragment order: for output tile T and k-block kb (16 inputs) lane
+// l reads one float4 = W[kb*16 + 4*(l/16) + s][T*16 + l%16], s = 0..3, and
+// the A operand uses the same permutation of k inside the block.
+#include <hip/hip_runtime.h>
+
+#include "../../include/dpa4c.h"
+#include "launch.h"
+#include "readout.h"
+
+namespace dpa4c {
+
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kRows = 16;
+constexpr int kThreads = 512;
+constexpr int kWavesPB = kThreads / 64;
+
+__device__ inline float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for up to
+// MAXT output tiles first, first + stride, ... (nt of them, wave-uniform).
+template <int MAXT>
+__device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int lda, int kblocks,
+                                  const float4* __restrict__ Wf, int first, int stride, int nt,
+                                  int lane) {
+  const int arow = lane & 15, aq = lane >> 4;
+  const float4* wp = Wf + lane;
+  float4 b[MAXT];
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t)
+    if (t < nt) b[t] = wp[size_t(first + t * stride) * kblocks * 64];
+#pragma unroll 1
+  for (int kb = 0; kb < kblocks; ++kb) {
+    float4 nb[MAXT];
+    const bool more = kb + 1 < kblocks;
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t)
+      if (more && t < nt) nb[t] = wp[(size_t(first + t * stride) * kblocks + kb + 1) * 64];
+    const float4 a = *reinterpret_cast<const float4*>(As + arow * lda + kb * 16 + aq * 4);
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) {
+      if (t < nt) {
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[t].x, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[t].y, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[t].z, acc[t], 0, 0, 0);
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
+      }
+    }
+    if (more) {
+#pragma unroll
+      for (int t = 0; t < MAXT; ++t) b[t] = nb[t];
+    }
+  }
+}
+
+struct MlpArgs {
+  const float4* W[3];     // forward weights, fragment order (K = Kp, F, F; N = F)
+  const float4* WT[3];    // transposed weights, fragment order (K = F; N = F, F, Kp)
+  const float* bias[3];
+  const float* w_head;
+  float b_head;
+  const float* E_ref;
+  int n_types1;
+};
+
+// P: model profile (KP = P::DSTR padded descriptor width), F: hidden width.
+template <class P, int F>
+__global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, int64_t n,
+                                                        const int32_t* __restrict__ species,
+                                                        const float* __restrict__ node,
+                                                        float* __restrict__ node_grad,
+                                                        double* __restrict__ e_atom,
+                                                        float* __restrict__ desc_out) {
+  constexpr int KP = P::DSTR;
+  constexpr int LDA = (KP > F ? KP : F) + 4;
+  constexpr int FT = F / 16;                          // output tiles of a hidden layer
+  constexpr int NT = (FT + kWavesPB - 1) / kWavesPB;  // per wave (round-robin)
+  constexpr int DT = KP / 16;                         // output tiles of dE/dD
+  constexpr int NTD = (DT + kWavesPB - 1) / kWavesPB;
+  constexpr int APW = kRows / kWavesPB;               // atoms per wave in the readouts
+  __shared__ float As[kRows * LDA];
+  __shared__ float epart[kWavesPB][kRows];
+  __shared__ ReadoutLds<P> rl_all[kWavesPB];
+  __shared__ float cpl[P::L >= 3 ? kCouplings : 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col_in = lane & 15, rgrp = lane >> 4;   // output element: row 4*rgrp + r
+  const int nt = (FT - wave + kWavesPB - 1) / kWavesPB;
+  ReadoutLds<P>& rl = rl_all[wave];
+  if constexpr (P::L >= 3) {
+    for (int t = threadIdx.x; t < kCouplings; t += kThreads) cpl[t] = md.cpl[t];
+    __syncthreads();
+  }
+
+  for (int64_t tile = blockIdx.x; tile * kRows < n; tile += gridDim.x) {
+    const int64_t row0 = tile * kRows;
+    // ---- readout of the tile's atoms: D rows into LDS
+    for (int a = 0; a < APW; ++a) {
+      const int r = wave * APW + a;
+      const int64_t i = row0 + r;
+      float* drow = As + r * LDA;
+      if (i < n) {
+        const float* ny = node + size_t(i) * P::NS;
+        for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
+        wave_sync();
+        readout_forward<P>(rl, md, cpl, clamp_type(species[i], md.n_types1), drow);
+        if (desc_out)
+          for (int t = lane; t < P::DOUT; t += 64) desc_out[size_t(i) * P::DOUT + t] = drow[t];
+      } else {
+        for (int t = lane; t < KP; t += 64) drow[t] = 0.0f;
+      }
+      wave_sync();
+    }
+    __syncthreads();
+
+    float s[3][NT][4];   // SiLU'(pre) of the three layers
+    float h[NT][4];      // current activation / backward carry
+#pragma unroll
+    for (int layer = 0; layer < 3; ++layer) {
+      v4f acc[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, p.W[layer], wave, kWavesPB, nt,
+                     lane);
+      __syncthreads();   // everyone has read the A tile
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t >= nt) continue;
+        const int col = (wave + kWavesPB * t) * 16 + col_in;
+        const float bc = p.bias[layer][col];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float pre = acc[t][r] + bc;
+          const float sg = sigm(pre);
+          const float act = pre * sg;
+          s[layer][t][r] = sg * (1.0f + pre * (1.0f - sg));
+          h[t][r] = layer == 0 ? act : act + h[t][r];   // identity residual for equal widths
+          As[(4 * rgrp + r) * LDA + col] = h[t][r];
+        }
+      }
+      __syncthreads();
+    }
+    // ---- head: E_i = h3 . w + b + E_ref, fixed-order reduction
+    float part[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (t >= nt) continue;
+      const float wc = p.w_head[(wave + kWavesPB * t) * 16 + col_in];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) part[r] += h[t][r] * wc;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) part[r] += __shfl_xor(part[r], off, 16);
+    }
+    if (col_in == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) epart[wave][4 * rgrp + r] = part[r];
+    }
+    // ---- backward seed: hbar3 = w, p3 = w * s3 as the next A operand
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (t >= nt) continue;
+      const int col = (wave + kWavesPB * t) * 16 + col_in;
+      const float wc = p.w_head[col];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        h[t][r] = wc;                                   // carry hbar3
+        As[(4 * rgrp + r) * LDA + col] = wc * s[2][t][r];
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x < kRows && row0 + threadIdx.x < n) {
+      const int i = static_cast<int>(threadIdx.x);
+      float e = epart[0][i];
+#pragma unroll
+      for (int w = 1; w < kWavesPB; ++w) e += epart[w][i];
+      int a = species[row0 + i];
+      a = static_cast<unsigned>(a) < static_cast<unsigned>(p.n_types1) ? a : p.n_types1 - 1;
+      e_atom[row0 + i] = double(e) + double(p.b_head) + double(p.E_ref[a]);
+    }
+    // ---- hbar_{t-1} = hbar_t + p_t Th_t^T,  p_{t-1} = hbar_{t-1} * s_{t-1}
+#pragma unroll
+    for (int layer = 2; layer >= 1; --layer) {
+      v4f acc[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+      mfma_tiles<NT>(acc, As, LDA, F / 16, p.WT[layer], wave, kWavesPB, nt, lane);
+      __syncthreads();
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        if (t >= nt) continue;
+        const int col = (wave + kWavesPB * t) * 16 + col_in;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          h[t][r] += acc[t][r];
+          As[(4 * rgrp + r) * LDA + col] = h[t][r] * s[layer - 1][t][r];
+        }
+      }
+      __syncthreads();
+    }
+    // ---- dE/dD = p1 Th1^T  (KP columns, tiles dealt round-robin) back into LDS
+    {
+      const int ntd = (DT - wave + kWavesPB - 1) / kWavesPB;
+      v4f acc[NTD];
+#pragma unroll
+      for (int t = 0; t < NTD; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+      mfma_tiles<NTD>(acc, As, LDA, F / 16, p.WT[0], wave, kWavesPB, ntd, lane);
+      __syncthreads();
+#pragma unroll
+      for (int t = 0; t < NTD; ++t) {
+        if (t >= ntd) continue;
+        const int col = (wave + kWavesPB * t) * 16 + col_in;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) As[(4 * rgrp + r) * LDA + col] = acc[t][r];
+      }
+      __syncthreads();
+    }
+    // ---- readout VJP: dE/d(node state) of the tile's atoms
+    for (int a = 0; a < APW; ++a) {
+      const int r = wave * APW + a;
+      const int64_t i = row0 + r;
+      if (i >= n) continue;
+      const float* ny = node + size_t(i) * P::NS;
+      for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
+      wave_sync();
+      readout_backward<P>(rl, md, cpl, As + r * LDA);
+      float* gout = node_grad + size_t(i) * P::NS;
+      for (int t = lane; t < P::NS; t += 64) gout[t] = rl.gy[t];
+      wave_sync();
+    }
+    __syncthreads();
+  }
+}
+
+template <class P, int F>
+int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
+                 float* node_grad, double* e_atom, float* desc_out, hipStream_t st) {
+  MlpArgs a{};
+  for (int t = 0; t < 3; ++t) {
+    a.W[t] = reinterpret_cast<const float4*>(m->wfrag[t]);
+    a.WT[t] = reinterpret_cast<const float4*>(m->wfragT[t]);
+    a.bias[t] = m->bias[t];
+  }
+  a.w_head = m->w_head;
+  a.b_head = m->b_head;
+  a.E_ref = m->E_ref;
+  a.n_types1 = m->n_types + 1;
+  int64_t tiles = (n + kRows - 1) / kRows;
+  int64_t grid = tiles < 16384 ? tiles : 16384;
+  if (grid < 1) grid = 1;
+  hipLaunchKernelGGL((atom_kernel<P, F>), dim3(grid), dim3(kThreads), 0, st, a, m->dev(), n,
+                     species, node, node_grad, e_atom, desc_out);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+}  // namespace
+
+int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
+                 float* node_grad, double* e_atom, float* desc_out, hipStream_t st) {
+  if (n <= 0) return 0;
+  if (m->n_layers != 3 || !m->wfrag[0]) {
+    set_error("the per-atom kernel needs three hidden layers");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  if (m->C0 == 32 && m->F == 192)
+    return launch_atoms<SmallProfile, 192>(m, n, species, node, node_grad, e_atom, desc_out, st);
+  if (m->C0 == 128 && m->F == 384)
+    return launch_atoms<FullProfile, 384>(m, n, species, node, node_grad, e_atom, desc_out, st);
+  set_error("no per-atom kernel instance for this (profile, MLP width)");
+  return DPA4C_ERR_UNSUPPORTED;
+}
+
+}  // namespace dpa4c

@@ -40,8 +40,8 @@ void DevBuf::release() {
 const char* stage_name(int s) {
   static const char* names[kNumStages] = {
       "neighbor_bin", "neighbor_count", "neighbor_scan", "neighbor_fill", "skin_rev",
-      "compact",      "rev",            "forward",       "mlp_forward",   "mlp_backward",
-      "backward",     "forces",         "energy",        "integrate"};
+      "compact",      "rev",            "forward",       "atoms",         "backward",
+      "forces",       "energy",         "integrate"};
   return (s >= 0 && s < kNumStages) ? names[s] : "?";
 }
 
@@ -334,25 +334,20 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     }
   }
 
-  // ---- coupling tensors (sparse lists for the generic triples) -----------
-  std::vector<int> i123, i233;
-  std::vector<float> v123, v233;
+  // ---- coupling tensors; (2,3,3) symmetrised over its two degree-3 indices
+  std::vector<float> cpl;
   m->gaunt[0] = coupling(1, 1, 2);
   m->gaunt[2] = coupling(2, 2, 2);
   if (L >= 3) {
     m->gaunt[1] = coupling(1, 2, 3);
     m->gaunt[3] = coupling(2, 3, 3);
-    auto sparse = [](const std::vector<double>& C, int n2, int n3, std::vector<int>& idx,
-                     std::vector<float>& val) {
-      for (size_t e = 0; e < C.size(); ++e)
-        if (std::fabs(C[e]) > 1e-12) {
-          int k = e % n3, j = (e / n3) % n2, i = e / (n3 * n2);
-          idx.push_back(i); idx.push_back(j); idx.push_back(k);
-          val.push_back(static_cast<float>(C[e]));
-        }
-    };
-    sparse(m->gaunt[1], 5, 7, i123, v123);
-    sparse(m->gaunt[3], 7, 7, i233, v233);
+    cpl.reserve(kCouplings);
+    for (double v : m->gaunt[1]) cpl.push_back(static_cast<float>(v));
+    const auto& g = m->gaunt[3];
+    for (int a = 0; a < 5; ++a)
+      for (int b = 0; b < 7; ++b)
+        for (int c = 0; c < 7; ++c)
+          cpl.push_back(static_cast<float>(0.5 * (g[(a * 7 + b) * 7 + c] + g[(a * 7 + c) * 7 + b])));
   }
 
   // ---- one device block for every parameter array ---------------------
@@ -393,16 +388,30 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     add((void**)&m->bias[t], bias[t], size_t(F) * 4);
     fan = F;
   }
+  // fragment order for the fused MLP kernel: for output tile T and k-block kb
+  // lane l holds W[kb*16 + 4*(l/16) + s][T*16 + l%16], s = 0..3
+  auto fragment = [](const std::vector<float>& src, int K, int N) {
+    std::vector<float> out(size_t(K) * N);
+    const int kbs = K / 16;
+    for (int T = 0; T < N / 16; ++T)
+      for (int kb = 0; kb < kbs; ++kb)
+        for (int l = 0; l < 64; ++l)
+          for (int s = 0; s < 4; ++s)
+            out[((size_t(T) * kbs + kb) * 64 + l) * 4 + s] =
+                src[size_t(kb * 16 + (l / 16) * 4 + s) * N + T * 16 + (l % 16)];
+    return out;
+  };
+  std::vector<std::vector<float>> frags(2 * m->n_layers);
+  for (int t = 0; t < m->n_layers; ++t) {
+    const int fin = t == 0 ? Dp : F;
+    frags[2 * t] = fragment(padded[t], fin, F);
+    frags[2 * t + 1] = fragment(transposed[t], F, fin);
+    add((void**)&m->wfrag[t], frags[2 * t].data(), frags[2 * t].size() * 4);
+    add((void**)&m->wfragT[t], frags[2 * t + 1].data(), frags[2 * t + 1].size() * 4);
+  }
   add((void**)&m->w_head, w_head, size_t(F) * 4);
   m->b_head = b_head[0];
-  m->c123_n = static_cast<int>(v123.size());
-  m->c233_n = static_cast<int>(v233.size());
-  if (m->c123_n) {
-    add((void**)&m->c123_idx, i123.data(), i123.size() * 4);
-    add((void**)&m->c123_val, v123.data(), v123.size() * 4);
-    add((void**)&m->c233_idx, i233.data(), i233.size() * 4);
-    add((void**)&m->c233_val, v233.data(), v233.size() * 4);
-  }
+  if (!cpl.empty()) add((void**)&m->cpl, cpl.data(), cpl.size() * 4);
   // raw pair-network weights, used once by the pair-cache kernel
   const float* raw_wp_in = nullptr;
   const float* raw_wp_out = nullptr;
@@ -454,8 +463,7 @@ dpa4c::ModelDev dpa4c_model::dev() const {
   d.A2 = A2;
   d.mu = mu;
   d.inv_sigma = inv_sigma;
-  d.c123 = {c123_n, c123_idx, c123_val};
-  d.c233 = {c233_n, c233_idx, c233_val};
+  d.cpl = cpl;
   d.E_ref = E_ref;
   return d;
 }

@@ -19,8 +19,7 @@ enum Stage {
   kStCompact,
   kStRev,
   kStForward,
-  kStMlpForward,
-  kStMlpBackward,
+  kStAtoms,
   kStBackward,
   kStForces,
   kStEnergy,
@@ -71,9 +70,8 @@ struct Workspace {
   DevBuf grad;          // float4 [cap]: dE/dr_ij
   // per-atom state
   DevBuf node;          // float [N][NS]
-  DevBuf desc;          // float [N][D_out]  (D, then dE/dD)
-  DevBuf h[3];          // float [N][F]
-  DevBuf ds[3];         // float [N][F]  SiLU'(pre) then back-propagated grads
+  DevBuf node_grad;     // float [N][NS]: dE/d(node state)
+  DevBuf desc;          // float [N][D_out]: D, written only for stage checks
   DevBuf epart;         // double partial sums
   DevBuf flags;         // int64 [8] device flags
   DevBuf ekin_atom;     // double [N]
@@ -119,14 +117,11 @@ struct dpa4c_model {
   float* theta[8] = {};             // Theta_t [in][F]
   float* thetaT[8] = {};            // Theta_t^T [F][in]
   float* bias[8] = {};
+  float* wfrag[8] = {};             // Theta_t in MFMA fragment order
+  float* wfragT[8] = {};            // Theta_t^T in MFMA fragment order
   float* w_head = nullptr;
   float b_head = 0;
-  int* c123_idx = nullptr;
-  float* c123_val = nullptr;
-  int c123_n = 0;
-  int* c233_idx = nullptr;
-  float* c233_val = nullptr;
-  int c233_n = 0;
+  float* cpl = nullptr;             // dense (1,2,3) and (2,3,3) couplings (degree three only)
   // host copies kept for tests of the host logic
   std::vector<double> gaunt[4];     // (1,1,2), (1,2,3), (2,2,2), (2,3,3) normalised couplings
   dpa4c::Workspace ws;

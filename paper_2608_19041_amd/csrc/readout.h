@@ -1,12 +1,17 @@
 // Per-atom invariant readout (Methods "Nonlinear readout and atomic energy",
 // Eqs. (alignment) .. (calibration)) and its vector-Jacobian product, run by
-// one 64-lane wavefront per atom on a wave-private LDS block.
+// one 64-lane wavefront per atom on a wave-private LDS block; the descriptor
+// row (D~, D or dE/dD) lives in a caller-provided LDS row.
 //
 // Each stage spreads its outputs over the lanes (gather form: every output is
 // computed by one lane from values written by the previous stage), so the
 // results do not depend on scheduling.  The (1,1,2) and (2,2,2) bispectrum
 // blocks use the closed forms of Eq. (closed-forms); (1,2,3) and (2,3,3)
-// contract sparse coupling lists.
+// contract the dense coupling tensors one index at a time:
+//   J123[k1][k2] = sum_m1 Z1[m1][k1] U[m1][k2],  U = T Z2,  T[m1][m2] = sum_m3 C123 Z3
+//   J233[e]      = sum_m1 Z2[m1][e] V[m1],       V = W Z3,  W[m1][m2] = sum_m3 C233 Z3
+// The couplings (``cpl``: C123 [3][5][7] then C233 [5][7][7], the latter
+// symmetric in its last two indices) are read from LDS staged by the caller.
 #pragma once
 
 #include "common.h"
@@ -19,12 +24,12 @@ struct ReadoutLds {
   float y[P::NS];                 // [S0, S1, Y]
   float xt1[3 * P::C1];           // aligned features, Eq. (alignment)
   float xt2[5 * P::C2];
-  float xt3[8];
+  float xt3[8];                   // degree three (identity probe: Z3 = X~3)
   float z1[3 * P::K1];            // probes, Eq. (probes)
   float z2[5 * P::K2];
   float q[P::K2][9];              // STF matrices of the degree-two probes
   float qv[P::K2][P::K1][3];      // Q_eta v_kappa
-  float d[P::DOUT];               // D~ (forward) or dE/dD~ (backward)
+  float t123[15], u123[3 * P::K2], w233[35], v233[5];
   // backward only
   float gxt1[3 * P::C1];
   float gxt2[5 * P::C2];
@@ -33,8 +38,8 @@ struct ReadoutLds {
   float gz2[5 * P::K2];
   float gz3[8];
   float gq[P::K2][9];
+  float ub123[3 * P::K2], tb123[15], vb233[5];
   float gy[P::NS];
-  float red[4];
 };
 
 constexpr float kSqrt2 = 1.4142135623730951f;
@@ -89,9 +94,17 @@ __device__ inline void e222(int t, int* a, int* b, int* c, float* w) {
   *w = (t == 0 || t == 3) ? 1.0f : r3;
 }
 
-// Forward intermediates from s.y: M, aligned features, probes, Q, Qv.
+// fixed-order sum over the 64 lanes (butterfly; every lane gets the same bits)
+__device__ inline float wave_sum(float v) {
+  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Forward intermediates from s.y: M, aligned features, probes, Q, Qv and the
+// partial contractions T, U, W, V of the generic couplings.
 template <class P>
-__device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md, float* M0, float* M1) {
+__device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
+                                      const float* __restrict__ cpl, float* M0, float* M1) {
   const int lane = lane_of();
   const float m0 = sqrtf(0.25f + s.y[0]);
   const float m1 = sqrtf(0.25f + s.y[1]);
@@ -136,10 +149,37 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md, floa
       s.z2[t] = acc;
     }
   }
+  if constexpr (P::L >= 3) {
+    // T[m1][m2] = sum_m3 C123 Z3 (15 entries), W[m1][m2] = sum_m3 C233 Z3 (35)
+    if (lane < 50) {
+      const float* c = cpl + 7 * lane;   // C233 follows C123 (15 rows of 7)
+      float acc = 0.0f;
+#pragma unroll
+      for (int m3 = 0; m3 < 7; ++m3) acc += c[m3] * s.xt3[m3];
+      if (lane < 15) s.t123[lane] = acc;
+      else s.w233[lane - 15] = acc;
+    }
+  }
   wave_sync();
   if (lane < P::K2 * 9) {
     int eta = lane / 9, ab = lane % 9;
     s.q[eta][ab] = stf_entry(s.z2 + eta, P::K2, ab / 3, ab % 3);
+  }
+  if constexpr (P::L >= 3) {
+    // U[m1][k2] = sum_m2 T[m1][m2] Z2[m2][k2],  V[m1] = sum_m2 W[m1][m2] Z3[m2]
+    if (lane >= 32 && lane < 32 + 3 * P::K2) {
+      const int o = lane - 32, m1 = o / P::K2, k2 = o % P::K2;
+      float acc = 0.0f;
+#pragma unroll
+      for (int m2 = 0; m2 < 5; ++m2) acc += s.t123[m1 * 5 + m2] * s.z2[m2 * P::K2 + k2];
+      s.u123[o] = acc;
+    } else if (lane >= 48 && lane < 53) {
+      const int m1 = lane - 48;
+      float acc = 0.0f;
+#pragma unroll
+      for (int m2 = 0; m2 < 7; ++m2) acc += s.w233[m1 * 7 + m2] * s.xt3[m2];
+      s.v233[m1] = acc;
+    }
   }
   wave_sync();
   for (int o = lane; o < P::K2 * P::K1 * 3; o += kWave) {
@@ -152,21 +192,22 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md, floa
 }
 
 // Eqs. (gram) .. (calibration): writes the calibrated descriptor of atom
-// ``ai`` to ``dout`` (global memory).  s.y must hold the node state.
+// type ``ai`` to the LDS row ``d`` (P::DSTR entries, zero padded).  s.y must
+// hold the node state.
 template <class P>
-__device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
-                                float* __restrict__ dout) {
+__device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, const float* cpl, int ai,
+                                float* d) {
   const int lane = lane_of();
   float M0, M1;
-  readout_intermediates<P>(s, md, &M0, &M1);
+  readout_intermediates<P>(s, md, cpl, &M0, &M1);
   const float i0 = 1.0f / M0;
   for (int c = lane; c < P::C0; c += kWave) {
-    s.d[P::oX0 + c] = md.type_embed[ai * P::C0 + c];
-    s.d[P::oX + c] = s.y[P::Y0 + c] * i0;
+    d[P::oX0 + c] = md.type_embed[ai * P::C0 + c];
+    d[P::oX + c] = s.y[P::Y0 + c] * i0;
   }
   if (lane == 0) {
-    s.d[P::oM0] = M0;
-    s.d[P::oM1] = M1;
+    d[P::oM0] = M0;
+    d[P::oM1] = M1;
   }
   // Gram blocks, Eq. (gram), vech with sqrt(2) off the diagonal
   for (int o = lane; o < P::nG1 + P::nG2 + P::nG3; o += kWave) {
@@ -184,7 +225,7 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
     } else {
       for (int m = 0; m < 7; ++m) acc += s.xt3[m] * s.xt3[m];
     }
-    s.d[P::oG1 + o] = acc;
+    d[P::oG1 + o] = acc;
   }
   // (1,1,2): -(f/sqrt5) v_k1 . Q_eta v_k2, k1 <= k2
   for (int o = lane; o < P::n112; o += kWave) {
@@ -192,7 +233,7 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
     vech_pair(pr, P::K1, &k1, &k2);
     float acc = 0.0f;
     for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];
-    s.d[P::o112 + o] = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc;
+    d[P::o112 + o] = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc;
   }
   // (2,2,2): -sqrt(12/35) w tr(Q_a Q_b Q_c)
   if (lane < P::n222) {
@@ -206,26 +247,22 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
         for (int u = 0; u < 3; ++u) ab += s.q[a][r * 3 + u] * s.q[b][u * 3 + t];
         tr += ab * s.q[c][t * 3 + r];
       }
-    s.d[P::o222 + lane] = -kSqrt12_35 * w * tr;
+    d[P::o222 + lane] = -kSqrt12_35 * w * tr;
   }
   if constexpr (P::L >= 3) {
-    // (1,2,3) and (2,3,3) through the sparse couplings
+    // (1,2,3) and (2,3,3): last contraction of the factored couplings
     for (int o = lane; o < P::n123 + P::n233; o += kWave) {
       float acc = 0.0f;
       if (o < P::n123) {
-        int k1 = o / P::K2, k2 = o % P::K2;
-        for (int e = 0; e < md.c123.n; ++e) {
-          const int* ix = md.c123.idx + 3 * e;
-          acc += md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] * s.z2[ix[1] * P::K2 + k2] * s.xt3[ix[2]];
-        }
-        s.d[P::o123 + o] = acc;
+        const int k1 = o / P::K2, k2 = o % P::K2;
+#pragma unroll
+        for (int m1 = 0; m1 < 3; ++m1) acc += s.z1[m1 * P::K1 + k1] * s.u123[m1 * P::K2 + k2];
+        d[P::o123 + o] = acc;
       } else {
-        int eta = o - P::n123;
-        for (int e = 0; e < md.c233.n; ++e) {
-          const int* ix = md.c233.idx + 3 * e;
-          acc += md.c233.val[e] * s.z2[ix[0] * P::K2 + eta] * s.xt3[ix[1]] * s.xt3[ix[2]];
-        }
-        s.d[P::o233 + eta] = acc;
+        const int eta = o - P::n123;
+#pragma unroll
+        for (int m1 = 0; m1 < 5; ++m1) acc += s.z2[m1 * P::K2 + eta] * s.v233[m1];
+        d[P::o233 + eta] = acc;
       }
     }
   }
@@ -234,30 +271,23 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, int ai,
     int eta = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
     for (int a = 0; a < 3; ++a) acc += s.qv[eta][k][a] * s.qv[eta][k][a];
-    s.d[P::oPi + o] = acc;
+    d[P::oPi + o] = acc;
   }
   wave_sync();
   for (int o = lane; o < P::DSTR; o += kWave)
-    dout[o] = o < P::DOUT ? (s.d[o] - md.mu[o]) * md.inv_sigma[o] : 0.0f;
+    d[o] = o < P::DOUT ? (d[o] - md.mu[o]) * md.inv_sigma[o] : 0.0f;
   wave_sync();
 }
 
-// fixed-order sum over the 64 lanes (butterfly; every lane gets the same bits)
-__device__ inline float wave_sum(float v) {
-  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off);
-  return v;
-}
-
-// Vector-Jacobian product of the readout: from dE/dD (global, calibrated
-// descriptor gradient) to dE/d(node state) in s.gy.  s.y must hold the
-// node state.
+// Vector-Jacobian product of the readout: from dE/dD (LDS row ``d``, scaled
+// in place to dE/dD~) to dE/d(node state) in s.gy.  s.y must hold the node
+// state.
 template <class P>
-__device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
-                                 const float* __restrict__ dD) {
+__device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md, const float* cpl, float* d) {
   const int lane = lane_of();
   float M0, M1;
-  readout_intermediates<P>(s, md, &M0, &M1);
-  for (int o = lane; o < P::DOUT; o += kWave) s.d[o] = dD[o] * md.inv_sigma[o];
+  readout_intermediates<P>(s, md, cpl, &M0, &M1);
+  for (int o = lane; o < P::DOUT; o += kWave) d[o] *= md.inv_sigma[o];
   wave_sync();
   // --- dE/dQ_eta (3x3, not symmetrised) from (1,1,2), quartic and (2,2,2)
   if (lane < P::K2 * 9) {
@@ -265,19 +295,19 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
     float acc = 0.0f;
     for (int k1 = 0; k1 < P::K1; ++k1)
       for (int k2 = k1; k2 < P::K1; ++k2) {
-        float jb = s.d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
+        float jb = d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
         float f = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2);
         acc += jb * f * s.z1[a * P::K1 + k1] * s.z1[b * P::K1 + k2];
       }
     for (int k = 0; k < P::K1; ++k) {
-      float pb = s.d[P::oPi + eta * P::K1 + k];
+      float pb = d[P::oPi + eta * P::K1 + k];
       acc += 2.0f * pb * s.qv[eta][k][a] * s.z1[b * P::K1 + k];
     }
     for (int t = 0; t < P::n222; ++t) {
       int ia, ib, ic;
       float w;
       e222(t, &ia, &ib, &ic, &w);
-      float jb = s.d[P::o222 + t] * (-kSqrt12_35) * w;
+      float jb = d[P::o222 + t] * (-kSqrt12_35) * w;
       // d tr(A B C) / dA = (B C)^T, / dB = (C A)^T, / dC = (A B)^T
       if (ia == eta) {
         float v = 0.0f;
@@ -297,78 +327,74 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
     }
     s.gq[eta][a * 3 + b] = acc;
   }
-  // --- dE/dv (probe gradients of degree one) from (1,1,2) and the quartic
+  // --- dE/dv (probe gradients of degree one) from (1,1,2), the quartic and (1,2,3)
   for (int o = lane; o < 3 * P::K1; o += kWave) {
     int m = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
     for (int eta = 0; eta < P::K2; ++eta) {
       for (int kp = 0; kp < P::K1; ++kp) {
         int k1 = k < kp ? k : kp, k2 = k < kp ? kp : k;
-        float jb = s.d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
+        float jb = d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
         float f = -kInvSqrt5 * (k1 == k2 ? 2.0f : kSqrt2);
         acc += jb * f * s.qv[eta][kp][m];
       }
-      float pb = s.d[P::oPi + eta * P::K1 + k];
+      float pb = d[P::oPi + eta * P::K1 + k];
       float v = 0.0f;
       for (int b = 0; b < 3; ++b) v += s.q[eta][m * 3 + b] * s.qv[eta][k][b];
       acc += 2.0f * pb * v;
     }
     if constexpr (P::L >= 3) {
-      for (int e = 0; e < md.c123.n; ++e) {
-        const int* ix = md.c123.idx + 3 * e;
-        if (ix[0] != m) continue;
-        for (int k2 = 0; k2 < P::K2; ++k2)
-          acc += s.d[P::o123 + k * P::K2 + k2] * md.c123.val[e] * s.z2[ix[1] * P::K2 + k2] *
-                 s.xt3[ix[2]];
-      }
+      for (int k2 = 0; k2 < P::K2; ++k2) acc += d[P::o123 + k * P::K2 + k2] * s.u123[m * P::K2 + k2];
     }
     s.gz1[o] = acc;
   }
   if constexpr (P::L >= 3) {
-    if (lane < 7) {
-      int m = lane;
+    // Ubar[m1][k2] = sum_k1 Jbar123[k1][k2] Z1[m1][k1],  Vbar[m1] = sum_e Jbar233[e] Z2[m1][e]
+    if (lane >= 32 && lane < 32 + 3 * P::K2) {
+      const int o = lane - 32, m1 = o / P::K2, k2 = o % P::K2;
       float acc = 0.0f;
-      for (int e = 0; e < md.c123.n; ++e) {
-        const int* ix = md.c123.idx + 3 * e;
-        if (ix[2] != m) continue;
-        for (int k1 = 0; k1 < P::K1; ++k1)
-          for (int k2 = 0; k2 < P::K2; ++k2)
-            acc += s.d[P::o123 + k1 * P::K2 + k2] * md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] *
-                   s.z2[ix[1] * P::K2 + k2];
-      }
-      for (int e = 0; e < md.c233.n; ++e) {
-        const int* ix = md.c233.idx + 3 * e;
-        for (int eta = 0; eta < P::K2; ++eta) {
-          float base = s.d[P::o233 + eta] * md.c233.val[e] * s.z2[ix[0] * P::K2 + eta];
-          if (ix[1] == m) acc += base * s.xt3[ix[2]];
-          if (ix[2] == m) acc += base * s.xt3[ix[1]];
-        }
-      }
-      s.gz3[m] = acc;
+      for (int k1 = 0; k1 < P::K1; ++k1) acc += d[P::o123 + k1 * P::K2 + k2] * s.z1[m1 * P::K1 + k1];
+      s.ub123[o] = acc;
+    } else if (lane >= 48 && lane < 53) {
+      const int m1 = lane - 48;
+      float acc = 0.0f;
+      for (int eta = 0; eta < P::K2; ++eta) acc += d[P::o233 + eta] * s.z2[m1 * P::K2 + eta];
+      s.vb233[m1] = acc;
     }
   }
   wave_sync();
-  // --- dE/dz2 = E_m : dE/dQ + generic couplings
+  if constexpr (P::L >= 3) {
+    // Tbar[m1][m2] = sum_k2 Ubar[m1][k2] Z2[m2][k2]
+    if (lane >= 32 && lane < 47) {
+      const int o = lane - 32, m1 = o / 5, m2 = o % 5;
+      float acc = 0.0f;
+      for (int k2 = 0; k2 < P::K2; ++k2) acc += s.ub123[m1 * P::K2 + k2] * s.z2[m2 * P::K2 + k2];
+      s.tb123[o] = acc;
+    }
+  }
+  // --- dE/dz2 = E_m : dE/dQ + the generic couplings
   if (lane < 5 * P::K2) {
     int m = lane / P::K2, eta = lane % P::K2;
     float acc = stf_adjoint(s.gq[eta], m);
     if constexpr (P::L >= 3) {
-      for (int e = 0; e < md.c123.n; ++e) {
-        const int* ix = md.c123.idx + 3 * e;
-        if (ix[1] != m) continue;
-        for (int k1 = 0; k1 < P::K1; ++k1)
-          acc += s.d[P::o123 + k1 * P::K2 + eta] * md.c123.val[e] * s.z1[ix[0] * P::K1 + k1] *
-                 s.xt3[ix[2]];
-      }
-      for (int e = 0; e < md.c233.n; ++e) {
-        const int* ix = md.c233.idx + 3 * e;
-        if (ix[0] != m) continue;
-        acc += s.d[P::o233 + eta] * md.c233.val[e] * s.xt3[ix[1]] * s.xt3[ix[2]];
-      }
+#pragma unroll
+      for (int m1 = 0; m1 < 3; ++m1) acc += s.ub123[m1 * P::K2 + eta] * s.t123[m1 * 5 + m];
+      acc += d[P::o233 + eta] * s.v233[m];
     }
     s.gz2[lane] = acc;
   }
   wave_sync();
+  if constexpr (P::L >= 3) {
+    // dE/dz3[m] = sum_{m1,m2} Tbar[m1][m2] C123[m1][m2][m] + 2 sum_m1 Vbar[m1] W[m1][m]
+    if (lane < 7) {
+      const int m = lane;
+      float acc = 0.0f;
+      for (int o = 0; o < 15; ++o) acc += s.tb123[o] * cpl[7 * o + m];
+      for (int m1 = 0; m1 < 5; ++m1) acc += 2.0f * s.vb233[m1] * s.w233[m1 * 7 + m];
+      s.gz3[m] = acc;
+    }
+    wave_sync();
+  }
   // --- dE/dX~ from the Gram blocks and the probes
   constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
   for (int o = lane; o < n1 + n2 + n3; o += kWave) {
@@ -377,7 +403,7 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
       float acc = 0.0f;
       for (int cp = 0; cp < P::C1; ++cp) {
         int a = c < cp ? c : cp, b = c < cp ? cp : c;
-        float gb = s.d[P::oG1 + tri_index(a, b, P::C1)];
+        float gb = d[P::oG1 + tri_index(a, b, P::C1)];
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt1[m * P::C1 + cp];
       }
       if constexpr (P::kHasA1) {
@@ -391,14 +417,14 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
       float acc = 0.0f;
       for (int cp = 0; cp < P::C2; ++cp) {
         int a = c < cp ? c : cp, b = c < cp ? cp : c;
-        float gb = s.d[P::oG2 + tri_index(a, b, P::C2)];
+        float gb = d[P::oG2 + tri_index(a, b, P::C2)];
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt2[m * P::C2 + cp];
       }
       for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * md.A2[c * P::K2 + k];
       s.gxt2[t] = acc;
     } else {
       int m = o - n1 - n2;
-      s.gxt3[m] = 2.0f * s.d[P::oG3] * s.xt3[m] + s.gz3[m];
+      s.gxt3[m] = 2.0f * d[P::oG3] * s.xt3[m] + s.gz3[m];
     }
   }
   wave_sync();
@@ -406,7 +432,7 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
   const float i0 = 1.0f / M0, i1 = 1.0f / M1;
   float part0 = 0.0f, part1 = 0.0f;   // sum Xbar * Y per normaliser
   for (int c = lane; c < P::C0; c += kWave) {
-    float xb = s.d[P::oX + c];
+    float xb = d[P::oX + c];
     s.gy[P::Y0 + c] = xb * i0;
     part0 += xb * s.y[P::Y0 + c];
   }
@@ -434,8 +460,8 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md,
   part0 = wave_sum(part0);
   part1 = wave_sum(part1);
   if (lane == 0) {
-    float mb0 = s.d[P::oM0] - part0 * i0 * i0;
-    float mb1 = s.d[P::oM1] - part1 * i1 * i1;
+    float mb0 = d[P::oM0] - part0 * i0 * i0;
+    float mb1 = d[P::oM1] - part1 * i1 * i1;
     s.gy[0] = mb0 * 0.5f * i0;   // M0 = sqrt(1/4 + S0)
     s.gy[1] = mb1 * 0.5f * i1;
   }
