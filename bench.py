@@ -62,8 +62,9 @@ def stage_work(name, spec, n_atoms, n_edges, n_skin):
         channel), psi and psi' (2(1+R) FMA per channel), two channel
         contractions per accumulated entry (2 FMA each) and the angular
         gradient (3 FMA per entry of degree >= 1)
-      MLP                  - matrix cores: forward and input-gradient
-        products, 2 x 2 (D_out F + (L-1) F^2) flop per atom
+      per-atom kernel      - matrix cores: forward and input-gradient
+        products of the MLP, 2 x 2 (D_out F + (L-1) F^2) flop per atom (the
+        readout and its VJP add ~1% VALU work, not counted)
       forces               - HBM: per edge 16 B gradient + 16 B gathered
         reverse gradient + 4 B reverse index, 24 B per atom out
     """
@@ -81,11 +82,55 @@ def stage_work(name, spec, n_atoms, n_edges, n_skin):
         return "alu", per_edge * n_edges, "flop"
     if name in ("mlp_forward", "mlp_backward"):
         return "mfma", 2 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
+    if name == "atoms":
+        # per-atom kernel: forward and input-gradient products of the MLP
+        return "mfma", 4 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "forces":
         return "hbm", 36 * n_edges + 24 * n_atoms, "byte"
     if name == "compact":
         return "hbm", 8 * n_skin + 16 * n_edges + 24 * n_atoms, "byte"
     return None
+
+
+# kernel behind each timed stage and the sources it is compiled from
+STAGE_KERNELS = {
+    "atoms": ("atom_kernel", "mlp_fused.hip"),
+    "forward": ("forward_kernel", "forward.hip"),
+    "backward": ("backward_kernel", "backward.hip"),
+    "forces": ("forces_kernel", "assemble.hip"),
+    "compact": ("compact_kernel", "neighbors.hip"),
+}
+
+
+def kernel_source_hash(stage):
+    """sha256 over the kernel's .hip file and every header it can include."""
+    import hashlib
+    csrc = os.path.join(HERE, "paper_2608_19041_amd", "csrc")
+    files = [STAGE_KERNELS[stage][1]] + sorted(f for f in os.listdir(csrc) if f.endswith(".h"))
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(stage, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None when there is none or the kernel's sources changed since."""
+    if stage not in STAGE_KERNELS:
+        return None
+    path = os.path.join(HERE, "profiles", f"traffic_{STAGE_KERNELS[stage][0]}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != kernel_source_hash(stage):
+        return None
+    return float(kv["traffic_bytes_per_dispatch"])
 
 
 def cpu_baseline(spec, weights, system, budget_s=15.0):
@@ -115,7 +160,8 @@ def cpu_baseline(spec, weights, system, budget_s=15.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: the workload's own step count)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="fcc4000_full", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -133,7 +179,9 @@ def main():
     import synth
 
     dev = torch.device("cuda", 0)
-    system, model_name, temp, dt, _, rebuild_every = synth.make_workload(args.workload)
+    system, model_name, temp, dt, wl_steps, rebuild_every = synth.make_workload(args.workload)
+    if args.steps is None:
+        args.steps = wl_steps
     spec, weights = synth.model_weights(model_name)
     model = dp.Model(synth.pack_blob(spec, weights))
     pos = torch.tensor(system.pos, dtype=torch.float64, device=dev)
@@ -164,6 +212,7 @@ def main():
     t1 = time.perf_counter()
     stages = model.timings()
     model.set_timing(False)
+    free_b, total_b = torch.cuda.mem_get_info(dev)
 
     wall = t1 - t0
     steps_per_s = args.steps / wall
@@ -189,8 +238,9 @@ def main():
             achieved = amount / avg_s / 1e9
             peak = PEAK_HBM_GBS
             u = "GB/s"
-        roof = {"bound": bound, "kernel": dominant, "achieved": round(achieved, 3), "peak": peak,
-                "unit": u, "frac": round(achieved / peak, 4), "traffic": None,
+        roof = {"bound": bound, "stage": dominant, "kernel": STAGE_KERNELS.get(dominant, ("?",))[0], "achieved": round(achieved, 3), "peak": peak,
+                "unit": u, "frac": round(achieved / peak, 4),
+                "traffic": measured_traffic(dominant, args.workload),
                 "avg_launch_ms": round(avg_s * 1e3, 5),
                 "work_per_launch": amount}
     out = {
@@ -213,6 +263,7 @@ def main():
         "nve_drift_ev_per_atom_ps": drift,
         "neighbor_rebuilds": nreb,
         "stage_ms_per_step": {k: round(v / args.steps, 5) for k, v in stage_ms.items()},
+        "hbm_in_use_gb": round((total_b - free_b) / 1e9, 3),
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -97,15 +97,13 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
   __shared__ float As[kRows * LDA];
   __shared__ float epart[kWavesPB][kRows];
   __shared__ ReadoutLds<P> rl_all[kWavesPB];
-  __shared__ float cpl[P::L >= 3 ? kCouplings : 1];
+  __shared__ ReadoutParams<P> rp;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col_in = lane & 15, rgrp = lane >> 4;   // output element: row 4*rgrp + r
   const int nt = (FT - wave + kWavesPB - 1) / kWavesPB;
   ReadoutLds<P>& rl = rl_all[wave];
-  if constexpr (P::L >= 3) {
-    for (int t = threadIdx.x; t < kCouplings; t += kThreads) cpl[t] = md.cpl[t];
-    __syncthreads();
-  }
+  stage_readout_params<P>(rp, md, threadIdx.x, kThreads);
+  __syncthreads();
 
   for (int64_t tile = blockIdx.x; tile * kRows < n; tile += gridDim.x) {
     const int64_t row0 = tile * kRows;
@@ -118,7 +116,8 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
         const float* ny = node + size_t(i) * P::NS;
         for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
         wave_sync();
-        readout_forward<P>(rl, md, cpl, clamp_type(species[i], md.n_types1), drow);
+        readout_forward<P>(rl, rp, md.type_embed + size_t(clamp_type(species[i], md.n_types1)) * P::C0,
+                           drow);
         if (desc_out)
           for (int t = lane; t < P::DOUT; t += 64) desc_out[size_t(i) * P::DOUT + t] = drow[t];
       } else {
@@ -240,7 +239,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       const float* ny = node + size_t(i) * P::NS;
       for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
       wave_sync();
-      readout_backward<P>(rl, md, cpl, As + r * LDA);
+      readout_backward<P>(rl, rp, As + r * LDA);
       float* gout = node_grad + size_t(i) * P::NS;
       for (int t = lane; t < P::NS; t += 64) gout[t] = rl.gy[t];
       wave_sync();

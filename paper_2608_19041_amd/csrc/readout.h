@@ -10,14 +10,48 @@
 // contract the dense coupling tensors one index at a time:
 //   J123[k1][k2] = sum_m1 Z1[m1][k1] U[m1][k2],  U = T Z2,  T[m1][m2] = sum_m3 C123 Z3
 //   J233[e]      = sum_m1 Z2[m1][e] V[m1],       V = W Z3,  W[m1][m2] = sum_m3 C233 Z3
-// The couplings (``cpl``: C123 [3][5][7] then C233 [5][7][7], the latter
-// symmetric in its last two indices) are read from LDS staged by the caller.
+// The couplings (C123 [3][5][7] then C233 [5][7][7], the latter symmetric in
+// its last two indices) and the other readout parameters are read from a
+// ReadoutParams block staged in LDS by the caller.  The two entry points are
+// not inlined: they get their own register allocation instead of adding to
+// the pressure of the MLP code around their call sites.
 #pragma once
 
 #include "common.h"
 #include "edge_math.h"
 
 namespace dpa4c {
+
+// Readout parameters staged once per workgroup into LDS (the readout reads
+// each of them many times per atom).
+template <class P>
+struct ReadoutParams {
+  float W1[P::C1 * P::C1];                 // alignment, degree 1 (I + W applied in-kernel)
+  float W2[P::C2 * P::C2];
+  float A1[P::kHasA1 ? P::C1 * P::K1 : 1]; // probes, degree 1 (identity when K1 = C1)
+  float A2[P::C2 * P::K2];
+  float mu[P::DSTR];                       // calibration, zero padded
+  float inv_sigma[P::DSTR];
+  float cpl[P::L >= 3 ? kCouplings : 1];   // C123 then C233
+};
+
+// Cooperative copy of the readout parameters by the ``nthreads`` threads of
+// a workgroup; the caller synchronises afterwards.
+template <class P>
+__device__ void stage_readout_params(ReadoutParams<P>& rp, const ModelDev& md, int tid,
+                                     int nthreads) {
+  for (int t = tid; t < P::C1 * P::C1; t += nthreads) rp.W1[t] = md.W1[t];
+  for (int t = tid; t < P::C2 * P::C2; t += nthreads) rp.W2[t] = md.W2[t];
+  if constexpr (P::kHasA1)
+    for (int t = tid; t < P::C1 * P::K1; t += nthreads) rp.A1[t] = md.A1[t];
+  for (int t = tid; t < P::C2 * P::K2; t += nthreads) rp.A2[t] = md.A2[t];
+  for (int t = tid; t < P::DSTR; t += nthreads) {
+    rp.mu[t] = t < P::DOUT ? md.mu[t] : 0.0f;
+    rp.inv_sigma[t] = t < P::DOUT ? md.inv_sigma[t] : 0.0f;
+  }
+  if constexpr (P::L >= 3)
+    for (int t = tid; t < kCouplings; t += nthreads) rp.cpl[t] = md.cpl[t];
+}
 
 template <class P>
 struct ReadoutLds {
@@ -103,8 +137,9 @@ __device__ inline float wave_sum(float v) {
 // Forward intermediates from s.y: M, aligned features, probes, Q, Qv and the
 // partial contractions T, U, W, V of the generic couplings.
 template <class P>
-__device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
-                                      const float* __restrict__ cpl, float* M0, float* M1) {
+__device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutParams<P>& rp,
+                                             float* M0, float* M1) {
+  const float* __restrict__ cpl = rp.cpl;
   const int lane = lane_of();
   const float m0 = sqrtf(0.25f + s.y[0]);
   const float m1 = sqrtf(0.25f + s.y[1]);
@@ -117,13 +152,13 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
       int m = o / P::C1, cp = o % P::C1;
       const float* x = s.y + P::Y1 + m * P::C1;
       float acc = x[cp];
-      for (int c = 0; c < P::C1; ++c) acc += x[c] * md.W1[c * P::C1 + cp];
+      for (int c = 0; c < P::C1; ++c) acc += x[c] * rp.W1[c * P::C1 + cp];
       s.xt1[o] = acc * i1;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, cp = t % P::C2;
       const float* x = s.y + P::Y2 + m * P::C2;
       float acc = x[cp];
-      for (int c = 0; c < P::C2; ++c) acc += x[c] * md.W2[c * P::C2 + cp];
+      for (int c = 0; c < P::C2; ++c) acc += x[c] * rp.W2[c * P::C2 + cp];
       s.xt2[t] = acc * i1;
     } else {
       int m = o - n1 - n2;
@@ -137,7 +172,7 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
       float acc;
       if constexpr (P::kHasA1) {
         acc = 0.0f;
-        for (int c = 0; c < P::C1; ++c) acc += s.xt1[m * P::C1 + c] * md.A1[c * P::K1 + k];
+        for (int c = 0; c < P::C1; ++c) acc += s.xt1[m * P::C1 + c] * rp.A1[c * P::K1 + k];
       } else {
         acc = s.xt1[m * P::C1 + k];
       }
@@ -145,7 +180,7 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
     } else {
       int t = o - 3 * P::K1, m = t / P::K2, k = t % P::K2;
       float acc = 0.0f;
-      for (int c = 0; c < P::C2; ++c) acc += s.xt2[m * P::C2 + c] * md.A2[c * P::K2 + k];
+      for (int c = 0; c < P::C2; ++c) acc += s.xt2[m * P::C2 + c] * rp.A2[c * P::K2 + k];
       s.z2[t] = acc;
     }
   }
@@ -191,18 +226,19 @@ __device__ void readout_intermediates(ReadoutLds<P>& s, const ModelDev& md,
   wave_sync();
 }
 
-// Eqs. (gram) .. (calibration): writes the calibrated descriptor of atom
-// type ``ai`` to the LDS row ``d`` (P::DSTR entries, zero padded).  s.y must
-// hold the node state.
+// Eqs. (gram) .. (calibration): writes the calibrated descriptor to the LDS
+// row ``d`` (P::DSTR entries, zero padded).  s.y must hold the node state and
+// ``x0`` is the atom's row of the type table (Eq. (init-features)).
 template <class P>
-__device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, const float* cpl, int ai,
-                                float* d) {
+__device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
+                                                          const ReadoutParams<P>& rp,
+                                                          const float* __restrict__ x0, float* d) {
   const int lane = lane_of();
   float M0, M1;
-  readout_intermediates<P>(s, md, cpl, &M0, &M1);
+  readout_intermediates<P>(s, rp, &M0, &M1);
   const float i0 = 1.0f / M0;
   for (int c = lane; c < P::C0; c += kWave) {
-    d[P::oX0 + c] = md.type_embed[ai * P::C0 + c];
+    d[P::oX0 + c] = x0[c];
     d[P::oX + c] = s.y[P::Y0 + c] * i0;
   }
   if (lane == 0) {
@@ -275,7 +311,7 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, const floa
   }
   wave_sync();
   for (int o = lane; o < P::DSTR; o += kWave)
-    d[o] = o < P::DOUT ? (d[o] - md.mu[o]) * md.inv_sigma[o] : 0.0f;
+    d[o] = o < P::DOUT ? (d[o] - rp.mu[o]) * rp.inv_sigma[o] : 0.0f;
   wave_sync();
 }
 
@@ -283,11 +319,13 @@ __device__ void readout_forward(ReadoutLds<P>& s, const ModelDev& md, const floa
 // in place to dE/dD~) to dE/d(node state) in s.gy.  s.y must hold the node
 // state.
 template <class P>
-__device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md, const float* cpl, float* d) {
+__device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
+                                                           const ReadoutParams<P>& rp, float* d) {
   const int lane = lane_of();
+  const float* __restrict__ cpl = rp.cpl;
   float M0, M1;
-  readout_intermediates<P>(s, md, cpl, &M0, &M1);
-  for (int o = lane; o < P::DOUT; o += kWave) d[o] *= md.inv_sigma[o];
+  readout_intermediates<P>(s, rp, &M0, &M1);
+  for (int o = lane; o < P::DOUT; o += kWave) d[o] *= rp.inv_sigma[o];
   wave_sync();
   // --- dE/dQ_eta (3x3, not symmetrised) from (1,1,2), quartic and (2,2,2)
   if (lane < P::K2 * 9) {
@@ -407,7 +445,7 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md, const flo
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt1[m * P::C1 + cp];
       }
       if constexpr (P::kHasA1) {
-        for (int k = 0; k < P::K1; ++k) acc += s.gz1[m * P::K1 + k] * md.A1[c * P::K1 + k];
+        for (int k = 0; k < P::K1; ++k) acc += s.gz1[m * P::K1 + k] * rp.A1[c * P::K1 + k];
       } else {
         acc += s.gz1[m * P::K1 + c];
       }
@@ -420,7 +458,7 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md, const flo
         float gb = d[P::oG2 + tri_index(a, b, P::C2)];
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt2[m * P::C2 + cp];
       }
-      for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * md.A2[c * P::K2 + k];
+      for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * rp.A2[c * P::K2 + k];
       s.gxt2[t] = acc;
     } else {
       int m = o - n1 - n2;
@@ -442,12 +480,12 @@ __device__ void readout_backward(ReadoutLds<P>& s, const ModelDev& md, const flo
     if (o < n1) {
       int m = o / P::C1, c = o % P::C1;
       xb = s.gxt1[o];
-      for (int cp = 0; cp < P::C1; ++cp) xb += s.gxt1[m * P::C1 + cp] * md.W1[c * P::C1 + cp];
+      for (int cp = 0; cp < P::C1; ++cp) xb += s.gxt1[m * P::C1 + cp] * rp.W1[c * P::C1 + cp];
       yi = P::Y1 + o;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, c = t % P::C2;
       xb = s.gxt2[t];
-      for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * md.W2[c * P::C2 + cp];
+      for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * rp.W2[c * P::C2 + cp];
       yi = P::Y2 + t;
     } else {
       int m = o - n1 - n2;
