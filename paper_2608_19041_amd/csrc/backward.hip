@@ -77,12 +77,28 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
     const float* pair_base = md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
+    // Two-stage software pipeline, as in the forward kernel: the record of
+    // round r+2 and the neighbour species of round r+1 are requested while
+    // round r computes.  Records are read only inside [0, cnt) of the row.
+    const float4* erow = edge + b;
+    float4 rec_n = make_float4(0.f, 0.f, 0.f, 0.f), rec_nn = rec_n;
+    int aj_n = ai;
+    if (cnt > 0) {
+      rec_n = erow[grp < cnt ? grp : 0];
+      aj_n = grp < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+      if (G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
+    }
     for (int base = 0; base < cnt; base += G) {
       const int el = base + grp;
       const bool valid = el < cnt;
-      const float4 rec = edge[b + (valid ? el : 0)];
-      const int j = __float_as_int(rec.w);
-      const int aj = clamp_type(species[valid ? j : i], T1);
+      const float4 rec = rec_n;
+      const int aj = aj_n;
+      if (base + G < cnt) {
+        const int el1 = el + G, el2 = el + 2 * G;
+        rec_n = rec_nn;
+        aj_n = el1 < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+        if (base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
+      }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
       float chi, dchi;
       envelope(g.rho, md.r_c, &chi, &dchi);

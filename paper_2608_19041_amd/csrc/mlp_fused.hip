@@ -33,40 +33,56 @@ constexpr int kWavesPB = kThreads / 64;
 
 __device__ inline float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
-// acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for up to
-// MAXT output tiles first, first + stride, ... (nt of them, wave-uniform).
+// acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for the
+// output tiles first + t * stride, t < MAXT.  Tiles past ``ntiles`` repeat
+// the last tile (their results are discarded by the caller), so every wave
+// runs the same straight-line code.  The B fragments of k-block kb+1 and the
+// A fragment are requested one k-block ahead (ping-pong registers), and the
+// MFMAs of one k-block are interleaved across tiles so that consecutive
+// instructions do not depend on each other.
 template <int MAXT>
 __device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int lda, int kblocks,
-                                  const float4* __restrict__ Wf, int first, int stride, int nt,
+                                  const float4* __restrict__ Wf, int first, int stride, int ntiles,
                                   int lane) {
-  const int arow = lane & 15, aq = lane >> 4;
-  const float4* wp = Wf + lane;
-  float4 b[MAXT];
+  const float* ap = As + (lane & 15) * lda + (lane >> 4) * 4;
+  const float4* wp[MAXT];
 #pragma unroll
-  for (int t = 0; t < MAXT; ++t)
-    if (t < nt) b[t] = wp[size_t(first + t * stride) * kblocks * 64];
-#pragma unroll 1
-  for (int kb = 0; kb < kblocks; ++kb) {
-    float4 nb[MAXT];
-    const bool more = kb + 1 < kblocks;
-#pragma unroll
-    for (int t = 0; t < MAXT; ++t)
-      if (more && t < nt) nb[t] = wp[(size_t(first + t * stride) * kblocks + kb + 1) * 64];
-    const float4 a = *reinterpret_cast<const float4*>(As + arow * lda + kb * 16 + aq * 4);
-#pragma unroll
-    for (int t = 0; t < MAXT; ++t) {
-      if (t < nt) {
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[t].x, acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[t].y, acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[t].z, acc[t], 0, 0, 0);
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
-      }
-    }
-    if (more) {
-#pragma unroll
-      for (int t = 0; t < MAXT; ++t) b[t] = nb[t];
-    }
+  for (int t = 0; t < MAXT; ++t) {
+    const int T = first + t * stride < ntiles ? first + t * stride : ntiles - 1;
+    wp[t] = Wf + size_t(T) * kblocks * 64 + lane;
   }
+  auto step = [&](const float4& a, const float4* b) {
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[t].x, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[t].y, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[t].z, acc[t], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
+  };
+  float4 b0[MAXT], b1[MAXT];
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t) b0[t] = wp[t][0];
+  float4 a0 = *reinterpret_cast<const float4*>(ap);
+  int kb = 0;
+#pragma unroll 1
+  for (; kb + 2 <= kblocks; kb += 2) {
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) b1[t] = wp[t][size_t(kb + 1) * 64];
+    const float4 a1 = *reinterpret_cast<const float4*>(ap + (kb + 1) * 16);
+    __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of the MFMAs
+    step(a0, b0);
+    // unconditional (clamped) so that the loop body is straight-line code
+    // and the wait counts do not have to cover a skipped prefetch
+    const int kn = kb + 2 < kblocks ? kb + 2 : kblocks - 1;
+#pragma unroll
+    for (int t = 0; t < MAXT; ++t) b0[t] = wp[t][size_t(kn) * 64];
+    a0 = *reinterpret_cast<const float4*>(ap + kn * 16);
+    __builtin_amdgcn_sched_barrier(0);
+    step(a1, b1);
+  }
+  if (kb < kblocks) step(a0, b0);   // odd number of k-blocks
 }
 
 struct MlpArgs {
@@ -96,34 +112,39 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
   constexpr int APW = kRows / kWavesPB;               // atoms per wave in the readouts
   __shared__ float As[kRows * LDA];
   __shared__ float epart[kWavesPB][kRows];
-  __shared__ ReadoutLds<P> rl_all[kWavesPB];
+  __shared__ ReadoutLds<P> rl_all[kRows];   // one per atom of the tile
   __shared__ ReadoutParams<P> rp;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col_in = lane & 15, rgrp = lane >> 4;   // output element: row 4*rgrp + r
   const int nt = (FT - wave + kWavesPB - 1) / kWavesPB;
-  ReadoutLds<P>& rl = rl_all[wave];
+  static_assert(APW == 2, "a wave reads out two atoms, one per half");
+  const int half = lane >> 5, hl = lane & 31;
+  const int ra = wave * APW + half;         // tile row of this half-wave's atom
+  // the same objects seen through LDS-address-space pointers (C-style casts:
+  // an address-space conversion)
+  DPA4C_LDS ReadoutLds<P>& rl = *(DPA4C_LDS ReadoutLds<P>*)(&rl_all[ra]);
+  const DPA4C_LDS ReadoutParams<P>& rpl = *(DPA4C_LDS ReadoutParams<P>*)(&rp);
+  DPA4C_LDS float* arow = (DPA4C_LDS float*)(As + ra * LDA);
   stage_readout_params<P>(rp, md, threadIdx.x, kThreads);
   __syncthreads();
 
   for (int64_t tile = blockIdx.x; tile * kRows < n; tile += gridDim.x) {
     const int64_t row0 = tile * kRows;
-    // ---- readout of the tile's atoms: D rows into LDS
-    for (int a = 0; a < APW; ++a) {
-      const int r = wave * APW + a;
-      const int64_t i = row0 + r;
-      float* drow = As + r * LDA;
-      if (i < n) {
-        const float* ny = node + size_t(i) * P::NS;
-        for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
-        wave_sync();
-        readout_forward<P>(rl, rp, md.type_embed + size_t(clamp_type(species[i], md.n_types1)) * P::C0,
-                           drow);
-        if (desc_out)
-          for (int t = lane; t < P::DOUT; t += 64) desc_out[size_t(i) * P::DOUT + t] = drow[t];
-      } else {
-        for (int t = lane; t < KP; t += 64) drow[t] = 0.0f;
-      }
+    // ---- readout of the tile's atoms: D rows into LDS (rows past n get
+    // a zero node state and are zeroed afterwards)
+    {
+      const int64_t i = row0 + ra;
+      const bool ok = i < n;
+      const float* ny = node + size_t(ok ? i : 0) * P::NS;
+      for (int t = hl; t < P::NS; t += kHalf) rl.y[t] = ok ? ny[t] : 0.0f;
+      const float* x0 =
+          md.type_embed + size_t(ok ? clamp_type(species[i], md.n_types1) : 0) * P::C0;
       wave_sync();
+      readout_forward<P>(rl, rpl, x0, arow);
+      if (ok && desc_out)
+        for (int t = hl; t < P::DOUT; t += kHalf) desc_out[size_t(i) * P::DOUT + t] = arow[t];
+      if (!ok)
+        for (int t = hl; t < KP; t += kHalf) arow[t] = 0.0f;
     }
     __syncthreads();
 
@@ -134,7 +155,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, p.W[layer], wave, kWavesPB, nt,
+      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, p.W[layer], wave, kWavesPB, FT,
                      lane);
       __syncthreads();   // everyone has read the A tile
 #pragma unroll
@@ -200,7 +221,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NT>(acc, As, LDA, F / 16, p.WT[layer], wave, kWavesPB, nt, lane);
+      mfma_tiles<NT>(acc, As, LDA, F / 16, p.WT[layer], wave, kWavesPB, FT, lane);
       __syncthreads();
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
@@ -220,7 +241,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       v4f acc[NTD];
 #pragma unroll
       for (int t = 0; t < NTD; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NTD>(acc, As, LDA, F / 16, p.WT[0], wave, kWavesPB, ntd, lane);
+      mfma_tiles<NTD>(acc, As, LDA, F / 16, p.WT[0], wave, kWavesPB, DT, lane);
       __syncthreads();
 #pragma unroll
       for (int t = 0; t < NTD; ++t) {
@@ -231,18 +252,15 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       }
       __syncthreads();
     }
-    // ---- readout VJP: dE/d(node state) of the tile's atoms
-    for (int a = 0; a < APW; ++a) {
-      const int r = wave * APW + a;
-      const int64_t i = row0 + r;
-      if (i >= n) continue;
-      const float* ny = node + size_t(i) * P::NS;
-      for (int t = lane; t < P::NS; t += 64) rl.y[t] = ny[t];
-      wave_sync();
-      readout_backward<P>(rl, rp, As + r * LDA);
-      float* gout = node_grad + size_t(i) * P::NS;
-      for (int t = lane; t < P::NS; t += 64) gout[t] = rl.gy[t];
-      wave_sync();
+    // ---- readout VJP: dE/d(node state) of the tile's atoms, from the
+    // forward intermediates still held in rl
+    {
+      const int64_t i = row0 + ra;
+      readout_backward<P>(rl, rpl, arow);
+      if (i < n) {
+        float* gout = node_grad + size_t(i) * P::NS;
+        for (int t = hl; t < P::NS; t += kHalf) gout[t] = rl.gy[t];
+      }
     }
     __syncthreads();
   }

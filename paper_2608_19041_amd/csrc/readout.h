@@ -1,7 +1,8 @@
 // Per-atom invariant readout (Methods "Nonlinear readout and atomic energy",
-// Eqs. (alignment) .. (calibration)) and its vector-Jacobian product, run by
-// one 64-lane wavefront per atom on a wave-private LDS block; the descriptor
-// row (D~, D or dE/dD) lives in a caller-provided LDS row.
+// Eqs. (alignment) .. (calibration)) and its vector-Jacobian product.  Half a
+// wavefront (32 lanes) serves one atom, so a wave reads out two atoms side by
+// side; each atom has its own LDS block, and the descriptor row (D~, D or
+// dE/dD) lives in a caller-provided LDS row.
 //
 // Each stage spreads its outputs over the lanes (gather form: every output is
 // computed by one lane from values written by the previous stage), so the
@@ -14,13 +15,18 @@
 // its last two indices) and the other readout parameters are read from a
 // ReadoutParams block staged in LDS by the caller.  The two entry points are
 // not inlined: they get their own register allocation instead of adding to
-// the pressure of the MLP code around their call sites.
+// the pressure of the MLP code around their call sites.  Their LDS arguments
+// carry the LDS address space, so every access is a ds_read / ds_write.
 #pragma once
 
 #include "common.h"
 #include "edge_math.h"
 
 namespace dpa4c {
+
+#define DPA4C_LDS __attribute__((address_space(3)))
+
+constexpr int kHalf = 32;   // lanes per atom
 
 // Readout parameters staged once per workgroup into LDS (the readout reads
 // each of them many times per atom).
@@ -95,7 +101,8 @@ __device__ inline void vech_pair(int t, int C, int* c, int* cp) {
 
 // STF(z) of Eq. (stf) in the basis order (xy, yz, z^2, xz, x^2 - y^2):
 // entry (a, b) of the symmetric trace-free matrix
-__device__ inline float stf_entry(const float* z, int stride, int a, int b) {
+template <class T>
+__device__ inline float stf_entry(const T* z, int stride, int a, int b) {
   float z0 = z[0], z1 = z[stride], z2 = z[2 * stride], z3 = z[3 * stride], z4 = z[4 * stride];
   if (a > b) { int t = a; a = b; b = t; }
   if (a == 0 && b == 0) return -z2 * kInvSqrt6 + z4 * kInvSqrt2;
@@ -106,7 +113,8 @@ __device__ inline float stf_entry(const float* z, int stride, int a, int b) {
   return z3 * kInvSqrt2;   // (0, 2)
 }
 // adjoint: dE/dz_m = E_m : Qbar for a (not necessarily symmetric) 3x3 Qbar
-__device__ inline float stf_adjoint(const float* g, int m) {
+template <class T>
+__device__ inline float stf_adjoint(const T* g, int m) {
   switch (m) {
     case 0: return (g[1] + g[3]) * kInvSqrt2;
     case 1: return (g[5] + g[7]) * kInvSqrt2;
@@ -128,35 +136,37 @@ __device__ inline void e222(int t, int* a, int* b, int* c, float* w) {
   *w = (t == 0 || t == 3) ? 1.0f : r3;
 }
 
-// fixed-order sum over the 64 lanes (butterfly; every lane gets the same bits)
-__device__ inline float wave_sum(float v) {
-  for (int off = 1; off < kWave; off <<= 1) v += __shfl_xor(v, off);
+// fixed-order sum over the 32 lanes of a half wave (butterfly; every lane of
+// the half gets the same bits)
+__device__ inline float half_sum(float v) {
+  for (int off = 1; off < kHalf; off <<= 1) v += __shfl_xor(v, off);
   return v;
 }
 
 // Forward intermediates from s.y: M, aligned features, probes, Q, Qv and the
 // partial contractions T, U, W, V of the generic couplings.
 template <class P>
-__device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutParams<P>& rp,
-                                             float* M0, float* M1) {
-  const float* __restrict__ cpl = rp.cpl;
-  const int lane = lane_of();
+__device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
+                                             const DPA4C_LDS ReadoutParams<P>& rp, float* M0,
+                                             float* M1) {
+  const DPA4C_LDS float* cpl = rp.cpl;
+  const int lane = lane_of() & (kHalf - 1);
   const float m0 = sqrtf(0.25f + s.y[0]);
   const float m1 = sqrtf(0.25f + s.y[1]);
   *M0 = m0;
   *M1 = m1;
   const float i1 = 1.0f / m1;
   constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
-  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
     if (o < n1) {
       int m = o / P::C1, cp = o % P::C1;
-      const float* x = s.y + P::Y1 + m * P::C1;
+      const DPA4C_LDS float* x = s.y + P::Y1 + m * P::C1;
       float acc = x[cp];
       for (int c = 0; c < P::C1; ++c) acc += x[c] * rp.W1[c * P::C1 + cp];
       s.xt1[o] = acc * i1;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, cp = t % P::C2;
-      const float* x = s.y + P::Y2 + m * P::C2;
+      const DPA4C_LDS float* x = s.y + P::Y2 + m * P::C2;
       float acc = x[cp];
       for (int c = 0; c < P::C2; ++c) acc += x[c] * rp.W2[c * P::C2 + cp];
       s.xt2[t] = acc * i1;
@@ -166,7 +176,7 @@ __device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutPara
     }
   }
   wave_sync();
-  for (int o = lane; o < 3 * P::K1 + 5 * P::K2; o += kWave) {
+  for (int o = lane; o < 3 * P::K1 + 5 * P::K2; o += kHalf) {
     if (o < 3 * P::K1) {
       int m = o / P::K1, k = o % P::K1;
       float acc;
@@ -186,13 +196,13 @@ __device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutPara
   }
   if constexpr (P::L >= 3) {
     // T[m1][m2] = sum_m3 C123 Z3 (15 entries), W[m1][m2] = sum_m3 C233 Z3 (35)
-    if (lane < 50) {
-      const float* c = cpl + 7 * lane;   // C233 follows C123 (15 rows of 7)
+    for (int o = lane; o < 50; o += kHalf) {
+      const DPA4C_LDS float* c = cpl + 7 * o;   // C233 follows C123 (15 rows of 7)
       float acc = 0.0f;
 #pragma unroll
       for (int m3 = 0; m3 < 7; ++m3) acc += c[m3] * s.xt3[m3];
-      if (lane < 15) s.t123[lane] = acc;
-      else s.w233[lane - 15] = acc;
+      if (o < 15) s.t123[o] = acc;
+      else s.w233[o - 15] = acc;
     }
   }
   wave_sync();
@@ -202,14 +212,15 @@ __device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutPara
   }
   if constexpr (P::L >= 3) {
     // U[m1][k2] = sum_m2 T[m1][m2] Z2[m2][k2],  V[m1] = sum_m2 W[m1][m2] Z3[m2]
-    if (lane >= 32 && lane < 32 + 3 * P::K2) {
-      const int o = lane - 32, m1 = o / P::K2, k2 = o % P::K2;
+    static_assert(P::K2 * 9 <= 18 && 3 * P::K2 <= 6, "lane plan of the readout");
+    if (lane >= 18 && lane < 18 + 3 * P::K2) {
+      const int o = lane - 18, m1 = o / P::K2, k2 = o % P::K2;
       float acc = 0.0f;
 #pragma unroll
       for (int m2 = 0; m2 < 5; ++m2) acc += s.t123[m1 * 5 + m2] * s.z2[m2 * P::K2 + k2];
       s.u123[o] = acc;
-    } else if (lane >= 48 && lane < 53) {
-      const int m1 = lane - 48;
+    } else if (lane >= 24 && lane < 29) {
+      const int m1 = lane - 24;
       float acc = 0.0f;
 #pragma unroll
       for (int m2 = 0; m2 < 7; ++m2) acc += s.w233[m1 * 7 + m2] * s.xt3[m2];
@@ -217,7 +228,7 @@ __device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutPara
     }
   }
   wave_sync();
-  for (int o = lane; o < P::K2 * P::K1 * 3; o += kWave) {
+  for (int o = lane; o < P::K2 * P::K1 * 3; o += kHalf) {
     int eta = o / (P::K1 * 3), k = (o / 3) % P::K1, a = o % 3;
     float acc = 0.0f;
     for (int b = 0; b < 3; ++b) acc += s.q[eta][a * 3 + b] * s.z1[b * P::K1 + k];
@@ -230,14 +241,15 @@ __device__ inline void readout_intermediates(ReadoutLds<P>& s, const ReadoutPara
 // row ``d`` (P::DSTR entries, zero padded).  s.y must hold the node state and
 // ``x0`` is the atom's row of the type table (Eq. (init-features)).
 template <class P>
-__device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
-                                                          const ReadoutParams<P>& rp,
-                                                          const float* __restrict__ x0, float* d) {
-  const int lane = lane_of();
+__device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P>& s,
+                                                          const DPA4C_LDS ReadoutParams<P>& rp,
+                                                          const float* __restrict__ x0,
+                                                          DPA4C_LDS float* d) {
+  const int lane = lane_of() & (kHalf - 1);
   float M0, M1;
   readout_intermediates<P>(s, rp, &M0, &M1);
   const float i0 = 1.0f / M0;
-  for (int c = lane; c < P::C0; c += kWave) {
+  for (int c = lane; c < P::C0; c += kHalf) {
     d[P::oX0 + c] = x0[c];
     d[P::oX + c] = s.y[P::Y0 + c] * i0;
   }
@@ -246,7 +258,7 @@ __device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
     d[P::oM1] = M1;
   }
   // Gram blocks, Eq. (gram), vech with sqrt(2) off the diagonal
-  for (int o = lane; o < P::nG1 + P::nG2 + P::nG3; o += kWave) {
+  for (int o = lane; o < P::nG1 + P::nG2 + P::nG3; o += kHalf) {
     float acc = 0.0f;
     if (o < P::nG1) {
       int c, cp;
@@ -264,7 +276,7 @@ __device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
     d[P::oG1 + o] = acc;
   }
   // (1,1,2): -(f/sqrt5) v_k1 . Q_eta v_k2, k1 <= k2
-  for (int o = lane; o < P::n112; o += kWave) {
+  for (int o = lane; o < P::n112; o += kHalf) {
     int eta = o % P::K2, pr = o / P::K2, k1, k2;
     vech_pair(pr, P::K1, &k1, &k2);
     float acc = 0.0f;
@@ -287,7 +299,7 @@ __device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
   }
   if constexpr (P::L >= 3) {
     // (1,2,3) and (2,3,3): last contraction of the factored couplings
-    for (int o = lane; o < P::n123 + P::n233; o += kWave) {
+    for (int o = lane; o < P::n123 + P::n233; o += kHalf) {
       float acc = 0.0f;
       if (o < P::n123) {
         const int k1 = o / P::K2, k2 = o % P::K2;
@@ -303,29 +315,31 @@ __device__ __attribute__((noinline)) void readout_forward(ReadoutLds<P>& s,
     }
   }
   // projected quartic, Eq. (quartic), eta-major
-  for (int o = lane; o < P::nPi; o += kWave) {
+  for (int o = lane; o < P::nPi; o += kHalf) {
     int eta = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
     for (int a = 0; a < 3; ++a) acc += s.qv[eta][k][a] * s.qv[eta][k][a];
     d[P::oPi + o] = acc;
   }
   wave_sync();
-  for (int o = lane; o < P::DSTR; o += kWave)
+  for (int o = lane; o < P::DSTR; o += kHalf)
     d[o] = o < P::DOUT ? (d[o] - rp.mu[o]) * rp.inv_sigma[o] : 0.0f;
   wave_sync();
 }
 
 // Vector-Jacobian product of the readout: from dE/dD (LDS row ``d``, scaled
-// in place to dE/dD~) to dE/d(node state) in s.gy.  s.y must hold the node
-// state.
+// in place to dE/dD~) to dE/d(node state) in s.gy.  ``s`` must still hold
+// what readout_forward left there for the same atom (node state and the
+// forward intermediates), which are reused rather than recomputed.
 template <class P>
-__device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
-                                                           const ReadoutParams<P>& rp, float* d) {
-  const int lane = lane_of();
-  const float* __restrict__ cpl = rp.cpl;
-  float M0, M1;
-  readout_intermediates<P>(s, rp, &M0, &M1);
-  for (int o = lane; o < P::DOUT; o += kWave) d[o] *= rp.inv_sigma[o];
+__device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<P>& s,
+                                                           const DPA4C_LDS ReadoutParams<P>& rp,
+                                                           DPA4C_LDS float* d) {
+  const int lane = lane_of() & (kHalf - 1);
+  const DPA4C_LDS float* cpl = rp.cpl;
+  const float M0 = sqrtf(0.25f + s.y[0]);
+  const float M1 = sqrtf(0.25f + s.y[1]);
+  for (int o = lane; o < P::DOUT; o += kHalf) d[o] *= rp.inv_sigma[o];
   wave_sync();
   // --- dE/dQ_eta (3x3, not symmetrised) from (1,1,2), quartic and (2,2,2)
   if (lane < P::K2 * 9) {
@@ -366,7 +380,7 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
     s.gq[eta][a * 3 + b] = acc;
   }
   // --- dE/dv (probe gradients of degree one) from (1,1,2), the quartic and (1,2,3)
-  for (int o = lane; o < 3 * P::K1; o += kWave) {
+  for (int o = lane; o < 3 * P::K1; o += kHalf) {
     int m = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
     for (int eta = 0; eta < P::K2; ++eta) {
@@ -388,13 +402,13 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
   }
   if constexpr (P::L >= 3) {
     // Ubar[m1][k2] = sum_k1 Jbar123[k1][k2] Z1[m1][k1],  Vbar[m1] = sum_e Jbar233[e] Z2[m1][e]
-    if (lane >= 32 && lane < 32 + 3 * P::K2) {
-      const int o = lane - 32, m1 = o / P::K2, k2 = o % P::K2;
+    if (lane >= 18 && lane < 18 + 3 * P::K2) {
+      const int o = lane - 18, m1 = o / P::K2, k2 = o % P::K2;
       float acc = 0.0f;
       for (int k1 = 0; k1 < P::K1; ++k1) acc += d[P::o123 + k1 * P::K2 + k2] * s.z1[m1 * P::K1 + k1];
       s.ub123[o] = acc;
-    } else if (lane >= 48 && lane < 53) {
-      const int m1 = lane - 48;
+    } else if (lane >= 24 && lane < 29) {
+      const int m1 = lane - 24;
       float acc = 0.0f;
       for (int eta = 0; eta < P::K2; ++eta) acc += d[P::o233 + eta] * s.z2[m1 * P::K2 + eta];
       s.vb233[m1] = acc;
@@ -403,8 +417,8 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
   wave_sync();
   if constexpr (P::L >= 3) {
     // Tbar[m1][m2] = sum_k2 Ubar[m1][k2] Z2[m2][k2]
-    if (lane >= 32 && lane < 47) {
-      const int o = lane - 32, m1 = o / 5, m2 = o % 5;
+    if (lane >= 16 && lane < 31) {
+      const int o = lane - 16, m1 = o / 5, m2 = o % 5;
       float acc = 0.0f;
       for (int k2 = 0; k2 < P::K2; ++k2) acc += s.ub123[m1 * P::K2 + k2] * s.z2[m2 * P::K2 + k2];
       s.tb123[o] = acc;
@@ -435,7 +449,7 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
   }
   // --- dE/dX~ from the Gram blocks and the probes
   constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
-  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
     if (o < n1) {
       int m = o / P::C1, c = o % P::C1;
       float acc = 0.0f;
@@ -469,12 +483,12 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
   // --- through the alignment (I + W) and the normalisation X = Y / M
   const float i0 = 1.0f / M0, i1 = 1.0f / M1;
   float part0 = 0.0f, part1 = 0.0f;   // sum Xbar * Y per normaliser
-  for (int c = lane; c < P::C0; c += kWave) {
+  for (int c = lane; c < P::C0; c += kHalf) {
     float xb = d[P::oX + c];
     s.gy[P::Y0 + c] = xb * i0;
     part0 += xb * s.y[P::Y0 + c];
   }
-  for (int o = lane; o < n1 + n2 + n3; o += kWave) {
+  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
     float xb;
     int yi;
     if (o < n1) {
@@ -495,8 +509,8 @@ __device__ __attribute__((noinline)) void readout_backward(ReadoutLds<P>& s,
     s.gy[yi] = xb * i1;
     part1 += xb * s.y[yi];
   }
-  part0 = wave_sum(part0);
-  part1 = wave_sum(part1);
+  part0 = half_sum(part0);
+  part1 = half_sum(part1);
   if (lane == 0) {
     float mb0 = d[P::oM0] - part0 * i0 * i0;
     float mb1 = d[P::oM1] - part1 * i1 * i1;
