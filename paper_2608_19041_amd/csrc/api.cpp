@@ -220,12 +220,13 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
                     &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.ekin_atom, &w.inv_mass, &w.mass,
-                    &w.eatom,
+                    &w.eatom,    &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
   for (DevBuf* b : bufs) b->release();
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
   if (w.host_flags) hipHostFree(w.host_flags);
+  if (w.fold_host) hipHostFree(w.fold_host);
   delete m;
 }
 
@@ -336,6 +337,8 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
     DPA4C_HIP_TRY(hipMemsetAsync(e_total, 0, sizeof(double), st));
     return 0;
   }
+  rc = prepare_species(mm, species, N, st);
+  if (rc) return rc;
   {
     StageScope t(m, kStSkinRev, st);
     rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), nullptr, st);
@@ -396,6 +399,8 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     DPA4C_HIP_TRY(hipMemcpyAsync(w.inv_mass.p, im.data(), 8 * T1, hipMemcpyHostToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(w.mass.p, mass_by_species, 8 * T1, hipMemcpyHostToDevice, st));
   }
+  rc = prepare_species(mm, species, N, st);
+  if (rc) return rc;
   int64_t* flags = w.flags.as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
 

@@ -31,9 +31,9 @@ namespace {
 
 constexpr int kTeam = 256;
 
-template <class P>
+template <class P, bool FOLD>
 __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
-                                                         const int32_t* __restrict__ species,
+                                                         const int32_t* __restrict__ typ,
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
                                                          const float4* __restrict__ edge,
@@ -46,9 +46,13 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
   const int k = tid % P::LPE;
   const int T1 = md.n_types1;
   const float inv_delta = md.inv_delta;
+  const int nf = md.fold_n;
+  // ``typ`` holds species (clamped here) or, with folded tables, the folded
+  // index of every atom
+  auto type_of = [&](int64_t a) { return FOLD ? typ[a] : clamp_type(typ[a], T1); };
 
   for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
-    const int ai = clamp_type(species[i], T1);
+    const int ai = type_of(i);
     const float* gyr = node_grad + size_t(i) * P::NS;
     // per-centre coefficients in the lane's channel layout
     float gy0[P::CPL];
@@ -76,7 +80,8 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
 
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
-    const float* pair_base = md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
+    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
+                                  : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
     // Two-stage software pipeline, as in the forward kernel: the record of
     // round r+2 and the neighbour species of round r+1 are requested while
     // round r computes.  Records are read only inside [0, cnt) of the row.
@@ -85,7 +90,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
     int aj_n = ai;
     if (cnt > 0) {
       rec_n = erow[grp < cnt ? grp : 0];
-      aj_n = grp < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+      aj_n = grp < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
       if (G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
     }
     for (int base = 0; base < cnt; base += G) {
@@ -96,7 +101,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       if (base + G < cnt) {
         const int el1 = el + G, el2 = el + 2 * G;
         rec_n = rec_nn;
-        aj_n = el1 < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+        aj_n = el1 < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
         if (base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
       }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
@@ -106,42 +111,60 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
       const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;
       const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
-      float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (P::R > 0) {
-        float c[6];
-        load6(md.qtab + (size_t(row) * P::R + (k < P::R ? k : 0)) * 6, c);
-        const float qk = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
-        const float dqk = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
-#pragma unroll
-        for (int mu = 0; mu < 4; ++mu) {
-          q[mu] = __shfl(qk, mu, P::LPE);
-          dq[mu] = __shfl(dqk, mu, P::LPE);
-        }
-      }
-      const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
-      const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
+      if constexpr (FOLD) {
+        // one quintic per channel from the table of the pair (a_i, a_j)
+        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * 6);
 #pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj) {
-        float c[6];
-        load6(gt + (jj * P::LPE + k) * 6, c);
-        const float gv = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
-        const float gd = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
-        const float* pp = pc + (jj * P::LPE + k) * P::PW;
-        const float2 gb = *reinterpret_cast<const float2*>(pp);
-        float psi = gb.x * gv + gb.y;
-        float dpsi = gb.x * gd;
-        if constexpr (P::R > 0) {
-          const float2 u01 = *reinterpret_cast<const float2*>(pp + 2);
-          const float2 u23 = *reinterpret_cast<const float2*>(pp + 4);
-          psi += u01.x * q[0] + u01.y * q[1] + u23.x * q[2] + u23.y * q[3];
-          dpsi += u01.x * dq[0] + u01.y * dq[1] + u23.x * dq[2] + u23.y * dq[3];
+        for (int jj = 0; jj < P::CPL; ++jj) {
+          float c[6];
+          load6(ft + (jj * P::LPE + k) * 6, c);
+          const float psi = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
+          const float dpsi = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+          a0 += gy0[jj] * psi;
+          b0 += gy0[jj] * dpsi;
+          if (jj == 0) {
+            psi0 = psi;
+            dpsi0 = dpsi;
+          }
         }
-        a0 += gy0[jj] * psi;
-        b0 += gy0[jj] * dpsi;
-        if (jj == 0) {
-          psi0 = psi;
-          dpsi0 = dpsi;
+      } else {
+        float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (P::R > 0) {
+          float c[6];
+          load6(md.qtab + (size_t(row) * P::R + (k < P::R ? k : 0)) * 6, c);
+          const float qk = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
+          const float dqk = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+#pragma unroll
+          for (int mu = 0; mu < 4; ++mu) {
+            q[mu] = __shfl(qk, mu, P::LPE);
+            dq[mu] = __shfl(dqk, mu, P::LPE);
+          }
+        }
+        const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
+        const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
+#pragma unroll
+        for (int jj = 0; jj < P::CPL; ++jj) {
+          float c[6];
+          load6(gt + (jj * P::LPE + k) * 6, c);
+          const float gv = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
+          const float gd = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+          const float* pp = pc + (jj * P::LPE + k) * P::PW;
+          const float2 gb = *reinterpret_cast<const float2*>(pp);
+          float psi = gb.x * gv + gb.y;
+          float dpsi = gb.x * gd;
+          if constexpr (P::R > 0) {
+            const float2 u01 = *reinterpret_cast<const float2*>(pp + 2);
+            const float2 u23 = *reinterpret_cast<const float2*>(pp + 4);
+            psi += u01.x * q[0] + u01.y * q[1] + u23.x * q[2] + u23.y * q[3];
+            dpsi += u01.x * dq[0] + u01.y * dq[1] + u23.x * dq[2] + u23.y * dq[3];
+          }
+          a0 += gy0[jj] * psi;
+          b0 += gy0[jj] * dpsi;
+          if (jj == 0) {
+            psi0 = psi;
+            dpsi0 = dpsi;
+          }
         }
       }
       // Q_k(u) and its gradient
@@ -192,8 +215,12 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
            hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
-  hipLaunchKernelGGL(backward_kernel<P>, dim3(blocks), dim3(kTeam), 0, st, m->dev(), n, species,
-                     row_ptr, ecount, edge, node_grad, grad);
+  if (m->fold_n > 0)
+    hipLaunchKernelGGL((backward_kernel<P, true>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
+                       m->ws.fidx.as<int32_t>(), row_ptr, ecount, edge, node_grad, grad);
+  else
+    hipLaunchKernelGGL((backward_kernel<P, false>), dim3(blocks), dim3(kTeam), 0, st, m->dev(),
+                       n, species, row_ptr, ecount, edge, node_grad, grad);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

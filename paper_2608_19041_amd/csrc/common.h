@@ -66,6 +66,7 @@ static_assert(FullProfile::DOUT == 541 && FullProfile::S == 223, "Table S2 (128,
 // ---------------------------------------------------------------------------
 // Device-side view of a model, passed to kernels by value.
 // ---------------------------------------------------------------------------
+constexpr int kMaxFoldTypes = 5;         // species for which pair-folded tables are built
 constexpr int kC123 = 3 * 5 * 7;          // dense (1,2,3) coupling, [m1][m2][m3]
 constexpr int kC233 = 5 * 7 * 7;          // dense (2,3,3) coupling
 constexpr int kCouplings = kC123 + kC233;
@@ -88,6 +89,10 @@ struct ModelDev {
   const float* inv_sigma;   // [D_out]
   const float* cpl;         // [kCouplings]: C123 then C233 (symmetric in m2, m3), or null
   const float* E_ref;       // [T+1]
+  // pair-folded tables (fold.hip), used when fold_n > 0:
+  // [fold_n^2 pairs][n_rows][CPL][LPE][6], pair (fa, fb) at fa * fold_n + fb
+  const float* ftab;
+  int fold_n;
 };
 
 // ---------------------------------------------------------------------------

@@ -1,0 +1,135 @@
+// Pair-folded radial tables.
+//
+// For an ordered type pair (a, b) the amplitude of channel c is a function of
+// rho alone (Eq. (amplitude)):
+//     psi_c(rho) = gamma_c g_c(rho) + beta_c + sum_mu U_c,mu q_mu(rho).
+// Quintic Hermite interpolation is linear in its knot data (value, first and
+// second derivative at both ends), and a constant is reproduced exactly, so
+// the interpolant of psi_c is gamma_c times the interpolant of g_c, plus
+// beta_c, plus U times the interpolants of q (Supplementary Note "Quintic
+// Hermite interpolation of the radial table").  Its normalised coefficients
+// are that same linear combination of the tabulated ones.
+//
+// For the few species of an MD system the library keeps one such table per
+// ordered pair present; the edge kernels then read one quintic per channel
+// instead of a g quintic, R q quintics and the pair coefficients.  Systems
+// with more than kMaxFoldTypes species use the separable tables directly.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <vector>
+
+#include "../../include/dpa4c.h"
+#include "edge_math.h"
+#include "launch.h"
+
+namespace dpa4c {
+
+namespace {
+
+__global__ void presence_kernel(const int32_t* __restrict__ species, int64_t n, int n_types1,
+                                uint32_t* __restrict__ mask) {
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x) {
+    const int a = clamp_type(species[i], n_types1);
+    atomicOr(&mask[a >> 5], 1u << (a & 31));
+  }
+}
+
+__global__ void fold_index_kernel(const int32_t* __restrict__ species, int64_t n, int n_types1,
+                                  const int32_t* __restrict__ map, int32_t* __restrict__ fidx) {
+  for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * blockDim.x)
+    fidx[i] = map[clamp_type(species[i], n_types1)];
+}
+
+struct FoldTypes {
+  int t[kMaxFoldTypes];
+};
+
+// one block per (table row, folded pair); thread = channel c
+__global__ void fold_build_kernel(const float* __restrict__ gtab, const float* __restrict__ qtab,
+                                  const float* __restrict__ pair, FoldTypes used, int n_used,
+                                  int n_types1, int C0, int R, int LPE, int rows,
+                                  float* __restrict__ ftab) {
+  const int s = blockIdx.x, p = blockIdx.y;
+  const int a = used.t[p / n_used], b = used.t[p % n_used];
+  const int PW = 2 + R, CPL = C0 / LPE;
+  for (int c = threadIdx.x; c < C0; c += blockDim.x) {
+    const int k = c % LPE, j = c / LPE;
+    const float* pc = pair + ((size_t(a * n_types1 + b) * CPL + j) * LPE + k) * PW;
+    const float* g = gtab + ((size_t(s) * CPL + j) * LPE + k) * 6;
+    float* out = ftab + (((size_t(p) * rows + s) * CPL + j) * LPE + k) * 6;
+    for (int q = 0; q < 6; ++q) {
+      double v = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
+      for (int mu = 0; mu < R; ++mu)
+        v += double(pc[2 + mu]) * double(qtab[(size_t(s) * R + mu) * 6 + q]);
+      out[q] = static_cast<float>(v);
+    }
+  }
+}
+
+int grid_for(int64_t n) {
+  int64_t b = (n + 255) / 256;
+  return static_cast<int>(b < 4096 ? (b < 1 ? 1 : b) : 4096);
+}
+
+}  // namespace
+
+int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream_t st) {
+  Workspace& w = m->ws;
+  const int T1 = m->n_types + 1;
+  if (n <= 0) return 0;
+  if (w.fold_mask.ensure(4 * sizeof(uint32_t)) || w.fidx.ensure(4 * size_t(n)) ||
+      w.fold_map.ensure(4 * size_t(T1)))
+    return DPA4C_ERR_HIP;
+  // pinned host words: [0, 16) the presence mask, [64, 64 + 4 T1) the type map
+  if (!w.fold_host)
+    DPA4C_HIP_TRY(hipHostMalloc((void**)&w.fold_host, 64 + 4 * size_t(T1), hipHostMallocDefault));
+  DPA4C_HIP_TRY(hipMemsetAsync(w.fold_mask.p, 0, 4 * sizeof(uint32_t), st));
+  hipLaunchKernelGGL(presence_kernel, dim3(grid_for(n)), dim3(256), 0, st, species, n, T1,
+                     w.fold_mask.as<uint32_t>());
+  DPA4C_HIP_TRY(hipGetLastError());
+  DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_host, w.fold_mask.p, 4 * sizeof(uint32_t),
+                               hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
+  uint32_t mask[4];
+  std::memcpy(mask, w.fold_host, sizeof(mask));
+  const bool same = m->fold_n >= 0 && std::memcmp(mask, m->fold_types_mask, sizeof(mask)) == 0;
+  if (!same) {
+    FoldTypes used{};
+    int n_used = 0;
+    std::vector<int32_t> map(T1, -1);
+    for (int a = 0; a < T1; ++a)
+      if (mask[a >> 5] >> (a & 31) & 1u) {
+        if (n_used < kMaxFoldTypes) {
+          used.t[n_used] = a;
+          map[a] = n_used;
+        }
+        ++n_used;
+      }
+    std::memcpy(m->fold_types_mask, mask, sizeof(mask));
+    if (n_used > kMaxFoldTypes) {
+      m->fold_n = 0;   // too many species: the separable tables are used
+    } else {
+      const size_t per_pair = size_t(m->n_rows) * m->C0 * 6;
+      if (w.ftab.ensure(4 * per_pair * n_used * n_used)) return DPA4C_ERR_HIP;
+      int32_t* hmap = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(w.fold_host) + 64);
+      std::memcpy(hmap, map.data(), 4 * size_t(T1));
+      DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_map.p, hmap, 4 * size_t(T1), hipMemcpyHostToDevice, st));
+      hipLaunchKernelGGL(fold_build_kernel, dim3(m->n_rows, n_used * n_used),
+                         dim3(m->C0 < 256 ? m->C0 : 256), 0, st, m->gtab, m->qtab, m->pair, used,
+                         n_used, T1, m->C0, m->R, m->C[1], m->n_rows, w.ftab.as<float>());
+      DPA4C_HIP_TRY(hipGetLastError());
+      m->fold_n = n_used;
+    }
+  }
+  if (m->fold_n > 0) {
+    hipLaunchKernelGGL(fold_index_kernel, dim3(grid_for(n)), dim3(256), 0, st, species, n, T1,
+                       w.fold_map.as<int32_t>(), w.fidx.as<int32_t>());
+    DPA4C_HIP_TRY(hipGetLastError());
+  }
+  return 0;
+}
+
+}  // namespace dpa4c

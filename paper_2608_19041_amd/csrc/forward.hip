@@ -26,9 +26,9 @@ namespace {
 constexpr int kTeam = 256;
 constexpr int kWaves = kTeam / kWave;
 
-template <class P>
+template <class P, bool FOLD>
 __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
-                                                        const int32_t* __restrict__ species,
+                                                        const int32_t* __restrict__ typ,
                                                         const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
                                                         const float4* __restrict__ edge,
@@ -41,9 +41,13 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
   const int k = tid % P::LPE;
   const int T1 = md.n_types1;
   const float inv_delta = md.inv_delta;
+  const int nf = md.fold_n;
+  // ``typ`` holds species (clamped here) or, with folded tables, the folded
+  // index of every atom
+  auto type_of = [&](int64_t a) { return FOLD ? typ[a] : clamp_type(typ[a], T1); };
 
   for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
-    const int ai = clamp_type(species[i], T1);
+    const int ai = type_of(i);
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
     float acc0[P::CPL];
@@ -53,7 +57,8 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
     float acc2[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
     float acc3[7] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     float s0 = 0.0f, s1 = 0.0f;
-    const float* pair_base = md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
+    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
+                                  : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
     const float w2mask = k < P::C2 ? 1.0f : 0.0f;
     const float w3mask = k == 0 ? 1.0f : 0.0f;
 
@@ -66,7 +71,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
     int aj_n = ai;
     if (cnt > 0) {
       rec_n = erow[grp < cnt ? grp : 0];
-      aj_n = grp < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+      aj_n = grp < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
       if (G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
     }
     for (int base = 0; base < cnt; base += G) {
@@ -77,7 +82,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       if (base + G < cnt) {
         const int el1 = el + G, el2 = el + 2 * G;
         rec_n = rec_nn;
-        aj_n = el1 < cnt ? clamp_type(species[__float_as_int(rec_n.w)], T1) : ai;
+        aj_n = el1 < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
         if (base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
       }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
@@ -86,33 +91,46 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       if (!valid) chi = 0.0f;
       float tau;
       const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
-      float q[P::R > 0 ? P::R : 1];
-      if constexpr (P::R > 0) {
-        // lane k < R evaluates q_k; the group shares it
-        float c[6];
-        load6(md.qtab + (size_t(row) * P::R + (k < P::R ? k : 0)) * 6, c);
-        const float qk = quintic_val(c, tau);
-#pragma unroll
-        for (int mu = 0; mu < P::R; ++mu) q[mu] = __shfl(qk, mu, P::LPE);
-      }
-      const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
-      const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
       float psi0 = 0.0f;
+      if constexpr (FOLD) {
+        // one quintic per channel from the table of the pair (a_i, a_j)
+        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * 6);
 #pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj) {
-        float c[6];
-        load6(gt + (jj * P::LPE + k) * 6, c);
-        const float gv = quintic_val(c, tau);
-        const float* pp = pc + (jj * P::LPE + k) * P::PW;
-        const float2 gb = *reinterpret_cast<const float2*>(pp);
-        float psi = gb.x * gv + gb.y;
-        if constexpr (P::R > 0) {
-          const float2 u01 = *reinterpret_cast<const float2*>(pp + 2);
-          const float2 u23 = *reinterpret_cast<const float2*>(pp + 4);
-          psi += u01.x * q[0] + u01.y * q[1] + u23.x * q[2] + u23.y * q[3];
+        for (int jj = 0; jj < P::CPL; ++jj) {
+          float c[6];
+          load6(ft + (jj * P::LPE + k) * 6, c);
+          const float psi = quintic_val(c, tau);
+          acc0[jj] += chi * psi;
+          if (jj == 0) psi0 = psi;
         }
-        acc0[jj] += chi * psi;
-        if (jj == 0) psi0 = psi;
+      } else {
+        float q[P::R > 0 ? P::R : 1];
+        if constexpr (P::R > 0) {
+          // lane k < R evaluates q_k; the group shares it
+          float c[6];
+          load6(md.qtab + (size_t(row) * P::R + (k < P::R ? k : 0)) * 6, c);
+          const float qk = quintic_val(c, tau);
+#pragma unroll
+          for (int mu = 0; mu < P::R; ++mu) q[mu] = __shfl(qk, mu, P::LPE);
+        }
+        const float* pc = pair_base + size_t(aj) * (P::C0 * P::PW);
+        const float* gt = md.gtab + size_t(row) * (P::C0 * 6);
+#pragma unroll
+        for (int jj = 0; jj < P::CPL; ++jj) {
+          float c[6];
+          load6(gt + (jj * P::LPE + k) * 6, c);
+          const float gv = quintic_val(c, tau);
+          const float* pp = pc + (jj * P::LPE + k) * P::PW;
+          const float2 gb = *reinterpret_cast<const float2*>(pp);
+          float psi = gb.x * gv + gb.y;
+          if constexpr (P::R > 0) {
+            const float2 u01 = *reinterpret_cast<const float2*>(pp + 2);
+            const float2 u23 = *reinterpret_cast<const float2*>(pp + 4);
+            psi += u01.x * q[0] + u01.y * q[1] + u23.x * q[2] + u23.y * q[3];
+          }
+          acc0[jj] += chi * psi;
+          if (jj == 0) psi0 = psi;
+        }
       }
       const float chi2 = chi * chi;
       s0 += chi2;
@@ -189,8 +207,12 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
            const int32_t* ecount, const float4* edge, float* node, hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
-  hipLaunchKernelGGL(forward_kernel<P>, dim3(blocks), dim3(kTeam), 0, st, m->dev(), n, species,
-                     row_ptr, ecount, edge, node);
+  if (m->fold_n > 0)
+    hipLaunchKernelGGL((forward_kernel<P, true>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
+                       m->ws.fidx.as<int32_t>(), row_ptr, ecount, edge, node);
+  else
+    hipLaunchKernelGGL((forward_kernel<P, false>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
+                       species, row_ptr, ecount, edge, node);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

@@ -41,7 +41,12 @@ int launch_rev(const int64_t* row_ptr, const int32_t* ecount, const int32_t* sid
                const int32_t* skin_rev, const int32_t* cidx, int64_t n, int32_t* rev,
                hipStream_t st);
 
-// model stages
+// species analysis of a call: builds the pair-folded tables of the species
+// present when they changed (at most kMaxFoldTypes species) and the folded
+// index of every atom; synchronises ``st``
+int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream_t st);
+
+// model stages (the edge kernels read ws.fidx when the model has folded tables)
 int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
                    const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
                    float* node, hipStream_t st);

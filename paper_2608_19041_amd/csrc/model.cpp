@@ -465,5 +465,7 @@ dpa4c::ModelDev dpa4c_model::dev() const {
   d.inv_sigma = inv_sigma;
   d.cpl = cpl;
   d.E_ref = E_ref;
+  d.ftab = ws.ftab.as<float>();
+  d.fold_n = fold_n > 0 ? fold_n : 0;
   return d;
 }

@@ -79,6 +79,12 @@ struct Workspace {
   DevBuf inv_mass;      // double [T+1]: 1 / (m * 103.6427)  (A/fs^2 per eV/A)
   DevBuf mass;          // double [T+1]
   int64_t* host_flags = nullptr;          // pinned [8]
+  // pair-folded tables of the species present (fold.hip)
+  DevBuf ftab;          // float [fold_n^2][n_rows][C0][6]
+  DevBuf fold_map;      // int32 [T+1]: type -> folded index, or -1
+  DevBuf fold_mask;     // uint32 [4]: species present in the last call
+  DevBuf fidx;          // int32 [N]: folded index of every atom
+  uint32_t* fold_host = nullptr;          // pinned
   const int32_t* last_species = nullptr;  // inputs of the last evaluation
   const int64_t* skin_row_used = nullptr;
   NeighborScratch nb;
@@ -128,6 +134,8 @@ struct dpa4c_model {
   dpa4c::Timing timing;
   std::mutex mu_lock;
   int64_t last_n = 0;
+  int fold_n = -1;                  // species with folded tables; 0 = separable path, -1 = unset
+  uint32_t fold_types_mask[4] = {};
 
   dpa4c::ModelDev dev() const;
 };

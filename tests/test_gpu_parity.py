@@ -168,6 +168,54 @@ def test_energy_forces_small_systems(dev, dp, name, structure):
     assert abs(F.sum(0)).max() < 1e-9
 
 
+def many_species_system(name):
+    """More species than the library folds into per-pair tables, with atomic
+    energies in the range the synthetic calibration covers: for the full
+    model a BCC cell of the alloy's, water's and copper's types (8 species),
+    for the small model (calibrated on copper alone) a copper cell with six
+    substituted atoms (7 species)."""
+    if name == "full":
+        s = synth.bcc_hea(3, 0.06, seed=7)
+        types = np.array(sorted(set(s.meta["types"]) | {0, 7, 28}), dtype=np.int32)
+        rng = np.random.Generator(np.random.PCG64(3))
+        s.species = types[rng.integers(0, len(types), size=s.n)].astype(np.int32)
+    else:
+        s = synth.fcc_copper(3, 0.08, seed=6)
+        rng = np.random.Generator(np.random.PCG64(8))
+        s.species = s.species.copy()
+        s.species[rng.choice(s.n, 6, replace=False)] = np.array([0, 4, 7, 53, 58, 87])
+    return s
+
+
+@pytest.mark.parametrize("name", ["small", "full"])
+def test_separable_tables_with_many_species(dev, dp, name):
+    """More species than the library folds into per-pair tables: the edge
+    kernels use the separable radial table and the pair cache."""
+    model, oracle, _ = gpu_model(dp, name)
+    s = many_species_system(name)
+    assert len(np.unique(s.species)) > 5
+    ea, F, et = evaluate(dp, model, s, dev)
+    ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc)
+    assert np.abs(ea - ref_e).max() < E_TOL
+    assert np.abs(F - ref_f).max() < F_TOL
+
+
+def test_species_change_between_calls(dev, dp):
+    """The per-pair tables follow the species of each call on one handle:
+    one species, two, seven (separable path), then one again."""
+    model, oracle, _ = gpu_model(dp, "small")
+    cell = np.diag([8.3, 8.9, 9.4])
+    systems = [synth.fcc_copper(3, 0.08, seed=4),
+               synth.random_periodic(24, seed=12, cell=cell, d_min=1.6),
+               many_species_system("small"),
+               synth.fcc_copper(3, 0.08, seed=5)]
+    for s in systems:
+        ea, F, et = evaluate(dp, model, s, dev)
+        ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc)
+        assert np.abs(ea - ref_e).max() < E_TOL
+        assert np.abs(F - ref_f).max() < F_TOL
+
+
 def test_energy_forces_config2_sampled(dev, dp):
     """4000-atom FCC with the full model: E_i of sampled centres and the forces
     of sampled atoms (whose exact value needs the centres k and N(k))."""
