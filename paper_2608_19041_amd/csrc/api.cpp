@@ -128,7 +128,7 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
       w.sidx.ensure(4 * cc) || w.rev.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
       w.skin_rev.ensure(4 * cc) || w.node.ensure(4 * nn * (m->S + 2)) ||
       w.node_grad.ensure(4 * nn * (m->S + 2)) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
-      w.flags.ensure(8 * 8) || w.ekin_atom.ensure(8 * nn) || w.eatom.ensure(8 * nn))
+      w.flags.ensure(8 * 8) || w.eatom.ensure(8 * nn))
     return DPA4C_ERR_HIP;
   (void)dstr;
   return 0;
@@ -140,6 +140,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
               const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
               double* forces, double* e_total, hipStream_t st) {
+  // e_total == nullptr: the caller sums the energy itself
   dpa4c_model* m = const_cast<dpa4c_model*>(mc);
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
@@ -181,7 +182,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
                        w.rev.as<int32_t>(), forces, st);
     if (rc) return rc;
   }
-  {
+  if (e_total) {
     StageScope t(m, kStEnergy, st);
     rc = launch_energy(n, e_atom, w.epart.as<double>(), e_total, st);
   }
@@ -219,8 +220,8 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   Workspace& w = m->ws;
   DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
                     &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
-                    &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.ekin_atom, &w.inv_mass, &w.mass,
-                    &w.eatom,    &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
+                    &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
+                    &w.eatom,    &w.tailpart,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
   for (DevBuf* b : bufs) b->release();
@@ -388,7 +389,9 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   const double box[3] = {cell[0], cell[4], cell[8]};
 
   // masses on the device
+  const int np_tail = tail_partial_count(N);
   if (w.inv_mass.ensure(8 * T1) || w.mass.ensure(8 * T1) || w.flags.ensure(64) ||
+      w.tailpart.ensure(16 * size_t(np_tail)) ||
       w.skin_row.ensure(8 * (N + 1)) || w.skin_row_new.ensure(8 * (N + 1)) ||
       w.qbuild.ensure(8 * 3 * N))
     return DPA4C_ERR_HIP;
@@ -440,11 +443,18 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   };
 
   int64_t rebuilds = 0;
+  double* part_e = w.tailpart.as<double>();
+  double* part_k = part_e + np_tail;
+  auto sums_of = [&](int s) {
+    return s < 0 ? StepSums{nullptr, nullptr, 0, nullptr, nullptr}
+                 : StepSums{part_e, part_k, np_tail, e_pot + s, e_kin + s};
+  };
   for (int step = 0; step < nsteps; ++step) {
     {
       StageScope t(m, kStIntegrate, st);
       rc = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs, 1,
-                             step == 0 ? nullptr : w.qbuild.as<int64_t>(), skq, flags, st);
+                             step == 0 ? nullptr : w.qbuild.as<int64_t>(), skq, flags,
+                             sums_of(step - 1), st);
       if (rc) return rc;
     }
     if (step == 0) {
@@ -480,17 +490,19 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     }
     rc = run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
                    w.skin_shift.as<int32_t>(), w.cap, w.skin_rev.as<int32_t>(), w.eatom.as<double>(),
-                   forces, e_pot + step, st);
+                   forces, nullptr, st);
     if (rc) return rc;
     {
       StageScope t(m, kStIntegrate, st);
-      rc = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs, 0, nullptr,
-                             0, flags, st);
-      if (rc) return rc;
-      rc = launch_kinetic(N, vel, species, w.mass.as<double>(), T1, w.ekin_atom.as<double>(),
-                          w.epart.as<double>(), e_kin + step, st);
+      rc = launch_tail(N, vel, forces, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
+                       dt_fs, w.eatom.as<double>(), part_e, part_k, st);
       if (rc) return rc;
     }
+  }
+  if (nsteps > 0) {
+    StageScope t(m, kStIntegrate, st);
+    rc = launch_final_step(sums_of(nsteps - 1), st);
+    if (rc) return rc;
   }
   DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));

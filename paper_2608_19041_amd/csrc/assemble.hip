@@ -98,6 +98,13 @@ __device__ inline int64_t qfix(double x) { return static_cast<int64_t>(__builtin
 // v += dt/2 F/m; optionally r += dt v and flag a rebuild when some atom moved
 // by more than half the skin since the last build (fixed-point norm:
 // 4 |dq|^2 > skin_q^2).
+// fixed-order sum of np block partials by one block (every thread gets it)
+__device__ inline double sum_partials(const double* __restrict__ part, int np, double* sh) {
+  double s = 0.0;
+  for (int t = threadIdx.x; t < np; t += kBlock) s += part[t];
+  return block_sum(s, sh);
+}
+
 __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__ pos, double* __restrict__ vel,
                                                             const double* __restrict__ forces,
                                                             const int32_t* __restrict__ species,
@@ -105,7 +112,19 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
                                                             int n_types1, int64_t n, double half_dt,
                                                             double dt,
                                                             int drift, const int64_t* __restrict__ qbuild,
-                                                            int64_t skin_q, int64_t* __restrict__ flags) {
+                                                            int64_t skin_q, int64_t* __restrict__ flags,
+                                                            StepSums prev) {
+  if (prev.np > 0 && blockIdx.x == 0) {
+    // totals of the previous step from the block partials of its tail kernel
+    __shared__ double sh[kBlock];
+    const double ep = sum_partials(prev.part_e, prev.np, sh);
+    __syncthreads();
+    const double ek = sum_partials(prev.part_k, prev.np, sh);
+    if (threadIdx.x == 0) {
+      *prev.e_pot = ep;
+      *prev.e_kin = ek;
+    }
+  }
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= n) return;
   int a0 = species[i];
@@ -135,18 +154,53 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
     atomicOr(reinterpret_cast<unsigned long long*>(flags + 1), 1ull);
 }
 
-__global__ void __launch_bounds__(kBlock) kinetic_kernel(int64_t n, const double* __restrict__ vel,
-                                                         const int32_t* __restrict__ species,
-                                                         const double* __restrict__ mass,
-                                                         int n_types1, double* __restrict__ ek) {
-  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
-  if (i >= n) return;
-  int a0 = species[i];
-  a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
-  const double m = mass[a0];
-  const double vx = vel[3 * i], vy = vel[3 * i + 1], vz = vel[3 * i + 2];
-  // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
-  ek[i] = 0.5 * m * (vx * vx + vy * vy + vz * vz) * (1.66053906660e-17 / 1.602176634e-19);
+// Second half kick v += dt/2 F/m, then the block partials (fixed tree) of
+// the potential energy sum_i E_i and of the kinetic energy of the block's
+// atoms; the next kick_drift_kernel (or final_step_kernel) adds the partials.
+__global__ void __launch_bounds__(kBlock) tail_kernel(int64_t n, double* __restrict__ vel,
+                                                      const double* __restrict__ forces,
+                                                      const int32_t* __restrict__ species,
+                                                      const double* __restrict__ inv_mass,
+                                                      const double* __restrict__ mass,
+                                                      int n_types1, double half_dt,
+                                                      const double* __restrict__ e_atom,
+                                                      double* __restrict__ part_e,
+                                                      double* __restrict__ part_k) {
+  __shared__ double sh[kBlock];
+  const int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  double ek = 0.0, ep = 0.0;
+  if (i < n) {
+    int a0 = species[i];
+    a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
+    const double im = inv_mass[a0];
+    double v2 = 0.0;
+    for (int a = 0; a < 3; ++a) {
+      const double v = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
+      vel[3 * i + a] = v;
+      v2 += v * v;
+    }
+    // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
+    ek = 0.5 * mass[a0] * v2 * (1.66053906660e-17 / 1.602176634e-19);
+    ep = e_atom[i];
+  }
+  const double te = block_sum(ep, sh);
+  __syncthreads();
+  const double tk = block_sum(ek, sh);
+  if (threadIdx.x == 0) {
+    part_e[blockIdx.x] = te;
+    part_k[blockIdx.x] = tk;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) final_step_kernel(StepSums prev) {
+  __shared__ double sh[kBlock];
+  const double ep = sum_partials(prev.part_e, prev.np, sh);
+  __syncthreads();
+  const double ek = sum_partials(prev.part_k, prev.np, sh);
+  if (threadIdx.x == 0) {
+    *prev.e_pot = ep;
+    *prev.e_kin = ek;
+  }
 }
 
 __global__ void __launch_bounds__(kBlock) snapshot_kernel(const double* __restrict__ pos, int64_t n,
@@ -193,20 +247,32 @@ int launch_energy(int64_t n, const double* e_atom, double* partials, double* out
 
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
-                      const int64_t* qbuild, int64_t skin_q, int64_t* flags, hipStream_t st) {
+                      const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
+                      hipStream_t st) {
   hipLaunchKernelGGL(kick_drift_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, pos, vel, forces,
-                     species, inv_mass, n_types1, n, 0.5 * dt, dt, drift, qbuild, skin_q, flags);
+                     species, inv_mass, n_types1, n, 0.5 * dt, dt, drift, qbuild, skin_q, flags,
+                     prev);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
 
-int launch_kinetic(int64_t n, const double* vel, const int32_t* species, const double* mass,
-                   int n_types1, double* ekin_atom, double* partials, double* out, hipStream_t st) {
-  hipLaunchKernelGGL(kinetic_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, n, vel, species, mass,
-                     n_types1, ekin_atom);
+int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* species,
+                const double* inv_mass, const double* mass, int n_types1, double dt,
+                const double* e_atom, double* part_e, double* part_k, hipStream_t st) {
+  hipLaunchKernelGGL(tail_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, n, vel, forces,
+                     species, inv_mass, mass, n_types1, 0.5 * dt, e_atom, part_e, part_k);
   DPA4C_HIP_TRY(hipGetLastError());
-  return fixed_sum(ekin_atom, n, partials, out, st);
+  return 0;
 }
+
+int launch_final_step(StepSums prev, hipStream_t st) {
+  if (prev.np <= 0) return 0;
+  hipLaunchKernelGGL(final_step_kernel, dim3(1), dim3(kBlock), 0, st, prev);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int tail_partial_count(int64_t n) { return blocks_for(n); }
 
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, const int64_t* active,
                       hipStream_t st) {

@@ -67,11 +67,27 @@ int launch_gemm_test(const float* A, const float* B, float* C, int M, int N, int
                      hipStream_t st);
 
 // velocity Verlet pieces
+// block partials of a step's energies and where their totals go (np = 0:
+// nothing to add)
+struct StepSums {
+  const double* part_e;
+  const double* part_k;
+  int np;
+  double* e_pot;
+  double* e_kin;
+};
+// half kick (and drift with the displacement check); block 0 first adds the
+// partials of the previous step
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
-                      const int64_t* qbuild, int64_t skin_q, int64_t* flags, hipStream_t st);
-int launch_kinetic(int64_t n, const double* vel, const int32_t* species, const double* mass,
-                   int n_types1, double* ekin_atom, double* partials, double* out, hipStream_t st);
+                      const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
+                      hipStream_t st);
+// second half kick and the energy partials of the step (tail_partial_count(n) blocks)
+int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* species,
+                const double* inv_mass, const double* mass, int n_types1, double dt,
+                const double* e_atom, double* part_e, double* part_k, hipStream_t st);
+int launch_final_step(StepSums prev, hipStream_t st);
+int tail_partial_count(int64_t n);
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, const int64_t* active,
                       hipStream_t st);
 // flags[idx] = value when (cond == null or *cond != 0)

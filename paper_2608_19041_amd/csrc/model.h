@@ -74,8 +74,8 @@ struct Workspace {
   DevBuf desc;          // float [N][D_out]: D, written only for stage checks
   DevBuf epart;         // double partial sums
   DevBuf flags;         // int64 [8] device flags
-  DevBuf ekin_atom;     // double [N]
   DevBuf eatom;         // double [N] (per-atom energies inside verlet_step)
+  DevBuf tailpart;      // double [2][blocks]: energy partials of a Verlet step
   DevBuf inv_mass;      // double [T+1]: 1 / (m * 103.6427)  (A/fs^2 per eV/A)
   DevBuf mass;          // double [T+1]
   int64_t* host_flags = nullptr;          // pinned [8]
