@@ -153,10 +153,16 @@ int compute_energy_forces(const dpa4c_model* model, const double* pos, const int
  *     v += dt/2 F/m;  r += dt v;  [rebuild];  F = F(r);  v += dt/2 F/m.
  * The library keeps its own skin list (radius r_c + skin) in the model
  * workspace.  It is rebuilt at the first step of a call, every
- * ``rebuild_every`` steps when that is > 0, and whenever some atom has moved
- * by more than skin/2 since the last build (checked on the device every
- * step).  With rebuild_every < 0 no rebuild happens after the first step and
- * a violation returns DPA4C_ERR_SKIN after the call.
+ * ``rebuild_every`` steps when that is > 0, and at every step where some
+ * atom has moved by more than skin/2 since the last build (fixed-point
+ * check on the device).  The steps between builds run in batches that the
+ * host checks after the fact: a batch that contains such a step is rolled
+ * back to its saved start (positions, velocities, forces), the steps before
+ * the violation are replayed and the violating step rebuilds, so the
+ * trajectory is the one a per-step check gives, bit for bit.  With
+ * rebuild_every < 0 no rebuild happens after the first step and a violation
+ * returns DPA4C_ERR_SKIN (pos, vel, forces then hold the state at the end of
+ * a batch that contains the violating step).
  *
  * pos, vel         device float64 [N][3], in/out (A, A/fs)
  * species          device int32 [N]
@@ -167,11 +173,10 @@ int compute_energy_forces(const dpa4c_model* model, const double* pos, const int
  * e_pot, e_kin     device float64 [nsteps] out: potential and kinetic energy
  *                  after each step (eV)
  * n_rebuilds       host int64 out (may be NULL): rebuilds done in this call
- * Synchronises ``stream`` twice: after the first neighbour build (to size
- * the skin list; capacity is then 1.5x that count plus 64 per atom) and at
- * the end (to read the device-side flags).  If a later rebuild would exceed
- * the capacity, returns DPA4C_ERR_CAPACITY and the trajectory from that step
- * on is not valid.
+ * Synchronises ``stream`` once per batch and at every rebuild (to size the
+ * skin list: its capacity grows to 1.5x the pair count plus 64 per atom
+ * whenever a build needs more).  The library holds 72 N bytes of device
+ * memory for the batch start state.
  */
 int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_t* species,
                 const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],

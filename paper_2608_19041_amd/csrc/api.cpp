@@ -221,7 +221,7 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
                     &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
-                    &w.eatom,    &w.tailpart,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
+                    &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
   for (DevBuf* b : bufs) b->release();
@@ -407,7 +407,8 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   int64_t* flags = w.flags.as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
 
-  // the first build of the call sizes the skin list
+  // a build of the skin list: count, read the size back, grow the capacity
+  // if needed, fill, reverse index and the positions of the build
   auto initial_build = [&]() -> int {
     int r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,
                             nullptr, flags, false, st);
@@ -417,14 +418,14 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags + 1, flags, 8, hipMemcpyDeviceToHost, st));
     DPA4C_HIP_TRY(hipStreamSynchronize(st));
     if (w.host_flags[1]) return flags_to_error(w.host_flags[1]);
-    int64_t need = w.host_flags[0];
-    int64_t cap = need + need / 2 + 64 * N;
-    if (cap >= (int64_t(1) << 31)) cap = (int64_t(1) << 31) - 1;
-    if (cap < need) {
-      set_error("verlet_step: more than 2^31 - 1 neighbour pairs");
-      return DPA4C_ERR_CAPACITY;
-    }
-    if (cap > w.cap || !w.skin_j.p) {
+    const int64_t need = w.host_flags[0];
+    if (need > w.cap || !w.skin_j.p) {
+      int64_t cap = need + need / 2 + 64 * N;
+      if (cap >= (int64_t(1) << 31)) cap = (int64_t(1) << 31) - 1;
+      if (cap < need) {
+        set_error("verlet_step: more than 2^31 - 1 neighbour pairs");
+        return DPA4C_ERR_CAPACITY;
+      }
       if (w.skin_j.ensure(4 * cap) || w.skin_shift.ensure(4 * cap)) return DPA4C_ERR_HIP;
       w.cap = cap;
     }
@@ -445,75 +446,128 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   int64_t rebuilds = 0;
   double* part_e = w.tailpart.as<double>();
   double* part_k = part_e + np_tail;
-  auto sums_of = [&](int s) {
+  auto sums_of = [&](int64_t s) {
     return s < 0 ? StepSums{nullptr, nullptr, 0, nullptr, nullptr}
                  : StepSums{part_e, part_k, np_tail, e_pot + s, e_kin + s};
   };
-  for (int step = 0; step < nsteps; ++step) {
+  // one step: kick/drift (with the displacement check against the last
+  // build when ``check``), an optional rebuild, the model and the tail
+  auto one_step = [&](int64_t step, bool check, bool rebuild, int64_t prev) -> int {
     {
       StageScope t(m, kStIntegrate, st);
-      rc = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs, 1,
-                             step == 0 ? nullptr : w.qbuild.as<int64_t>(), skq, flags,
-                             sums_of(step - 1), st);
-      if (rc) return rc;
+      int r = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs,
+                                1, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
+                                sums_of(prev), step, st);
+      if (r) return r;
     }
-    if (step == 0) {
-      rc = initial_build();
-      if (rc) return rc;
+    if (rebuild) {
+      int r = initial_build();
+      if (r) return r;
       ++rebuilds;
-    } else if (rebuild_every >= 0) {
-      const bool forced = rebuild_every > 0 && step % rebuild_every == 0;
-      if (forced) {
-        rc = launch_set_flag(flags, 1, 1, st);
-        if (rc) return rc;
-      }
-      const int64_t* active = flags + 1;
-      {
-        // the scan goes to a scratch row array; it replaces the live one only
-        // when the new list fits the capacity
-        StageScope t(m, kStNeighborCount, st);
-        rc = build_skin_list(w.nb, pos, N, g_list, w.skin_row_new.as<int64_t>(),
-                             w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap, active,
-                             flags, true, st);
-        if (rc) return rc;
-        rc = commit_rows(w.skin_row_new.as<int64_t>(), w.skin_row.as<int64_t>(), N, w.cap, flags,
-                         active, st);
-        if (rc) return rc;
-      }
-      rc = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
-                           w.skin_shift.as<int32_t>(), N, w.skin_rev.as<int32_t>(), active, st);
-      if (rc) return rc;
-      rc = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), active, st);
-      if (rc) return rc;
-      rc = launch_rebuild_done(flags, st);
-      if (rc) return rc;
     }
-    rc = run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
-                   w.skin_shift.as<int32_t>(), w.cap, w.skin_rev.as<int32_t>(), w.eatom.as<double>(),
-                   forces, nullptr, st);
-    if (rc) return rc;
-    {
-      StageScope t(m, kStIntegrate, st);
-      rc = launch_tail(N, vel, forces, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
-                       dt_fs, w.eatom.as<double>(), part_e, part_k, st);
-      if (rc) return rc;
-    }
-  }
-  if (nsteps > 0) {
+    int r = run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(),
+                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
+                      w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, st);
+    if (r) return r;
     StageScope t(m, kStIntegrate, st);
-    rc = launch_final_step(sums_of(nsteps - 1), st);
+    return launch_tail(N, vel, forces, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
+                       dt_fs, w.eatom.as<double>(), part_e, part_k, st);
+  };
+  auto finish = [&](int64_t last) -> int {
+    StageScope t(m, kStIntegrate, st);
+    return launch_final_step(sums_of(last), st);
+  };
+
+  // Step 0 builds the list.  Later steps run in speculative batches without
+  // rebuild checks on the host: kick/drift records the first step whose
+  // displacement exceeds half the skin.  A batch without one stands; after
+  // one at step v the state saved at the start of the batch is restored,
+  // steps before v are replayed (bit-identical) and step v rebuilds the
+  // list, exactly as a per-step check would.  Forced rebuilds
+  // (rebuild_every > 0) start batches of their own.
+  if (nsteps > 0) {
+    rc = one_step(0, false, true, -1);
     if (rc) return rc;
+    rc = finish(0);
+    if (rc) return rc;
+  }
+  if (w.backup.ensure(3 * 24 * size_t(N))) return DPA4C_ERR_HIP;
+  double* bk = w.backup.as<double>();
+  const size_t state = 24 * size_t(N);
+  const double half_skin = 0.5 * skin;
+  int64_t last_build = 0, batch = 8;
+  double growth = 0.0;   // A per step since the last build, from the last batch
+  for (int64_t s = 1; s < nsteps;) {
+    if (rebuild_every > 0 && s % rebuild_every == 0) {
+      rc = one_step(s, true, true, -1);
+      if (rc) return rc;
+      rc = finish(s);
+      if (rc) return rc;
+      last_build = s++;
+      continue;
+    }
+    int64_t e = s + batch < nsteps ? s + batch : nsteps;
+    if (rebuild_every > 0) {
+      const int64_t next_forced = (s / rebuild_every + 1) * rebuild_every;
+      if (next_forced < e) e = next_forced;
+    }
+    DPA4C_HIP_TRY(hipMemcpyAsync(bk, pos, state, hipMemcpyDeviceToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(bk + 3 * N, vel, state, hipMemcpyDeviceToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(bk + 6 * N, forces, state, hipMemcpyDeviceToDevice, st));
+    rc = launch_set_flag(flags, 4, INT64_MAX, st);
+    if (rc) return rc;
+    rc = launch_set_flag(flags, 5, 0, st);
+    if (rc) return rc;
+    for (int64_t t = s; t < e; ++t) {
+      rc = one_step(t, true, false, t > s ? t - 1 : -1);
+      if (rc) return rc;
+    }
+    rc = finish(e - 1);
+    if (rc) return rc;
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
+    DPA4C_HIP_TRY(hipStreamSynchronize(st));
+    rc = flags_to_error(w.host_flags[0]);
+    if (rc) return rc;
+    const int64_t v = w.host_flags[4];
+    if (v == INT64_MAX) {
+      // no violation: size the next batch from the displacement growth
+      const double d = std::sqrt(double(w.host_flags[5])) / kQScale;
+      growth = d / double(e - last_build);
+      const double left = growth > 0.0 ? (half_skin - d) / growth : 64.0;
+      batch = static_cast<int64_t>(0.75 * left);
+      batch = batch < 1 ? 1 : (batch > 64 ? 64 : batch);
+      s = e;
+      continue;
+    }
+    if (rebuild_every < 0) {
+      set_error("verlet_step: an atom moved more than skin/2 and rebuilds are disabled");
+      return DPA4C_ERR_SKIN;
+    }
+    // violation at step v: restore, replay [s, v), rebuild at v
+    DPA4C_HIP_TRY(hipMemcpyAsync(pos, bk, state, hipMemcpyDeviceToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(vel, bk + 3 * N, state, hipMemcpyDeviceToDevice, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(forces, bk + 6 * N, state, hipMemcpyDeviceToDevice, st));
+    for (int64_t t = s; t < v; ++t) {
+      rc = one_step(t, false, false, t > s ? t - 1 : -1);
+      if (rc) return rc;
+    }
+    if (v > s) {
+      rc = finish(v - 1);
+      if (rc) return rc;
+    }
+    rc = one_step(v, false, true, -1);
+    if (rc) return rc;
+    rc = finish(v);
+    if (rc) return rc;
+    last_build = v;
+    s = v + 1;
+    batch = growth > 0.0 ? static_cast<int64_t>(0.75 * half_skin / growth) : 8;
+    batch = batch < 1 ? 1 : (batch > 64 ? 64 : batch);
   }
   DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
-  if (n_rebuilds) *n_rebuilds = rebuilds + w.host_flags[3];
-  rc = flags_to_error(w.host_flags[0]);
-  if (rc) return rc;
-  if (rebuild_every < 0 && w.host_flags[1]) {
-    set_error("verlet_step: an atom moved more than skin/2 and rebuilds are disabled");
-    return DPA4C_ERR_SKIN;
-  }
-  return 0;
+  if (n_rebuilds) *n_rebuilds = rebuilds;
+  return flags_to_error(w.host_flags[0]);
 }
 
 int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float* descriptor,

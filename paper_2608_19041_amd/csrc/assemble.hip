@@ -95,9 +95,10 @@ int fixed_sum(const double* x, int64_t n, double* partials, double* out, hipStre
 
 __device__ inline int64_t qfix(double x) { return static_cast<int64_t>(__builtin_rint(x * kQScale)); }
 
-// v += dt/2 F/m; optionally r += dt v and flag a rebuild when some atom moved
-// by more than half the skin since the last build (fixed-point norm:
-// 4 |dq|^2 > skin_q^2).
+// v += dt/2 F/m; optionally r += dt v and, against the fixed-point positions
+// of the last build, flag a rebuild when some atom moved by more than half
+// the skin (4 |dq|^2 > skin_q^2): flags[1] is set, flags[4] takes the
+// smallest such step index and flags[5] the largest |dq|^2 below the limit.
 // fixed-order sum of np block partials by one block (every thread gets it)
 __device__ inline double sum_partials(const double* __restrict__ part, int np, double* sh) {
   double s = 0.0;
@@ -113,7 +114,7 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
                                                             double dt,
                                                             int drift, const int64_t* __restrict__ qbuild,
                                                             int64_t skin_q, int64_t* __restrict__ flags,
-                                                            StepSums prev) {
+                                                            StepSums prev, int64_t step) {
   if (prev.np > 0 && blockIdx.x == 0) {
     // totals of the previous step from the block partials of its tail kernel
     __shared__ double sh[kBlock];
@@ -150,8 +151,13 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
     }
   }
   if (bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), 8ull);
-  if (bad || far || 4 * d2 > skin_q * skin_q)
+  if (!qbuild) return;
+  if (bad || far || 4 * d2 > skin_q * skin_q) {
     atomicOr(reinterpret_cast<unsigned long long*>(flags + 1), 1ull);
+    atomicMin(reinterpret_cast<unsigned long long*>(flags + 4), (unsigned long long)step);
+  } else {
+    atomicMax(reinterpret_cast<unsigned long long*>(flags + 5), (unsigned long long)d2);
+  }
 }
 
 // Second half kick v += dt/2 F/m, then the block partials (fixed tree) of
@@ -248,10 +254,10 @@ int launch_energy(int64_t n, const double* e_atom, double* partials, double* out
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
                       const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
-                      hipStream_t st) {
+                      int64_t step, hipStream_t st) {
   hipLaunchKernelGGL(kick_drift_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, pos, vel, forces,
                      species, inv_mass, n_types1, n, 0.5 * dt, dt, drift, qbuild, skin_q, flags,
-                     prev);
+                     prev, step);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

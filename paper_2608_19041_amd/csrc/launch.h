@@ -76,12 +76,12 @@ struct StepSums {
   double* e_pot;
   double* e_kin;
 };
-// half kick (and drift with the displacement check); block 0 first adds the
-// partials of the previous step
+// half kick (and drift with the displacement check of step ``step`` when
+// qbuild is given); block 0 first adds the partials of the previous step
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
                       const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
-                      hipStream_t st);
+                      int64_t step, hipStream_t st);
 // second half kick and the energy partials of the step (tail_partial_count(n) blocks)
 int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* species,
                 const double* inv_mass, const double* mass, int n_types1, double dt,

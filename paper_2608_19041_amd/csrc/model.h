@@ -76,6 +76,7 @@ struct Workspace {
   DevBuf flags;         // int64 [8] device flags
   DevBuf eatom;         // double [N] (per-atom energies inside verlet_step)
   DevBuf tailpart;      // double [2][blocks]: energy partials of a Verlet step
+  DevBuf backup;        // double [3][N][3]: positions, velocities, forces at a batch start
   DevBuf inv_mass;      // double [T+1]: 1 / (m * 103.6427)  (A/fs^2 per eV/A)
   DevBuf mass;          // double [T+1]
   int64_t* host_flags = nullptr;          // pinned [8]

@@ -262,3 +262,50 @@ def test_verlet_matches_oracle_dynamics(dev, dp):
                                     1.0, 100, 0, F)
     et = (ep2 + ek2).cpu().numpy()
     assert abs(md.drift_ev_per_atom_ps(et, 1.0, s.n)) < 1e-5
+
+
+def test_verlet_with_frequent_rebuilds_matches_oracle(dev, dp):
+    """A 0.15 A skin forces rebuilds every few steps, so batches roll back and
+    replay; the trajectory must still follow the oracle, which finds the
+    exact neighbours at every step."""
+    from oracle import md
+    model, oracle, _ = gpu_model(dp, "small")
+    s = synth.make_workload("fcc108_small")[0]
+    v0 = synth.maxwell_boltzmann(s, 600.0)
+    pos, species = on_dev(s, dev)
+    vel = torch.tensor(v0, dtype=torch.float64, device=dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 6.2)
+    _, F, _ = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
+    ep, ek, nreb = model.verlet_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0, 0.15,
+                                     1.0, 30, 0, F)
+    torch.cuda.synchronize()
+    assert nreb >= 3
+    rep, rek, rpos, rvel = md.nve(oracle, s.pos, v0, s.species, s.cell, s.pbc,
+                                  s.mass_by_type[s.species], 1.0, 30)
+    assert np.abs(pos.cpu().numpy() - rpos).max() < 1e-6
+    assert np.abs(ep.cpu().numpy() - rep[1:]).max() < E_TOL * s.n
+    assert np.abs(ek.cpu().numpy() - rek[1:]).max() < E_TOL * s.n
+
+
+@pytest.mark.parametrize("every", [0, 7])
+def test_verlet_is_bit_reproducible(dev, dp, every):
+    """Two calls from the same state give the same bits (displacement-checked
+    and forced rebuilds)."""
+    model, _, _ = gpu_model(dp, "full")
+    s = synth.make_workload("fcc4000_full")[0]
+    v0 = synth.maxwell_boltzmann(s, 600.0)
+    outs = []
+    for _ in range(2):
+        pos, species = on_dev(s, dev)
+        vel = torch.tensor(v0, dtype=torch.float64, device=dev)
+        rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 7.0)
+        _, F, _ = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
+        ep, ek, nreb = model.verlet_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0,
+                                         0.5, 1.0, 40, every, F)
+        torch.cuda.synchronize()
+        outs.append((pos.cpu().numpy(), vel.cpu().numpy(), F.cpu().numpy(), ep.cpu().numpy(),
+                     ek.cpu().numpy(), nreb))
+    a, b = outs
+    assert a[5] == b[5] and a[5] >= 2
+    for x, y in zip(a[:5], b[:5]):
+        assert np.array_equal(x, y)
