@@ -197,14 +197,17 @@ int dpa4c_debug_stages(const dpa4c_model* model, int64_t N, float* node_state,
                        float* descriptor, int32_t* edge_count, void* stream);
 
 /*
- * Per-stage timing.  When enabled, the library records HIP events around
- * every kernel it launches on the caller's stream and accumulates their
- * durations per stage.  dpa4c_get_timings writes up to ``n`` stage times
- * (milliseconds, summed over calls since the last reset) to ``ms``, launch
- * counts to ``count`` (either may be NULL) and returns the number of stages;
+ * Per-stage timing.  For every stage s whose bit (1 << s) is set in
+ * ``stage_mask`` (0: none, -1: all), the library records HIP events around
+ * the kernels of that stage on the caller's stream and accumulates their
+ * durations.  The events cost a few microseconds per stage and launch, so
+ * timing only the stage of interest keeps a timed run close to an untimed
+ * one.  dpa4c_get_timings writes up to ``n`` stage times (milliseconds,
+ * summed over calls since the last read) to ``ms``, launch counts to
+ * ``count`` (either may be NULL) and returns the number of stages;
  * dpa4c_stage_name gives their names.  Reading synchronises the device.
  */
-int dpa4c_set_timing(dpa4c_model* model, int enable);
+int dpa4c_set_timing(dpa4c_model* model, int64_t stage_mask);
 int dpa4c_get_timings(dpa4c_model* model, double* ms, int64_t* count, int n);
 const char* dpa4c_stage_name(int stage);
 

@@ -53,7 +53,7 @@ def library():
             "verlet_step": (i32, [vp, vp, vp, vp, vp, i64, vp, vp, dbl, dbl, dbl, i32, i32,
                                   vp, vp, vp, ctypes.POINTER(i64), vp]),
             "dpa4c_debug_stages": (i32, [vp, i64, vp, vp, vp, vp]),
-            "dpa4c_set_timing": (i32, [vp, i32]),
+            "dpa4c_set_timing": (i32, [vp, i64]),
             "dpa4c_get_timings": (i32, [vp, vp, vp, i32]),
             "dpa4c_stage_name": (ctypes.c_char_p, [i32]),
             "dpa4c_debug_gemm": (i32, [vp, vp, vp, i32, i32, i32, vp]),
@@ -71,6 +71,17 @@ def exported_symbols() -> list[str]:
     return ["dpa4c_model_create", "dpa4c_model_destroy", "dpa4c_model_info", "build_neighbors",
             "compute_energy_forces", "verlet_step", "dpa4c_debug_stages", "dpa4c_set_timing",
             "dpa4c_get_timings", "dpa4c_stage_name", "dpa4c_debug_gemm", "dpa4c_last_error"]
+
+
+def stage_names() -> list[str]:
+    """Names of the timed stages, in stage-index order."""
+    lib = library()
+    names = []
+    while True:
+        name = lib.dpa4c_stage_name(len(names)).decode()
+        if name == "?":
+            return names
+        names.append(name)
 
 
 def _check(rc: int):
@@ -231,8 +242,18 @@ class Model:
                                             _stream(stream)))
         return node, desc, cnt
 
-    def set_timing(self, on: bool):
-        _check(library().dpa4c_set_timing(self._h, int(bool(on))))
+    def set_timing(self, on=True):
+        """True: time every stage; False: none; a list of stage names: those."""
+        if on is True:
+            mask = -1
+        elif not on:
+            mask = 0
+        else:
+            names = stage_names()
+            mask = 0
+            for name in on:
+                mask |= 1 << names.index(name)
+        _check(library().dpa4c_set_timing(self._h, mask))
 
     def timings(self) -> dict:
         """{stage name: (milliseconds, launches)} since the last read."""

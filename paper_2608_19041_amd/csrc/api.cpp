@@ -84,7 +84,7 @@ struct StageScope {
   size_t slot = SIZE_MAX;
   StageScope(const dpa4c_model* mm, int s, hipStream_t stream)
       : m(const_cast<dpa4c_model*>(mm)), st(stream), stage(s) {
-    if (!m || !m->timing.enabled) return;
+    if (!m || !((m->timing.mask >> s) & 1)) return;
     Timing& t = m->timing;
     if (t.used + 2 > t.pool.size()) {
       size_t grow = t.pool.size() < 256 ? 256 : t.pool.size();
@@ -601,14 +601,14 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   return 0;
 }
 
-int dpa4c_set_timing(dpa4c_model* m, int enable) {
+int dpa4c_set_timing(dpa4c_model* m, int64_t stage_mask) {
   if (!m) {
     set_error("dpa4c_set_timing: null model");
     return DPA4C_ERR_INVALID_ARG;
   }
   DeviceGuard guard(m->device);
   collect_timing(m);
-  m->timing.enabled = enable != 0;
+  m->timing.mask = stage_mask;
   return 0;
 }
 

@@ -92,7 +92,7 @@ struct Workspace {
 };
 
 struct Timing {
-  bool enabled = false;
+  int64_t mask = 0;               // stages (bit s = stage s) that record events
   std::vector<hipEvent_t> pool;
   std::vector<int> ev_stage;      // stage of each recorded pair
   size_t used = 0;
