@@ -231,6 +231,44 @@ def test_energy_forces_config2_sampled(dev, dp):
     assert np.abs(F[ks] - ref_f[ks]).max() < F_TOL
 
 
+@pytest.mark.parametrize("workload", ["bcc_hea31250_full", "water24000_full", "fcc1m_full"])
+def test_energy_forces_large_sampled(dev, dp, workload):
+    """Configs 3-5 at full size (five-species alloy, two-species liquid,
+    1,000,188-atom crystal): E_i of sampled centres and forces of sampled
+    atoms, each against the oracle evaluated on exactly the centres it needs."""
+    model, oracle, _ = gpu_model(dp, "full")
+    s = synth.make_workload(workload)[0]
+    ea, F, et = evaluate(dp, model, s, dev)
+    rng = np.random.Generator(np.random.PCG64(17))
+    ks = np.unique(np.concatenate([[0, s.n - 1], rng.choice(s.n, 3, replace=False)])).astype(np.int64)
+    _, ej, _ = onb.neighbor_list(s.pos, s.cell, s.pbc, 6.0, centres=ks)
+    centres = np.unique(np.concatenate([ks, ej]))
+    ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc, centres=centres)
+    assert np.abs(ea[centres] - ref_e).max() < E_TOL
+    assert np.abs(F[ks] - ref_f[ks]).max() < F_TOL
+    assert np.isfinite(et)
+
+
+@pytest.mark.parametrize("name", ["small", "full"])
+def test_atoms_without_neighbours(dev, dp, name):
+    """Degenerate rows: an isolated atom (no pair at all), and two atoms
+    6.5 A apart, inside the 7 A skin list but outside the cutoff, so their
+    rows hold skin pairs that compaction removes.  Forces vanish and E_i is
+    the readout of an empty neighbourhood."""
+    model, oracle, _ = gpu_model(dp, name)
+    box = np.diag([20.0, 20.0, 20.0])
+    one = synth.System("one", np.array([[3.0, 4.0, 5.0]]), np.array([28], np.int32), box,
+                       np.ones(3, np.int32), synth._mass_table(), {})
+    two = synth.System("two", np.array([[3.0, 4.0, 5.0], [9.5, 4.0, 5.0]]),
+                       np.array([28, 28], np.int32), box, np.ones(3, np.int32),
+                       synth._mass_table(), {})
+    for s in (one, two):
+        ea, F, et = evaluate(dp, model, s, dev)
+        ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc)
+        assert np.abs(ea - ref_e).max() < E_TOL
+        assert np.abs(F).max() == 0.0 and np.abs(ref_f).max() < 1e-12
+
+
 def test_runs_are_bit_identical(dev, dp):
     model, _, _ = gpu_model(dp, "full")
     s = synth.make_workload("fcc4000_full")[0]
