@@ -4,7 +4,7 @@
 
 A step is one velocity-Verlet NVE step through the C ABI (verlet_step):
 half kick, drift and displacement check, a cell-list rebuild when due,
-compaction of the skin list, the fused forward edge kernel, the per-atom
+the fused forward edge kernel (which first compacts its skin row), the per-atom
 kernel (readout, MLP forward and input gradient on the matrix cores,
 readout VJP), the fused backward edge kernel, force assembly and the
 second half kick with the energy sums.  Inputs are synthetic (seeded
@@ -53,7 +53,7 @@ DESCRIPTIONS = {
 }
 
 
-def stage_work(name, spec, n_atoms, n_edges, n_skin):
+def stage_work(name, spec, n_atoms, n_edges):
     """Algorithmic work of one launch of a stage: (bound, amount, unit).
 
     Per-edge and per-atom figures (full-width profile numbers in comments):
@@ -67,8 +67,9 @@ def stage_work(name, spec, n_atoms, n_edges, n_skin):
       per-atom kernel      - matrix cores: forward and input-gradient
         products of the MLP, 2 x 2 (D_out F + (L-1) F^2) flop per atom (the
         readout and its VJP add ~1% VALU work, not counted)
-      forces               - HBM: per edge 16 B gradient + 16 B gathered
-        reverse gradient + 4 B reverse index, 24 B per atom out
+      forces               - HBM: per edge 16 B gradient, 12 B for the
+        reverse slot (sidx, skin_rev, cidx) and 16 B gathered reverse
+        gradient; per atom 12 B row bounds in, 24 B force out
     """
     C0, R, L = spec.C0, spec.R, spec.L
     C1 = max(4, 1 << math.ceil(0.5 * math.log2(C0)))
@@ -82,15 +83,11 @@ def stage_work(name, spec, n_atoms, n_edges, n_skin):
     if name == "backward":
         per_edge = 2 * (9 * (C0 + R) + 2 * (1 + R) * C0 + 2 * S + 3 * (S - C0))
         return "alu", per_edge * n_edges, "flop"
-    if name in ("mlp_forward", "mlp_backward"):
-        return "mfma", 2 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "atoms":
         # per-atom kernel: forward and input-gradient products of the MLP
         return "mfma", 4 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "forces":
-        return "hbm", 36 * n_edges + 24 * n_atoms, "byte"
-    if name == "compact":
-        return "hbm", 8 * n_skin + 16 * n_edges + 24 * n_atoms, "byte"
+        return "hbm", 44 * n_edges + 36 * n_atoms, "byte"
     return None
 
 
@@ -100,7 +97,6 @@ STAGE_KERNELS = {
     "forward": ("forward_kernel", "forward.hip"),
     "backward": ("backward_kernel", "backward.hip"),
     "forces": ("forces_kernel", "assemble.hip"),
-    "compact": ("compact_kernel", "neighbors.hip"),
 }
 
 
@@ -235,11 +231,10 @@ def main():
     tt = np.arange(len(et)) * dt * 1e-3
     drift = float(np.polyfit(tt, et / system.n, 1)[0]) if len(et) > 2 else None
 
-    n_skin = None
     stage_ms = {k: v[0] for k, v in stages.items() if v[1]}
     stage_cnt = {k: v[1] for k, v in stages.items() if v[1]}
     roof = None
-    work = stage_work(dominant, spec, system.n, n_edges, n_skin or 0)
+    work = stage_work(dominant, spec, system.n, n_edges)
     if work:
         bound, amount, unit = work
         avg_s = stage_ms[dominant] / stage_cnt[dominant] * 1e-3

@@ -191,6 +191,8 @@ int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_
  *               features Y (degree -> m -> channel)]   Eq. (payload)
  *   descriptor  float32 [N][D_out]: calibrated D       Eq. (calibration)
  *   edge_count  int32 [N]: edges within r_c per centre
+ * The stages are recomputed from the inputs of that call (positions,
+ * species and skin list), which must still hold the same values.
  * Synchronous on ``stream``.
  */
 int dpa4c_debug_stages(const dpa4c_model* model, int64_t N, float* node_state,

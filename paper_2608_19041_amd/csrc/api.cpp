@@ -123,19 +123,17 @@ void collect_timing(dpa4c_model* m) {
 int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   Workspace& w = m->ws;
   const int64_t nn = n < 1 ? 1 : n, cc = cap < 1 ? 1 : cap;
-  const int dstr = (m->D_out + 15) / 16 * 16;
   if (w.ecount.ensure(4 * nn) || w.edge.ensure(16 * cc) || w.cidx.ensure(4 * cc) ||
-      w.sidx.ensure(4 * cc) || w.rev.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
+      w.sidx.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
       w.skin_rev.ensure(4 * cc) || w.node.ensure(4 * nn * (m->S + 2)) ||
       w.node_grad.ensure(4 * nn * (m->S + 2)) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
       w.flags.ensure(8 * 8) || w.eatom.ensure(8 * nn))
     return DPA4C_ERR_HIP;
-  (void)dstr;
   return 0;
 }
 
-// Everything after the skin list: compaction, reverse index, forward,
-// MLP, backward, forces and the energy sum.
+// Everything after the skin list: forward (with the compaction of the skin
+// rows), per-atom kernel, backward, forces and the energy sum.
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
               const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
@@ -145,23 +143,12 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
   int rc;
-  {
-    StageScope t(m, kStCompact, st);
-    rc = launch_compact_edges(pos, n, g, rcq, box, row_ptr, nbr_j, nbr_shift, cap,
-                              w.ecount.as<int32_t>(), w.edge.as<float4>(), w.cidx.as<int32_t>(),
-                              w.sidx.as<int32_t>(), st);
-    if (rc) return rc;
-  }
-  {
-    StageScope t(m, kStRev, st);
-    rc = launch_rev(row_ptr, w.ecount.as<int32_t>(), w.sidx.as<int32_t>(), skin_rev,
-                    w.cidx.as<int32_t>(), n, w.rev.as<int32_t>(), st);
-    if (rc) return rc;
-  }
+  CompactArgs ca{pos, nbr_j, nbr_shift, g.Lq[0], g.Lq[1], g.Lq[2], rcq, box[0], box[1], box[2],
+                 cap, w.ecount.as<int32_t>(), w.edge.as<float4>(), w.cidx.as<int32_t>(),
+                 w.sidx.as<int32_t>()};
   {
     StageScope t(m, kStForward, st);
-    rc = launch_forward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                        w.node.as<float>(), st);
+    rc = launch_forward(m, n, species, row_ptr, ca, w.node.as<float>(), st);
     if (rc) return rc;
   }
   {
@@ -179,7 +166,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStForces, st);
     rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.grad.as<float4>(),
-                       w.rev.as<int32_t>(), forces, st);
+                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, st);
     if (rc) return rc;
   }
   if (e_total) {
@@ -188,7 +175,15 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   }
   m->last_n = n;
   w.last_species = species;
+  w.last_pos = pos;
+  for (int a = 0; a < 3; ++a) w.last_Lq[a] = g.Lq[a];
+  w.last_box[0] = box[0];
+  w.last_box[1] = box[1];
+  w.last_box[2] = box[2];
   w.skin_row_used = row_ptr;
+  w.skin_j_used = nbr_j;
+  w.skin_shift_used = nbr_shift;
+  w.cap_used = cap;
   return rc;
 }
 
@@ -218,8 +213,8 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   hipDeviceSynchronize();
   m->params.release();
   Workspace& w = m->ws;
-  DevBuf* bufs[] = {&w.skin_row, &w.skin_row_new, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
-                    &w.edge,     &w.cidx,   &w.sidx,       &w.rev,      &w.grad,   &w.node,
+  DevBuf* bufs[] = {&w.skin_row, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
+                    &w.edge,     &w.cidx,   &w.sidx,       &w.grad,   &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
@@ -284,7 +279,7 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
   }
   int64_t* flags = fl->as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
-  rc = build_skin_list(*nb, pos, N, g, row_ptr, nullptr, nullptr, cap, nullptr, flags, false, st);
+  rc = build_skin_list(*nb, pos, N, g, row_ptr, nullptr, nullptr, cap, flags, false, st);
   if (rc) return rc;
   DPA4C_HIP_TRY(hipMemcpyAsync(hflag, row_ptr + N, 8, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 1, flags, 8, hipMemcpyDeviceToHost, st));
@@ -342,7 +337,7 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
   if (rc) return rc;
   {
     StageScope t(m, kStSkinRev, st);
-    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), nullptr, st);
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), st);
     if (rc) return rc;
   }
   return run_model(m, pos, species, N, g, box, row_ptr, nbr_j, nbr_shift, n_pairs,
@@ -392,8 +387,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   const int np_tail = tail_partial_count(N);
   if (w.inv_mass.ensure(8 * T1) || w.mass.ensure(8 * T1) || w.flags.ensure(64) ||
       w.tailpart.ensure(16 * size_t(np_tail)) ||
-      w.skin_row.ensure(8 * (N + 1)) || w.skin_row_new.ensure(8 * (N + 1)) ||
-      w.qbuild.ensure(8 * 3 * N))
+      w.skin_row.ensure(8 * (N + 1)) || w.qbuild.ensure(8 * 3 * N))
     return DPA4C_ERR_HIP;
   if (!w.host_flags) DPA4C_HIP_TRY(hipHostMalloc((void**)&w.host_flags, 64, hipHostMallocDefault));
   {
@@ -410,9 +404,13 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   // a build of the skin list: count, read the size back, grow the capacity
   // if needed, fill, reverse index and the positions of the build
   auto initial_build = [&]() -> int {
-    int r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,
-                            nullptr, flags, false, st);
-    if (r) return r;
+    int r;
+    {
+      StageScope t(m, kStNeighbor, st);
+      r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,
+                          flags, false, st);
+      if (r) return r;
+    }
     DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, w.skin_row.as<int64_t>() + N, 8,
                                  hipMemcpyDeviceToHost, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags + 1, flags, 8, hipMemcpyDeviceToHost, st));
@@ -431,16 +429,14 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     }
     r = ensure_workspace(mm, N, w.cap);
     if (r) return r;
-    {
-      StageScope t(m, kStNeighborFill, st);
-      r = fill_skin_list(w.nb, N, g_list, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
-                         w.skin_shift.as<int32_t>(), w.cap, flags, st);
-      if (r) return r;
-    }
-    r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.skin_rev.as<int32_t>(), nullptr, st);
+    StageScope t(m, kStNeighbor, st);
+    r = fill_skin_list(w.nb, N, g_list, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
+                       w.skin_shift.as<int32_t>(), w.cap, flags, st);
     if (r) return r;
-    return launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), nullptr, st);
+    r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
+                        N, w.skin_rev.as<int32_t>(), st);
+    if (r) return r;
+    return launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
   };
 
   int64_t rebuilds = 0;
@@ -583,8 +579,11 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (N == 0) return 0;
   // recompute node state and descriptor from the stored compacted edges
-  int rc = launch_forward(m, N, w.last_species, w.skin_row_used, w.ecount.as<int32_t>(),
-                          w.edge.as<float4>(), w.node.as<float>(), st);
+  CompactArgs ca{w.last_pos, w.skin_j_used, w.skin_shift_used, w.last_Lq[0],
+                 w.last_Lq[1], w.last_Lq[2], qfix_host(m->r_c), w.last_box[0],
+                 w.last_box[1], w.last_box[2], w.cap_used, w.ecount.as<int32_t>(),
+                 w.edge.as<float4>(), w.cidx.as<int32_t>(), w.sidx.as<int32_t>()};
+  int rc = launch_forward(m, N, w.last_species, w.skin_row_used, ca, w.node.as<float>(), st);
   if (rc) return rc;
   if (w.desc.ensure(size_t(4) * N * m->D_out) || w.eatom.ensure(size_t(8) * N)) return DPA4C_ERR_HIP;
   rc = launch_atoms(m, N, w.last_species, w.node.as<float>(), w.node_grad.as<float>(),

@@ -1,8 +1,8 @@
 // Force assembly, energy reduction and velocity-Verlet kernels.
 //
 // Forces, Eq. (forces): F_k = sum_{j in N_k} dE/dr_kj - sum_{i: k in N_i} dE/dr_ik.
-// Every edge e = (k -> j, n) of row k has a reverse edge rev[e] = (j -> k, -n)
-// in row j, so F_k = sum over row k of (g_e - g_rev[e]): one reduction per
+// Every edge e = (k -> j, n) of row k has a reverse edge rev(e) = (j -> k, -n)
+// in row j, so F_k = sum over row k of (g_e - g_rev(e)): one reduction per
 // atom over its own row, in a fixed order, in float64, with no atomics.
 // The total energy is a fixed-order two-pass float64 sum.
 #include <hip/hip_runtime.h>
@@ -19,10 +19,14 @@ constexpr int kLanesPerAtom = 16;
 constexpr int kRedBlock = 256;
 constexpr int kRedPer = 16;                 // elements per thread in the first pass
 
+// The reverse of compact slot s is cidx[skin_rev[sidx[s]]]: the compact slot
+// of the reverse skin edge (every edge inside r_c has its reverse inside r_c).
 __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
                                                         const float4* __restrict__ grad,
-                                                        const int32_t* __restrict__ rev,
+                                                        const int32_t* __restrict__ sidx,
+                                                        const int32_t* __restrict__ skin_rev,
+                                                        const int32_t* __restrict__ cidx,
                                                         double* __restrict__ forces) {
   const int sub = threadIdx.x % kLanesPerAtom;
   const int64_t per_grid = int64_t(gridDim.x) * (kBlock / kLanesPerAtom);
@@ -32,7 +36,9 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
     double fx = 0.0, fy = 0.0, fz = 0.0;
     for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
       const float4 g = grad[s];
-      const float4 r = grad[rev[s]];
+      const int32_t sr = skin_rev[sidx[s]];
+      const int32_t c = sr >= 0 ? cidx[sr] : -1;
+      const float4 r = c >= 0 ? grad[c] : g;   // a valid list always has the reverse
       fx += double(g.x) - double(r.x);
       fy += double(g.y) - double(r.y);
       fz += double(g.z) - double(r.z);
@@ -210,9 +216,7 @@ __global__ void __launch_bounds__(kBlock) final_step_kernel(StepSums prev) {
 }
 
 __global__ void __launch_bounds__(kBlock) snapshot_kernel(const double* __restrict__ pos, int64_t n,
-                                                          int64_t* __restrict__ qbuild,
-                                                          const int64_t* active) {
-  if (active && *active == 0) return;
+                                                          int64_t* __restrict__ qbuild) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= 3 * n) return;
   qbuild[i] = qfix(pos[i]);
@@ -220,13 +224,6 @@ __global__ void __launch_bounds__(kBlock) snapshot_kernel(const double* __restri
 
 __global__ void set_flag_kernel(int64_t* flags, int idx, int64_t value) {
   if (threadIdx.x == 0) flags[idx] = value;
-}
-
-__global__ void rebuild_done_kernel(int64_t* flags) {
-  if (threadIdx.x == 0 && flags[1]) {
-    flags[1] = 0;
-    flags[3] += 1;
-  }
 }
 
 int blocks_for(int64_t n) {
@@ -237,12 +234,13 @@ int blocks_for(int64_t n) {
 }  // namespace
 
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* rev, double* forces, hipStream_t st) {
+                  const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
+                  double* forces, hipStream_t st) {
   int64_t blocks = (n + (kBlock / kLanesPerAtom) - 1) / (kBlock / kLanesPerAtom);
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(forces_kernel, dim3(blocks), dim3(kBlock), 0, st, n, row_ptr, ecount, grad,
-                     rev, forces);
+                     sidx, skin_rev, cidx, forces);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -280,22 +278,14 @@ int launch_final_step(StepSums prev, hipStream_t st) {
 
 int tail_partial_count(int64_t n) { return blocks_for(n); }
 
-int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, const int64_t* active,
-                      hipStream_t st) {
-  hipLaunchKernelGGL(snapshot_kernel, dim3(blocks_for(3 * n)), dim3(kBlock), 0, st, pos, n, qbuild,
-                     active);
+int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st) {
+  hipLaunchKernelGGL(snapshot_kernel, dim3(blocks_for(3 * n)), dim3(kBlock), 0, st, pos, n, qbuild);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
 
 int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st) {
   hipLaunchKernelGGL(set_flag_kernel, dim3(1), dim3(64), 0, st, flags, idx, value);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
-int launch_rebuild_done(int64_t* flags, hipStream_t st) {
-  hipLaunchKernelGGL(rebuild_done_kernel, dim3(1), dim3(64), 0, st, flags);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

@@ -106,7 +106,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
       float chi, dchi;
-      envelope(g.rho, md.r_c, &chi, &dchi);
+      envelope(g.rho, md.inv_rc, &chi, &dchi);
       float tau;
       const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
       const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;

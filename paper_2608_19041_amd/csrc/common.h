@@ -78,6 +78,7 @@ struct ModelDev {
   int n_rows;
   float inv_delta;
   float r_c;
+  float inv_rc;             // 1 / r_c
   int n_types1;             // T + 1
   const float* pair;        // [(T+1)^2][CPL][LPE][PW]
   const float* type_embed;  // [T+1][C0]

@@ -1,0 +1,102 @@
+// Per-row compaction of the skin list to the edges inside r_c (Eq.
+// (neighbor-set) with the fixed-point predicate of the neighbour builder),
+// done by the workgroup that then evaluates the row.
+#pragma once
+
+#include "common.h"
+#include "edge_math.h"
+
+namespace dpa4c {
+
+// inputs and outputs of the compaction (one struct, passed by value)
+struct CompactArgs {
+  const double* pos;          // [N][3]
+  const int32_t* nbr_j;       // skin list
+  const int32_t* nbr_shift;
+  int64_t Lq0, Lq1, Lq2;      // box lengths, fixed point
+  int64_t rcq;                // cutoff, fixed point
+  double L0, L1, L2;          // box lengths, Angstrom
+  int64_t cap;                // skin-list capacity
+  int32_t* ecount;            // [N] out: edges kept per row
+  float4* edge;               // [cap] out: (r_ij, bits of j) at the head of each skin row
+  int32_t* cidx;              // [cap] out: compact slot of each skin edge, or -1
+  int32_t* sidx;              // [cap] out: skin edge of each compact slot
+};
+
+__device__ inline int64_t qfix_dev(double x) {
+  return static_cast<int64_t>(__builtin_rint(x * kQScale));
+}
+
+// strictly within the fixed-point radius; components are rejected before
+// squaring, so nothing overflows
+__device__ inline bool within_q(int64_t dx, int64_t dy, int64_t dz, int64_t rq) {
+  if (dx >= rq || dx <= -rq || dy >= rq || dy <= -rq || dz >= rq || dz <= -rq) return false;
+  return dx * dx + dy * dy + dz * dz < rq * rq;
+}
+
+// Keeps the skin edges of row i inside r_c, in canonical order, and writes
+// their records r_ij = (r_j + n.h) - r_i (float64 difference stored as
+// float32) to the first slots of the row.  All TEAM threads of the
+// workgroup take part; ``wtot`` is LDS scratch of TEAM/64 ints.  Returns
+// the number kept (the same in every thread); the records are visible to
+// the whole workgroup on return.
+template <int TEAM>
+__device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, int64_t b, int64_t e,
+                                  int* wtot) {
+  constexpr int W = TEAM / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const double xi = a.pos[3 * i], yi = a.pos[3 * i + 1], zi = a.pos[3 * i + 2];
+  const int64_t qi0 = qfix_dev(xi), qi1 = qfix_dev(yi), qi2 = qfix_dev(zi);
+  if (b < 0 || e > a.cap || e < b) e = b;   // malformed row: keep nothing
+  int kept = 0;
+  for (int64_t base = b; base < e; base += TEAM) {
+    const int64_t s = base + tid;
+    bool pred = false;
+    int32_t j = 0;
+    int nx = 0, ny = 0, nz = 0;
+    if (s < e) {
+      j = a.nbr_j[s];
+      const int32_t sh = a.nbr_shift[s];
+      nx = unpack_x(sh);
+      ny = unpack_y(sh);
+      nz = unpack_z(sh);
+      if (j >= 0 && j < n) {
+        const int64_t dx = qfix_dev(a.pos[3 * j]) + nx * a.Lq0 - qi0;
+        const int64_t dy = qfix_dev(a.pos[3 * j + 1]) + ny * a.Lq1 - qi1;
+        const int64_t dz = qfix_dev(a.pos[3 * j + 2]) + nz * a.Lq2 - qi2;
+        pred = within_q(dx, dy, dz, a.rcq);
+      }
+    }
+    const uint64_t m = __ballot(pred);
+    const int pre = __popcll(m & ((uint64_t(1) << lane) - 1));
+    if (lane == 0) wtot[wave] = __popcll(m);
+    __syncthreads();
+    int off = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+      const int c = wtot[w];
+      off += w < wave ? c : 0;
+      total += c;
+    }
+    if (s < e) {
+      if (pred) {
+        const int64_t slot = b + kept + off + pre;
+        const double rx = (a.pos[3 * j] + nx * a.L0) - xi;
+        const double ry = (a.pos[3 * j + 1] + ny * a.L1) - yi;
+        const double rz = (a.pos[3 * j + 2] + nz * a.L2) - zi;
+        a.edge[slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
+                                   static_cast<float>(rz), __int_as_float(j));
+        a.sidx[slot] = static_cast<int32_t>(s);
+        a.cidx[s] = static_cast<int32_t>(slot);
+      } else {
+        a.cidx[s] = -1;
+      }
+    }
+    kept += total;
+    __syncthreads();   // wtot is reused; the records are written
+  }
+  if (tid == 0) a.ecount[i] = kept;
+  return kept;
+}
+
+}  // namespace dpa4c

@@ -16,15 +16,17 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Eq. (edge-geometry) in float32
+// Eq. (edge-geometry) in float32: rho = sqrt(|r|^2 + eps^2) and u = r / rho
+// from one hardware reciprocal square root (v_rsq_f32, about 1 ulp; the
+// argument is at least eps^2 = 1e-14, far from denormals).
 struct EdgeGeom {
   float rho, ux, uy, uz, inv_rho;
 };
 __device__ inline EdgeGeom edge_geom(float rx, float ry, float rz) {
   EdgeGeom g;
-  float r2 = rx * rx + ry * ry + rz * rz + float(kEps * kEps);
-  g.rho = sqrtf(r2);
-  g.inv_rho = 1.0f / g.rho;
+  const float r2 = rx * rx + ry * ry + rz * rz + float(kEps * kEps);
+  g.inv_rho = __builtin_amdgcn_rsqf(r2);
+  g.rho = r2 * g.inv_rho;
   g.ux = rx * g.inv_rho;
   g.uy = ry * g.inv_rho;
   g.uz = rz * g.inv_rho;
@@ -33,15 +35,15 @@ __device__ inline EdgeGeom edge_geom(float rx, float ry, float rz) {
 
 // Eq. (envelope): chi = t^4 (1 + 4x + 10x^2 + 20x^3 + 35x^4), x = rho/r_c,
 // t = 1 - x, clipped; d chi / d rho = -280 x^4 t^3 / r_c.
-__device__ inline void envelope(float rho, float r_c, float* chi, float* dchi) {
-  float x = fminf(rho / r_c, 1.0f);
+__device__ inline void envelope(float rho, float inv_rc, float* chi, float* dchi) {
+  float x = fminf(rho * inv_rc, 1.0f);
   float t = 1.0f - x;
   float t2 = t * t;
   float p = 1.0f + x * (4.0f + x * (10.0f + x * (20.0f + x * 35.0f)));
   *chi = t2 * t2 * p;
   if (dchi) {
     float x2 = x * x;
-    *dchi = -280.0f * x2 * x2 * t2 * t / r_c;
+    *dchi = -280.0f * x2 * x2 * t2 * t * inv_rc;
   }
 }
 

@@ -1,10 +1,13 @@
-// Fused forward edge kernel: featurisation, single aggregation and readout.
+// Fused forward edge kernel: compaction, featurisation and single
+// aggregation.
 //
-// Methods Eqs. (edge-geometry) .. (moments): for every centre i, the edges of
-// its row are scanned once; per edge the envelope, the tabulated radial maps
+// Methods Eqs. (edge-geometry) .. (moments): for every centre i, the skin
+// row is first compacted to the edges inside r_c (compact.h), then those
+// edges are scanned once; per edge the envelope, the tabulated radial maps
 // g and q, the cached pair coefficients gamma, beta, U, the amplitude psi and
 // the harmonics are formed in registers and accumulated into the node state
-// [sum chi^2, sum chi^4, Y_lmc].  No per-edge quantity is written to memory.
+// [sum chi^2, sum chi^4, Y_lmc].  Apart from the compacted edge records, no
+// per-edge quantity is written to memory.
 // The readout runs in the per-atom kernel.
 //
 // Mapping: one 256-thread workgroup per centre (striding over centres).  The
@@ -16,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
+#include "compact.h"
 #include "edge_math.h"
 #include "launch.h"
 
@@ -30,11 +34,12 @@ template <class P, bool FOLD>
 __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
                                                         const int32_t* __restrict__ typ,
                                                         const int64_t* __restrict__ row_ptr,
-                                                        const int32_t* __restrict__ ecount,
-                                                        const float4* __restrict__ edge,
+                                                        CompactArgs ca,
                                                         float* __restrict__ node) {
   constexpr int G = kTeam / P::LPE;          // edge groups in the workgroup
   __shared__ float part[kWaves][P::NS];
+  __shared__ int wtot[kWaves];
+  const float4* __restrict__ edge = ca.edge;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1), wave = tid / kWave;
   const int grp = tid / P::LPE;
@@ -49,7 +54,8 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
   for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
     const int ai = type_of(i);
     const int64_t b = row_ptr[i];
-    const int cnt = ecount[i];
+    // the row's edges inside r_c, compacted to the head of its skin row
+    const int cnt = compact_row<kTeam>(ca, n, i, b, row_ptr[i + 1], wtot);
     float acc0[P::CPL];
 #pragma unroll
     for (int j = 0; j < P::CPL; ++j) acc0[j] = 0.0f;
@@ -87,7 +93,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
       float chi;
-      envelope(g.rho, md.r_c, &chi, nullptr);
+      envelope(g.rho, md.inv_rc, &chi, nullptr);
       if (!valid) chi = 0.0f;
       float tau;
       const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
@@ -204,15 +210,15 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 
 template <class P>
 int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_t* row_ptr,
-           const int32_t* ecount, const float4* edge, float* node, hipStream_t st) {
+           const CompactArgs& ca, float* node, hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
   if (m->fold_n > 0)
     hipLaunchKernelGGL((forward_kernel<P, true>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
-                       m->ws.fidx.as<int32_t>(), row_ptr, ecount, edge, node);
+                       m->ws.fidx.as<int32_t>(), row_ptr, ca, node);
   else
     hipLaunchKernelGGL((forward_kernel<P, false>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
-                       species, row_ptr, ecount, edge, node);
+                       species, row_ptr, ca, node);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -220,10 +226,9 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 }  // namespace
 
 int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
-                   const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                   float* node, hipStream_t st) {
-  if (m->C0 == 32) return launch<SmallProfile>(m, n, species, row_ptr, ecount, edge, node, st);
-  return launch<FullProfile>(m, n, species, row_ptr, ecount, edge, node, st);
+                   const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st) {
+  if (m->C0 == 32) return launch<SmallProfile>(m, n, species, row_ptr, ca, node, st);
+  return launch<FullProfile>(m, n, species, row_ptr, ca, node, st);
 }
 
 }  // namespace dpa4c

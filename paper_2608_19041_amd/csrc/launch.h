@@ -1,6 +1,7 @@
 // Kernel launchers (defined in the .hip sources) called by the host code.
 #pragma once
 
+#include "compact.h"
 #include "model.h"
 
 namespace dpa4c {
@@ -8,9 +9,7 @@ namespace dpa4c {
 int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out);
 int launch_pair_cache(dpa4c_model* m, const float* wp_in, const float* wp_out);
 
-// neighbour lists (orthorhombic, periodic); all on ``st``.  Kernels given a
-// non-null ``active`` pointer do nothing when *active == 0 (device-side
-// conditional rebuild).
+// neighbour lists (orthorhombic, periodic); all on ``st``
 struct CellGrid {
   int64_t Lq[3];      // box lengths in fixed point
   int nc[3];          // cells per axis
@@ -22,34 +21,22 @@ int make_grid(const double cell[9], int64_t rq, CellGrid* g);
 // bin, count and scan (row_ptr); with ``fill`` also the sorted rows
 int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const CellGrid& g,
                     int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift, int64_t cap,
-                    const int64_t* active, int64_t* flags, bool fill, hipStream_t st);
+                    int64_t* flags, bool fill, hipStream_t st);
 int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
                    hipStream_t st);
 // skin_rev[s] = index of the reverse of skin edge s
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int32_t* skin_rev, const int64_t* active, hipStream_t st);
-// keep skin edges inside radius rcq; padded rows at the skin offsets
-int launch_compact_edges(const double* pos, int64_t n, const CellGrid& g, int64_t rcq,
-                         const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
-                         const int32_t* nbr_shift, int64_t cap, int32_t* ecount, float4* edge,
-                         int32_t* cidx, int32_t* sidx, hipStream_t st);
-// live[0..n] = fresh[0..n] when fresh[n] <= cap, else raise the capacity flag
-int commit_rows(const int64_t* fresh, int64_t* live, int64_t n, int64_t cap, int64_t* flags,
-                const int64_t* active, hipStream_t st);
-int launch_rev(const int64_t* row_ptr, const int32_t* ecount, const int32_t* sidx,
-               const int32_t* skin_rev, const int32_t* cidx, int64_t n, int32_t* rev,
-               hipStream_t st);
-
+                    int64_t n, int32_t* skin_rev, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
 // index of every atom; synchronises ``st``
 int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream_t st);
 
 // model stages (the edge kernels read ws.fidx when the model has folded tables)
+// compaction of every skin row (compact.h) and the forward pass
 int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
-                   const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                   float* node, hipStream_t st);
+                   const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st);
 // readout + MLP + head + MLP gradient + readout VJP on 16-atom tiles;
 // desc_out (float [N][D_out]) receives D when not null
 int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
@@ -58,7 +45,8 @@ int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
                     const float* node_grad, float4* grad, hipStream_t st);
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* rev, double* forces, hipStream_t st);
+                  const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
+                  double* forces, hipStream_t st);
 int launch_energy(int64_t n, const double* e_atom, double* partials, double* out,
                   hipStream_t st);
 
@@ -88,12 +76,9 @@ int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* spe
                 const double* e_atom, double* part_e, double* part_k, hipStream_t st);
 int launch_final_step(StepSums prev, hipStream_t st);
 int tail_partial_count(int64_t n);
-int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, const int64_t* active,
-                      hipStream_t st);
-// flags[idx] = value when (cond == null or *cond != 0)
+int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st);
+// flags[idx] = value
 int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st);
-// after a conditional rebuild: if flags[1] then flags[1] = 0, flags[3] += 1
-int launch_rebuild_done(int64_t* flags, hipStream_t st);
 int partial_count(int64_t n);
 
 }  // namespace dpa4c

@@ -36,10 +36,10 @@ __device__ inline float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
 // acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for the
 // output tiles first + t * stride, t < MAXT.  Tiles past ``ntiles`` repeat
 // the last tile (their results are discarded by the caller), so every wave
-// runs the same straight-line code.  The B fragments of k-block kb+1 and the
-// A fragment are requested one k-block ahead (ping-pong registers), and the
-// MFMAs of one k-block are interleaved across tiles so that consecutive
-// instructions do not depend on each other.
+// runs the same straight-line code.  The B and A fragments are requested two
+// k-blocks ahead (three register sets), and the MFMAs of one k-block are
+// interleaved across tiles so that consecutive instructions do not depend on
+// each other.
 template <int MAXT>
 __device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int lda, int kblocks,
                                   const float4* __restrict__ Wf, int first, int stride, int ntiles,
@@ -61,28 +61,42 @@ __device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int ld
 #pragma unroll
     for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
   };
-  float4 b0[MAXT], b1[MAXT];
+  // three k-blocks of B and A in flight: k-block kb+2 is requested before the
+  // MFMAs of kb start (loads past the last k-block are clamped to it and
+  // never used)
+  const int last = kblocks - 1;
+  auto ld_b = [&](float4* b, int kk) {
+    const int kc = kk < last ? kk : last;
 #pragma unroll
-  for (int t = 0; t < MAXT; ++t) b0[t] = wp[t][0];
-  float4 a0 = *reinterpret_cast<const float4*>(ap);
+    for (int t = 0; t < MAXT; ++t) b[t] = wp[t][size_t(kc) * 64];
+  };
+  auto ld_a = [&](int kk) {
+    const int kc = kk < last ? kk : last;
+    return *reinterpret_cast<const float4*>(ap + kc * 16);
+  };
+  float4 b0[MAXT], b1[MAXT], b2[MAXT];
+  ld_b(b0, 0);
+  ld_b(b1, 1);
+  float4 a0 = ld_a(0), a1 = ld_a(1), a2;
   int kb = 0;
 #pragma unroll 1
-  for (; kb + 2 <= kblocks; kb += 2) {
-#pragma unroll
-    for (int t = 0; t < MAXT; ++t) b1[t] = wp[t][size_t(kb + 1) * 64];
-    const float4 a1 = *reinterpret_cast<const float4*>(ap + (kb + 1) * 16);
+  for (; kb + 3 <= kblocks; kb += 3) {
+    ld_b(b2, kb + 2);
+    a2 = ld_a(kb + 2);
     __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of the MFMAs
     step(a0, b0);
-    // unconditional (clamped) so that the loop body is straight-line code
-    // and the wait counts do not have to cover a skipped prefetch
-    const int kn = kb + 2 < kblocks ? kb + 2 : kblocks - 1;
-#pragma unroll
-    for (int t = 0; t < MAXT; ++t) b0[t] = wp[t][size_t(kn) * 64];
-    a0 = *reinterpret_cast<const float4*>(ap + kn * 16);
+    ld_b(b0, kb + 3);
+    a0 = ld_a(kb + 3);
     __builtin_amdgcn_sched_barrier(0);
     step(a1, b1);
+    ld_b(b1, kb + 4);
+    a1 = ld_a(kb + 4);
+    __builtin_amdgcn_sched_barrier(0);
+    step(a2, b2);
   }
-  if (kb < kblocks) step(a0, b0);   // odd number of k-blocks
+  // remaining one or two k-blocks, already in b0/a0 and b1/a1
+  if (kb < kblocks) step(a0, b0);
+  if (kb + 1 < kblocks) step(a1, b1);
 }
 
 struct MlpArgs {

@@ -38,10 +38,8 @@ void DevBuf::release() {
 }
 
 const char* stage_name(int s) {
-  static const char* names[kNumStages] = {
-      "neighbor_bin", "neighbor_count", "neighbor_scan", "neighbor_fill", "skin_rev",
-      "compact",      "rev",            "forward",       "atoms",         "backward",
-      "forces",       "energy",         "integrate"};
+  static const char* names[kNumStages] = {"neighbor", "skin_rev", "forward", "atoms",
+                                          "backward", "forces",   "energy",  "integrate"};
   return (s >= 0 && s < kNumStages) ? names[s] : "?";
 }
 
@@ -454,6 +452,7 @@ dpa4c::ModelDev dpa4c_model::dev() const {
   d.n_rows = n_rows;
   d.inv_delta = static_cast<float>(1.0 / delta);
   d.r_c = static_cast<float>(r_c);
+  d.inv_rc = static_cast<float>(1.0 / r_c);
   d.n_types1 = n_types + 1;
   d.pair = pair;
   d.type_embed = type_embed;

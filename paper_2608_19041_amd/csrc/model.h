@@ -11,13 +11,8 @@ struct dpa4c_model;
 namespace dpa4c {
 
 enum Stage {
-  kStNeighborBin = 0,
-  kStNeighborCount,
-  kStNeighborScan,
-  kStNeighborFill,
-  kStSkinRev,
-  kStCompact,
-  kStRev,
+  kStNeighbor = 0,   // skin-list builds (count, fill, reverse index, snapshot)
+  kStSkinRev,        // reverse index of a caller-built skin list
   kStForward,
   kStAtoms,
   kStBackward,
@@ -56,7 +51,6 @@ struct Workspace {
   int64_t cap = 0;
   // skin list owned by verlet_step
   DevBuf skin_row;      // int64 [N+1]
-  DevBuf skin_row_new;  // int64 [N+1]: scan of a device-side rebuild before commit
   DevBuf skin_j;        // int32 [cap]
   DevBuf skin_shift;    // int32 [cap]
   DevBuf skin_rev;      // int32 [cap]
@@ -66,7 +60,6 @@ struct Workspace {
   DevBuf edge;          // float4 [cap]: r_ij (x, y, z) and j (bits)
   DevBuf cidx;          // int32 [cap]: compact slot of each skin edge or -1
   DevBuf sidx;          // int32 [cap]: skin edge of each compact slot
-  DevBuf rev;           // int32 [cap]
   DevBuf grad;          // float4 [cap]: dE/dr_ij
   // per-atom state
   DevBuf node;          // float [N][NS]
@@ -86,8 +79,15 @@ struct Workspace {
   DevBuf fold_mask;     // uint32 [4]: species present in the last call
   DevBuf fidx;          // int32 [N]: folded index of every atom
   uint32_t* fold_host = nullptr;          // pinned
-  const int32_t* last_species = nullptr;  // inputs of the last evaluation
+  // inputs of the last evaluation (the stage-check entry point re-runs it)
+  const int32_t* last_species = nullptr;
+  const double* last_pos = nullptr;
   const int64_t* skin_row_used = nullptr;
+  const int32_t* skin_j_used = nullptr;
+  const int32_t* skin_shift_used = nullptr;
+  int64_t cap_used = 0;
+  int64_t last_Lq[3] = {};
+  double last_box[3] = {};
   NeighborScratch nb;
 };
 

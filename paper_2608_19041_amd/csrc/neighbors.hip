@@ -48,8 +48,6 @@ __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-__device__ inline bool inactive(const int64_t* active) { return active && *active == 0; }
-
 struct GridDev {
   int64_t Lq0, Lq1, Lq2;
   int nc0, nc1, nc2;
@@ -70,9 +68,7 @@ __device__ inline bool within(int64_t dx, int64_t dy, int64_t dz, int64_t rq) {
 }
 
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kBlock) zero_i32_kernel(int32_t* __restrict__ p, int64_t n,
-                                                          const int64_t* active) {
-  if (inactive(active)) return;
+__global__ void __launch_bounds__(kBlock) zero_i32_kernel(int32_t* __restrict__ p, int64_t n) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i < n) p[i] = 0;
 }
@@ -82,9 +78,7 @@ __global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ 
                                                      int32_t* __restrict__ wrap,
                                                      int32_t* __restrict__ cell_of,
                                                      int32_t* __restrict__ cell_cnt,
-                                                     int64_t* __restrict__ flags,
-                                                     const int64_t* active) {
-  if (inactive(active)) return;
+                                                     int64_t* __restrict__ flags) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= n) return;
   const int64_t Lq[3] = {g.Lq0, g.Lq1, g.Lq2};
@@ -113,9 +107,7 @@ __global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ 
 // exclusive scan of the (few thousand) cell counts in one block
 __global__ void __launch_bounds__(1024) cell_scan_kernel(const int32_t* __restrict__ cnt,
                                                          int64_t ncell, int32_t* __restrict__ start,
-                                                         int32_t* __restrict__ fill,
-                                                         const int64_t* active) {
-  if (inactive(active)) return;
+                                                         int32_t* __restrict__ fill) {
   __shared__ int32_t part[1024];
   int64_t per = (ncell + 1023) / 1024;
   int64_t b = threadIdx.x * per, e = b + per < ncell ? b + per : ncell;
@@ -144,9 +136,7 @@ __global__ void __launch_bounds__(1024) cell_scan_kernel(const int32_t* __restri
 __global__ void __launch_bounds__(kBlock) place_kernel(int64_t n, const int32_t* __restrict__ cell_of,
                                                        const int32_t* __restrict__ start,
                                                        int32_t* __restrict__ fill,
-                                                       int32_t* __restrict__ atoms,
-                                                       const int64_t* active) {
-  if (inactive(active)) return;
+                                                       int32_t* __restrict__ atoms) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= n) return;
   int cid = cell_of[i];
@@ -209,9 +199,7 @@ __global__ void __launch_bounds__(kBlock) count_kernel(int64_t n, GridDev g,
                                                        const int32_t* __restrict__ wrap,
                                                        const int32_t* __restrict__ start,
                                                        const int32_t* __restrict__ atoms,
-                                                       int64_t* __restrict__ counts,
-                                                       const int64_t* active) {
-  if (inactive(active)) return;
+                                                       int64_t* __restrict__ counts) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
     int64_t total = 0;
@@ -245,9 +233,7 @@ __device__ inline int64_t block_exclusive_scan(int64_t v, int64_t* sh, int64_t* 
 
 __global__ void __launch_bounds__(kBlock) scan_partials_kernel(const int64_t* __restrict__ in,
                                                                int64_t n,
-                                                               int64_t* __restrict__ partials,
-                                                               const int64_t* active) {
-  if (inactive(active)) return;
+                                                               int64_t* __restrict__ partials) {
   __shared__ int64_t sh[kBlock];
   int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
   int64_t s = 0;
@@ -259,8 +245,7 @@ __global__ void __launch_bounds__(kBlock) scan_partials_kernel(const int64_t* __
 }
 
 __global__ void __launch_bounds__(kBlock) scan_top_kernel(int64_t* __restrict__ partials,
-                                                          int64_t nparts, const int64_t* active) {
-  if (inactive(active)) return;
+                                                          int64_t nparts) {
   __shared__ int64_t sh[kBlock];
   int64_t carry = 0;
   for (int64_t b = 0; b < nparts; b += kBlock) {
@@ -276,9 +261,7 @@ __global__ void __launch_bounds__(kBlock) scan_top_kernel(int64_t* __restrict__ 
 __global__ void __launch_bounds__(kBlock) scan_apply_kernel(const int64_t* __restrict__ in,
                                                             int64_t n,
                                                             const int64_t* __restrict__ partials,
-                                                            int64_t* __restrict__ out,
-                                                            const int64_t* active) {
-  if (inactive(active)) return;
+                                                            int64_t* __restrict__ out) {
   __shared__ int64_t sh[kBlock];
   int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
   int64_t v[kScanPer];
@@ -297,16 +280,15 @@ __global__ void __launch_bounds__(kBlock) scan_apply_kernel(const int64_t* __res
 }
 
 int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
-                   const int64_t* active, hipStream_t st) {
+                   hipStream_t st) {
   int64_t nb = (n + kScanTile - 1) / kScanTile;
   if (nb == 0) nb = 1;
   if (partials.ensure(sizeof(int64_t) * nb)) return DPA4C_ERR_HIP;
   hipLaunchKernelGGL(scan_partials_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
-                     partials.as<int64_t>(), active);
-  hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kBlock), 0, st, partials.as<int64_t>(), nb,
-                     active);
+                     partials.as<int64_t>());
+  hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kBlock), 0, st, partials.as<int64_t>(), nb);
   hipLaunchKernelGGL(scan_apply_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
-                     partials.as<int64_t>(), out, active);
+                     partials.as<int64_t>(), out);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -320,9 +302,7 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       const int64_t* __restrict__ row_ptr,
                                                       int32_t* __restrict__ nbr_j,
                                                       int32_t* __restrict__ nbr_shift, int64_t cap,
-                                                      int64_t* __restrict__ flags,
-                                                      const int64_t* active) {
-  if (inactive(active)) return;
+                                                      int64_t* __restrict__ flags) {
   __shared__ int64_t keys_all[kWavesPerBlock][kMaxRow];
   if (row_ptr[n] > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -391,9 +371,7 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                           const int32_t* __restrict__ nbr_j,
                                                           const int32_t* __restrict__ nbr_shift,
-                                                          int32_t* __restrict__ rev,
-                                                          const int64_t* active) {
-  if (inactive(active)) return;
+                                                          int32_t* __restrict__ rev) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
@@ -417,100 +395,6 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
       rev[s] = found ? static_cast<int32_t>(lo) : -1;
     }
   }
-}
-
-// Keep the skin edges inside r_c (same fixed-point predicate) and write the
-// edge record r_ij = (r_j + n.h) - r_i, computed in float64 and stored
-// float32, with j in the w lane.  Slots are the first ecount[i] entries of
-// the skin row of i, in canonical order.
-__global__ void __launch_bounds__(kBlock) compact_kernel(
-    const double* __restrict__ pos, int64_t n, int64_t Lq0, int64_t Lq1, int64_t Lq2, int64_t rcq,
-    double L0, double L1, double L2, int64_t cap, const int64_t* __restrict__ row_ptr,
-    const int32_t* __restrict__ nbr_j, const int32_t* __restrict__ nbr_shift,
-    int32_t* __restrict__ ecount, float4* __restrict__ edge, int32_t* __restrict__ cidx,
-    int32_t* __restrict__ sidx) {
-  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
-  const int lane = lane_id();
-  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
-    const double xi = pos[3 * i], yi = pos[3 * i + 1], zi = pos[3 * i + 2];
-    const int64_t qi0 = qfix(xi), qi1 = qfix(yi), qi2 = qfix(zi);
-    const int64_t b = row_ptr[i];
-    int64_t e = row_ptr[i + 1];
-    if (b < 0 || e > cap || e < b) e = b;   // malformed row: keep nothing
-    int kept = 0;
-    for (int64_t base = b; base < e; base += kWave) {
-      int64_t s = base + lane;
-      bool pred = false;
-      int32_t j = 0;
-      int nx = 0, ny = 0, nz = 0;
-      if (s < e) {
-        j = nbr_j[s];
-        int32_t sh = nbr_shift[s];
-        nx = unpack_x(sh); ny = unpack_y(sh); nz = unpack_z(sh);
-        if (j >= 0 && j < n) {
-          int64_t dx = qfix(pos[3 * j]) + nx * Lq0 - qi0;
-          int64_t dy = qfix(pos[3 * j + 1]) + ny * Lq1 - qi1;
-          int64_t dz = qfix(pos[3 * j + 2]) + nz * Lq2 - qi2;
-          pred = within(dx, dy, dz, rcq);
-        }
-      }
-      uint64_t m;
-      int pre = ballot_prefix(pred, &m);
-      if (s < e) {
-        if (pred) {
-          int64_t slot = b + kept + pre;
-          double rx = (pos[3 * j] + nx * L0) - xi;
-          double ry = (pos[3 * j + 1] + ny * L1) - yi;
-          double rz = (pos[3 * j + 2] + nz * L2) - zi;
-          edge[slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
-                                   static_cast<float>(rz), __int_as_float(j));
-          sidx[slot] = static_cast<int32_t>(s);
-          cidx[s] = static_cast<int32_t>(slot);
-        } else {
-          cidx[s] = -1;
-        }
-      }
-      kept += __popcll(m);
-    }
-    if (lane == 0) ecount[i] = kept;
-  }
-}
-
-__global__ void __launch_bounds__(kBlock) rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
-                                                     const int32_t* __restrict__ ecount,
-                                                     const int32_t* __restrict__ sidx,
-                                                     const int32_t* __restrict__ skin_rev,
-                                                     const int32_t* __restrict__ cidx,
-                                                     int32_t* __restrict__ rev) {
-  const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
-  const int lane = lane_id();
-  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
-    int64_t b = row_ptr[i], e = b + ecount[i];
-    for (int64_t s = b + lane; s < e; s += kWave) {
-      const int32_t sr = skin_rev[sidx[s]];
-      const int32_t c = sr >= 0 ? cidx[sr] : -1;
-      rev[s] = c >= 0 ? c : static_cast<int32_t>(s);   // never happens for a valid list
-    }
-  }
-}
-
-// Copy a freshly scanned row_ptr over the live one when it fits the
-// capacity; otherwise keep the old (consistent) list and raise the flag.
-__global__ void __launch_bounds__(kBlock) commit_rows_kernel(const int64_t* __restrict__ fresh,
-                                                             int64_t* __restrict__ live, int64_t n,
-                                                             int64_t cap, int64_t* __restrict__ flags,
-                                                             const int64_t* active) {
-  if (inactive(active)) return;
-  const int64_t total = fresh[n];
-  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
-  if (total > cap) {
-    if (i == 0) {
-      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagCapacity);
-      atomicMax(reinterpret_cast<unsigned long long*>(flags + 2), (unsigned long long)total);
-    }
-    return;
-  }
-  if (i <= n) live[i] = fresh[i];
 }
 
 int waves_grid(int64_t n) {
@@ -563,32 +447,32 @@ int ensure_scratch(NeighborScratch& nb, int64_t n, const CellGrid& g) {
 
 int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const CellGrid& g,
                     int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift, int64_t cap,
-                    const int64_t* active, int64_t* flags, bool fill, hipStream_t st) {
+                    int64_t* flags, bool fill, hipStream_t st) {
   int rc = ensure_scratch(nb, n, g);
   if (rc) return rc;
   GridDev gd = to_dev(g);
   int blocks = static_cast<int>((n + kBlock - 1) / kBlock);
   int cblocks = static_cast<int>((g.ncell + kBlock - 1) / kBlock);
   hipLaunchKernelGGL(zero_i32_kernel, dim3(cblocks), dim3(kBlock), 0, st,
-                     nb.cell_cnt.as<int32_t>(), g.ncell, active);
+                     nb.cell_cnt.as<int32_t>(), g.ncell);
   hipLaunchKernelGGL(bin_kernel, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
                      nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                     nb.cell_cnt.as<int32_t>(), flags, active);
+                     nb.cell_cnt.as<int32_t>(), flags);
   hipLaunchKernelGGL(cell_scan_kernel, dim3(1), dim3(1024), 0, st, nb.cell_cnt.as<int32_t>(),
-                     g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(), active);
+                     g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>());
   hipLaunchKernelGGL(place_kernel, dim3(blocks), dim3(kBlock), 0, st, n, nb.cell_of.as<int32_t>(),
                      nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>(), active);
+                     nb.cell_atoms.as<int32_t>());
   hipLaunchKernelGGL(count_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                      nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>(), nb.counts.as<int64_t>(), active);
+                     nb.cell_atoms.as<int32_t>(), nb.counts.as<int64_t>());
   DPA4C_HIP_TRY(hipGetLastError());
-  rc = exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, active, st);
+  rc = exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, st);
   if (rc) return rc;
   if (fill) {
     hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                       nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags, active);
+                       nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags);
     DPA4C_HIP_TRY(hipGetLastError());
   }
   return 0;
@@ -600,45 +484,15 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
   GridDev gd = to_dev(g);
   hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                      nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags,
-                     (const int64_t*)nullptr);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
-int commit_rows(const int64_t* fresh, int64_t* live, int64_t n, int64_t cap, int64_t* flags,
-                const int64_t* active, hipStream_t st) {
-  int blocks = static_cast<int>((n + 1 + kBlock - 1) / kBlock);
-  hipLaunchKernelGGL(commit_rows_kernel, dim3(blocks), dim3(kBlock), 0, st, fresh, live, n, cap,
-                     flags, active);
+                     nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int32_t* skin_rev, const int64_t* active, hipStream_t st) {
+                    int64_t n, int32_t* skin_rev, hipStream_t st) {
   hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
-                     nbr_shift, skin_rev, active);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
-int launch_compact_edges(const double* pos, int64_t n, const CellGrid& g, int64_t rcq,
-                         const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
-                         const int32_t* nbr_shift, int64_t cap, int32_t* ecount, float4* edge,
-                         int32_t* cidx, int32_t* sidx, hipStream_t st) {
-  hipLaunchKernelGGL(compact_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, pos, n, g.Lq[0],
-                     g.Lq[1], g.Lq[2], rcq, box[0], box[1], box[2], cap, row_ptr, nbr_j, nbr_shift,
-                     ecount, edge, cidx, sidx);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
-int launch_rev(const int64_t* row_ptr, const int32_t* ecount, const int32_t* sidx,
-               const int32_t* skin_rev, const int32_t* cidx, int64_t n, int32_t* rev,
-               hipStream_t st) {
-  hipLaunchKernelGGL(rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, ecount,
-                     sidx, skin_rev, cidx, rev);
+                     nbr_shift, skin_rev);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

@@ -162,12 +162,14 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
       int m = o / P::C1, cp = o % P::C1;
       const DPA4C_LDS float* x = s.y + P::Y1 + m * P::C1;
       float acc = x[cp];
+#pragma unroll
       for (int c = 0; c < P::C1; ++c) acc += x[c] * rp.W1[c * P::C1 + cp];
       s.xt1[o] = acc * i1;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, cp = t % P::C2;
       const DPA4C_LDS float* x = s.y + P::Y2 + m * P::C2;
       float acc = x[cp];
+#pragma unroll
       for (int c = 0; c < P::C2; ++c) acc += x[c] * rp.W2[c * P::C2 + cp];
       s.xt2[t] = acc * i1;
     } else {
@@ -182,6 +184,7 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
       float acc;
       if constexpr (P::kHasA1) {
         acc = 0.0f;
+#pragma unroll
         for (int c = 0; c < P::C1; ++c) acc += s.xt1[m * P::C1 + c] * rp.A1[c * P::K1 + k];
       } else {
         acc = s.xt1[m * P::C1 + k];
@@ -190,6 +193,7 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
     } else {
       int t = o - 3 * P::K1, m = t / P::K2, k = t % P::K2;
       float acc = 0.0f;
+#pragma unroll
       for (int c = 0; c < P::C2; ++c) acc += s.xt2[m * P::C2 + c] * rp.A2[c * P::K2 + k];
       s.z2[t] = acc;
     }
@@ -231,6 +235,7 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
   for (int o = lane; o < P::K2 * P::K1 * 3; o += kHalf) {
     int eta = o / (P::K1 * 3), k = (o / 3) % P::K1, a = o % 3;
     float acc = 0.0f;
+#pragma unroll
     for (int b = 0; b < 3; ++b) acc += s.q[eta][a * 3 + b] * s.z1[b * P::K1 + k];
     s.qv[eta][k][a] = acc;
   }
@@ -263,14 +268,17 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     if (o < P::nG1) {
       int c, cp;
       vech_pair(o, P::C1, &c, &cp);
+#pragma unroll
       for (int m = 0; m < 3; ++m) acc += s.xt1[m * P::C1 + c] * s.xt1[m * P::C1 + cp];
       if (c != cp) acc *= kSqrt2;
     } else if (o < P::nG1 + P::nG2) {
       int c, cp;
       vech_pair(o - P::nG1, P::C2, &c, &cp);
+#pragma unroll
       for (int m = 0; m < 5; ++m) acc += s.xt2[m * P::C2 + c] * s.xt2[m * P::C2 + cp];
       if (c != cp) acc *= kSqrt2;
     } else {
+#pragma unroll
       for (int m = 0; m < 7; ++m) acc += s.xt3[m] * s.xt3[m];
     }
     d[P::oG1 + o] = acc;
@@ -280,6 +288,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     int eta = o % P::K2, pr = o / P::K2, k1, k2;
     vech_pair(pr, P::K1, &k1, &k2);
     float acc = 0.0f;
+#pragma unroll
     for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];
     d[P::o112 + o] = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc;
   }
@@ -289,9 +298,12 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     float w;
     e222(lane, &a, &b, &c, &w);
     float tr = 0.0f;
+#pragma unroll
     for (int r = 0; r < 3; ++r)
+#pragma unroll
       for (int t = 0; t < 3; ++t) {
         float ab = 0.0f;
+#pragma unroll
         for (int u = 0; u < 3; ++u) ab += s.q[a][r * 3 + u] * s.q[b][u * 3 + t];
         tr += ab * s.q[c][t * 3 + r];
       }
@@ -318,6 +330,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
   for (int o = lane; o < P::nPi; o += kHalf) {
     int eta = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
+#pragma unroll
     for (int a = 0; a < 3; ++a) acc += s.qv[eta][k][a] * s.qv[eta][k][a];
     d[P::oPi + o] = acc;
   }
@@ -345,16 +358,20 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
   if (lane < P::K2 * 9) {
     int eta = lane / 9, a = (lane % 9) / 3, b = lane % 3;
     float acc = 0.0f;
+#pragma unroll
     for (int k1 = 0; k1 < P::K1; ++k1)
+#pragma unroll
       for (int k2 = k1; k2 < P::K1; ++k2) {
         float jb = d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
         float f = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2);
         acc += jb * f * s.z1[a * P::K1 + k1] * s.z1[b * P::K1 + k2];
       }
+#pragma unroll
     for (int k = 0; k < P::K1; ++k) {
       float pb = d[P::oPi + eta * P::K1 + k];
       acc += 2.0f * pb * s.qv[eta][k][a] * s.z1[b * P::K1 + k];
     }
+#pragma unroll
     for (int t = 0; t < P::n222; ++t) {
       int ia, ib, ic;
       float w;
@@ -363,16 +380,19 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
       // d tr(A B C) / dA = (B C)^T, / dB = (C A)^T, / dC = (A B)^T
       if (ia == eta) {
         float v = 0.0f;
+#pragma unroll
         for (int u = 0; u < 3; ++u) v += s.q[ib][b * 3 + u] * s.q[ic][u * 3 + a];
         acc += jb * v;
       }
       if (ib == eta) {
         float v = 0.0f;
+#pragma unroll
         for (int u = 0; u < 3; ++u) v += s.q[ic][b * 3 + u] * s.q[ia][u * 3 + a];
         acc += jb * v;
       }
       if (ic == eta) {
         float v = 0.0f;
+#pragma unroll
         for (int u = 0; u < 3; ++u) v += s.q[ia][b * 3 + u] * s.q[ib][u * 3 + a];
         acc += jb * v;
       }
@@ -383,7 +403,9 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
   for (int o = lane; o < 3 * P::K1; o += kHalf) {
     int m = o / P::K1, k = o % P::K1;
     float acc = 0.0f;
+#pragma unroll
     for (int eta = 0; eta < P::K2; ++eta) {
+#pragma unroll
       for (int kp = 0; kp < P::K1; ++kp) {
         int k1 = k < kp ? k : kp, k2 = k < kp ? kp : k;
         float jb = d[P::o112 + tri_index(k1, k2, P::K1) * P::K2 + eta];
@@ -392,10 +414,12 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
       }
       float pb = d[P::oPi + eta * P::K1 + k];
       float v = 0.0f;
+#pragma unroll
       for (int b = 0; b < 3; ++b) v += s.q[eta][m * 3 + b] * s.qv[eta][k][b];
       acc += 2.0f * pb * v;
     }
     if constexpr (P::L >= 3) {
+#pragma unroll
       for (int k2 = 0; k2 < P::K2; ++k2) acc += d[P::o123 + k * P::K2 + k2] * s.u123[m * P::K2 + k2];
     }
     s.gz1[o] = acc;
@@ -405,11 +429,13 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     if (lane >= 18 && lane < 18 + 3 * P::K2) {
       const int o = lane - 18, m1 = o / P::K2, k2 = o % P::K2;
       float acc = 0.0f;
+#pragma unroll
       for (int k1 = 0; k1 < P::K1; ++k1) acc += d[P::o123 + k1 * P::K2 + k2] * s.z1[m1 * P::K1 + k1];
       s.ub123[o] = acc;
     } else if (lane >= 24 && lane < 29) {
       const int m1 = lane - 24;
       float acc = 0.0f;
+#pragma unroll
       for (int eta = 0; eta < P::K2; ++eta) acc += d[P::o233 + eta] * s.z2[m1 * P::K2 + eta];
       s.vb233[m1] = acc;
     }
@@ -420,6 +446,7 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     if (lane >= 16 && lane < 31) {
       const int o = lane - 16, m1 = o / 5, m2 = o % 5;
       float acc = 0.0f;
+#pragma unroll
       for (int k2 = 0; k2 < P::K2; ++k2) acc += s.ub123[m1 * P::K2 + k2] * s.z2[m2 * P::K2 + k2];
       s.tb123[o] = acc;
     }
@@ -441,7 +468,9 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     if (lane < 7) {
       const int m = lane;
       float acc = 0.0f;
+#pragma unroll
       for (int o = 0; o < 15; ++o) acc += s.tb123[o] * cpl[7 * o + m];
+#pragma unroll
       for (int m1 = 0; m1 < 5; ++m1) acc += 2.0f * s.vb233[m1] * s.w233[m1 * 7 + m];
       s.gz3[m] = acc;
     }
@@ -453,12 +482,14 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     if (o < n1) {
       int m = o / P::C1, c = o % P::C1;
       float acc = 0.0f;
+#pragma unroll
       for (int cp = 0; cp < P::C1; ++cp) {
         int a = c < cp ? c : cp, b = c < cp ? cp : c;
         float gb = d[P::oG1 + tri_index(a, b, P::C1)];
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt1[m * P::C1 + cp];
       }
       if constexpr (P::kHasA1) {
+#pragma unroll
         for (int k = 0; k < P::K1; ++k) acc += s.gz1[m * P::K1 + k] * rp.A1[c * P::K1 + k];
       } else {
         acc += s.gz1[m * P::K1 + c];
@@ -467,11 +498,13 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, c = t % P::C2;
       float acc = 0.0f;
+#pragma unroll
       for (int cp = 0; cp < P::C2; ++cp) {
         int a = c < cp ? c : cp, b = c < cp ? cp : c;
         float gb = d[P::oG2 + tri_index(a, b, P::C2)];
         acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt2[m * P::C2 + cp];
       }
+#pragma unroll
       for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * rp.A2[c * P::K2 + k];
       s.gxt2[t] = acc;
     } else {
@@ -494,11 +527,13 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     if (o < n1) {
       int m = o / P::C1, c = o % P::C1;
       xb = s.gxt1[o];
+#pragma unroll
       for (int cp = 0; cp < P::C1; ++cp) xb += s.gxt1[m * P::C1 + cp] * rp.W1[c * P::C1 + cp];
       yi = P::Y1 + o;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, c = t % P::C2;
       xb = s.gxt2[t];
+#pragma unroll
       for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * rp.W2[c * P::C2 + cp];
       yi = P::Y2 + t;
     } else {
