@@ -1,6 +1,8 @@
 """Fix the calibration vectors and the head scale of the random-init models.
 
-Writes ``synth/calibration.json``; run as ``python -m oracle.calibrate``.
+Writes ``synth/calibration.json``; run as ``python -m oracle.calibrate
+[model ...]`` (default: every model of ``synth.MODELS``; named models are
+recomputed and merged into the existing file).
 
 Eq. (calibration) holds fixed statistics estimated from sample frames.  With
 no training frames available, the sample is frame 0 of the synthetic
@@ -90,12 +92,20 @@ def calibrate(model_name: str, n_centres: int = 200, n_force: int = 12, seed: in
             "frames": [s.name for s in frames]}
 
 
-def main():
-    out = {name: calibrate(name) for name in ("small", "full")}
+def main(names=None):
+    import sys
+    names = names or sys.argv[1:] or list(synth.MODELS)
+    out = {}
+    if os.path.exists(OUT):
+        with open(OUT) as f:
+            out = json.load(f)
+    for name in names:
+        out[name] = calibrate(name)
+        v = out[name]
+        print(name, "head_scale", v["head_scale"], "rms_force_unscaled", v["rms_force_unscaled"],
+              flush=True)
     with open(OUT, "w") as f:
-        json.dump(out, f)
-    for k, v in out.items():
-        print(k, "head_scale", v["head_scale"], "rms_force_unscaled", v["rms_force_unscaled"])
+        json.dump({k: out[k] for k in synth.MODELS if k in out}, f)
 
 
 if __name__ == "__main__":

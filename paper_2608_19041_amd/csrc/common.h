@@ -5,6 +5,7 @@
 
 #include <cstdint>
 #include <string>
+#include <type_traits>
 
 namespace dpa4c {
 
@@ -58,10 +59,32 @@ struct Profile {
   static_assert(kWave % LPE == 0, "edge groups");
 };
 
-using SmallProfile = Profile<32, 2, 0>;
-using FullProfile = Profile<128, 3, 4>;
-static_assert(SmallProfile::DOUT == 144 && SmallProfile::S == 76, "Table S2 (32, 2)");
-static_assert(FullProfile::DOUT == 541 && FullProfile::S == 223, "Table S2 (128, 3)");
+// The compiled profiles: the five DPA4C variants of Supplementary Table S3,
+// each with its MLP width.
+using NanoProfile = Profile<8, 2, 0>;      // MLP width 96
+using MiniProfile = Profile<32, 2, 0>;     // 192
+using NeoProfile = Profile<64, 2, 0>;      // 256
+using AirProfile = Profile<64, 3, 4>;      // 256
+using PlusProfile = Profile<128, 3, 4>;    // 384
+static_assert(NanoProfile::DOUT == 70 && NanoProfile::S == 40, "Table S2 (8, 2)");
+static_assert(MiniProfile::DOUT == 144 && MiniProfile::S == 76, "Table S2 (32, 2)");
+static_assert(NeoProfile::DOUT == 208 && NeoProfile::S == 108, "Table S2 (64, 2)");
+static_assert(AirProfile::DOUT == 219 && AirProfile::S == 115, "Table S2 (64, 3)");
+static_assert(PlusProfile::DOUT == 541 && PlusProfile::S == 223, "Table S2 (128, 3)");
+
+// Calls fn(P{}, std::integral_constant<int, F>{}) for the compiled profile
+// matching (C0, L, R) and MLP width F and returns its result; returns
+// kNoProfile when none matches.
+constexpr int kNoProfile = -1000;
+template <class Fn>
+int with_profile(int C0, int L, int R, int F, Fn&& fn) {
+  if (C0 == 8 && L == 2 && R == 0 && F == 96) return fn(NanoProfile{}, std::integral_constant<int, 96>{});
+  if (C0 == 32 && L == 2 && R == 0 && F == 192) return fn(MiniProfile{}, std::integral_constant<int, 192>{});
+  if (C0 == 64 && L == 2 && R == 0 && F == 256) return fn(NeoProfile{}, std::integral_constant<int, 256>{});
+  if (C0 == 64 && L == 3 && R == 4 && F == 256) return fn(AirProfile{}, std::integral_constant<int, 256>{});
+  if (C0 == 128 && L == 3 && R == 4 && F == 384) return fn(PlusProfile{}, std::integral_constant<int, 384>{});
+  return kNoProfile;
+}
 
 // ---------------------------------------------------------------------------
 // Device-side view of a model, passed to kernels by value.

@@ -102,7 +102,7 @@ __device__ inline int table_row(float rho, float inv_delta, int n_rows, float* t
   return r;
 }
 
-// Sum over aligned groups of G = 8 or 16 lanes with DPP row permutations
+// Sum over aligned groups of G = 4, 8 or 16 lanes with DPP row permutations
 // (quad xor 1, quad xor 2, half-row mirror, row mirror).  Every lane of the
 // group ends with the same bits: each step adds a value and its partner, in
 // the same order on both sides of the pair.
@@ -112,10 +112,10 @@ __device__ inline float dpp_f(float v) {
 }
 template <int G>
 __device__ inline float group_sum(float v) {
-  static_assert(G == 8 || G == 16, "group of 8 or 16 lanes");
+  static_assert(G == 4 || G == 8 || G == 16, "group of 4, 8 or 16 lanes");
   v += dpp_f<0xB1>(v);
   v += dpp_f<0x4E>(v);
-  v += dpp_f<0x141>(v);
+  if constexpr (G >= 8) v += dpp_f<0x141>(v);
   if constexpr (G == 16) v += dpp_f<0x140>(v);
   return v;
 }

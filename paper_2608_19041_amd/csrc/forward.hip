@@ -227,8 +227,14 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 
 int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
                    const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st) {
-  if (m->C0 == 32) return launch<SmallProfile>(m, n, species, row_ptr, ca, node, st);
-  return launch<FullProfile>(m, n, species, row_ptr, ca, node, st);
+  const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
+    return launch<decltype(p)>(m, n, species, row_ptr, ca, node, st);
+  });
+  if (rc == kNoProfile) {
+    set_error("forward: profile not compiled");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  return rc;
 }
 
 }  // namespace dpa4c

@@ -311,10 +311,11 @@ int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const 
     set_error("the per-atom kernel needs three hidden layers");
     return DPA4C_ERR_UNSUPPORTED;
   }
-  if (m->C0 == 32 && m->F == 192)
-    return launch_atoms<SmallProfile, 192>(m, n, species, node, node_grad, e_atom, desc_out, st);
-  if (m->C0 == 128 && m->F == 384)
-    return launch_atoms<FullProfile, 384>(m, n, species, node, node_grad, e_atom, desc_out, st);
+  const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto f) {
+    return launch_atoms<decltype(p), decltype(f)::value>(m, n, species, node, node_grad, e_atom,
+                                                         desc_out, st);
+  });
+  if (rc != kNoProfile) return rc;
   set_error("no per-atom kernel instance for this (profile, MLP width)");
   return DPA4C_ERR_UNSUPPORTED;
 }

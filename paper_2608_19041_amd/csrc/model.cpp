@@ -248,10 +248,14 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
   m->F = hdr[5]; m->n_layers = hdr[6]; m->n_types = hdr[7];
   m->r_c = rc_delta[0];
   m->delta = rc_delta[1];
-  bool small = (m->C0 == 32 && m->L == 2 && m->R == 0);
-  bool full = (m->C0 == 128 && m->L == 3 && m->R == 4);
-  if (!small && !full) {
-    set_error("dpa4c_model_create: profile (C0, L, R) not compiled into this library");
+  int widths[2] = {0, 0};   // S, D_out of the compiled profile
+  if (with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
+        widths[0] = decltype(p)::S;
+        widths[1] = decltype(p)::DOUT;
+        return 0;
+      }) == kNoProfile) {
+    set_error("dpa4c_model_create: (C0, L, R, MLP width) is not one of the compiled variants "
+              "(8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384)");
     return DPA4C_ERR_UNSUPPORTED;
   }
   if (m->n_rbf <= 0 || m->F <= 0 || m->F % 16 || m->n_layers < 1 || m->n_layers > 7 ||
@@ -265,8 +269,8 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
   int C2 = std::max(4, C1 / 2);
   m->C[0] = C0; m->C[1] = C1; m->C[2] = C2; m->C[3] = 1; m->C[4] = 1;
   m->K[1] = C2; m->K[2] = 2; m->K[3] = 1; m->K[4] = 1;
-  m->S = small ? SmallProfile::S : FullProfile::S;
-  m->D_out = small ? SmallProfile::DOUT : FullProfile::DOUT;
+  m->S = widths[0];
+  m->D_out = widths[1];
   m->H = 8 * ((C0 + 2) / 3);
   m->Hp = 8 * ((2 * C0 + 2) / 3);
   const int H = m->H, Hp = m->Hp, F = m->F, D = m->D_out, K1 = C2, K2 = 2;

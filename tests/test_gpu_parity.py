@@ -200,6 +200,30 @@ def test_separable_tables_with_many_species(dev, dp, name):
     assert np.abs(F - ref_f).max() < F_TOL
 
 
+@pytest.mark.parametrize("name", ["nano", "mini", "neo", "air", "plus"])
+def test_table_s3_variants(dev, dp, name):
+    """Every compiled profile, the five variants of Supplementary Table S3,
+    against the oracle: a copper cell (one species, pair-folded tables) and
+    an eight-species BCC cell (separable tables)."""
+    model, oracle, _ = gpu_model(dp, name)
+    for s in (synth.fcc_copper(3, 0.08, seed=3), many_species_system("full")):
+        ea, F, et = evaluate(dp, model, s, dev)
+        ref_e, ref_f = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc)
+        assert np.abs(ea - ref_e).max() < E_TOL
+        assert np.abs(F - ref_f).max() < F_TOL
+
+
+def test_uncompiled_profile_is_rejected(dev, dp):
+    """A (C0, L, R, width) outside the compiled variants fails cleanly."""
+    spec = synth.ModelSpec(C0=16, L=2, R=0, n_rbf=8, F=128, n_layers=3)
+    w = synth.random_weights(spec)
+    w["mu"] = np.zeros(synth.descriptor_width(16, 2), np.float32)
+    w["sigma"] = np.ones(synth.descriptor_width(16, 2), np.float32)
+    with pytest.raises(dp.DPA4CError) as err:
+        dp.Model(synth.pack_blob(spec, w))
+    assert err.value.code == dp.ERR_UNSUPPORTED
+
+
 def test_species_change_between_calls(dev, dp):
     """The per-pair tables follow the species of each call on one handle:
     one species, two, seven (separable path), then one again."""
