@@ -539,7 +539,11 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
       set_error("verlet_step: an atom moved more than skin/2 and rebuilds are disabled");
       return DPA4C_ERR_SKIN;
     }
-    // violation at step v: restore, replay [s, v), rebuild at v
+    // violation at step v: the displacement reached half the skin within
+    // v - last_build steps, a growth rate for sizing the batches that follow
+    const double g_viol = half_skin / double(v - last_build > 0 ? v - last_build : 1);
+    growth = growth > g_viol ? growth : g_viol;
+    // restore, replay [s, v), rebuild at v
     DPA4C_HIP_TRY(hipMemcpyAsync(pos, bk, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(vel, bk + 3 * N, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(forces, bk + 6 * N, state, hipMemcpyDeviceToDevice, st));
@@ -557,7 +561,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     if (rc) return rc;
     last_build = v;
     s = v + 1;
-    batch = growth > 0.0 ? static_cast<int64_t>(0.75 * half_skin / growth) : 8;
+    batch = static_cast<int64_t>(0.75 * half_skin / growth);
     batch = batch < 1 ? 1 : (batch > 64 ? 64 : batch);
   }
   DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));

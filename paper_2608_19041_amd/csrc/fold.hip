@@ -13,7 +13,10 @@
 // For the few species of an MD system the library keeps one such table per
 // ordered pair present; the edge kernels then read one quintic per channel
 // instead of a g quintic, R q quintics and the pair coefficients.  Systems
-// with more than kMaxFoldTypes species use the separable tables directly.
+// with more than kMaxFoldTypes species, or whose folded tables would exceed
+// kMaxFoldBytes (beyond that the tables fall out of the caches and the
+// separable path is faster: five species at full width need 230 MB), use the
+// separable tables directly.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -109,10 +112,11 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
         ++n_used;
       }
     std::memcpy(m->fold_types_mask, mask, sizeof(mask));
-    if (n_used > kMaxFoldTypes) {
-      m->fold_n = 0;   // too many species: the separable tables are used
+    const size_t per_pair = size_t(m->n_rows) * m->C0 * 6;
+    if (n_used > kMaxFoldTypes ||
+        4 * per_pair * size_t(n_used) * size_t(n_used) > kMaxFoldBytes) {
+      m->fold_n = 0;   // the separable tables are used
     } else {
-      const size_t per_pair = size_t(m->n_rows) * m->C0 * 6;
       if (w.ftab.ensure(4 * per_pair * n_used * n_used)) return DPA4C_ERR_HIP;
       int32_t* hmap = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(w.fold_host) + 64);
       std::memcpy(hmap, map.data(), 4 * size_t(T1));

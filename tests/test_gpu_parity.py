@@ -226,11 +226,17 @@ def test_uncompiled_profile_is_rejected(dev, dp):
 
 def test_species_change_between_calls(dev, dp):
     """The per-pair tables follow the species of each call on one handle:
-    one species, two, seven (separable path), then one again."""
+    one species, two, five (25 folded pairs), seven (separable path), then
+    one again."""
     model, oracle, _ = gpu_model(dp, "small")
     cell = np.diag([8.3, 8.9, 9.4])
+    five = synth.fcc_copper(3, 0.08, seed=6)
+    five.species = five.species.copy()
+    five.species[np.random.Generator(np.random.PCG64(9)).choice(five.n, 4, replace=False)] = \
+        np.array([0, 7, 53, 58])
     systems = [synth.fcc_copper(3, 0.08, seed=4),
                synth.random_periodic(24, seed=12, cell=cell, d_min=1.6),
+               five,
                many_species_system("small"),
                synth.fcc_copper(3, 0.08, seed=5)]
     for s in systems:
