@@ -33,54 +33,82 @@ constexpr int kWavesPB = kThreads / 64;
 
 __device__ inline float sigm(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
-// acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for the
-// output tiles first + t * stride, t < MAXT.  Tiles past ``ntiles`` repeat
-// the last tile (their results are discarded by the caller), so every wave
-// runs the same straight-line code.  The B and A fragments are requested two
-// k-blocks ahead (three register sets), and the MFMAs of one k-block are
-// interleaved across tiles so that consecutive instructions do not depend on
-// each other.
+// One 16-byte load through a buffer resource: descriptor and tile offset in
+// scalar registers, only the lane offset in a vector register (no per-lane
+// 64-bit addresses to keep alive; reads past the resource return zero).
+typedef unsigned u4 __attribute__((ext_vector_type(4)));
+constexpr int kBufWord3 = 0x00020000;   // raw 32-bit buffer, gfx9 data format
+
+__device__ inline float4 buf_load16(__amdgpu_buffer_rsrc_t rs, unsigned voff, int soff) {
+  const u4 v = __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(voff), soff, 0);
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+
+// B operand stream of one product: the weight resource, the byte offset of
+// each of the wave's output tiles and the first two k-blocks, which do not
+// depend on the A tile and so are requested before the barrier that
+// publishes it (by the drain of the previous product).  Tiles past
+// ``ntiles`` repeat the last tile; ``first`` must be wave-uniform.
 template <int MAXT>
-__device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int lda, int kblocks,
-                                  const float4* __restrict__ Wf, int first, int stride, int ntiles,
-                                  int lane) {
-  const float* ap = As + (lane & 15) * lda + (lane >> 4) * 4;
-  const float4* wp[MAXT];
+struct BStream {
+  __amdgpu_buffer_rsrc_t rs;
+  int toff[MAXT];
+  float4 b0[MAXT], b1[MAXT];
+};
+
+template <int MAXT>
+__device__ inline void bstream_open(BStream<MAXT>& bs, const float4* __restrict__ Wf, int kblocks,
+                                    int first, int stride, int ntiles, unsigned lane16) {
+  bs.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float4*>(Wf), 0, ntiles * kblocks * 1024,
+                                            kBufWord3);
 #pragma unroll
   for (int t = 0; t < MAXT; ++t) {
     const int T = first + t * stride < ntiles ? first + t * stride : ntiles - 1;
-    wp[t] = Wf + size_t(T) * kblocks * 64 + lane;
+    bs.toff[t] = T * kblocks * 1024;
   }
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t) bs.b0[t] = buf_load16(bs.rs, lane16, bs.toff[t]);
+#pragma unroll
+  for (int t = 0; t < MAXT; ++t)
+    bs.b1[t] = buf_load16(bs.rs, lane16, bs.toff[t] + (kblocks > 1 ? 1024 : 0));
+}
+
+// acc[t] += A (16 x K, LDS, row stride lda) * W (fragment order) for the
+// first NT tiles of ``bs`` (NT <= MAXT).  Three k-blocks of B and A are in
+// flight: k-block kb+2 is requested before the MFMAs of kb start, and the
+// MFMAs of one k-block are interleaved across tiles so that consecutive
+// instructions do not depend on each other.  No load runs past the last
+// k-block; ``drain()`` is called once the last one is requested, so the
+// caller can start the loads of what follows the product.
+template <int NT, int MAXT, class Drain>
+__device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int lda, int kblocks,
+                                  BStream<MAXT>& bs, unsigned lane, unsigned lane16,
+                                  Drain&& drain) {
+  static_assert(NT <= MAXT, "tile count");
+  const float* ap = As + (lane & 15) * lda + (lane >> 4) * 4;
   auto step = [&](const float4& a, const float4* b) {
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[t].x, acc[t], 0, 0, 0);
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[t].x, acc[t], 0, 0, 0);
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[t].y, acc[t], 0, 0, 0);
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[t].y, acc[t], 0, 0, 0);
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[t].z, acc[t], 0, 0, 0);
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[t].z, acc[t], 0, 0, 0);
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
+    for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[t].w, acc[t], 0, 0, 0);
   };
-  // three k-blocks of B and A in flight: k-block kb+2 is requested before the
-  // MFMAs of kb start (loads past the last k-block are clamped to it and
-  // never used)
-  const int last = kblocks - 1;
   auto ld_b = [&](float4* b, int kk) {
-    const int kc = kk < last ? kk : last;
 #pragma unroll
-    for (int t = 0; t < MAXT; ++t) b[t] = wp[t][size_t(kc) * 64];
+    for (int t = 0; t < NT; ++t) b[t] = buf_load16(bs.rs, lane16, bs.toff[t] + kk * 1024);
   };
-  auto ld_a = [&](int kk) {
-    const int kc = kk < last ? kk : last;
-    return *reinterpret_cast<const float4*>(ap + kc * 16);
-  };
-  float4 b0[MAXT], b1[MAXT], b2[MAXT];
-  ld_b(b0, 0);
-  ld_b(b1, 1);
-  float4 a0 = ld_a(0), a1 = ld_a(1), a2;
+  auto ld_a = [&](int kk) { return *reinterpret_cast<const float4*>(ap + kk * 16); };
+  float4* b0 = bs.b0;
+  float4* b1 = bs.b1;
+  float4 b2[NT];
+  float4 a0 = ld_a(0), a1 = ld_a(kblocks > 1 ? 1 : 0), a2;
   int kb = 0;
 #pragma unroll 1
-  for (; kb + 3 <= kblocks; kb += 3) {
+  for (; kb + 5 <= kblocks; kb += 3) {
     ld_b(b2, kb + 2);
     a2 = ld_a(kb + 2);
     __builtin_amdgcn_sched_barrier(0);   // keep the prefetch ahead of the MFMAs
@@ -94,9 +122,24 @@ __device__ inline void mfma_tiles(v4f* acc, const float* __restrict__ As, int ld
     __builtin_amdgcn_sched_barrier(0);
     step(a2, b2);
   }
-  // remaining one or two k-blocks, already in b0/a0 and b1/a1
-  if (kb < kblocks) step(a0, b0);
-  if (kb + 1 < kblocks) step(a1, b1);
+  // the last two to four k-blocks; kb and kb + 1 are already in b0/a0, b1/a1
+  const int rem = kblocks - kb;
+  if (rem >= 3) {
+    ld_b(b2, kb + 2);
+    a2 = ld_a(kb + 2);
+  }
+  if (rem <= 3) drain();
+  __builtin_amdgcn_sched_barrier(0);
+  step(a0, b0);
+  if (rem == 4) {
+    ld_b(b0, kb + 3);
+    a0 = ld_a(kb + 3);
+    drain();
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (rem >= 2) step(a1, b1);
+  if (rem >= 3) step(a2, b2);
+  if (rem == 4) step(a0, b0);
 }
 
 struct MlpArgs {
@@ -123,13 +166,16 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
   constexpr int NT = (FT + kWavesPB - 1) / kWavesPB;  // per wave (round-robin)
   constexpr int DT = KP / 16;                         // output tiles of dE/dD
   constexpr int NTD = (DT + kWavesPB - 1) / kWavesPB;
+  constexpr int NTD1 = NTD > 1 ? NTD - 1 : 1;         // the shorter dE/dD product
   constexpr int APW = kRows / kWavesPB;               // atoms per wave in the readouts
   __shared__ float As[kRows * LDA];
   __shared__ float epart[kWavesPB][kRows];
   __shared__ ReadoutLds<P> rl_all[kRows];   // one per atom of the tile
   __shared__ ReadoutParams<P> rp;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // wave index made visibly uniform, so per-wave addresses stay scalar
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int col_in = lane & 15, rgrp = lane >> 4;   // output element: row 4*rgrp + r
+  const unsigned lane16 = 16u * lane;               // byte offset of a lane's fragment
   const int nt = (FT - wave + kWavesPB - 1) / kWavesPB;
   static_assert(APW == 2, "a wave reads out two atoms, one per half");
   const int half = lane >> 5, hl = lane & 31;
@@ -160,26 +206,42 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       if (!ok)
         for (int t = hl; t < KP; t += kHalf) arow[t] = 0.0f;
     }
+    BStream<NT> bs;    // the B stream of the next hidden-width product
+    bstream_open(bs, p.W[0], KP / 16, wave, kWavesPB, FT, lane16);
     __syncthreads();
 
     float s[3][NT][4];   // SiLU'(pre) of the three layers
     float h[NT][4];      // current activation / backward carry
+    float wh[NT];        // head weights of the wave's columns
 #pragma unroll
     for (int layer = 0; layer < 3; ++layer) {
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, p.W[layer], wave, kWavesPB, FT,
-                     lane);
+      float bias[NT];
+      BStream<NT> bsn;
+      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, bs, lane, lane16, [&] {
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          bias[t] = t < nt ? p.bias[layer][(wave + kWavesPB * t) * 16 + col_in] : 0.0f;
+        if (layer < 2) {
+          bstream_open(bsn, p.W[layer + 1], F / 16, wave, kWavesPB, FT, lane16);
+        } else {
+#pragma unroll
+          for (int t = 0; t < NT; ++t)
+            wh[t] = t < nt ? p.w_head[(wave + kWavesPB * t) * 16 + col_in] : 0.0f;
+          bstream_open(bsn, p.WT[2], F / 16, wave, kWavesPB, FT, lane16);
+        }
+      });
+      bs = bsn;
       __syncthreads();   // everyone has read the A tile
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if (t >= nt) continue;
         const int col = (wave + kWavesPB * t) * 16 + col_in;
-        const float bc = p.bias[layer][col];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float pre = acc[t][r] + bc;
+          const float pre = acc[t][r] + bias[t];
           const float sg = sigm(pre);
           const float act = pre * sg;
           s[layer][t][r] = sg * (1.0f + pre * (1.0f - sg));
@@ -194,9 +256,8 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       if (t >= nt) continue;
-      const float wc = p.w_head[(wave + kWavesPB * t) * 16 + col_in];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) part[r] += h[t][r] * wc;
+      for (int r = 0; r < 4; ++r) part[r] += h[t][r] * wh[t];
     }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -212,11 +273,10 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
     for (int t = 0; t < NT; ++t) {
       if (t >= nt) continue;
       const int col = (wave + kWavesPB * t) * 16 + col_in;
-      const float wc = p.w_head[col];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        h[t][r] = wc;                                   // carry hbar3
-        As[(4 * rgrp + r) * LDA + col] = wc * s[2][t][r];
+        h[t][r] = wh[t];                                // carry hbar3
+        As[(4 * rgrp + r) * LDA + col] = wh[t] * s[2][t][r];
       }
     }
     __syncthreads();
@@ -230,12 +290,20 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       e_atom[row0 + i] = double(e) + double(p.b_head) + double(p.E_ref[a]);
     }
     // ---- hbar_{t-1} = hbar_t + p_t Th_t^T,  p_{t-1} = hbar_{t-1} * s_{t-1}
+    BStream<NTD> bsd;   // the B stream of dE/dD
 #pragma unroll
     for (int layer = 2; layer >= 1; --layer) {
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NT>(acc, As, LDA, F / 16, p.WT[layer], wave, kWavesPB, FT, lane);
+      BStream<NT> bsn;
+      mfma_tiles<NT>(acc, As, LDA, F / 16, bs, lane, lane16, [&] {
+        if (layer == 2)
+          bstream_open(bsn, p.WT[1], F / 16, wave, kWavesPB, FT, lane16);
+        else
+          bstream_open(bsd, p.WT[0], F / 16, wave, kWavesPB, DT, lane16);
+      });
+      if (layer == 2) bs = bsn;
       __syncthreads();
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
@@ -249,13 +317,17 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       }
       __syncthreads();
     }
-    // ---- dE/dD = p1 Th1^T  (KP columns, tiles dealt round-robin) back into LDS
+    // ---- dE/dD = p1 Th1^T  (KP columns, tiles dealt round-robin) back into LDS;
+    // a wave with one tile fewer runs the shorter product
     {
       const int ntd = (DT - wave + kWavesPB - 1) / kWavesPB;
       v4f acc[NTD];
 #pragma unroll
       for (int t = 0; t < NTD; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
-      mfma_tiles<NTD>(acc, As, LDA, F / 16, p.WT[0], wave, kWavesPB, DT, lane);
+      if (ntd == NTD)
+        mfma_tiles<NTD>(acc, As, LDA, F / 16, bsd, lane, lane16, [] {});
+      else
+        mfma_tiles<NTD1>(acc, As, LDA, F / 16, bsd, lane, lane16, [] {});
       __syncthreads();
 #pragma unroll
       for (int t = 0; t < NTD; ++t) {
