@@ -118,7 +118,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           float c[6];
-          load6(ft + (jj * P::LPE + k) * 6, c);
+          load6_planar<P::LPE>(ft + jj * P::LPE * 6, k, c);
           const float psi = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
           const float dpsi = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
           a0 += gy0[jj] * psi;

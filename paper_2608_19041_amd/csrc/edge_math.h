@@ -202,4 +202,14 @@ __device__ inline void load6(const float* __restrict__ p, float* c) {
   c[0] = a.x; c[1] = a.y; c[2] = b.x; c[3] = b.y; c[4] = d.x; c[5] = d.y;
 }
 
+// the 6 coefficients of lane k from a coefficient-planar block of LPE
+// lanes: [LPE][c0..c3] then [LPE][c4, c5]; the lanes of one edge read 16-byte
+// and 8-byte words at unit stride, so each request covers whole cache lines
+template <int LPE>
+__device__ inline void load6_planar(const float* __restrict__ blk, int k, float* c) {
+  const float4 a = reinterpret_cast<const float4*>(blk)[k];
+  const float2 b = reinterpret_cast<const float2*>(blk + 4 * LPE)[k];
+  c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w; c[4] = b.x; c[5] = b.y;
+}
+
 }  // namespace dpa4c

@@ -62,12 +62,13 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
     const int k = c % LPE, j = c / LPE;
     const float* pc = pair + ((size_t(a * n_types1 + b) * CPL + j) * LPE + k) * PW;
     const float* g = gtab + ((size_t(s) * CPL + j) * LPE + k) * 6;
-    float* out = ftab + (((size_t(p) * rows + s) * CPL + j) * LPE + k) * 6;
+    // coefficient-planar block of slot j: [LPE][c0..c3] then [LPE][c4, c5]
+    float* blk = ftab + ((size_t(p) * rows + s) * CPL + j) * LPE * 6;
     for (int q = 0; q < 6; ++q) {
       double v = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
       for (int mu = 0; mu < R; ++mu)
         v += double(pc[2 + mu]) * double(qtab[(size_t(s) * R + mu) * 6 + q]);
-      out[q] = static_cast<float>(v);
+      blk[q < 4 ? 4 * k + q : 4 * LPE + 2 * k + (q - 4)] = static_cast<float>(v);
     }
   }
 }

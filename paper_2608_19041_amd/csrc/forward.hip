@@ -104,7 +104,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           float c[6];
-          load6(ft + (jj * P::LPE + k) * 6, c);
+          load6_planar<P::LPE>(ft + jj * P::LPE * 6, k, c);
           const float psi = quintic_val(c, tau);
           acc0[jj] += chi * psi;
           if (jj == 0) psi0 = psi;
