@@ -72,7 +72,11 @@ typedef struct dpa4c_model dpa4c_model;
  *     w_head [F], b_head [1]    Eq. (fitting)
  *     E_ref  [T+1]              Eq. (atomic-energy)
  *     mu [D_out], sigma [D_out] Eq. (calibration)
- * Supported profiles (C0, L, R): (32, 2, 0) and (128, 3, 4).
+ * Supported (C0, L, R, F): the five variants of Supplementary Table S3,
+ * (8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384), with
+ * n_layers = 3 for the per-atom kernel; others fail with UNSUPPORTED, as
+ * does n_types > 127 (the type table, padding row included, holds at most
+ * 128 rows).
  *
  * Creates a model on ``device``: uploads the weights, tabulates [g, q] on
  * knots rho_s = s*delta (values and first two derivatives evaluated in

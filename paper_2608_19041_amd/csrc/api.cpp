@@ -137,8 +137,9 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
               const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
-              double* forces, double* e_total, hipStream_t st) {
-  // e_total == nullptr: the caller sums the energy itself
+              double* forces, double* e_total, const StepTail* tail, hipStream_t st) {
+  // e_total == nullptr: the caller sums the energy itself; ``tail``: the
+  // velocity-Verlet work fused into the force assembly
   dpa4c_model* m = const_cast<dpa4c_model*>(mc);
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
@@ -166,7 +167,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStForces, st);
     rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.grad.as<float4>(),
-                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, st);
+                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, tail, st);
     if (rc) return rc;
   }
   if (e_total) {
@@ -198,6 +199,11 @@ using namespace dpa4c;
 extern "C" {
 
 int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model** out) {
+  if (!out) {
+    set_error("dpa4c_model_create: null blob/out or blob shorter than its header");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (int rc = check_blob_header(blob, nbytes)) return rc;   // before any device call
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) {
     set_error("dpa4c_model_create: no such HIP device");
@@ -341,7 +347,7 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
     if (rc) return rc;
   }
   return run_model(m, pos, species, N, g, box, row_ptr, nbr_j, nbr_shift, n_pairs,
-                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, st);
+                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr, st);
 }
 
 int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
@@ -386,7 +392,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   // masses on the device
   const int np_tail = tail_partial_count(N);
   if (w.inv_mass.ensure(8 * T1) || w.mass.ensure(8 * T1) || w.flags.ensure(64) ||
-      w.tailpart.ensure(16 * size_t(np_tail)) ||
+      w.tailpart.ensure(32 * size_t(np_tail)) ||
       w.skin_row.ensure(8 * (N + 1)) || w.qbuild.ensure(8 * 3 * N))
     return DPA4C_ERR_HIP;
   if (!w.host_flags) DPA4C_HIP_TRY(hipHostMalloc((void**)&w.host_flags, 64, hipHostMallocDefault));
@@ -440,20 +446,26 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   };
 
   int64_t rebuilds = 0;
-  double* part_e = w.tailpart.as<double>();
-  double* part_k = part_e + np_tail;
+  // energy partials of step s in buffer s % 2, so that a step can add up
+  // those of the step before while writing its own
+  auto part_e = [&](int64_t s) { return w.tailpart.as<double>() + (s & 1) * 2 * size_t(np_tail); };
   auto sums_of = [&](int64_t s) {
     return s < 0 ? StepSums{nullptr, nullptr, 0, nullptr, nullptr}
-                 : StepSums{part_e, part_k, np_tail, e_pot + s, e_kin + s};
+                 : StepSums{part_e(s), part_e(s) + np_tail, np_tail, e_pot + s, e_kin + s};
   };
-  // one step: kick/drift (with the displacement check against the last
-  // build when ``check``), an optional rebuild, the model and the tail
-  auto one_step = [&](int64_t step, bool check, bool rebuild, int64_t prev) -> int {
-    {
+  // One step: kick/drift (unless ``kicked``: the force assembly of the step
+  // before did it), with the displacement check against the last build when
+  // ``check``; an optional rebuild; the model, whose force assembly also
+  // does the second half kick, the energy partials of the step, the totals
+  // of step ``prev`` and, with ``kick_next``, the kick and drift of the next
+  // step (checked when ``check``).
+  auto one_step = [&](int64_t step, bool check, bool rebuild, int64_t prev, bool kicked,
+                      bool kick_next) -> int {
+    if (!kicked) {
       StageScope t(m, kStIntegrate, st);
       int r = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs,
                                 1, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
-                                sums_of(prev), step, st);
+                                sums_of(-1), step, st);
       if (r) return r;
     }
     if (rebuild) {
@@ -461,13 +473,13 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
       if (r) return r;
       ++rebuilds;
     }
-    int r = run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(),
-                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
-                      w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, st);
-    if (r) return r;
-    StageScope t(m, kStIntegrate, st);
-    return launch_tail(N, vel, forces, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
-                       dt_fs, w.eatom.as<double>(), part_e, part_k, st);
+    const StepTail tail{pos, vel, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
+                        0.5 * dt_fs, dt_fs, w.eatom.as<double>(), part_e(step),
+                        part_e(step) + np_tail, sums_of(prev), kick_next ? 1 : 0,
+                        check ? w.qbuild.as<int64_t>() : nullptr, skq, flags, step + 1};
+    return run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(),
+                     w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
+                     w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail, st);
   };
   auto finish = [&](int64_t last) -> int {
     StageScope t(m, kStIntegrate, st);
@@ -482,7 +494,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   // list, exactly as a per-step check would.  Forced rebuilds
   // (rebuild_every > 0) start batches of their own.
   if (nsteps > 0) {
-    rc = one_step(0, false, true, -1);
+    rc = one_step(0, false, true, -1, false, false);
     if (rc) return rc;
     rc = finish(0);
     if (rc) return rc;
@@ -495,7 +507,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   double growth = 0.0;   // A per step since the last build, from the last batch
   for (int64_t s = 1; s < nsteps;) {
     if (rebuild_every > 0 && s % rebuild_every == 0) {
-      rc = one_step(s, true, true, -1);
+      rc = one_step(s, true, true, -1, false, false);
       if (rc) return rc;
       rc = finish(s);
       if (rc) return rc;
@@ -515,7 +527,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     rc = launch_set_flag(flags, 5, 0, st);
     if (rc) return rc;
     for (int64_t t = s; t < e; ++t) {
-      rc = one_step(t, true, false, t > s ? t - 1 : -1);
+      rc = one_step(t, true, false, t > s ? t - 1 : -1, t > s, t + 1 < e);
       if (rc) return rc;
     }
     rc = finish(e - 1);
@@ -548,14 +560,14 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     DPA4C_HIP_TRY(hipMemcpyAsync(vel, bk + 3 * N, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(forces, bk + 6 * N, state, hipMemcpyDeviceToDevice, st));
     for (int64_t t = s; t < v; ++t) {
-      rc = one_step(t, false, false, t > s ? t - 1 : -1);
+      rc = one_step(t, false, false, t > s ? t - 1 : -1, t > s, t + 1 < v);
       if (rc) return rc;
     }
     if (v > s) {
       rc = finish(v - 1);
       if (rc) return rc;
     }
-    rc = one_step(v, false, true, -1);
+    rc = one_step(v, false, true, -1, false, false);
     if (rc) return rc;
     rc = finish(v);
     if (rc) return rc;

@@ -19,43 +19,6 @@ constexpr int kLanesPerAtom = 16;
 constexpr int kRedBlock = 256;
 constexpr int kRedPer = 16;                 // elements per thread in the first pass
 
-// The reverse of compact slot s is cidx[skin_rev[sidx[s]]]: the compact slot
-// of the reverse skin edge (every edge inside r_c has its reverse inside r_c).
-__global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
-                                                        const int32_t* __restrict__ ecount,
-                                                        const float4* __restrict__ grad,
-                                                        const int32_t* __restrict__ sidx,
-                                                        const int32_t* __restrict__ skin_rev,
-                                                        const int32_t* __restrict__ cidx,
-                                                        double* __restrict__ forces) {
-  const int sub = threadIdx.x % kLanesPerAtom;
-  const int64_t per_grid = int64_t(gridDim.x) * (kBlock / kLanesPerAtom);
-  for (int64_t k = blockIdx.x * int64_t(kBlock / kLanesPerAtom) + threadIdx.x / kLanesPerAtom; k < n;
-       k += per_grid) {
-    const int64_t b = row_ptr[k], e = b + ecount[k];
-    double fx = 0.0, fy = 0.0, fz = 0.0;
-    for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
-      const float4 g = grad[s];
-      const int32_t sr = skin_rev[sidx[s]];
-      const int32_t c = sr >= 0 ? cidx[sr] : -1;
-      const float4 r = c >= 0 ? grad[c] : g;   // a valid list always has the reverse
-      fx += double(g.x) - double(r.x);
-      fy += double(g.y) - double(r.y);
-      fz += double(g.z) - double(r.z);
-    }
-    for (int off = 1; off < kLanesPerAtom; off <<= 1) {
-      fx += __shfl_xor(fx, off, kLanesPerAtom);
-      fy += __shfl_xor(fy, off, kLanesPerAtom);
-      fz += __shfl_xor(fz, off, kLanesPerAtom);
-    }
-    if (sub == 0) {
-      forces[3 * k] = fx;
-      forces[3 * k + 1] = fy;
-      forces[3 * k + 2] = fz;
-    }
-  }
-}
-
 // first pass: block b sums the fixed slice [b*T, (b+1)*T) of x (times w if
 // given), in a fixed tree order
 __device__ inline double block_sum(double v, double* sh) {
@@ -101,10 +64,6 @@ int fixed_sum(const double* x, int64_t n, double* partials, double* out, hipStre
 
 __device__ inline int64_t qfix(double x) { return static_cast<int64_t>(__builtin_rint(x * kQScale)); }
 
-// v += dt/2 F/m; optionally r += dt v and, against the fixed-point positions
-// of the last build, flag a rebuild when some atom moved by more than half
-// the skin (4 |dq|^2 > skin_q^2): flags[1] is set, flags[4] takes the
-// smallest such step index and flags[5] the largest |dq|^2 below the limit.
 // fixed-order sum of np block partials by one block (every thread gets it)
 __device__ inline double sum_partials(const double* __restrict__ part, int np, double* sh) {
   double s = 0.0;
@@ -112,6 +71,71 @@ __device__ inline double sum_partials(const double* __restrict__ part, int np, d
   return block_sum(s, sh);
 }
 
+// block 0 of a launch writes the totals of the previous step from its block
+// partials (all threads of the block take part)
+__device__ inline void write_step_sums(const StepSums& prev) {
+  __shared__ double sh[kBlock];
+  const double ep = sum_partials(prev.part_e, prev.np, sh);
+  __syncthreads();
+  const double ek = sum_partials(prev.part_k, prev.np, sh);
+  if (threadIdx.x == 0) {
+    *prev.e_pot = ep;
+    *prev.e_kin = ek;
+  }
+}
+
+// Outcome of the displacement check of one or more atoms
+struct DriftCheck {
+  int bad;       // a non-finite or absurd position
+  int viol;      // moved by more than half the skin since the last build
+  int64_t d2;    // largest |dq|^2 among the atoms below the limit
+};
+
+// r += dt v for atom i (``x0``: the position before the drift) and, against
+// the fixed-point build snapshot ``qb`` (null: no check), the displacement
+// check: |dq| > skin/2 in fixed point (4 |dq|^2 > skin_q^2) is a violation
+__device__ inline DriftCheck drift_check(int64_t i, const double* v, const double* x0,
+                                         double* __restrict__ pos, double dt, const int64_t* qb,
+                                         int64_t skin_q) {
+  DriftCheck c{0, 0, 0};
+  bool far = false;
+  int64_t d2 = 0;
+  for (int a = 0; a < 3; ++a) {
+    const double x = x0[a] + dt * v[a];
+    pos[3 * i + a] = x;
+    if (!isfinite(x) || fabs(x) > 1.0e12) c.bad = 1;
+    if (!c.bad && qb) {
+      const int64_t dq = qfix(x) - qb[a];
+      if (dq > skin_q || dq < -skin_q) far = true;
+      else d2 += dq * dq;
+    }
+  }
+  if (qb && (c.bad || far || 4 * d2 > skin_q * skin_q)) c.viol = 1;
+  else if (qb) c.d2 = d2;
+  return c;
+}
+
+__device__ inline DriftCheck merge(DriftCheck a, const DriftCheck& b) {
+  a.bad |= b.bad;
+  a.viol |= b.viol;
+  a.d2 = a.d2 > b.d2 ? a.d2 : b.d2;
+  return a;
+}
+
+// one set of atomics for the merged checks of several atoms of step
+// ``step``: flags[0] bit 3 marks a bad position, flags[1] a violation,
+// flags[4] takes the smallest violating step and flags[5] the largest |dq|^2
+__device__ inline void record_check(const DriftCheck& c, int64_t* __restrict__ flags, int64_t step) {
+  if (c.bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), 8ull);
+  if (c.viol) {
+    atomicOr(reinterpret_cast<unsigned long long*>(flags + 1), 1ull);
+    atomicMin(reinterpret_cast<unsigned long long*>(flags + 4), (unsigned long long)step);
+  }
+  if (c.d2 > 0) atomicMax(reinterpret_cast<unsigned long long*>(flags + 5), (unsigned long long)c.d2);
+}
+
+// v += dt/2 F/m and optionally the drift with its displacement check
+// (merged per wave); block 0 first writes the totals of ``prev``
 __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__ pos, double* __restrict__ vel,
                                                             const double* __restrict__ forces,
                                                             const int32_t* __restrict__ species,
@@ -121,86 +145,149 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
                                                             int drift, const int64_t* __restrict__ qbuild,
                                                             int64_t skin_q, int64_t* __restrict__ flags,
                                                             StepSums prev, int64_t step) {
-  if (prev.np > 0 && blockIdx.x == 0) {
-    // totals of the previous step from the block partials of its tail kernel
-    __shared__ double sh[kBlock];
-    const double ep = sum_partials(prev.part_e, prev.np, sh);
-    __syncthreads();
-    const double ek = sum_partials(prev.part_k, prev.np, sh);
-    if (threadIdx.x == 0) {
-      *prev.e_pot = ep;
-      *prev.e_kin = ek;
-    }
-  }
-  int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
-  if (i >= n) return;
-  int a0 = species[i];
-  a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
-  const double im = inv_mass[a0];
-  double v[3], x[3];
-  for (int a = 0; a < 3; ++a) {
-    v[a] = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
-    vel[3 * i + a] = v[a];
-  }
-  if (!drift) return;
-  bool bad = false;
-  int64_t d2 = 0;
-  bool far = false;
-  for (int a = 0; a < 3; ++a) {
-    x[a] = pos[3 * i + a] + dt * v[a];
-    pos[3 * i + a] = x[a];
-    if (!isfinite(x[a]) || fabs(x[a]) > 1.0e12) bad = true;
-    if (!bad && qbuild) {
-      int64_t dq = qfix(x[a]) - qbuild[3 * i + a];
-      if (dq > skin_q || dq < -skin_q) far = true;
-      else d2 += dq * dq;
-    }
-  }
-  if (bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), 8ull);
-  if (!qbuild) return;
-  if (bad || far || 4 * d2 > skin_q * skin_q) {
-    atomicOr(reinterpret_cast<unsigned long long*>(flags + 1), 1ull);
-    atomicMin(reinterpret_cast<unsigned long long*>(flags + 4), (unsigned long long)step);
-  } else {
-    atomicMax(reinterpret_cast<unsigned long long*>(flags + 5), (unsigned long long)d2);
-  }
-}
-
-// Second half kick v += dt/2 F/m, then the block partials (fixed tree) of
-// the potential energy sum_i E_i and of the kinetic energy of the block's
-// atoms; the next kick_drift_kernel (or final_step_kernel) adds the partials.
-__global__ void __launch_bounds__(kBlock) tail_kernel(int64_t n, double* __restrict__ vel,
-                                                      const double* __restrict__ forces,
-                                                      const int32_t* __restrict__ species,
-                                                      const double* __restrict__ inv_mass,
-                                                      const double* __restrict__ mass,
-                                                      int n_types1, double half_dt,
-                                                      const double* __restrict__ e_atom,
-                                                      double* __restrict__ part_e,
-                                                      double* __restrict__ part_k) {
-  __shared__ double sh[kBlock];
+  if (prev.np > 0 && blockIdx.x == 0) write_step_sums(prev);
   const int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
-  double ek = 0.0, ep = 0.0;
+  DriftCheck c{0, 0, 0};
   if (i < n) {
     int a0 = species[i];
     a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
     const double im = inv_mass[a0];
-    double v2 = 0.0;
+    double v[3];
     for (int a = 0; a < 3; ++a) {
-      const double v = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
-      vel[3 * i + a] = v;
-      v2 += v * v;
+      v[a] = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
+      vel[3 * i + a] = v[a];
     }
-    // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
-    ek = 0.5 * mass[a0] * v2 * (1.66053906660e-17 / 1.602176634e-19);
-    ep = e_atom[i];
+    if (drift) {
+      const double x0[3] = {pos[3 * i], pos[3 * i + 1], pos[3 * i + 2]};
+      int64_t qb[3] = {0, 0, 0};
+      if (qbuild)
+        for (int a = 0; a < 3; ++a) qb[a] = qbuild[3 * i + a];
+      c = drift_check(i, v, x0, pos, dt, qbuild ? qb : nullptr, skin_q);
+    }
   }
-  const double te = block_sum(ep, sh);
-  __syncthreads();
-  const double tk = block_sum(ek, sh);
-  if (threadIdx.x == 0) {
-    part_e[blockIdx.x] = te;
-    part_k[blockIdx.x] = tk;
+  if (!drift) return;
+  for (int off = 1; off < kWave; off <<= 1) {
+    DriftCheck o;
+    o.bad = __shfl_xor(c.bad, off);
+    o.viol = __shfl_xor(c.viol, off);
+    o.d2 = __shfl_xor(c.d2, off);
+    c = merge(c, o);
+  }
+  if ((threadIdx.x & (kWave - 1)) == 0) record_check(c, flags, step);
+}
+
+// Force assembly.  The reverse of compact slot s is cidx[skin_rev[sidx[s]]]:
+// the compact slot of the reverse skin edge (every edge inside r_c has its
+// reverse inside r_c).  Sixteen lanes per atom, sixteen atoms per group.
+//
+// With TAIL (a velocity-Verlet step) the lane that holds F_k also applies
+// the second half kick v += dt/2 F/m, and the group's potential and kinetic
+// energies are summed in a fixed order into partial ``group`` of this step;
+// one extra block writes the totals of the previous step (a separate
+// partial buffer).  With kick_next the same lane goes on with the first
+// half kick and the drift of the next step (drift_check): both use F_k, so
+// the arithmetic is that of separate kick kernels.
+template <bool TAIL>
+__global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
+                                                        const int32_t* __restrict__ ecount,
+                                                        const float4* __restrict__ grad,
+                                                        const int32_t* __restrict__ sidx,
+                                                        const int32_t* __restrict__ skin_rev,
+                                                        const int32_t* __restrict__ cidx,
+                                                        double* __restrict__ forces, StepTail tl) {
+  constexpr int APG = kBlock / kLanesPerAtom;
+  __shared__ double she[APG], shk[APG];
+  __shared__ DriftCheck shc[APG];
+  // with TAIL the last block only writes the totals of the previous step
+  // (off the path of the atoms' blocks)
+  const int64_t nblk = TAIL ? gridDim.x - 1 : gridDim.x;
+  if (TAIL && blockIdx.x == nblk) {
+    if (tl.prev.np > 0) write_step_sums(tl.prev);
+    return;
+  }
+  const int sub = threadIdx.x % kLanesPerAtom, slot = threadIdx.x / kLanesPerAtom;
+  const int64_t groups = (n + APG - 1) / APG;
+  for (int64_t grp = blockIdx.x; grp < groups; grp += nblk) {
+    const int64_t k = grp * APG + slot;
+    // the step's per-atom inputs, requested before the row so that their
+    // latency overlaps the gathers
+    double im = 0.0, ms = 0.0, eat = 0.0, v0[3] = {0.0, 0.0, 0.0}, x0[3] = {0.0, 0.0, 0.0};
+    int64_t qb[3] = {0, 0, 0};
+    if (TAIL && sub == 0 && k < n) {
+      int a0 = tl.species[k];
+      a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(tl.n_types1) ? a0 : tl.n_types1 - 1;
+      im = tl.inv_mass[a0];
+      ms = tl.mass[a0];
+      eat = tl.e_atom[k];
+      for (int a = 0; a < 3; ++a) v0[a] = tl.vel[3 * k + a];
+      if (tl.kick_next) {
+        for (int a = 0; a < 3; ++a) x0[a] = tl.pos[3 * k + a];
+        if (tl.qbuild)
+          for (int a = 0; a < 3; ++a) qb[a] = tl.qbuild[3 * k + a];
+      }
+    }
+    double fx = 0.0, fy = 0.0, fz = 0.0;
+    if (k < n) {
+      const int64_t b = row_ptr[k], e = b + ecount[k];
+      for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
+        const float4 g = grad[s];
+        const int32_t sr = skin_rev[sidx[s]];
+        const int32_t c = sr >= 0 ? cidx[sr] : -1;
+        const float4 r = c >= 0 ? grad[c] : g;   // a valid list always has the reverse
+        fx += double(g.x) - double(r.x);
+        fy += double(g.y) - double(r.y);
+        fz += double(g.z) - double(r.z);
+      }
+    }
+    for (int off = 1; off < kLanesPerAtom; off <<= 1) {
+      fx += __shfl_xor(fx, off, kLanesPerAtom);
+      fy += __shfl_xor(fy, off, kLanesPerAtom);
+      fz += __shfl_xor(fz, off, kLanesPerAtom);
+    }
+    double ep = 0.0, ek = 0.0;
+    DriftCheck chk{0, 0, 0};
+    if (sub == 0 && k < n) {
+      forces[3 * k] = fx;
+      forces[3 * k + 1] = fy;
+      forces[3 * k + 2] = fz;
+      if (TAIL) {
+        const double f[3] = {fx, fy, fz};
+        double v[3], v2 = 0.0;
+        for (int a = 0; a < 3; ++a) {
+          v[a] = v0[a] + tl.half_dt * f[a] * im;
+          v2 += v[a] * v[a];
+        }
+        // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
+        ek = 0.5 * ms * v2 * (1.66053906660e-17 / 1.602176634e-19);
+        ep = eat;
+        if (tl.kick_next) {
+          for (int a = 0; a < 3; ++a) v[a] = v[a] + tl.half_dt * f[a] * im;
+          chk = drift_check(k, v, x0, tl.pos, tl.dt, tl.qbuild ? qb : nullptr, tl.skin_q);
+        }
+        for (int a = 0; a < 3; ++a) tl.vel[3 * k + a] = v[a];
+      }
+    }
+    if (TAIL) {
+      if (sub == 0) {
+        she[slot] = ep;
+        shk[slot] = ek;
+        shc[slot] = chk;
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        double se = she[0], sk = shk[0];
+        DriftCheck c = shc[0];
+        for (int q = 1; q < APG; ++q) {
+          se += she[q];
+          sk += shk[q];
+          c = merge(c, shc[q]);
+        }
+        tl.part_e[grp] = se;
+        tl.part_k[grp] = sk;
+        if (tl.kick_next) record_check(c, tl.flags, tl.next_step);
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -235,12 +322,16 @@ int blocks_for(int64_t n) {
 
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
-                  double* forces, hipStream_t st) {
-  int64_t blocks = (n + (kBlock / kLanesPerAtom) - 1) / (kBlock / kLanesPerAtom);
+                  double* forces, const StepTail* tail, hipStream_t st) {
+  int64_t blocks = tail_partial_count(n);
   if (blocks > 8192) blocks = 8192;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(forces_kernel, dim3(blocks), dim3(kBlock), 0, st, n, row_ptr, ecount, grad,
-                     sidx, skin_rev, cidx, forces);
+  if (tail) {
+    hipLaunchKernelGGL(forces_kernel<true>, dim3(blocks + 1), dim3(kBlock), 0, st, n, row_ptr, ecount,
+                       grad, sidx, skin_rev, cidx, forces, *tail);
+  } else {
+    hipLaunchKernelGGL(forces_kernel<false>, dim3(blocks), dim3(kBlock), 0, st, n, row_ptr, ecount,
+                       grad, sidx, skin_rev, cidx, forces, StepTail{});
+  }
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -260,15 +351,6 @@ int launch_kick_drift(double* pos, double* vel, const double* forces, const int3
   return 0;
 }
 
-int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* species,
-                const double* inv_mass, const double* mass, int n_types1, double dt,
-                const double* e_atom, double* part_e, double* part_k, hipStream_t st) {
-  hipLaunchKernelGGL(tail_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, n, vel, forces,
-                     species, inv_mass, mass, n_types1, 0.5 * dt, e_atom, part_e, part_k);
-  DPA4C_HIP_TRY(hipGetLastError());
-  return 0;
-}
-
 int launch_final_step(StepSums prev, hipStream_t st) {
   if (prev.np <= 0) return 0;
   hipLaunchKernelGGL(final_step_kernel, dim3(1), dim3(kBlock), 0, st, prev);
@@ -276,7 +358,10 @@ int launch_final_step(StepSums prev, hipStream_t st) {
   return 0;
 }
 
-int tail_partial_count(int64_t n) { return blocks_for(n); }
+int tail_partial_count(int64_t n) {
+  const int64_t g = (n + kBlock / kLanesPerAtom - 1) / (kBlock / kLanesPerAtom);
+  return static_cast<int>(g < 1 ? 1 : g);
+}
 
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st) {
   hipLaunchKernelGGL(snapshot_kernel, dim3(blocks_for(3 * n)), dim3(kBlock), 0, st, pos, n, qbuild);

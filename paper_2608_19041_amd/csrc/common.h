@@ -89,6 +89,7 @@ int with_profile(int C0, int L, int R, int F, Fn&& fn) {
 // ---------------------------------------------------------------------------
 // Device-side view of a model, passed to kernels by value.
 // ---------------------------------------------------------------------------
+constexpr int kMaxTypeRows = 128;        // type-table rows (species + padding) a model may have
 constexpr int kMaxFoldTypes = 5;         // species for which pair-folded tables are built
 constexpr size_t kMaxFoldBytes = size_t(64) << 20;   // and their largest total size
 constexpr int kC123 = 3 * 5 * 7;          // dense (1,2,3) coupling, [m1][m2][m3]

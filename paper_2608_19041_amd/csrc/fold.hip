@@ -30,13 +30,21 @@ namespace dpa4c {
 
 namespace {
 
+// species bitmask: each thread collects the bits of its atoms, a wave merges
+// them and issues one atomic per word
 __global__ void presence_kernel(const int32_t* __restrict__ species, int64_t n, int n_types1,
                                 uint32_t* __restrict__ mask) {
+  uint32_t m[4] = {0u, 0u, 0u, 0u};
   for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * blockDim.x) {
     const int a = clamp_type(species[i], n_types1);
-    atomicOr(&mask[a >> 5], 1u << (a & 31));
+    m[a >> 5] |= 1u << (a & 31);
   }
+  for (int off = 1; off < kWave; off <<= 1)
+    for (int w = 0; w < 4; ++w) m[w] |= __shfl_xor(m[w], off);
+  if ((threadIdx.x & (kWave - 1)) == 0)
+    for (int w = 0; w < 4; ++w)
+      if (m[w]) atomicOr(&mask[w], m[w]);
 }
 
 __global__ void fold_index_kernel(const int32_t* __restrict__ species, int64_t n, int n_types1,

@@ -6,6 +6,8 @@
 
 namespace dpa4c {
 
+// host-only checks of a weight blob's header (no device is touched)
+int check_blob_header(const void* blob, size_t nbytes);
 int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out);
 int launch_pair_cache(dpa4c_model* m, const float* wp_in, const float* wp_out);
 
@@ -44,9 +46,12 @@ int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const 
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
                     const float* node_grad, float4* grad, hipStream_t st);
+struct StepTail;
+// force assembly; with ``tail`` also the velocity-Verlet work of the step
+// that needs only F_k (see StepTail)
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
-                  double* forces, hipStream_t st);
+                  double* forces, const StepTail* tail, hipStream_t st);
 int launch_energy(int64_t n, const double* e_atom, double* partials, double* out,
                   hipStream_t st);
 
@@ -64,16 +69,36 @@ struct StepSums {
   double* e_pot;
   double* e_kin;
 };
+// The velocity-Verlet work fused into the force assembly of a step: the
+// second half kick, the block partials of E_pot and E_kin (tail_partial_count(n)
+// of each) and, with kick_next, the first half kick and the drift of step
+// next_step with its displacement check against qbuild (none when null).
+// An extra block writes the totals of ``prev``, whose partials must be a
+// different buffer from part_e/part_k.
+struct StepTail {
+  double* pos;
+  double* vel;
+  const int32_t* species;
+  const double* inv_mass;
+  const double* mass;
+  int n_types1;
+  double half_dt, dt;
+  const double* e_atom;
+  double* part_e;
+  double* part_k;
+  StepSums prev;
+  int kick_next;
+  const int64_t* qbuild;
+  int64_t skin_q;
+  int64_t* flags;
+  int64_t next_step;
+};
 // half kick (and drift with the displacement check of step ``step`` when
 // qbuild is given); block 0 first adds the partials of the previous step
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
                       const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
                       int64_t step, hipStream_t st);
-// second half kick and the energy partials of the step (tail_partial_count(n) blocks)
-int launch_tail(int64_t n, double* vel, const double* forces, const int32_t* species,
-                const double* inv_mass, const double* mass, int n_types1, double dt,
-                const double* e_atom, double* part_e, double* part_k, hipStream_t st);
 int launch_final_step(StepSums prev, hipStream_t st);
 int tail_partial_count(int64_t n);
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st);

@@ -224,8 +224,10 @@ struct Reader {
 
 }  // namespace
 
-int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out) {
-  if (!blob || !out || nbytes < 64) {
+// The header checks, on the host only: magic, version, a compiled profile
+// and sane values.  Fills the header fields of ``m`` and the widths.
+int read_header(const void* blob, size_t nbytes, dpa4c_model* m, int widths[2]) {
+  if (!blob || nbytes < 64) {
     set_error("dpa4c_model_create: null blob/out or blob shorter than its header");
     return DPA4C_ERR_INVALID_ARG;
   }
@@ -242,13 +244,10 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     set_error("dpa4c_model_create: unknown blob version");
     return DPA4C_ERR_INVALID_ARG;
   }
-  std::unique_ptr<dpa4c_model> m(new dpa4c_model());
-  m->device = device;
   m->C0 = hdr[1]; m->L = hdr[2]; m->R = hdr[3]; m->n_rbf = hdr[4];
   m->F = hdr[5]; m->n_layers = hdr[6]; m->n_types = hdr[7];
   m->r_c = rc_delta[0];
   m->delta = rc_delta[1];
-  int widths[2] = {0, 0};   // S, D_out of the compiled profile
   if (with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
         widths[0] = decltype(p)::S;
         widths[1] = decltype(p)::DOUT;
@@ -263,6 +262,29 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     set_error("dpa4c_model_create: bad header values");
     return DPA4C_ERR_INVALID_ARG;
   }
+  if (m->n_types + 1 > kMaxTypeRows) {   // the per-call species bitmask has 128 bits
+    set_error("dpa4c_model_create: more than 127 species (the type table holds at most 128 rows)");
+    return DPA4C_ERR_UNSUPPORTED;
+  }
+  return 0;
+}
+
+int check_blob_header(const void* blob, size_t nbytes) {
+  dpa4c_model m;
+  int widths[2] = {0, 0};
+  return read_header(blob, nbytes, &m, widths);
+}
+
+int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out) {
+  if (!out) {
+    set_error("dpa4c_model_create: null blob/out or blob shorter than its header");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  std::unique_ptr<dpa4c_model> m(new dpa4c_model());
+  m->device = device;
+  int widths[2] = {0, 0};   // S, D_out of the compiled profile
+  if (int rc = read_header(blob, nbytes, m.get(), widths)) return rc;
+  const uint8_t* b = static_cast<const uint8_t*>(blob);
   const int C0 = m->C0, L = m->L, R = m->R, T1 = m->n_types + 1;
   auto ceil_log2 = [](int x) { int k = 0; while ((1 << k) < x) ++k; return k; };
   int C1 = std::max(4, 1 << ((ceil_log2(C0) + 1) / 2));

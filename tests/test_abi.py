@@ -39,3 +39,22 @@ def test_error_path_without_device():
     rc = lib.dpa4c_model_create(None, 0, 0, ctypes.byref(h))
     assert rc < 0
     assert lib.dpa4c_last_error()
+
+
+def test_too_many_species_rejected_before_device_work():
+    # the per-call species bitmask covers 128 type rows: a header with more is
+    # refused as unsupported, before any device call
+    import struct
+
+    import synth
+
+    spec, weights = synth.model_weights("small")
+    blob = bytearray(synth.pack_blob(spec, weights))
+    assert blob[:8] == b"DPA4CW01"
+    struct.pack_into("<i", blob, 36, 200)   # n_types, the seventh int32 after the version
+    lib = dp.library()
+    h = ctypes.c_void_p()
+    buf = (ctypes.c_char * len(blob)).from_buffer(blob)
+    rc = lib.dpa4c_model_create(buf, len(blob), 0, ctypes.byref(h))
+    assert rc == -2
+    assert b"127 species" in lib.dpa4c_last_error()
