@@ -69,7 +69,9 @@ def stage_work(name, spec, n_atoms, n_edges):
         readout and its VJP add ~1% VALU work, not counted)
       forces               - HBM: per edge 16 B gradient, 12 B for the
         reverse slot (sidx, skin_rev, cidx) and 16 B gathered reverse
-        gradient; per atom 12 B row bounds in, 24 B force out
+        gradient; per atom 12 B row bounds in, 24 B force out, and the
+        velocity-Verlet work fused into it: species 4 B, E_i 8 B, velocity
+        24 B in and out, position 24 B in and out, build snapshot 24 B
     """
     C0, R, L = spec.C0, spec.R, spec.L
     C1 = max(4, 1 << math.ceil(0.5 * math.log2(C0)))
@@ -87,7 +89,7 @@ def stage_work(name, spec, n_atoms, n_edges):
         # per-atom kernel: forward and input-gradient products of the MLP
         return "mfma", 4 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "forces":
-        return "hbm", 44 * n_edges + 36 * n_atoms, "byte"
+        return "hbm", 44 * n_edges + (36 + 132) * n_atoms, "byte"
     return None
 
 
