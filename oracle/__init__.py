@@ -3,9 +3,10 @@
 A plain, slow, float64 CPU implementation of the potential exactly as the
 paper's Methods define it (neighbour set, edge geometry, envelope, Bessel
 basis, radial map, ordered-pair modulation, Cartesian harmonics, one
-aggregation, Gram / bispectrum / quartic invariants, calibration, MLP) and of
-velocity-Verlet dynamics over it.  Forces are the autograd gradient of the
-float64 energy.
+aggregation, Gram / bispectrum / quartic invariants, calibration, MLP), of
+the virial of Eq. (forces), and of velocity-Verlet (NVE) and Nose-Hoover-chain
+(NVT) dynamics over it.  Forces are the autograd gradient of the float64
+energy.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import, call, link or execute anything in this directory.

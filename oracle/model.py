@@ -366,13 +366,15 @@ class Oracle:
         local = np.searchsorted(centres, ei)
         r = pos_t[torch.as_tensor(ej)] + torch.as_tensor(en, dtype=F64) @ cell_t \
             - pos_t[torch.as_tensor(ei)]
+        if r.requires_grad:
+            r.retain_grad()                    # dE/dr_ij, for the virial
         agg = self.aggregate(r, torch.as_tensor(local, dtype=torch.long), len(centres),
                              species[ei], species[ej])
         Dt, D = self.descriptor(agg, species[centres])
-        return self.mlp_energy(D, species[centres]), {"agg": agg, "Dt": Dt, "D": D}
+        return self.mlp_energy(D, species[centres]), {"agg": agg, "Dt": Dt, "D": D, "r": r}
 
     def energy_forces(self, pos, species, cell, pbc, centres=None, chunk: int = 256,
-                      edges=None):
+                      edges=None, virial: bool = False):
         """Per-atom energies of ``centres`` (all atoms if None) and the forces
         F = -dE/dr of their sum, E = sum over those centres of E_i.
 
@@ -380,6 +382,11 @@ class Oracle:
         Eq. (forces).  The sum is split over chunks of centres, each chunk
         differentiated separately; E_i of different centres are independent
         (Eq. (energy-decomposition)), so the split is exact.
+
+        With ``virial`` also returns the virial of Eq. (forces),
+        Xi = -sum_i sum_{j in N_i} dE/dr_ij (x) r_ij (eV, [a][b] = -sum g_a r_b),
+        and the per-centre terms W_i = -sum_{j in N_i} dE/dr_ij (x) r_ij, whose
+        sum over all centres is Xi.
         """
         pos = np.asarray(pos, dtype=np.float64)
         n = pos.shape[0]
@@ -393,13 +400,21 @@ class Oracle:
         e_out = np.empty(len(centres))
         starts = np.searchsorted(ei, centres)
         ends = np.searchsorted(ei, centres, side="right")
+        w_atom = np.zeros((len(centres), 3, 3))
         for c0 in range(0, len(centres), chunk):
             cs = centres[c0:c0 + chunk]
             a, b = starts[c0], ends[min(c0 + chunk, len(centres)) - 1]
-            E, _ = self.atomic_energies(pos_t, species, cell, (ei[a:b], ej[a:b], en[a:b]), cs)
+            E, aux = self.atomic_energies(pos_t, species, cell, (ei[a:b], ej[a:b], en[a:b]), cs)
             E.sum().backward()
             e_out[c0:c0 + chunk] = E.detach().numpy()
+            if virial and b > a:
+                g = aux["r"].grad.numpy()                       # dE/dr_ij
+                r = aux["r"].detach().numpy()
+                local = np.searchsorted(cs, ei[a:b])
+                np.add.at(w_atom[c0:c0 + chunk], local, -g[:, :, None] * r[:, None, :])
         forces = -pos_t.grad.numpy()
+        if virial:
+            return e_out, forces, w_atom.sum(axis=0), w_atom
         return e_out, forces
 
     def stages(self, pos, species, cell, pbc, centres=None, edges=None):

@@ -206,3 +206,37 @@ def test_nve_energy_conservation_config1(small):
     et = ep + ek
     assert abs(md.drift_ev_per_atom_ps(et, 1.0, s.n)) < 1e-5
     assert (et.max() - et.min()) / s.n < 1e-5
+
+
+def triclinic_cell_system(seed=5, n=20):
+    cell = np.array([[8.3, 0.0, 0.0], [1.2, 8.9, 0.0], [0.7, -0.9, 9.4]])
+    return synth.random_periodic(n, seed=seed, cell=cell, d_min=1.6)
+
+
+@pytest.mark.parametrize("which", ["small", "full"])
+def test_virial_is_minus_the_strain_derivative_of_the_energy(which, request):
+    # Eq. (forces): Xi = -sum g (x) r.  Independently, under a homogeneous
+    # deformation x -> (I + eps) x of positions and cell every edge vector
+    # becomes (I + eps) r, so dE/d eps_ab = sum_e g_a r_b = -Xi_ab; checked by
+    # central differences with the neighbour list held fixed, on a triclinic
+    # cell so that every component is distinct.
+    o = request.getfixturevalue(which)
+    s = triclinic_cell_system()
+    edges = nb.neighbor_list(s.pos, s.cell, s.pbc, o.r_c)
+    e, F, Xi, W = o.energy_forces(s.pos, s.species, s.cell, s.pbc, edges=edges, virial=True)
+    assert np.allclose(W.sum(axis=0), Xi, rtol=0, atol=1e-12)
+    h = 1e-5
+    fd = np.zeros((3, 3))
+    for a in range(3):
+        for b in range(3):
+            es = []
+            for sgn in (1.0, -1.0):
+                A = np.eye(3)
+                A[a, b] += sgn * h
+                st = o.stages(s.pos @ A.T, s.species, s.cell @ A.T, s.pbc, edges=edges)
+                es.append(st["E"].sum())
+            fd[a, b] = -(es[0] - es[1]) / (2 * h)
+    scale = np.abs(Xi).max()
+    assert np.abs(fd - Xi).max() < 1e-7 * scale, (fd, Xi)
+    # rotation invariance makes the virial symmetric
+    assert np.abs(Xi - Xi.T).max() < 1e-12 * scale
