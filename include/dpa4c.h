@@ -152,6 +152,25 @@ int compute_energy_forces(const dpa4c_model* model, const double* pos, const int
                           void* stream);
 
 /*
+ * compute_energy_forces plus the virial of Eq. (forces),
+ *     Xi = -sum_i sum_{j in N_i} dE/dr_ij (x) r_ij      (eV),
+ * from the same per-edge gradients: r_ij is the float64 difference stored in
+ * float32, products and sums are float64, in a fixed order.  The stress is
+ * -Xi / V (Methods, benchmark metrics).
+ *
+ * virial       device float64 [9] out (required): Xi[a][b], row-major
+ * atom_virial  device float64 [N][9] out, or NULL: the per-centre terms
+ *              W_i = -sum_{j in N_i} dE/dr_ij (x) r_ij, which sum to Xi
+ * Other arguments, errors and determinism as compute_energy_forces.
+ */
+int compute_energy_forces_virial(const dpa4c_model* model, const double* pos,
+                                 const int32_t* species, int64_t N, const double cell[9],
+                                 const int pbc[3], double r_c, const int64_t* row_ptr,
+                                 const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
+                                 double* e_atom, double* forces, double* e_total, double* virial,
+                                 double* atom_virial, void* stream);
+
+/*
  * ``nsteps`` velocity-Verlet NVE steps (Supplementary Note on the MD
  * protocol: full neighbour list with a skin, checked every step):
  *     v += dt/2 F/m;  r += dt v;  [rebuild];  F = F(r);  v += dt/2 F/m.
@@ -186,6 +205,40 @@ int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_
                 const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
                 double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
                 double* e_pot, double* e_kin, double* forces, int64_t* n_rebuilds, void* stream);
+
+/*
+ * ``nsteps`` NVT steps with a Nose-Hoover chain thermostat (the paper's
+ * whole-step benchmark propagates NVT at 300 K): the chain of Martyna, Klein
+ * and Tuckerman (J. Chem. Phys. 97, 2635, 1992), propagated over half steps
+ * by the Trotter factorisation of Martyna, Tuckerman, Tobias and Klein (Mol.
+ * Phys. 87, 1117, 1996).  Per step:
+ *     chain dt/2;  v += dt/2 F/m;  r += dt v;  [rebuild];  F = F(r);
+ *     v += dt/2 F/m;  chain dt/2,
+ * where a chain half step scales all velocities by exp(-dt/2 v_xi1).  Chain
+ * masses Q_1 = N_f kT tau^2 and Q_k = kT tau^2 (tau = t_damp_fs), with
+ * N_f = 3N - 3.  The virial of Eq. (forces) is assembled at every step.
+ * Neighbour list, rebuilds, batches and replay as verlet_step; the chain
+ * state is saved with the batch start state.
+ *
+ * temperature      target T (K), > 0
+ * t_damp_fs        damping time tau (fs), > 0
+ * chain_length     M, 1..8
+ * chain            device float64 [2M], in/out: xi_1..xi_M then v_xi1..v_xiM
+ *                  (zeros for a fresh thermostat)
+ * e_pot, e_kin     device float64 [nsteps] out: potential and kinetic energy
+ *                  after each step (eV)
+ * e_thermo         device float64 [nsteps] out: thermostat energy after each
+ *                  step, sum Q_k v_k^2/2 + N_f kT xi_1 + kT sum_{k>1} xi_k;
+ *                  e_pot + e_kin + e_thermo is the conserved quantity
+ * virial           device float64 [nsteps][9] out, or NULL: Xi at each step
+ * Other arguments, errors and synchronisation as verlet_step; N >= 2.
+ */
+int nvt_step(const dpa4c_model* model, double* pos, double* vel, const int32_t* species,
+             const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+             double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
+             double temperature, double t_damp_fs, int chain_length, double* chain,
+             double* e_pot, double* e_kin, double* e_thermo, double* virial, double* forces,
+             int64_t* n_rebuilds, void* stream);
 
 /*
  * Intermediate quantities of the last compute_energy_forces (or the last

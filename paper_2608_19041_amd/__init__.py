@@ -50,8 +50,12 @@ def library():
                                       ctypes.POINTER(i64), vp]),
             "compute_energy_forces": (i32, [vp, vp, vp, i64, vp, vp, dbl, vp, vp, vp, i64,
                                             vp, vp, vp, vp]),
+            "compute_energy_forces_virial": (i32, [vp, vp, vp, i64, vp, vp, dbl, vp, vp, vp,
+                                                   i64, vp, vp, vp, vp, vp, vp]),
             "verlet_step": (i32, [vp, vp, vp, vp, vp, i64, vp, vp, dbl, dbl, dbl, i32, i32,
                                   vp, vp, vp, ctypes.POINTER(i64), vp]),
+            "nvt_step": (i32, [vp, vp, vp, vp, vp, i64, vp, vp, dbl, dbl, dbl, i32, i32, dbl, dbl,
+                               i32, vp, vp, vp, vp, vp, vp, ctypes.POINTER(i64), vp]),
             "dpa4c_debug_stages": (i32, [vp, i64, vp, vp, vp, vp]),
             "dpa4c_set_timing": (i32, [vp, i64]),
             "dpa4c_get_timings": (i32, [vp, vp, vp, i32]),
@@ -69,7 +73,8 @@ def library():
 
 def exported_symbols() -> list[str]:
     return ["dpa4c_model_create", "dpa4c_model_destroy", "dpa4c_model_info", "build_neighbors",
-            "compute_energy_forces", "verlet_step", "dpa4c_debug_stages", "dpa4c_set_timing",
+            "compute_energy_forces", "compute_energy_forces_virial", "verlet_step", "nvt_step",
+            "dpa4c_debug_stages", "dpa4c_set_timing",
             "dpa4c_get_timings", "dpa4c_stage_name", "dpa4c_debug_gemm", "dpa4c_last_error"]
 
 
@@ -210,6 +215,59 @@ class Model:
             _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
             _ptr(e_total), _stream(stream)))
         return e_atom, forces, e_total
+
+    def compute_energy_forces_virial(self, pos, species, cell, pbc, r_c, row_ptr, nbr_j,
+                                     nbr_shift, n_pairs, atom_virial=False, stream=None):
+        """(e_atom, forces, e_total, virial [3, 3], atom_virial [N, 3, 3] or None)."""
+        import torch
+        n = pos.shape[0]
+        _require(pos, torch.float64, (n, 3), "pos")
+        _require(species, torch.int32, (n,), "species")
+        dev = pos.device
+        e_atom = torch.empty(n, dtype=torch.float64, device=dev)
+        forces = torch.empty(n, 3, dtype=torch.float64, device=dev)
+        e_total = torch.empty(1, dtype=torch.float64, device=dev)
+        virial = torch.empty(3, 3, dtype=torch.float64, device=dev)
+        w_atom = torch.empty(n, 3, 3, dtype=torch.float64, device=dev) if atom_virial else None
+        cellh = _host_f64(cell, 9)
+        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        _check(library().compute_energy_forces_virial(
+            self._h, _ptr(pos), _ptr(species), n, cellh.ctypes.data, pbch.ctypes.data, float(r_c),
+            _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
+            _ptr(e_total), _ptr(virial), _ptr(w_atom), _stream(stream)))
+        return e_atom, forces, e_total, virial, w_atom
+
+    def nvt_step(self, pos, vel, species, mass_by_species, cell, pbc, r_c, skin, dt_fs, nsteps,
+                 rebuild_every, forces, temperature, t_damp_fs, chain, virial=False, stream=None):
+        """NVT steps; ``chain`` is a float64 device tensor [2M] (in/out).
+        Returns (e_pot, e_kin, e_thermo, virial [nsteps, 3, 3] or None, n_rebuilds)."""
+        import torch
+        n = pos.shape[0]
+        _require(pos, torch.float64, (n, 3), "pos")
+        _require(vel, torch.float64, (n, 3), "vel")
+        _require(forces, torch.float64, (n, 3), "forces")
+        _require(species, torch.int32, (n,), "species")
+        _require(chain, torch.float64, None, "chain")
+        if chain.dim() != 1 or chain.shape[0] % 2:
+            raise ValueError("chain must hold 2M values")
+        dev = pos.device
+        k = max(nsteps, 1)
+        e_pot = torch.empty(k, dtype=torch.float64, device=dev)
+        e_kin = torch.empty(k, dtype=torch.float64, device=dev)
+        e_th = torch.empty(k, dtype=torch.float64, device=dev)
+        vir = torch.empty(k, 3, 3, dtype=torch.float64, device=dev) if virial else None
+        masses = _host_f64(mass_by_species, self.info["n_types"] + 1)
+        cellh = _host_f64(cell, 9)
+        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        nreb = ctypes.c_int64(0)
+        _check(library().nvt_step(
+            self._h, _ptr(pos), _ptr(vel), _ptr(species), masses.ctypes.data, n, cellh.ctypes.data,
+            pbch.ctypes.data, float(r_c), float(skin), float(dt_fs), int(nsteps), int(rebuild_every),
+            float(temperature), float(t_damp_fs), int(chain.shape[0] // 2), _ptr(chain),
+            _ptr(e_pot), _ptr(e_kin), _ptr(e_th), _ptr(vir), _ptr(forces), ctypes.byref(nreb),
+            _stream(stream)))
+        return (e_pot[:nsteps], e_kin[:nsteps], e_th[:nsteps],
+                None if vir is None else vir[:nsteps], int(nreb.value))
 
     def verlet_step(self, pos, vel, species, mass_by_species, cell, pbc, r_c, skin, dt_fs,
                     nsteps, rebuild_every, forces, e_pot=None, e_kin=None, stream=None):

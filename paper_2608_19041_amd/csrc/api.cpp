@@ -132,14 +132,26 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   return 0;
 }
 
+// NVT parameters of a dynamics call (nvt_step)
+struct NvtConfig {
+  double temperature;   // K
+  double t_damp;        // fs
+  int length;           // chain length M
+  double* chain;        // device [2M]: xi_1..M then v_1..M, in/out
+  double* e_thermo;     // device [nsteps]
+  double* virial;       // device [nsteps][9] or null
+};
+
 // Everything after the skin list: forward (with the compaction of the skin
 // rows), per-atom kernel, backward, forces and the energy sum.
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
               const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
-              double* forces, double* e_total, const StepTail* tail, hipStream_t st) {
+              double* forces, double* e_total, const StepTail* tail, const VirialOut* vir,
+              double* virial, hipStream_t st) {
   // e_total == nullptr: the caller sums the energy itself; ``tail``: the
-  // velocity-Verlet work fused into the force assembly
+  // velocity-Verlet work fused into the force assembly; ``vir``: the virial
+  // partials (and per-atom terms), summed into virial[9] when that is given
   dpa4c_model* m = const_cast<dpa4c_model*>(mc);
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
@@ -167,8 +179,13 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStForces, st);
     rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.grad.as<float4>(),
-                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, tail, st);
+                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, tail, vir,
+                       st);
     if (rc) return rc;
+    if (vir && virial) {
+      rc = launch_sum_components(vir->part_v, tail_partial_count(n), 9, virial, st);
+      if (rc) return rc;
+    }
   }
   if (e_total) {
     StageScope t(m, kStEnergy, st);
@@ -304,11 +321,16 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
   return flags_to_error(hflag[1]);
 }
 
-int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t* species,
-                          int64_t N, const double cell[9], const int pbc[3], double r_c,
-                          const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                          int64_t n_pairs, double* e_atom, double* forces, double* e_total,
-                          void* stream) {
+}  // extern "C"
+
+namespace {
+
+// compute_energy_forces with the optional virial (virial == nullptr: none)
+int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* species,
+                       int64_t N, const double cell[9], const int pbc[3], double r_c,
+                       const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
+                       int64_t n_pairs, double* e_atom, double* forces, double* e_total,
+                       double* virial, double* atom_virial, void* stream) {
   if (!m || N < 0 || n_pairs < 0 || !row_ptr || !e_total ||
       (N > 0 && (!pos || !species || !e_atom || !forces)) ||
       (n_pairs > 0 && (!nbr_j || !nbr_shift))) {
@@ -337,6 +359,7 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
   double box[3] = {cell[0], cell[4], cell[8]};
   if (N == 0) {
     DPA4C_HIP_TRY(hipMemsetAsync(e_total, 0, sizeof(double), st));
+    if (virial) DPA4C_HIP_TRY(hipMemsetAsync(virial, 0, 9 * sizeof(double), st));
     return 0;
   }
   rc = prepare_species(mm, species, N, st);
@@ -346,32 +369,71 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
     rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), st);
     if (rc) return rc;
   }
+  VirialOut vo{};
+  if (virial) {
+    if (mm->ws.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N)))) return DPA4C_ERR_HIP;
+    vo = VirialOut{mm->ws.edge.as<float4>(), mm->ws.virpart.as<double>(), atom_virial};
+  }
   return run_model(m, pos, species, N, g, box, row_ptr, nbr_j, nbr_shift, n_pairs,
-                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr, st);
+                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr,
+                   virial ? &vo : nullptr, virial, st);
 }
 
-int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
-                const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
-                double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
-                double* e_pot, double* e_kin, double* forces, int64_t* n_rebuilds, void* stream) {
+}  // namespace
+
+extern "C" {
+
+int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t* species,
+                          int64_t N, const double cell[9], const int pbc[3], double r_c,
+                          const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
+                          int64_t n_pairs, double* e_atom, double* forces, double* e_total,
+                          void* stream) {
+  return energy_forces_impl(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
+                            e_atom, forces, e_total, nullptr, nullptr, stream);
+}
+
+int compute_energy_forces_virial(const dpa4c_model* m, const double* pos,
+                                 const int32_t* species, int64_t N, const double cell[9],
+                                 const int pbc[3], double r_c, const int64_t* row_ptr,
+                                 const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
+                                 double* e_atom, double* forces, double* e_total, double* virial,
+                                 double* atom_virial, void* stream) {
+  if (!virial) {
+    set_error("compute_energy_forces_virial: null virial");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  return energy_forces_impl(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
+                            e_atom, forces, e_total, virial, atom_virial, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Velocity-Verlet dynamics, NVE or (with ``nvt``) Nose-Hoover-chain NVT.
+int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
+             const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+             double r_c, double skin, double dt_fs, int nsteps, int rebuild_every, double* e_pot,
+             double* e_kin, double* forces, int64_t* n_rebuilds, void* stream,
+             const NvtConfig* nvt) {
   if (!m || N <= 0 || nsteps < 0 || !pos || !vel || !species || !mass_by_species || !forces ||
       (nsteps > 0 && (!e_pot || !e_kin))) {
-    set_error("verlet_step: bad pointer or size");
+    set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "bad pointer or size");
     return DPA4C_ERR_INVALID_ARG;
   }
   if (N >= (int64_t(1) << 31)) {
-    set_error("verlet_step: at most 2^31 - 1 atoms");
+    set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "at most 2^31 - 1 atoms");
     return DPA4C_ERR_INVALID_ARG;
   }
   if (std::fabs(r_c - m->r_c) > 1e-12 || !(skin >= 0.0) || skin > 100.0 || !(dt_fs > 0.0) ||
       !(dt_fs < 100.0)) {
-    set_error("verlet_step: r_c must equal the model's; skin in [0, 100] A; dt in (0, 100) fs");
+    set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "r_c must equal the model's; skin in [0, 100] A; dt in (0, 100) fs");
     return DPA4C_ERR_INVALID_ARG;
   }
   const int T1 = m->n_types + 1;
   for (int t = 0; t < T1; ++t)
     if (!(mass_by_species[t] > 0.0) || !std::isfinite(mass_by_species[t])) {
-      set_error("verlet_step: masses must be positive and finite");
+      set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "masses must be positive and finite");
       return DPA4C_ERR_INVALID_ARG;
     }
   int rc = check_cell(cell, pbc);
@@ -407,6 +469,33 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   int64_t* flags = w.flags.as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
 
+  // NVT: the chain state [xi, v, scale] (S words), its batch backup, the
+  // kinetic partials of the current velocities and the virial partials
+  NhcArgs nhc{};
+  double* nvt_state = nullptr;
+  double* nvt_backup = nullptr;
+  double* kin_part = nullptr;
+  const int npk = kinetic_partial_count(N);
+  if (nvt) {
+    const int M = nvt->length;
+    const size_t S = 2 * size_t(M) + 1;
+    if (w.nvt.ensure(8 * (2 * S + size_t(npk))) ||
+        w.virpart.ensure(2 * 9 * 8 * size_t(np_tail)))
+      return DPA4C_ERR_HIP;
+    nvt_state = w.nvt.as<double>();
+    nvt_backup = nvt_state + S;
+    kin_part = nvt_backup + S;
+    DPA4C_HIP_TRY(hipMemcpyAsync(nvt_state, nvt->chain, 16 * size_t(M), hipMemcpyDeviceToDevice, st));
+    nhc.state = nvt_state;
+    nhc.M = M;
+    nhc.kT = 8.617333262e-5 * nvt->temperature;   // Boltzmann constant in eV/K (CODATA 2018)
+    nhc.nf = double(3 * N - 3);
+    nhc.dt = dt_fs;
+    for (int k = 0; k < M; ++k)
+      nhc.Q[k] = (k == 0 ? nhc.nf : 1.0) * nhc.kT * nvt->t_damp * nvt->t_damp;
+  }
+  auto vir_part = [&](int64_t s) { return w.virpart.as<double>() + (s & 1) * 9 * size_t(np_tail); };
+
   // a build of the skin list: count, read the size back, grow the capacity
   // if needed, fill, reverse index and the positions of the build
   auto initial_build = [&]() -> int {
@@ -427,7 +516,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
       int64_t cap = need + need / 2 + 64 * N;
       if (cap >= (int64_t(1) << 31)) cap = (int64_t(1) << 31) - 1;
       if (cap < need) {
-        set_error("verlet_step: more than 2^31 - 1 neighbour pairs");
+        set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "more than 2^31 - 1 neighbour pairs");
         return DPA4C_ERR_CAPACITY;
       }
       if (w.skin_j.ensure(4 * cap) || w.skin_shift.ensure(4 * cap)) return DPA4C_ERR_HIP;
@@ -459,13 +548,45 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
   // does the second half kick, the energy partials of the step, the totals
   // of step ``prev`` and, with ``kick_next``, the kick and drift of the next
   // step (checked when ``check``).
+  // NVT: the chain launch before a kick closes step ``prev`` (when >= 0) and
+  // opens the next step
+  auto chain_launch = [&](int64_t prev, bool open) -> int {
+    NhcArgs a = nhc;
+    if (prev >= 0) {
+      a.part_k = part_e(prev) + np_tail;
+      a.part_e = part_e(prev);
+      a.part_v = vir_part(prev);
+      a.np = np_tail;
+      a.close_prev = 1;
+      a.e_pot = e_pot + prev;
+      a.e_kin = e_kin + prev;
+      a.e_thermo = nvt->e_thermo + prev;
+      a.virial = nvt->virial ? nvt->virial + 9 * prev : nullptr;
+    } else {
+      int r = launch_kinetic(vel, species, w.mass.as<double>(), T1, N, kin_part, st);
+      if (r) return r;
+      a.part_k = kin_part;
+      a.np = npk;
+    }
+    a.open_next = open ? 1 : 0;
+    return launch_nhc(a, st);
+  };
   auto one_step = [&](int64_t step, bool check, bool rebuild, int64_t prev, bool kicked,
                       bool kick_next) -> int {
+    if (nvt) {
+      kicked = false;
+      kick_next = false;
+    }
     if (!kicked) {
       StageScope t(m, kStIntegrate, st);
+      if (nvt) {
+        int r = chain_launch(prev, true);
+        if (r) return r;
+      }
       int r = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs,
                                 1, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
-                                sums_of(-1), step, st);
+                                sums_of(-1), step, nvt ? nvt_state + 2 * nvt->length : nullptr,
+                                st);
       if (r) return r;
     }
     if (rebuild) {
@@ -473,18 +594,30 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
       if (r) return r;
       ++rebuilds;
     }
+    // (NVT: the chain launch adds the step's partials up, not the force assembly)
     const StepTail tail{pos, vel, species, w.inv_mass.as<double>(), w.mass.as<double>(), T1,
                         0.5 * dt_fs, dt_fs, w.eatom.as<double>(), part_e(step),
-                        part_e(step) + np_tail, sums_of(prev), kick_next ? 1 : 0,
-                        check ? w.qbuild.as<int64_t>() : nullptr, skq, flags, step + 1};
+                        part_e(step) + np_tail, nvt ? sums_of(-1) : sums_of(prev),
+                        kick_next ? 1 : 0, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
+                        step + 1};
+    const VirialOut vo{w.edge.as<float4>(), nvt ? vir_part(step) : nullptr, nullptr};
     return run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(),
                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
-                     w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail, st);
+                     w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
+                     nvt ? &vo : nullptr, nullptr, st);
   };
+  // the end of a batch: the totals of step ``last`` (NVT: its closing chain
+  // half step and velocity scaling)
   auto finish = [&](int64_t last) -> int {
     StageScope t(m, kStIntegrate, st);
+    if (nvt) {
+      int r = chain_launch(last, false);
+      if (r) return r;
+      return launch_scale(vel, N, nvt_state + 2 * nvt->length, st);
+    }
     return launch_final_step(sums_of(last), st);
   };
+  const size_t nvt_words = nvt ? 2 * size_t(nvt->length) + 1 : 0;
 
   // Step 0 builds the list.  Later steps run in speculative batches without
   // rebuild checks on the host: kick/drift records the first step whose
@@ -522,6 +655,8 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     DPA4C_HIP_TRY(hipMemcpyAsync(bk, pos, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(bk + 3 * N, vel, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(bk + 6 * N, forces, state, hipMemcpyDeviceToDevice, st));
+    if (nvt)
+      DPA4C_HIP_TRY(hipMemcpyAsync(nvt_backup, nvt_state, 8 * nvt_words, hipMemcpyDeviceToDevice, st));
     rc = launch_set_flag(flags, 4, INT64_MAX, st);
     if (rc) return rc;
     rc = launch_set_flag(flags, 5, 0, st);
@@ -548,7 +683,7 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
       continue;
     }
     if (rebuild_every < 0) {
-      set_error("verlet_step: an atom moved more than skin/2 and rebuilds are disabled");
+      set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "an atom moved more than skin/2 and rebuilds are disabled");
       return DPA4C_ERR_SKIN;
     }
     // violation at step v: the displacement reached half the skin within
@@ -559,6 +694,8 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     DPA4C_HIP_TRY(hipMemcpyAsync(pos, bk, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(vel, bk + 3 * N, state, hipMemcpyDeviceToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(forces, bk + 6 * N, state, hipMemcpyDeviceToDevice, st));
+    if (nvt)
+      DPA4C_HIP_TRY(hipMemcpyAsync(nvt_state, nvt_backup, 8 * nvt_words, hipMemcpyDeviceToDevice, st));
     for (int64_t t = s; t < v; ++t) {
       rc = one_step(t, false, false, t > s ? t - 1 : -1, t > s, t + 1 < v);
       if (rc) return rc;
@@ -576,10 +713,43 @@ int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* s
     batch = static_cast<int64_t>(0.75 * half_skin / growth);
     batch = batch < 1 ? 1 : (batch > 64 ? 64 : batch);
   }
+  if (nvt)
+    DPA4C_HIP_TRY(hipMemcpyAsync(nvt->chain, nvt_state, 16 * size_t(nvt->length),
+                                 hipMemcpyDeviceToDevice, st));
   DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
   if (n_rebuilds) *n_rebuilds = rebuilds;
   return flags_to_error(w.host_flags[0]);
+}
+
+}  // namespace
+
+extern "C" {
+
+int verlet_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
+                const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+                double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
+                double* e_pot, double* e_kin, double* forces, int64_t* n_rebuilds, void* stream) {
+  return dynamics(m, pos, vel, species, mass_by_species, N, cell, pbc, r_c, skin, dt_fs, nsteps,
+                  rebuild_every, e_pot, e_kin, forces, n_rebuilds, stream, nullptr);
+}
+
+int nvt_step(const dpa4c_model* m, double* pos, double* vel, const int32_t* species,
+             const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
+             double r_c, double skin, double dt_fs, int nsteps, int rebuild_every,
+             double temperature, double t_damp_fs, int chain_length, double* chain, double* e_pot,
+             double* e_kin, double* e_thermo, double* virial, double* forces,
+             int64_t* n_rebuilds, void* stream) {
+  if (!(temperature > 0.0) || !std::isfinite(temperature) || !(t_damp_fs > 0.0) ||
+      !std::isfinite(t_damp_fs) || chain_length < 1 || chain_length > kMaxChain || !chain ||
+      (nsteps > 0 && !e_thermo) || N < 2) {
+    set_error("nvt_step: temperature and damping time must be positive, chain length in [1, 8], "
+              "chain and e_thermo given, N >= 2");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  const NvtConfig cfg{temperature, t_damp_fs, chain_length, chain, e_thermo, virial};
+  return dynamics(m, pos, vel, species, mass_by_species, N, cell, pbc, r_c, skin, dt_fs, nsteps,
+                  rebuild_every, e_pot, e_kin, forces, n_rebuilds, stream, &cfg);
 }
 
 int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float* descriptor,

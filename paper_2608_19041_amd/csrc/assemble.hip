@@ -84,6 +84,10 @@ __device__ inline void write_step_sums(const StepSums& prev) {
   }
 }
 
+// The kicks v += (dt/2 F) / m and the drift r += dt v are written as explicit
+// fused multiply-adds, so that every kernel that applies them rounds alike
+// (the same step gives the same bits whichever kernel performs it).
+
 // Outcome of the displacement check of one or more atoms
 struct DriftCheck {
   int bad;       // a non-finite or absurd position
@@ -101,7 +105,7 @@ __device__ inline DriftCheck drift_check(int64_t i, const double* v, const doubl
   bool far = false;
   int64_t d2 = 0;
   for (int a = 0; a < 3; ++a) {
-    const double x = x0[a] + dt * v[a];
+    const double x = __fma_rn(dt, v[a], x0[a]);
     pos[3 * i + a] = x;
     if (!isfinite(x) || fabs(x) > 1.0e12) c.bad = 1;
     if (!c.bad && qb) {
@@ -134,8 +138,9 @@ __device__ inline void record_check(const DriftCheck& c, int64_t* __restrict__ f
   if (c.d2 > 0) atomicMax(reinterpret_cast<unsigned long long*>(flags + 5), (unsigned long long)c.d2);
 }
 
-// v += dt/2 F/m and optionally the drift with its displacement check
-// (merged per wave); block 0 first writes the totals of ``prev``
+// v += dt/2 F/m (after v *= *scale when a scale is given) and optionally the
+// drift with its displacement check (merged per wave); block 0 first writes
+// the totals of ``prev``
 __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__ pos, double* __restrict__ vel,
                                                             const double* __restrict__ forces,
                                                             const int32_t* __restrict__ species,
@@ -144,7 +149,8 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
                                                             double dt,
                                                             int drift, const int64_t* __restrict__ qbuild,
                                                             int64_t skin_q, int64_t* __restrict__ flags,
-                                                            StepSums prev, int64_t step) {
+                                                            StepSums prev, int64_t step,
+                                                            const double* __restrict__ scale) {
   if (prev.np > 0 && blockIdx.x == 0) write_step_sums(prev);
   const int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   DriftCheck c{0, 0, 0};
@@ -153,8 +159,15 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
     a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
     const double im = inv_mass[a0];
     double v[3];
+    for (int a = 0; a < 3; ++a) v[a] = vel[3 * i + a];
+    if (scale) {   // the thermostat's velocity scale, applied before the kick
+      // (rounded on its own, not contracted into the kick: with s = 1 the kick
+      // is then exactly the NVE one)
+      const double s = *scale;
+      for (int a = 0; a < 3; ++a) v[a] = __dmul_rn(v[a], s);
+    }
     for (int a = 0; a < 3; ++a) {
-      v[a] = vel[3 * i + a] + half_dt * forces[3 * i + a] * im;
+      v[a] = __fma_rn(half_dt * forces[3 * i + a], im, v[a]);
       vel[3 * i + a] = v[a];
     }
     if (drift) {
@@ -187,17 +200,24 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
 // partial buffer).  With kick_next the same lane goes on with the first
 // half kick and the drift of the next step (drift_check): both use F_k, so
 // the arithmetic is that of separate kick kernels.
-template <bool TAIL>
+//
+// With VIR the same lanes form the virial of Eq. (forces) from the atom's own
+// row: W_k = -sum_{e in row k} g_e (x) r_e (r_e from the compact edge
+// records, g_e and r_e promoted to float64), written per atom when asked and
+// summed per group in a fixed order into part_v[group][9].
+template <bool TAIL, bool VIR>
 __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
                                                         const float4* __restrict__ grad,
                                                         const int32_t* __restrict__ sidx,
                                                         const int32_t* __restrict__ skin_rev,
                                                         const int32_t* __restrict__ cidx,
-                                                        double* __restrict__ forces, StepTail tl) {
+                                                        double* __restrict__ forces, StepTail tl,
+                                                        VirialOut vo) {
   constexpr int APG = kBlock / kLanesPerAtom;
   __shared__ double she[APG], shk[APG];
   __shared__ DriftCheck shc[APG];
+  __shared__ double shv[VIR ? APG : 1][9];
   // with TAIL the last block only writes the totals of the previous step
   // (off the path of the atoms' blocks)
   const int64_t nblk = TAIL ? gridDim.x - 1 : gridDim.x;
@@ -227,6 +247,8 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
       }
     }
     double fx = 0.0, fy = 0.0, fz = 0.0;
+    double w[VIR ? 9 : 1];
+    for (int c = 0; c < (VIR ? 9 : 1); ++c) w[c] = 0.0;
     if (k < n) {
       const int64_t b = row_ptr[k], e = b + ecount[k];
       for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
@@ -237,12 +259,24 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
         fx += double(g.x) - double(r.x);
         fy += double(g.y) - double(r.y);
         fz += double(g.z) - double(r.z);
+        if (VIR) {
+          const float4 d = vo.edge[s];
+          const double ga[3] = {double(g.x), double(g.y), double(g.z)};
+          const double rb[3] = {double(d.x), double(d.y), double(d.z)};
+#pragma unroll
+          for (int a = 0; a < 3; ++a)
+#pragma unroll
+            for (int bb = 0; bb < 3; ++bb) w[3 * a + bb] -= ga[a] * rb[bb];
+        }
       }
     }
     for (int off = 1; off < kLanesPerAtom; off <<= 1) {
       fx += __shfl_xor(fx, off, kLanesPerAtom);
       fy += __shfl_xor(fy, off, kLanesPerAtom);
       fz += __shfl_xor(fz, off, kLanesPerAtom);
+      if (VIR)
+#pragma unroll
+        for (int c = 0; c < 9; ++c) w[c] += __shfl_xor(w[c], off, kLanesPerAtom);
     }
     double ep = 0.0, ek = 0.0;
     DriftCheck chk{0, 0, 0};
@@ -250,31 +284,37 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
       forces[3 * k] = fx;
       forces[3 * k + 1] = fy;
       forces[3 * k + 2] = fz;
+      if (VIR && vo.atom)
+        for (int c = 0; c < 9; ++c) vo.atom[9 * k + c] = w[c];
       if (TAIL) {
         const double f[3] = {fx, fy, fz};
         double v[3], v2 = 0.0;
         for (int a = 0; a < 3; ++a) {
-          v[a] = v0[a] + tl.half_dt * f[a] * im;
+          v[a] = __fma_rn(tl.half_dt * f[a], im, v0[a]);
           v2 += v[a] * v[a];
         }
         // 1 u (A/fs)^2 = 103.6427 eV (CODATA 2018 atomic mass unit and elementary charge)
         ek = 0.5 * ms * v2 * (1.66053906660e-17 / 1.602176634e-19);
         ep = eat;
         if (tl.kick_next) {
-          for (int a = 0; a < 3; ++a) v[a] = v[a] + tl.half_dt * f[a] * im;
+          for (int a = 0; a < 3; ++a) v[a] = __fma_rn(tl.half_dt * f[a], im, v[a]);
           chk = drift_check(k, v, x0, tl.pos, tl.dt, tl.qbuild ? qb : nullptr, tl.skin_q);
         }
         for (int a = 0; a < 3; ++a) tl.vel[3 * k + a] = v[a];
       }
     }
-    if (TAIL) {
+    if (TAIL || VIR) {
       if (sub == 0) {
-        she[slot] = ep;
-        shk[slot] = ek;
-        shc[slot] = chk;
+        if (TAIL) {
+          she[slot] = ep;
+          shk[slot] = ek;
+          shc[slot] = chk;
+        }
+        if (VIR)
+          for (int c = 0; c < 9; ++c) shv[slot][c] = k < n ? w[c] : 0.0;
       }
       __syncthreads();
-      if (threadIdx.x == 0) {
+      if (TAIL && threadIdx.x == 0) {
         double se = she[0], sk = shk[0];
         DriftCheck c = shc[0];
         for (int q = 1; q < APG; ++q) {
@@ -286,9 +326,122 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
         tl.part_k[grp] = sk;
         if (tl.kick_next) record_check(c, tl.flags, tl.next_step);
       }
+      if (VIR && threadIdx.x < 9) {
+        const int c = threadIdx.x;
+        double sv = shv[0][c];
+        for (int q = 1; q < APG; ++q) sv += shv[q][c];
+        vo.part_v[9 * grp + c] = sv;
+      }
       __syncthreads();
     }
   }
+}
+
+// ---- Nose-Hoover chain (NVT) ------------------------------------------------
+// The chain of Martyna, Klein and Tuckerman (J. Chem. Phys. 97, 2635, 1992)
+// with masses Q_1 = N_f kT tau^2, Q_k = kT tau^2, propagated over dt/2 by the
+// Trotter factorisation of Martyna, Tuckerman, Tobias and Klein (Mol. Phys.
+// 87, 1117, 1996), one pass: thermostat velocities from the end of the chain
+// inwards, the particle velocities scaled by exp(-dt/2 v_1), the positions
+// xi_k advanced by dt/2 v_k, and the velocities outwards again.  Chain forces:
+// G_1 = (2K - N_f kT)/Q_1, G_k = (Q_{k-1} v_{k-1}^2 - kT)/Q_k.  Returns the
+// velocity scale; ``ke`` is the kinetic energy before the scaling.
+__device__ double chain_half_step(const NhcArgs& a, double* xi, double* v, double ke) {
+  const int M = a.M;
+  const double q = 0.25 * a.dt, e = 0.125 * a.dt;
+  auto force = [&](int k, double kin) {
+    return k == 0 ? (2.0 * kin - a.nf * a.kT) / a.Q[0]
+                  : (a.Q[k - 1] * v[k - 1] * v[k - 1] - a.kT) / a.Q[k];
+  };
+  auto update = [&](int k, double kin) {
+    if (k == M - 1) {
+      v[k] += q * force(k, kin);
+    } else {
+      const double f = exp(-e * v[k + 1]);
+      v[k] = (v[k] * f + q * force(k, kin)) * f;
+    }
+  };
+  for (int k = M - 1; k >= 0; --k) update(k, ke);
+  const double s = exp(-0.5 * a.dt * v[0]);
+  ke *= s * s;
+  for (int k = 0; k < M; ++k) xi[k] += 0.5 * a.dt * v[k];
+  for (int k = 0; k < M; ++k) update(k, ke);
+  return s;
+}
+
+// fixed-order sum over p < np of part[stride p + c] by one block
+__device__ inline double sum_strided(const double* __restrict__ part, int64_t np, int stride, int c,
+                                     double* sh) {
+  double s = 0.0;
+  for (int64_t p = threadIdx.x; p < np; p += kBlock) s += part[stride * p + c];
+  return block_sum(s, sh);
+}
+
+// One block.  Closing a step: its kinetic energy K (partials part_k), the
+// chain half step, K s^2 as the step's kinetic energy, the potential energy,
+// the thermostat energy and the virial of the step.  Opening a step: the
+// chain half step for the current K.  state[2M] = the product of the scales
+// of both, which the next kick (or launch_scale) applies.
+__global__ void __launch_bounds__(kBlock) nhc_kernel(NhcArgs a) {
+  __shared__ double sh[kBlock];
+  double ke = sum_strided(a.part_k, a.np, 1, 0, sh);
+  __syncthreads();
+  double pe = 0.0, vir[9];
+  if (a.close_prev && a.e_pot) {
+    pe = sum_strided(a.part_e, a.np, 1, 0, sh);
+    __syncthreads();
+  }
+  for (int c = 0; c < 9; ++c) {
+    vir[c] = 0.0;
+    if (a.close_prev && a.virial) {
+      vir[c] = sum_strided(a.part_v, a.np, 9, c, sh);
+      __syncthreads();
+    }
+  }
+  if (threadIdx.x != 0) return;
+  double* xi = a.state;
+  double* v = a.state + a.M;
+  double scale = 1.0;
+  if (a.close_prev) {
+    const double s = chain_half_step(a, xi, v, ke);
+    ke *= s * s;
+    scale *= s;
+    double eth = a.nf * a.kT * xi[0];
+    for (int k = 0; k < a.M; ++k) eth += 0.5 * a.Q[k] * v[k] * v[k] + (k > 0 ? a.kT * xi[k] : 0.0);
+    if (a.e_pot) *a.e_pot = pe;
+    if (a.e_kin) *a.e_kin = ke;
+    if (a.e_thermo) *a.e_thermo = eth;
+    if (a.virial)
+      for (int c = 0; c < 9; ++c) a.virial[c] = vir[c];
+  }
+  if (a.open_next) scale *= chain_half_step(a, xi, v, ke);
+  a.state[2 * a.M] = scale;
+}
+
+// block partials (256 atoms each, fixed tree) of the kinetic energy
+__global__ void __launch_bounds__(kBlock) kinetic_kernel(const double* __restrict__ vel,
+                                                         const int32_t* __restrict__ species,
+                                                         const double* __restrict__ mass,
+                                                         int n_types1, int64_t n,
+                                                         double* __restrict__ part_k) {
+  __shared__ double sh[kBlock];
+  const int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  double ek = 0.0;
+  if (i < n) {
+    int a0 = species[i];
+    a0 = static_cast<unsigned>(a0) < static_cast<unsigned>(n_types1) ? a0 : n_types1 - 1;
+    double v2 = 0.0;
+    for (int a = 0; a < 3; ++a) v2 += vel[3 * i + a] * vel[3 * i + a];
+    ek = 0.5 * mass[a0] * v2 * (1.66053906660e-17 / 1.602176634e-19);
+  }
+  const double tk = block_sum(ek, sh);
+  if (threadIdx.x == 0) part_k[blockIdx.x] = tk;
+}
+
+__global__ void __launch_bounds__(kBlock) scale_kernel(double* __restrict__ vel, int64_t n3,
+                                                       const double* __restrict__ scale) {
+  const int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
+  if (i < n3) vel[i] = vel[i] * *scale;
 }
 
 __global__ void __launch_bounds__(kBlock) final_step_kernel(StepSums prev) {
@@ -322,16 +475,46 @@ int blocks_for(int64_t n) {
 
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
-                  double* forces, const StepTail* tail, hipStream_t st) {
+                  double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st) {
   int64_t blocks = tail_partial_count(n);
   if (blocks > 8192) blocks = 8192;
-  if (tail) {
-    hipLaunchKernelGGL(forces_kernel<true>, dim3(blocks + 1), dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, sidx, skin_rev, cidx, forces, *tail);
-  } else {
-    hipLaunchKernelGGL(forces_kernel<false>, dim3(blocks), dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, sidx, skin_rev, cidx, forces, StepTail{});
+  const StepTail tl = tail ? *tail : StepTail{};
+  const VirialOut vo = vir ? *vir : VirialOut{};
+  if (vir && (!vir->edge || !vir->part_v)) return DPA4C_ERR_INVALID_ARG;
+  const dim3 grid(static_cast<unsigned>(blocks + (tail ? 1 : 0)));
+  if (tail && vir)
+    hipLaunchKernelGGL((forces_kernel<true, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
+                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+  else if (tail)
+    hipLaunchKernelGGL((forces_kernel<true, false>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
+                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+  else if (vir)
+    hipLaunchKernelGGL((forces_kernel<false, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
+                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+  else
+    hipLaunchKernelGGL((forces_kernel<false, false>), grid, dim3(kBlock), 0, st, n, row_ptr,
+                       ecount, grad, sidx, skin_rev, cidx, forces, tl, vo);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+// out[c] = sum over p < np of part[ncomp p + c], c < ncomp, in a fixed order
+// (one block)
+__global__ void __launch_bounds__(kRedBlock) sum_components_kernel(const double* __restrict__ part,
+                                                                   int64_t np, int ncomp,
+                                                                   double* __restrict__ out) {
+  __shared__ double sh[kRedBlock];
+  for (int c = 0; c < ncomp; ++c) {
+    double s = 0.0;
+    for (int64_t p = threadIdx.x; p < np; p += kRedBlock) s += part[ncomp * p + c];
+    const double tot = block_sum(s, sh);
+    if (threadIdx.x == 0) out[c] = tot;
+    __syncthreads();
   }
+}
+
+int launch_sum_components(const double* part, int64_t np, int ncomp, double* out, hipStream_t st) {
+  hipLaunchKernelGGL(sum_components_kernel, dim3(1), dim3(kRedBlock), 0, st, part, np, ncomp, out);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -343,10 +526,33 @@ int launch_energy(int64_t n, const double* e_atom, double* partials, double* out
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
                       const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
-                      int64_t step, hipStream_t st) {
+                      int64_t step, const double* scale, hipStream_t st) {
   hipLaunchKernelGGL(kick_drift_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, pos, vel, forces,
                      species, inv_mass, n_types1, n, 0.5 * dt, dt, drift, qbuild, skin_q, flags,
-                     prev, step);
+                     prev, step, scale);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_nhc(const NhcArgs& a, hipStream_t st) {
+  if (a.M < 1 || a.M > kMaxChain || !a.state || !a.part_k || a.np < 1) return DPA4C_ERR_INVALID_ARG;
+  hipLaunchKernelGGL(nhc_kernel, dim3(1), dim3(kBlock), 0, st, a);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int kinetic_partial_count(int64_t n) { return blocks_for(n); }
+
+int launch_kinetic(const double* vel, const int32_t* species, const double* mass, int n_types1,
+                   int64_t n, double* part_k, hipStream_t st) {
+  hipLaunchKernelGGL(kinetic_kernel, dim3(blocks_for(n)), dim3(kBlock), 0, st, vel, species, mass,
+                     n_types1, n, part_k);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_scale(double* vel, int64_t n, const double* scale, hipStream_t st) {
+  hipLaunchKernelGGL(scale_kernel, dim3(blocks_for(3 * n)), dim3(kBlock), 0, st, vel, 3 * n, scale);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

@@ -47,11 +47,21 @@ int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
                     const float* node_grad, float4* grad, hipStream_t st);
 struct StepTail;
+// the virial of Eq. (forces) formed in the force assembly: edge = the compact
+// edge records (r_ij), part_v = [tail_partial_count(n)][9] group partials,
+// atom = [N][9] per-atom terms or null
+struct VirialOut {
+  const float4* edge;
+  double* part_v;
+  double* atom;
+};
 // force assembly; with ``tail`` also the velocity-Verlet work of the step
-// that needs only F_k (see StepTail)
+// that needs only F_k (see StepTail), with ``vir`` the virial
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
-                  double* forces, const StepTail* tail, hipStream_t st);
+                  double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st);
+// out[c] = fixed-order sum over p < np of part[ncomp p + c]
+int launch_sum_components(const double* part, int64_t np, int ncomp, double* out, hipStream_t st);
 int launch_energy(int64_t n, const double* e_atom, double* partials, double* out,
                   hipStream_t st);
 
@@ -94,11 +104,40 @@ struct StepTail {
   int64_t next_step;
 };
 // half kick (and drift with the displacement check of step ``step`` when
-// qbuild is given); block 0 first adds the partials of the previous step
+// qbuild is given), after v *= *scale when scale is not null; block 0 first
+// adds the partials of the previous step
 int launch_kick_drift(double* pos, double* vel, const double* forces, const int32_t* species,
                       const double* inv_mass, int n_types1, int64_t n, double dt, int drift,
                       const int64_t* qbuild, int64_t skin_q, int64_t* flags, StepSums prev,
-                      int64_t step, hipStream_t st);
+                      int64_t step, const double* scale, hipStream_t st);
+
+// Nose-Hoover chain (NVT): one launch closes a step (its chain half step,
+// kinetic, potential and thermostat energies and virial, from the step's
+// partials) and/or opens the next (the chain half step at the current
+// kinetic energy); state = [xi_1..M, v_1..M, velocity scale to apply]
+constexpr int kMaxChain = 8;
+struct NhcArgs {
+  double* state;
+  int M;
+  double kT, nf, dt;        // kT (eV), N_f, time step (fs)
+  double Q[kMaxChain];      // chain masses (eV fs^2)
+  const double* part_k;     // kinetic-energy partials [np]
+  const double* part_e;     // potential-energy partials [np] (closing only)
+  const double* part_v;     // virial partials [np][9] (closing only)
+  int64_t np;
+  int close_prev, open_next;
+  double* e_pot;            // outputs of the closed step, each may be null
+  double* e_kin;
+  double* e_thermo;
+  double* virial;           // [9]
+};
+int launch_nhc(const NhcArgs& a, hipStream_t st);
+// kinetic-energy partials of the current velocities (kinetic_partial_count(n))
+int kinetic_partial_count(int64_t n);
+int launch_kinetic(const double* vel, const int32_t* species, const double* mass, int n_types1,
+                   int64_t n, double* part_k, hipStream_t st);
+// vel *= *scale
+int launch_scale(double* vel, int64_t n, const double* scale, hipStream_t st);
 int launch_final_step(StepSums prev, hipStream_t st);
 int tail_partial_count(int64_t n);
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st);

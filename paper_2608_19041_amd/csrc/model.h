@@ -68,7 +68,9 @@ struct Workspace {
   DevBuf epart;         // double partial sums
   DevBuf flags;         // int64 [8] device flags
   DevBuf eatom;         // double [N] (per-atom energies inside verlet_step)
-  DevBuf tailpart;      // double [2][blocks]: energy partials of a Verlet step
+  DevBuf tailpart;      // double [2][2][groups]: energy partials of a Verlet step
+  DevBuf virpart;       // double [2][groups][9]: virial partials
+  DevBuf nvt;           // double: chain state of an NVT call and its batch backup
   DevBuf backup;        // double [3][N][3]: positions, velocities, forces at a batch start
   DevBuf inv_mass;      // double [T+1]: 1 / (m * 103.6427)  (A/fs^2 per eV/A)
   DevBuf mass;          // double [T+1]
