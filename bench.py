@@ -7,8 +7,11 @@ half kick, drift and displacement check, a cell-list rebuild when due,
 the fused forward edge kernel (which first compacts its skin row), the per-atom
 kernel (readout, MLP forward and input gradient on the matrix cores,
 readout VJP), the fused backward edge kernel, force assembly and the
-second half kick with the energy sums.  Inputs are synthetic (seeded
-lattice, random-init weights) and resident in HBM before timing starts.
+second half kick with the energy sums.  On the NVT workload (diamond carbon
+at 300 K, the shape of the paper's whole-step benchmark) a step is one
+nvt_step step: the same path plus the Nose-Hoover-chain half steps and the
+virial assembled at every step.  Inputs are synthetic (seeded lattice,
+random-init weights) and resident in HBM before timing starts.
 
 Prints one JSON line.  ``stage_ms_per_step`` comes from a short pass with
 HIP events around every stage; the timed region then records events only
@@ -50,6 +53,9 @@ DESCRIPTIONS = {
                        "model, NVE 0.5 fs from 300 K, 1 A skin",
     "fcc1m_full": "1000188-atom FCC crystal (63^3 cells), full-width model, NVE 1 fs, "
                   "rebuild every 20 steps, 1 A skin",
+    "diamond1m_nvt_full": "1000000-atom diamond-carbon crystal (50^3 cells, a=3.567 A, jitter "
+                          "0.03 A), full-width model calibrated on carbon, NVT 300 K "
+                          "(Nose-Hoover chain of 3, 100 fs), 1 fs, 1 A skin, virial every step",
 }
 
 
@@ -193,11 +199,31 @@ def main():
                                                rp, nj, ns, npairs)
     n_edges = int(np.sum(model.debug_stages(system.n)[2].cpu().numpy()))
     del rp, nj, ns
-    e_pot = torch.empty(max(args.steps, args.warmup, 1), dtype=torch.float64, device=dev)
+    kmax = max(args.steps, args.warmup, 1)
+    e_pot = torch.empty(kmax, dtype=torch.float64, device=dev)
     e_kin = torch.empty_like(e_pot)
+    nvt = synth.NVT_WORKLOADS.get(args.workload)
+    if nvt:
+        t_damp, chain_len = nvt
+        chain = torch.zeros(2 * chain_len, dtype=torch.float64, device=dev)
+        e_th = torch.empty_like(e_pot)
+        vir = torch.empty(kmax, 3, 3, dtype=torch.float64, device=dev)
+
+    def run(n):
+        """n steps of the workload's ensemble: (e_pot, e_kin, e_thermostat or None, rebuilds)."""
+        if nvt:
+            ep, ek, eth, _, nr = model.nvt_step(pos, vel, species, system.mass_by_type, system.cell,
+                                                system.pbc, spec.r_c, skin, dt, n, rebuild_every,
+                                                forces, temp, t_damp, chain,
+                                                out=(e_pot, e_kin, e_th, vir))
+            return ep, ek, eth, nr
+        ep, ek, nr = model.verlet_step(pos, vel, species, system.mass_by_type, system.cell,
+                                       system.pbc, spec.r_c, skin, dt, n, rebuild_every, forces,
+                                       e_pot, e_kin)
+        return ep, ek, None, nr
+
     if args.warmup:
-        model.verlet_step(pos, vel, species, system.mass_by_type, system.cell, system.pbc, spec.r_c,
-                          skin, dt, args.warmup, rebuild_every, forces, e_pot, e_kin)
+        run(args.warmup)
     torch.cuda.synchronize()
 
     # stage split: a short pass with HIP events around every stage (the
@@ -206,8 +232,7 @@ def main():
     n_split = min(100, args.steps)
     model.set_timing(True)
     model.timings()
-    model.verlet_step(pos, vel, species, system.mass_by_type, system.cell, system.pbc, spec.r_c,
-                      skin, dt, n_split, rebuild_every, forces, e_pot, e_kin)
+    run(n_split)
     split = model.timings()
     split_ms = {k: v[0] / n_split for k, v in split.items() if v[1]}
     dominant = max(split_ms, key=split_ms.get)
@@ -217,9 +242,7 @@ def main():
     model.timings()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ep, ek, nreb = model.verlet_step(pos, vel, species, system.mass_by_type, system.cell,
-                                     system.pbc, spec.r_c, skin, dt, args.steps, rebuild_every,
-                                     forces, e_pot, e_kin)
+    ep, ek, eth, nreb = run(args.steps)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     stages = model.timings()
@@ -229,7 +252,7 @@ def main():
     wall = t1 - t0
     steps_per_s = args.steps / wall
     value = system.n * steps_per_s
-    et = (ep + ek).cpu().numpy()
+    et = (ep + ek + (eth if eth is not None else 0.0)).cpu().numpy()
     tt = np.arange(len(et)) * dt * 1e-3
     drift = float(np.polyfit(tt, et / system.n, 1)[0]) if len(et) > 2 else None
 
@@ -270,7 +293,9 @@ def main():
                    "atoms": system.n, "edges_within_rc": n_edges, "dt_fs": dt,
                    "rebuild_every": rebuild_every, "table_spacing_A": spec.delta},
         "ns_per_day": round(steps_per_s * dt * 86400 * 1e-6, 4),
-        "nve_drift_ev_per_atom_ps": drift,
+        "ensemble": "NVT" if nvt else "NVE",
+        # NVE: E_pot + E_kin; NVT: the conserved extended energy (plus the chain's)
+        ("nvt_extended_energy_drift_ev_per_atom_ps" if nvt else "nve_drift_ev_per_atom_ps"): drift,
         "neighbor_rebuilds": nreb,
         "stage_ms_per_step": {k: round(v, 5) for k, v in split_ms.items()},
         "stage_split_steps": n_split,

@@ -50,6 +50,8 @@ def _frames(model_name: str):
     are sampled at a realistic spread and not amplified by a tiny sigma."""
     if model_name == "small":
         return [synth.fcc_copper(3, RATTLE, seed=101)]
+    if model_name == "full_carbon":
+        return [synth.diamond_carbon(4, RATTLE, seed=104)]
     return [synth.fcc_copper(10, RATTLE, seed=102), synth.bcc_hea(25, RATTLE, seed=103),
             synth.make_workload("water24000_full")[0]]
 

@@ -238,8 +238,11 @@ class Model:
         return e_atom, forces, e_total, virial, w_atom
 
     def nvt_step(self, pos, vel, species, mass_by_species, cell, pbc, r_c, skin, dt_fs, nsteps,
-                 rebuild_every, forces, temperature, t_damp_fs, chain, virial=False, stream=None):
+                 rebuild_every, forces, temperature, t_damp_fs, chain, virial=False, out=None,
+                 stream=None):
         """NVT steps; ``chain`` is a float64 device tensor [2M] (in/out).
+        ``out``: optional preallocated (e_pot, e_kin, e_thermo, virial [k, 3, 3]
+        or None) with k >= nsteps.
         Returns (e_pot, e_kin, e_thermo, virial [nsteps, 3, 3] or None, n_rebuilds)."""
         import torch
         n = pos.shape[0]
@@ -252,10 +255,20 @@ class Model:
             raise ValueError("chain must hold 2M values")
         dev = pos.device
         k = max(nsteps, 1)
-        e_pot = torch.empty(k, dtype=torch.float64, device=dev)
-        e_kin = torch.empty(k, dtype=torch.float64, device=dev)
-        e_th = torch.empty(k, dtype=torch.float64, device=dev)
-        vir = torch.empty(k, 3, 3, dtype=torch.float64, device=dev) if virial else None
+        if out is not None:
+            e_pot, e_kin, e_th, vir = out
+            for x in (e_pot, e_kin, e_th):
+                _require(x, torch.float64, None, "energy output")
+                if x.numel() < nsteps:
+                    raise ValueError("output buffers shorter than nsteps")
+            if vir is not None and (vir.dtype != torch.float64 or vir.numel() < 9 * nsteps
+                                    or not vir.is_contiguous()):
+                raise ValueError("virial output must be contiguous float64 [k, 3, 3], k >= nsteps")
+        else:
+            e_pot = torch.empty(k, dtype=torch.float64, device=dev)
+            e_kin = torch.empty(k, dtype=torch.float64, device=dev)
+            e_th = torch.empty(k, dtype=torch.float64, device=dev)
+            vir = torch.empty(k, 3, 3, dtype=torch.float64, device=dev) if virial else None
         masses = _host_f64(mass_by_species, self.info["n_types"] + 1)
         cellh = _host_f64(cell, 9)
         pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))

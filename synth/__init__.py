@@ -112,6 +112,19 @@ def fcc_copper(reps: int, jitter: float, seed: int = 0, a: float = 3.615,
                    "seed": seed})
 
 
+def diamond_carbon(reps: int, jitter: float, seed: int = 0, a: float = 3.567) -> System:
+    """Diamond-carbon supercell (8-atom conventional cell, lattice constant
+    3.567 A) with Gaussian coordinate perturbations: the structure of the
+    paper's whole-step MD benchmark."""
+    pos, cell = lattice("diamond", a, (reps, reps, reps))
+    rng = np.random.Generator(np.random.PCG64(seed))
+    pos = pos + rng.normal(0.0, jitter, size=pos.shape)
+    species = np.full(pos.shape[0], 5, dtype=np.int32)        # C, Z = 6
+    return System(f"diamond_c_{reps}", pos, species, cell, np.ones(3, np.int32),
+                  _mass_table(), {"lattice": "diamond", "a": a, "reps": reps,
+                                  "jitter": jitter, "seed": seed})
+
+
 def bcc_hea(reps: int = 25, jitter: float = 0.06, seed: int = 0,
             species_seed: int = 1, a: float = 2.87) -> System:
     """BCC high-entropy alloy: every site takes one of 5 types uniformly."""
@@ -259,6 +272,16 @@ WORKLOADS = {
     "bcc_hea31250_full": (lambda: bcc_hea(25, 0.06, seed=0), "full", 1000.0, 1.0, 500, 10),
     "water24000_full": (lambda: water_box(8000, 1.0, seed=2), "full", 300.0, 0.5, 500, 0),
     "fcc1m_full": (lambda: fcc_copper(63, 0.08, seed=0), "full", 300.0, 1.0, 200, 20),
+    # the paper's whole-step benchmark shape: diamond carbon, sigma 0.03 A,
+    # NVT at 300 K, 1 fs, 1 A skin checked every step (50^3 cells, 1,000,000 atoms)
+    "diamond1m_nvt_full": (lambda: diamond_carbon(50, 0.03, seed=0), "full_carbon", 300.0, 1.0,
+                           200, 0),
+}
+
+# thermostat of the NVT workloads: (damping time fs, chain length); the
+# benchmark listing's 0.1 ps damping and a chain of three
+NVT_WORKLOADS = {
+    "diamond1m_nvt_full": (100.0, 3),
 }
 
 
@@ -315,6 +338,8 @@ MODELS = {
     "neo": ModelSpec(C0=64, L=2, R=0, n_rbf=16, F=256, n_layers=3),
     "air": ModelSpec(C0=64, L=3, R=4, n_rbf=16, F=256, n_layers=3),
     "plus": ModelSpec(C0=128, L=3, R=4, n_rbf=16, F=384, n_layers=3),
+    # the full model with its calibration taken on diamond carbon
+    "full_carbon": ModelSpec(C0=128, L=3, R=4, n_rbf=16, F=384, n_layers=3),
 }
 
 

@@ -214,3 +214,24 @@ def test_nvt_rejects_bad_parameters(dev, dp):
             model.nvt_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0, 1.0, 1.0, 5, 0, F,
                            **kw)
         assert ei.value.code == -1
+
+
+def test_diamond_nvt_matches_oracle(dev, dp):
+    """The benchmark's diamond carbon (3^3 conventional cells, 216 atoms, 158
+    neighbours each) with the carbon-calibrated full model: 10 NVT steps at
+    300 K with the 0.1 ps damping time against the oracle."""
+    model, oracle, _ = gpu_model(dp, "full_carbon")
+    s = synth.diamond_carbon(3, 0.03, seed=0)
+    v0, pos, species, vel, F = start_state(dp, model, s, dev, 300.0)
+    chain = torch.zeros(6, dtype=torch.float64, device=dev)
+    ep, ek, eth, vir, _ = model.nvt_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc, 6.0,
+                                         1.0, 1.0, 10, 0, F, 300.0, 100.0, chain, virial=True)
+    torch.cuda.synchronize()
+    rep, rek, reth, rpos, rvel, _ = md.nvt(oracle, s.pos, v0, s.species, s.cell, s.pbc,
+                                           s.mass_by_type[s.species], 1.0, 10, 300.0, 100.0)
+    assert np.abs(pos.cpu().numpy() - rpos).max() < 1e-6
+    assert np.abs(ep.cpu().numpy() - rep[1:]).max() < E_TOL * s.n
+    assert np.abs(ek.cpu().numpy() - rek[1:]).max() < E_TOL * s.n
+    assert np.abs(eth.cpu().numpy() - reth[1:]).max() < E_TOL * s.n
+    _, _, ref_vir, _ = oracle.energy_forces(rpos, s.species, s.cell, s.pbc, virial=True)
+    assert np.abs(vir[-1].cpu().numpy() - ref_vir).max() < E_TOL * s.n
