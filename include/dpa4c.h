@@ -3,7 +3,7 @@
  * machine-learning potential (arXiv 2608.19041).
  *
  * The library evaluates, for N atoms with positions r_i, species a_i and a
- * periodic orthorhombic cell, the neighbour graph of Methods Eq.
+ * periodic cell (orthorhombic or triclinic), the neighbour graph of Methods Eq.
  * (neighbor-set), the single message-passing layer of Eqs. (edge-geometry)
  * .. (moments), the invariant readout and MLP of Eqs. (alignment) ..
  * (fitting), and the forces of Eq. (forces), F_k = -dE/dr_k.  The compressed
@@ -42,7 +42,7 @@ extern "C" {
 
 #define DPA4C_OK 0
 #define DPA4C_ERR_INVALID_ARG (-1) /* bad pointer, size or value */
-#define DPA4C_ERR_UNSUPPORTED (-2) /* non-orthorhombic or non-periodic cell, profile not built */
+#define DPA4C_ERR_UNSUPPORTED (-2) /* non-periodic cell, profile not built, row too long */
 #define DPA4C_ERR_CAPACITY (-3)    /* neighbour capacity too small; *n_pairs holds the need */
 #define DPA4C_ERR_HIP (-4)         /* a HIP runtime call failed */
 #define DPA4C_ERR_NONFINITE (-5)   /* a non-finite position was found */
@@ -98,10 +98,11 @@ int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
 
 /*
  * Neighbour list of Eq. (neighbor-set) at radius r_list (typically r_c plus
- * a skin), for an orthorhombic fully periodic cell.
+ * a skin), for a fully periodic cell, orthorhombic or triclinic.
  *
  * Membership uses the exact fixed-point predicate
- *     |Q(r_j) + n.Q(h) - Q(r_i)|^2 < Q(r_list)^2,  Q(x) = rint(x * 2^20)
+ *     |Q(r_j) + sum_b n_b Q(h_b) - Q(r_i)|^2 < Q(r_list)^2,  Q(x) = rint(x * 2^20)
+ * (Q of every component of every lattice vector h_b)
  * in 64-bit integers, so the list is a deterministic function of the float64
  * positions.  Periodic images are distinct neighbours, only (j = i, n = 0)
  * is excluded, both orientations are stored and there is no capacity per
@@ -109,7 +110,9 @@ int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
  * Positions need not lie inside the cell.
  *
  * pos       device float64 [N][3]
- * cell      host float64 [9], rows are lattice vectors; must be diagonal
+ * cell      host float64 [9], rows are the lattice vectors h_0, h_1, h_2
+ *           (any non-singular matrix, entries below 1e6 A; a diagonal cell
+ *           must have a positive diagonal)
  * pbc       host int [3]; must be {1, 1, 1}
  * row_ptr   device int64 [N+1] out: CSR row offsets
  * nbr_j     device int32 [cap] out: neighbour index j

@@ -32,12 +32,6 @@ int check_cell(const double* cell, const int* pbc) {
     set_error("the GPU path needs a fully periodic cell");
     return DPA4C_ERR_UNSUPPORTED;
   }
-  for (int a = 0; a < 3; ++a)
-    for (int b = 0; b < 3; ++b)
-      if (a != b && cell[3 * a + b] != 0.0) {
-        set_error("the GPU path needs an orthorhombic cell (diagonal lattice matrix)");
-        return DPA4C_ERR_UNSUPPORTED;
-      }
   return 0;
 }
 
@@ -132,6 +126,27 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   return 0;
 }
 
+// the compaction inputs and outputs of a model evaluation
+CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nbr_j,
+                         const int32_t* nbr_shift, int64_t rcq, int64_t cap, Workspace& w) {
+  CompactArgs ca{};
+  ca.pos = pos;
+  ca.nbr_j = nbr_j;
+  ca.nbr_shift = nbr_shift;
+  for (int k = 0; k < 9; ++k) {
+    ca.qh[k] = g.qh[k];
+    ca.h[k] = g.h[k];
+  }
+  ca.rcq = rcq;
+  ca.tric = g.tric;
+  ca.cap = cap;
+  ca.ecount = w.ecount.as<int32_t>();
+  ca.edge = w.edge.as<float4>();
+  ca.cidx = w.cidx.as<int32_t>();
+  ca.sidx = w.sidx.as<int32_t>();
+  return ca;
+}
+
 // NVT parameters of a dynamics call (nvt_step)
 struct NvtConfig {
   double temperature;   // K
@@ -145,7 +160,7 @@ struct NvtConfig {
 // Everything after the skin list: forward (with the compaction of the skin
 // rows), per-atom kernel, backward, forces and the energy sum.
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
-              const CellGrid& g, const double* box, const int64_t* row_ptr, const int32_t* nbr_j,
+              const CellGrid& g, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
               double* forces, double* e_total, const StepTail* tail, const VirialOut* vir,
               double* virial, hipStream_t st) {
@@ -156,9 +171,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
   int rc;
-  CompactArgs ca{pos, nbr_j, nbr_shift, g.Lq[0], g.Lq[1], g.Lq[2], rcq, box[0], box[1], box[2],
-                 cap, w.ecount.as<int32_t>(), w.edge.as<float4>(), w.cidx.as<int32_t>(),
-                 w.sidx.as<int32_t>()};
+  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, rcq, cap, w);
   {
     StageScope t(m, kStForward, st);
     rc = launch_forward(m, n, species, row_ptr, ca, w.node.as<float>(), st);
@@ -194,10 +207,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   m->last_n = n;
   w.last_species = species;
   w.last_pos = pos;
-  for (int a = 0; a < 3; ++a) w.last_Lq[a] = g.Lq[a];
-  w.last_box[0] = box[0];
-  w.last_box[1] = box[1];
-  w.last_box[2] = box[2];
+  w.last_grid = g;
   w.skin_row_used = row_ptr;
   w.skin_j_used = nbr_j;
   w.skin_shift_used = nbr_shift;
@@ -356,7 +366,6 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
   hipStream_t st = static_cast<hipStream_t>(stream);
   rc = ensure_workspace(mm, N, n_pairs);
   if (rc) return rc;
-  double box[3] = {cell[0], cell[4], cell[8]};
   if (N == 0) {
     DPA4C_HIP_TRY(hipMemsetAsync(e_total, 0, sizeof(double), st));
     if (virial) DPA4C_HIP_TRY(hipMemsetAsync(virial, 0, 9 * sizeof(double), st));
@@ -374,7 +383,7 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
     if (mm->ws.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N)))) return DPA4C_ERR_HIP;
     vo = VirialOut{mm->ws.edge.as<float4>(), mm->ws.virpart.as<double>(), atom_virial};
   }
-  return run_model(m, pos, species, N, g, box, row_ptr, nbr_j, nbr_shift, n_pairs,
+  return run_model(m, pos, species, N, g, row_ptr, nbr_j, nbr_shift, n_pairs,
                    mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr,
                    virial ? &vo : nullptr, virial, st);
 }
@@ -449,7 +458,6 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   if (rc) return rc;
   rc = make_grid(cell, rcq, &g_cut);
   if (rc) return rc;
-  const double box[3] = {cell[0], cell[4], cell[8]};
 
   // masses on the device
   const int np_tail = tail_partial_count(N);
@@ -601,7 +609,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                         kick_next ? 1 : 0, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
                         step + 1};
     const VirialOut vo{w.edge.as<float4>(), nvt ? vir_part(step) : nullptr, nullptr};
-    return run_model(m, pos, species, N, g_cut, box, w.skin_row.as<int64_t>(),
+    return run_model(m, pos, species, N, g_cut, w.skin_row.as<int64_t>(),
                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
                      w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
                      nvt ? &vo : nullptr, nullptr, st);
@@ -765,10 +773,8 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (N == 0) return 0;
   // recompute node state and descriptor from the stored compacted edges
-  CompactArgs ca{w.last_pos, w.skin_j_used, w.skin_shift_used, w.last_Lq[0],
-                 w.last_Lq[1], w.last_Lq[2], qfix_host(m->r_c), w.last_box[0],
-                 w.last_box[1], w.last_box[2], w.cap_used, w.ecount.as<int32_t>(),
-                 w.edge.as<float4>(), w.cidx.as<int32_t>(), w.sidx.as<int32_t>()};
+  const CompactArgs ca = compact_args(w.last_grid, w.last_pos, w.skin_j_used, w.skin_shift_used,
+                                      qfix_host(m->r_c), w.cap_used, mm->ws);
   int rc = launch_forward(m, N, w.last_species, w.skin_row_used, ca, w.node.as<float>(), st);
   if (rc) return rc;
   if (w.desc.ensure(size_t(4) * N * m->D_out) || w.eatom.ensure(size_t(8) * N)) return DPA4C_ERR_HIP;

@@ -13,9 +13,10 @@ struct CompactArgs {
   const double* pos;          // [N][3]
   const int32_t* nbr_j;       // skin list
   const int32_t* nbr_shift;
-  int64_t Lq0, Lq1, Lq2;      // box lengths, fixed point
+  int64_t qh[9];              // lattice vectors, fixed point, row b = Q(h_b)
   int64_t rcq;                // cutoff, fixed point
-  double L0, L1, L2;          // box lengths, Angstrom
+  double h[9];                // lattice vectors (A), row b = h_b
+  int tric;                   // 0: diagonal cell (only h_00, h_11, h_22 are used)
   int64_t cap;                // skin-list capacity
   int32_t* ecount;            // [N] out: edges kept per row
   float4* edge;               // [cap] out: (r_ij, bits of j) at the head of each skin row
@@ -35,7 +36,7 @@ __device__ inline bool within_q(int64_t dx, int64_t dy, int64_t dz, int64_t rq) 
 }
 
 // Keeps the skin edges of row i inside r_c, in canonical order, and writes
-// their records r_ij = (r_j + n.h) - r_i (float64 difference stored as
+// their records r_ij = (r_j + sum_b n_b h_b) - r_i (float64 difference stored as
 // float32) to the first slots of the row.  All TEAM threads of the
 // workgroup take part; ``wtot`` is LDS scratch of TEAM/64 ints.  Returns
 // the number kept (the same in every thread); the records are visible to
@@ -61,9 +62,17 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
       ny = unpack_y(sh);
       nz = unpack_z(sh);
       if (j >= 0 && j < n) {
-        const int64_t dx = qfix_dev(a.pos[3 * j]) + nx * a.Lq0 - qi0;
-        const int64_t dy = qfix_dev(a.pos[3 * j + 1]) + ny * a.Lq1 - qi1;
-        const int64_t dz = qfix_dev(a.pos[3 * j + 2]) + nz * a.Lq2 - qi2;
+        int64_t dx = qfix_dev(a.pos[3 * j]) - qi0, dy = qfix_dev(a.pos[3 * j + 1]) - qi1,
+                dz = qfix_dev(a.pos[3 * j + 2]) - qi2;
+        if (!a.tric) {
+          dx += nx * a.qh[0];
+          dy += ny * a.qh[4];
+          dz += nz * a.qh[8];
+        } else {   // sum_b n_b Q(h_b)
+          dx += nx * a.qh[0] + ny * a.qh[3] + nz * a.qh[6];
+          dy += nx * a.qh[1] + ny * a.qh[4] + nz * a.qh[7];
+          dz += nx * a.qh[2] + ny * a.qh[5] + nz * a.qh[8];
+        }
         pred = within_q(dx, dy, dz, a.rcq);
       }
     }
@@ -81,9 +90,16 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
     if (s < e) {
       if (pred) {
         const int64_t slot = b + kept + off + pre;
-        const double rx = (a.pos[3 * j] + nx * a.L0) - xi;
-        const double ry = (a.pos[3 * j + 1] + ny * a.L1) - yi;
-        const double rz = (a.pos[3 * j + 2] + nz * a.L2) - zi;
+        double rx, ry, rz;
+        if (!a.tric) {
+          rx = (a.pos[3 * j] + nx * a.h[0]) - xi;
+          ry = (a.pos[3 * j + 1] + ny * a.h[4]) - yi;
+          rz = (a.pos[3 * j + 2] + nz * a.h[8]) - zi;
+        } else {   // (r_j + sum_b n_b h_b) - r_i
+          rx = (a.pos[3 * j] + (nx * a.h[0] + ny * a.h[3] + nz * a.h[6])) - xi;
+          ry = (a.pos[3 * j + 1] + (nx * a.h[1] + ny * a.h[4] + nz * a.h[7])) - yi;
+          rz = (a.pos[3 * j + 2] + (nx * a.h[2] + ny * a.h[5] + nz * a.h[8])) - zi;
+        }
         a.edge[slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
                                    static_cast<float>(rz), __int_as_float(j));
         a.sidx[slot] = static_cast<int32_t>(s);

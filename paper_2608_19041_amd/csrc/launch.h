@@ -12,13 +12,7 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
 int launch_pair_cache(dpa4c_model* m, const float* wp_in, const float* wp_out);
 
 // neighbour lists (orthorhombic, periodic); all on ``st``
-struct CellGrid {
-  int64_t Lq[3];      // box lengths in fixed point
-  int nc[3];          // cells per axis
-  int reach[3];       // stencil half width per axis
-  int64_t rq;         // fixed-point neighbour radius
-  int64_t ncell;
-};
+// (CellGrid: model.h)
 int make_grid(const double cell[9], int64_t rq, CellGrid* g);
 // bin, count and scan (row_ptr); with ``fill`` also the sorted rows
 int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const CellGrid& g,

@@ -24,6 +24,18 @@ enum Stage {
 const char* stage_name(int s);
 
 // grow-only device buffer
+// cell-list grid of a periodic cell (neighbors.hip, make_grid)
+struct CellGrid {
+  int64_t qh[9];      // lattice vectors in fixed point, row b = Q(h_b)
+  double h[9];        // lattice vectors (A), row b = h_b
+  double inv[9];      // inverse of the lattice matrix: fractional f = x inv
+  int tric;           // 0: diagonal (orthorhombic) cell, binned in integers
+  int nc[3];          // cells per axis
+  int reach[3];       // stencil half width per axis
+  int64_t rq;         // fixed-point neighbour radius
+  int64_t ncell;
+};
+
 struct DevBuf {
   void* p = nullptr;
   size_t bytes = 0;
@@ -88,8 +100,7 @@ struct Workspace {
   const int32_t* skin_j_used = nullptr;
   const int32_t* skin_shift_used = nullptr;
   int64_t cap_used = 0;
-  int64_t last_Lq[3] = {};
-  double last_box[3] = {};
+  CellGrid last_grid{};
   NeighborScratch nb;
 };
 

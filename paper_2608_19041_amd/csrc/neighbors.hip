@@ -2,15 +2,23 @@
 // (neighbor-set), integer arithmetic only.
 //
 // Positions are mapped to fixed point Q(x) = rint(x * 2^20) (int64) and the
-// membership test |Q(r_j) + n.Q(h) - Q(r_i)|^2 < Q(r)^2 is exact, so every
-// list built here is a deterministic function of the float64 positions.
+// membership test |Q(r_j) + sum_b n_b Q(h_b) - Q(r_i)|^2 < Q(r)^2 is exact, so
+// every list built here is a deterministic function of the float64 positions.
 // Rows come out in canonical order (ascending j, then n_x, n_y, n_z).
+//
+// Binning: positions are wrapped into the cell by integer multiples of the
+// quantised lattice vectors, which keeps the test exact.  A diagonal cell is
+// binned in integers; a triclinic cell by fractional coordinates in float64,
+// which only decides the candidate set: its stencil reach carries a 1e-6 A
+// margin, far above the rounding of the fractional coordinates, so every
+// pair within the radius is visited and the integer test decides.
 //
 // Work mapping: one 64-lane wavefront per centre atom, waves striding over
 // centres; candidate atoms of a stencil cell are spread over the lanes and
 // compacted with a wave ballot, which keeps their relative order.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "../../include/dpa4c.h"
@@ -49,15 +57,27 @@ __device__ inline void wave_lds_sync() {
 }
 
 struct GridDev {
-  int64_t Lq0, Lq1, Lq2;
+  int64_t qh[9];          // Q(h_b) in row b
+  double inv[9];          // inverse lattice matrix (triclinic binning)
   int nc0, nc1, nc2;
   int re0, re1, re2;
   int64_t rq;
 };
 
 GridDev to_dev(const CellGrid& g) {
-  return {g.Lq[0], g.Lq[1], g.Lq[2], g.nc[0], g.nc[1], g.nc[2], g.reach[0], g.reach[1],
-          g.reach[2], g.rq};
+  GridDev d;
+  for (int k = 0; k < 9; ++k) {
+    d.qh[k] = g.qh[k];
+    d.inv[k] = g.inv[k];
+  }
+  d.nc0 = g.nc[0];
+  d.nc1 = g.nc[1];
+  d.nc2 = g.nc[2];
+  d.re0 = g.reach[0];
+  d.re1 = g.reach[1];
+  d.re2 = g.reach[2];
+  d.rq = g.rq;
+  return d;
 }
 
 // within (strictly) the fixed-point radius; no overflow: components are
@@ -73,6 +93,9 @@ __global__ void __launch_bounds__(kBlock) zero_i32_kernel(int32_t* __restrict__ 
   if (i < n) p[i] = 0;
 }
 
+// qpos = the position wrapped into the cell, Q(x) - sum_b m_b Q(h_b);
+// wrap = m; cell_of = its bin
+template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ pos, int64_t n,
                                                      GridDev g, int64_t* __restrict__ qpos,
                                                      int32_t* __restrict__ wrap,
@@ -81,22 +104,42 @@ __global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ 
                                                      int64_t* __restrict__ flags) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= n) return;
-  const int64_t Lq[3] = {g.Lq0, g.Lq1, g.Lq2};
   const int nc[3] = {g.nc0, g.nc1, g.nc2};
   int c[3];
   bool bad = false;
+  double x[3];
   for (int a = 0; a < 3; ++a) {
-    double x = pos[3 * i + a];
-    if (!isfinite(x) || fabs(x) > 1.0e12) {
+    x[a] = pos[3 * i + a];
+    if (!isfinite(x[a]) || fabs(x[a]) > 1.0e12) {
       bad = true;
-      x = 0.0;
+      x[a] = 0.0;
     }
-    int64_t q = qfix(x);
-    int64_t m = floor_div(q, Lq[a]);
-    int64_t qw = q - m * Lq[a];
-    qpos[3 * i + a] = qw;
-    wrap[3 * i + a] = static_cast<int32_t>(m);
-    c[a] = static_cast<int>((qw * nc[a]) / Lq[a]);
+  }
+  if (!TRIC) {
+    for (int a = 0; a < 3; ++a) {
+      const int64_t L = g.qh[4 * a];
+      int64_t q = qfix(x[a]);
+      int64_t m = floor_div(q, L);
+      int64_t qw = q - m * L;
+      qpos[3 * i + a] = qw;
+      wrap[3 * i + a] = static_cast<int32_t>(m);
+      c[a] = static_cast<int>((qw * nc[a]) / L);
+    }
+  } else {
+    int64_t m[3];
+    double fw[3];
+    for (int b = 0; b < 3; ++b) {
+      const double f = x[0] * g.inv[b] + x[1] * g.inv[3 + b] + x[2] * g.inv[6 + b];
+      const double fl = floor(f);
+      m[b] = static_cast<int64_t>(fl);
+      fw[b] = f - fl;
+    }
+    for (int a = 0; a < 3; ++a) {
+      qpos[3 * i + a] = qfix(x[a]) - m[0] * g.qh[a] - m[1] * g.qh[3 + a] - m[2] * g.qh[6 + a];
+      wrap[3 * i + a] = static_cast<int32_t>(m[a]);
+      int cb = static_cast<int>(fw[a] * nc[a]);
+      c[a] = cb < 0 ? 0 : (cb >= nc[a] ? nc[a] - 1 : cb);
+    }
   }
   if (bad) atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagNonFinite);
   int cid = (c[0] * nc[1] + c[1]) * nc[2] + c[2];
@@ -147,16 +190,18 @@ __global__ void __launch_bounds__(kBlock) place_kernel(int64_t n, const int32_t*
 // Visits every (cell, image) of the stencil of centre i and calls
 // f(j, nx, ny, nz, pred) on chunks of candidates (one per lane, pred false on
 // idle lanes).  Wave-uniform control flow.
-template <class Fn>
+template <bool TRIC, class Fn>
 __device__ inline void for_candidates(const GridDev& g, int64_t i, const int64_t* __restrict__ qpos,
                                       const int32_t* __restrict__ wrap,
+                                      const int32_t* __restrict__ cell_of,
                                       const int32_t* __restrict__ start,
                                       const int32_t* __restrict__ atoms, Fn&& f) {
   const int64_t qi0 = qpos[3 * i], qi1 = qpos[3 * i + 1], qi2 = qpos[3 * i + 2];
   const int mi0 = wrap[3 * i], mi1 = wrap[3 * i + 1], mi2 = wrap[3 * i + 2];
-  const int ci0 = static_cast<int>((qi0 * g.nc0) / g.Lq0);
-  const int ci1 = static_cast<int>((qi1 * g.nc1) / g.Lq1);
-  const int ci2 = static_cast<int>((qi2 * g.nc2) / g.Lq2);
+  const int cid_i = cell_of[i];
+  const int ci0 = cid_i / (g.nc1 * g.nc2);
+  const int ci1 = (cid_i / g.nc2) % g.nc1;
+  const int ci2 = cid_i % g.nc2;
   const int lane = lane_id();
   for (int d0 = -g.re0; d0 <= g.re0; ++d0) {
     int t0 = ci0 + d0;
@@ -179,9 +224,16 @@ __device__ inline void for_candidates(const GridDev& g, int64_t i, const int64_t
           int nx = 0, ny = 0, nz = 0;
           if (idx < ce) {
             j = atoms[idx];
-            int64_t dx = qpos[3 * j] + s0 * g.Lq0 - qi0;
-            int64_t dy = qpos[3 * j + 1] + s1 * g.Lq1 - qi1;
-            int64_t dz = qpos[3 * j + 2] + s2 * g.Lq2 - qi2;
+            int64_t dx, dy, dz;
+            if (!TRIC) {
+              dx = qpos[3 * j] + s0 * g.qh[0] - qi0;
+              dy = qpos[3 * j + 1] + s1 * g.qh[4] - qi1;
+              dz = qpos[3 * j + 2] + s2 * g.qh[8] - qi2;
+            } else {   // image displacement sum_b s_b Q(h_b)
+              dx = qpos[3 * j] + s0 * g.qh[0] + s1 * g.qh[3] + s2 * g.qh[6] - qi0;
+              dy = qpos[3 * j + 1] + s0 * g.qh[1] + s1 * g.qh[4] + s2 * g.qh[7] - qi1;
+              dz = qpos[3 * j + 2] + s0 * g.qh[2] + s1 * g.qh[5] + s2 * g.qh[8] - qi2;
+            }
             nx = s0 - wrap[3 * j] + mi0;
             ny = s1 - wrap[3 * j + 1] + mi1;
             nz = s2 - wrap[3 * j + 2] + mi2;
@@ -194,16 +246,18 @@ __device__ inline void for_candidates(const GridDev& g, int64_t i, const int64_t
   }
 }
 
+template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) count_kernel(int64_t n, GridDev g,
                                                        const int64_t* __restrict__ qpos,
                                                        const int32_t* __restrict__ wrap,
+                                                       const int32_t* __restrict__ cell_of,
                                                        const int32_t* __restrict__ start,
                                                        const int32_t* __restrict__ atoms,
                                                        int64_t* __restrict__ counts) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
     int64_t total = 0;
-    for_candidates(g, i, qpos, wrap, start, atoms, [&](int32_t, int, int, int, bool pred) {
+    for_candidates<TRIC>(g, i, qpos, wrap, cell_of, start, atoms, [&](int32_t, int, int, int, bool pred) {
       total += __popcll(__ballot(pred));
     });
     if (lane_id() == 0) counts[i] = total;
@@ -294,9 +348,11 @@ int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
 }
 
 // ---------------------------------------------------------------------------
+template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       const int64_t* __restrict__ qpos,
                                                       const int32_t* __restrict__ wrap,
+                                                      const int32_t* __restrict__ cell_of,
                                                       const int32_t* __restrict__ start,
                                                       const int32_t* __restrict__ atoms,
                                                       const int64_t* __restrict__ row_ptr,
@@ -324,7 +380,7 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
     }
     int fill = 0;
     bool shift_bad = false;
-    for_candidates(g, i, qpos, wrap, start, atoms, [&](int32_t j, int nx, int ny, int nz, bool pred) {
+    for_candidates<TRIC>(g, i, qpos, wrap, cell_of, start, atoms, [&](int32_t j, int nx, int ny, int nz, bool pred) {
       uint64_t m;
       int pre = ballot_prefix(pred, &m);
       if (pred) {
@@ -406,30 +462,76 @@ int waves_grid(int64_t n) {
 }  // namespace
 
 int make_grid(const double cell[9], int64_t rq, CellGrid* g) {
-  for (int a = 0; a < 3; ++a)
-    for (int b = 0; b < 3; ++b)
-      if (a != b && cell[3 * a + b] != 0.0) {
-        set_error("only orthorhombic cells (diagonal lattice matrix) are supported on the GPU");
-        return DPA4C_ERR_UNSUPPORTED;
-      }
   if (rq <= 0 || rq > int64_t(1000) * int64_t(kQScale)) {
     set_error("bad neighbour radius");
     return DPA4C_ERR_INVALID_ARG;
   }
-  g->rq = rq;
-  g->ncell = 1;
-  for (int a = 0; a < 3; ++a) {
-    double L = cell[4 * a];
-    if (!(L > 0) || L > 1.0e6) {
-      set_error("cell lengths must be positive and below 1e6 A");
+  for (int k = 0; k < 9; ++k)
+    if (!std::isfinite(cell[k]) || std::fabs(cell[k]) > 1.0e6) {
+      set_error("cell entries must be finite and below 1e6 A");
       return DPA4C_ERR_INVALID_ARG;
     }
-    g->Lq[a] = static_cast<int64_t>(std::rint(L * kQScale));
-    int64_t nc = g->Lq[a] / g->rq;
-    if (nc < 1) nc = 1;
-    if (nc > 1024) nc = 1024;
+  g->rq = rq;
+  g->ncell = 1;
+  g->tric = 0;
+  for (int a = 0; a < 3; ++a)
+    for (int b = 0; b < 3; ++b)
+      if (a != b && cell[3 * a + b] != 0.0) g->tric = 1;
+  for (int k = 0; k < 9; ++k) {
+    g->h[k] = cell[k];
+    g->qh[k] = static_cast<int64_t>(std::rint(cell[k] * kQScale));
+  }
+  // inverse lattice matrix (rows of ``cell`` are the lattice vectors)
+  const double* h = cell;
+  const double det = h[0] * (h[4] * h[8] - h[5] * h[7]) - h[1] * (h[3] * h[8] - h[5] * h[6]) +
+                     h[2] * (h[3] * h[7] - h[4] * h[6]);
+  if (!g->tric) {
+    for (int a = 0; a < 3; ++a)
+      if (!(cell[4 * a] > 0)) {
+        set_error("the diagonal of an orthorhombic cell must be positive");
+        return DPA4C_ERR_INVALID_ARG;
+      }
+  }
+  double vol = std::fabs(det);
+  double hmax = 0.0;
+  for (int k = 0; k < 9; ++k) hmax = std::max(hmax, std::fabs(cell[k]));
+  if (!(vol > 1e-9 * hmax * hmax * hmax) || !(vol > 0)) {
+    set_error("the cell is singular");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  const double cof[9] = {h[4] * h[8] - h[5] * h[7], h[2] * h[7] - h[1] * h[8],
+                         h[1] * h[5] - h[2] * h[4], h[5] * h[6] - h[3] * h[8],
+                         h[0] * h[8] - h[2] * h[6], h[2] * h[3] - h[0] * h[5],
+                         h[3] * h[7] - h[4] * h[6], h[1] * h[6] - h[0] * h[7],
+                         h[0] * h[4] - h[1] * h[3]};
+  for (int k = 0; k < 9; ++k) g->inv[k] = cof[k] / det;
+  const double r = double(rq) / kQScale;
+  for (int a = 0; a < 3; ++a) {
+    int64_t nc;
+    if (!g->tric) {
+      const int64_t L = g->qh[4 * a];
+      nc = L / g->rq;
+      if (nc < 1) nc = 1;
+      if (nc > 1024) nc = 1024;
+      g->reach[a] = static_cast<int>((g->rq * nc + L - 1) / L);
+    } else {
+      // distance between the lattice planes of axis a: V / |h_b x h_c|
+      const double* u = h + 3 * ((a + 1) % 3);
+      const double* v = h + 3 * ((a + 2) % 3);
+      const double cx = u[1] * v[2] - u[2] * v[1], cy = u[2] * v[0] - u[0] * v[2],
+                   cz = u[0] * v[1] - u[1] * v[0];
+      const double d = vol / std::sqrt(cx * cx + cy * cy + cz * cz);
+      nc = static_cast<int64_t>(std::floor(d / r));
+      if (nc < 1) nc = 1;
+      if (nc > 1024) nc = 1024;
+      const double re = std::ceil((r + 1e-6) * double(nc) / d);
+      if (re > 1024.0) {
+        set_error("the cell is too thin for the neighbour radius");
+        return DPA4C_ERR_UNSUPPORTED;
+      }
+      g->reach[a] = static_cast<int>(re);
+    }
     g->nc[a] = static_cast<int>(nc);
-    g->reach[a] = static_cast<int>((g->rq * nc + g->Lq[a] - 1) / g->Lq[a]);
     g->ncell *= nc;
   }
   return 0;
@@ -455,26 +557,33 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
   int cblocks = static_cast<int>((g.ncell + kBlock - 1) / kBlock);
   hipLaunchKernelGGL(zero_i32_kernel, dim3(cblocks), dim3(kBlock), 0, st,
                      nb.cell_cnt.as<int32_t>(), g.ncell);
-  hipLaunchKernelGGL(bin_kernel, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
-                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                     nb.cell_cnt.as<int32_t>(), flags);
+  if (g.tric)
+    hipLaunchKernelGGL(bin_kernel<true>, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_cnt.as<int32_t>(), flags);
+  else
+    hipLaunchKernelGGL(bin_kernel<false>, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_cnt.as<int32_t>(), flags);
   hipLaunchKernelGGL(cell_scan_kernel, dim3(1), dim3(1024), 0, st, nb.cell_cnt.as<int32_t>(),
                      g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>());
   hipLaunchKernelGGL(place_kernel, dim3(blocks), dim3(kBlock), 0, st, n, nb.cell_of.as<int32_t>(),
                      nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(),
                      nb.cell_atoms.as<int32_t>());
-  hipLaunchKernelGGL(count_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
-                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>(), nb.counts.as<int64_t>());
+  if (g.tric)
+    hipLaunchKernelGGL(count_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(),
+                       nb.counts.as<int64_t>());
+  else
+    hipLaunchKernelGGL(count_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(),
+                       nb.counts.as<int64_t>());
   DPA4C_HIP_TRY(hipGetLastError());
   rc = exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, st);
   if (rc) return rc;
-  if (fill) {
-    hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
-                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                       nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags);
-    DPA4C_HIP_TRY(hipGetLastError());
-  }
+  if (fill) return fill_skin_list(nb, n, g, row_ptr, nbr_j, nbr_shift, cap, flags, st);
   return 0;
 }
 
@@ -482,9 +591,16 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
                    hipStream_t st) {
   GridDev gd = to_dev(g);
-  hipLaunchKernelGGL(fill_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
-                     nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_start.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j, nbr_shift, cap, flags);
+  if (g.tric)
+    hipLaunchKernelGGL(fill_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j,
+                       nbr_shift, cap, flags);
+  else
+    hipLaunchKernelGGL(fill_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
+                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j,
+                       nbr_shift, cap, flags);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
