@@ -15,8 +15,9 @@
 // non-scalar degrees the channel c = k contributes
 //     psi_k * Q_k(u),  Q_k(u) = sum_{l>=1, m} Ybar_lmk B_lm(u),
 // and Q_k is a fixed polynomial per centre: v.u (degree one), u.W u (degree
-// two, W symmetric) and a cubic (degree three).  Its coefficients are formed
-// once per centre, so per edge each lane evaluates one short polynomial and
+// two, W symmetric), a cubic (degree three) and a quartic (degree four).  Its
+// coefficients are formed once per centre, so per edge each lane evaluates
+// one short polynomial and
 // its gradient instead of every harmonic.  The LPE partial sums of an edge
 // are combined with a fixed DPP butterfly.
 #include <hip/hip_runtime.h>
@@ -74,6 +75,14 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
 #pragma unroll
       for (int m = 0; m < 7; ++m) w[m] = (P::L >= 3 && k == 0) ? gyr[P::Y3 + m] : 0.0f;
       cubic_form3(w, G3);
+    }
+    float G4[P::L >= 4 ? 3 : 1][10];   // gradient of the degree-four polynomial
+    if constexpr (P::L >= 4) {
+      float w[9], pc[15];
+#pragma unroll
+      for (int m = 0; m < 9; ++m) w[m] = k == 0 ? gyr[P::Y4 + m] : 0.0f;
+      quartic_coeffs4(w, pc);
+      quartic_grad4(pc, G4);
     }
     const float gs0 = k == 0 ? gyr[0] : 0.0f;
     const float gs1 = k == 0 ? gyr[1] : 0.0f;
@@ -182,17 +191,29 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
           for (int qq = 0; qq < 6; ++qq) c3[a] += G3[a][qq] * mono[qq];
         }
       }
-      // Q = v.u + (1/2) u.M u + (1/3) u.grad P3 (Euler's relation per degree)
-      const float Q = (v1[0] * x + v1[1] * y + v1[2] * z) +
-                      0.5f * (gq[0] * x + gq[1] * y + gq[2] * z) +
-                      (1.0f / 3.0f) * (c3[0] * x + c3[1] * y + c3[2] * z);
+      float c4[3] = {0.f, 0.f, 0.f};   // grad P4
+      if constexpr (P::L >= 4) {
+        float mono3[10];
+        cubic_monomials(x, y, z, mono3);
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+#pragma unroll
+          for (int qq = 0; qq < 10; ++qq) c4[a] += G4[a][qq] * mono3[qq];
+        }
+      }
+      // Q = v.u + (1/2) u.M u + (1/3) u.grad P3 + (1/4) u.grad P4 (Euler's
+      // relation per degree)
+      float Q = (v1[0] * x + v1[1] * y + v1[2] * z) +
+                0.5f * (gq[0] * x + gq[1] * y + gq[2] * z) +
+                (1.0f / 3.0f) * (c3[0] * x + c3[1] * y + c3[2] * z);
+      if constexpr (P::L >= 4) Q += 0.25f * (c4[0] * x + c4[1] * y + c4[2] * z);
       const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
       float drho = dchi * a0 + chi * b0 + Q * (dchi2 * psi0 + chi2 * dpsi0) +
                    gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2;
       const float wu = chi2 * psi0;
-      float dux = wu * (v1[0] + gq[0] + c3[0]);
-      float duy = wu * (v1[1] + gq[1] + c3[1]);
-      float duz = wu * (v1[2] + gq[2] + c3[2]);
+      float dux = wu * (v1[0] + gq[0] + c3[0] + c4[0]);
+      float duy = wu * (v1[1] + gq[1] + c3[1] + c4[1]);
+      float duz = wu * (v1[2] + gq[2] + c3[2] + c4[2]);
       if (!valid) drho = dux = duy = duz = 0.0f;
       drho = group_sum<P::LPE>(drho);
       dux = group_sum<P::LPE>(dux);

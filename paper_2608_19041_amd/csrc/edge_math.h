@@ -180,6 +180,80 @@ __device__ inline void cubic_form3(const float* w, float (*G)[6]) {
   G[2][3] = pyyz;        G[2][4] = 2.0f * pyzz; G[2][5] = 3.0f * pzzz;
 }
 
+// Degree four (Supplementary Note, real solid harmonics of degrees three and
+// four), as homogeneous quartics in (x, y, z), so exact off the unit sphere.
+__device__ inline void harm4_h(float x, float y, float z, float* b) {
+  const float x2 = x * x, y2 = y * y, z2 = z * z;
+  const float h35 = 2.958039891549808f;    // sqrt(35)/2
+  const float q70 = 2.091650066335189f;    // sqrt(70)/4
+  const float h5 = 1.118033988749895f;     // sqrt(5)/2
+  const float q10 = 0.7905694150420949f;   // sqrt(10)/4
+  const float q5 = 0.5590169943749475f;    // sqrt(5)/4
+  const float e35 = 0.739509972887452f;    // sqrt(35)/8
+  b[0] = h35 * x * y * (x2 - y2);
+  b[1] = q70 * y * z * (3.0f * x2 - y2);
+  b[2] = h5 * x * y * (6.0f * z2 - x2 - y2);
+  b[3] = q10 * y * z * (4.0f * z2 - 3.0f * x2 - 3.0f * y2);
+  b[4] = 0.375f * (x2 * x2 + y2 * y2) + z2 * z2 + 0.75f * x2 * y2 - 3.0f * z2 * (x2 + y2);
+  b[5] = q10 * x * z * (4.0f * z2 - 3.0f * x2 - 3.0f * y2);
+  b[6] = q5 * (x2 - y2) * (6.0f * z2 - x2 - y2);
+  b[7] = q70 * x * z * (x2 - 3.0f * y2);
+  b[8] = e35 * (x2 * x2 - 6.0f * x2 * y2 + y2 * y2);
+}
+
+// Monomial coefficients p[15] of P(u) = sum_m w_m B_4m(u) over the quartic
+// monomials x^a y^b z^c (a+b+c = 4) in the order index(a, c) =
+// (4-a)(5-a)/2 + c: x^4, x^3y, x^3z, x^2y^2, x^2yz, x^2z^2, xy^3, xy^2z,
+// xyz^2, xz^3, y^4, y^3z, y^2z^2, yz^3, z^4.
+__device__ inline void quartic_coeffs4(const float* w, float* p) {
+  const float h35 = 2.958039891549808f, q70 = 2.091650066335189f, h5 = 1.118033988749895f;
+  const float r10 = 3.1622776601683795f, q5 = 0.5590169943749475f, e35 = 0.739509972887452f;
+  const float t10 = 0.75f * r10, t70 = 3.0f * q70;   // 3 sqrt(10)/4, 3 sqrt(70)/4
+  p[0] = 0.375f * w[4] - q5 * w[6] + e35 * w[8];
+  p[1] = h35 * w[0] - h5 * w[2];
+  p[2] = -t10 * w[5] + q70 * w[7];
+  p[3] = 0.75f * w[4] - 6.0f * e35 * w[8];
+  p[4] = t70 * w[1] - t10 * w[3];
+  p[5] = -3.0f * w[4] + 6.0f * q5 * w[6];
+  p[6] = -h35 * w[0] - h5 * w[2];
+  p[7] = -t10 * w[5] - t70 * w[7];
+  p[8] = 6.0f * h5 * w[2];
+  p[9] = r10 * w[5];
+  p[10] = 0.375f * w[4] + q5 * w[6] + e35 * w[8];
+  p[11] = -q70 * w[1] - t10 * w[3];
+  p[12] = -3.0f * w[4] - 6.0f * q5 * w[6];
+  p[13] = r10 * w[3];
+  p[14] = w[4];
+}
+
+// Gradient of the quartic with monomial coefficients p[15]: dP/du_d =
+// sum_q G[d][q] mono3_q over the cubic monomials in the order index(a, c) =
+// (3-a)(4-a)/2 + c: x^3, x^2y, x^2z, xy^2, xyz, xz^2, y^3, y^2z, yz^2, z^3.
+// P = u . grad P / 4.
+__device__ inline void quartic_grad4(const float* p, float (*G)[10]) {
+#pragma unroll
+  for (int d = 0; d < 3; ++d)
+#pragma unroll
+    for (int q = 0; q < 10; ++q) G[d][q] = 0.0f;
+#pragma unroll
+  for (int a = 4; a >= 0; --a)
+#pragma unroll
+    for (int c = 0; c <= 4 - a; ++c) {
+      const int b = 4 - a - c;
+      const float v = p[(4 - a) * (5 - a) / 2 + c];
+      if (a > 0) G[0][(4 - a) * (5 - a) / 2 + c] += float(a) * v;       // x^(a-1) y^b z^c
+      if (b > 0) G[1][(3 - a) * (4 - a) / 2 + c] += float(b) * v;       // x^a y^(b-1) z^c
+      if (c > 0) G[2][(3 - a) * (4 - a) / 2 + c - 1] += float(c) * v;   // x^a y^b z^(c-1)
+    }
+}
+
+// the ten cubic monomials of quartic_grad4's order
+__device__ inline void cubic_monomials(float x, float y, float z, float* m) {
+  const float x2 = x * x, y2 = y * y, z2 = z * z;
+  m[0] = x2 * x; m[1] = x2 * y; m[2] = x2 * z; m[3] = x * y2; m[4] = x * y * z;
+  m[5] = x * z2; m[6] = y2 * y; m[7] = y2 * z; m[8] = y * z2; m[9] = z2 * z;
+}
+
 // species index clamped into the type table (the padding type for bad input)
 __device__ inline int clamp_type(int a, int n_types1) {
   return static_cast<unsigned>(a) < static_cast<unsigned>(n_types1) ? a : n_types1 - 1;

@@ -62,6 +62,9 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
     float acc1[3] = {0.f, 0.f, 0.f};
     float acc2[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
     float acc3[7] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float acc4[P::L >= 4 ? 9 : 1];
+#pragma unroll
+    for (int m = 0; m < (P::L >= 4 ? 9 : 1); ++m) acc4[m] = 0.0f;
     float s0 = 0.0f, s1 = 0.0f;
     const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
@@ -157,6 +160,13 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 #pragma unroll
         for (int m = 0; m < 7; ++m) acc3[m] += w3 * b3[m];
       }
+      if constexpr (P::L >= 4) {   // degree four: one channel, as degree three
+        float b4[9];
+        harm4_h(g.ux, g.uy, g.uz, b4);
+        const float w4 = w * w3mask;
+#pragma unroll
+        for (int m = 0; m < 9; ++m) acc4[m] += w4 * b4[m];
+      }
     }
     // combine the groups of a wave (fixed xor butterfly over the group index)
 #pragma unroll
@@ -170,6 +180,10 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       if constexpr (P::L >= 3) {
 #pragma unroll
         for (int m = 0; m < 7; ++m) acc3[m] += __shfl_xor(acc3[m], off);
+      }
+      if constexpr (P::L >= 4) {
+#pragma unroll
+        for (int m = 0; m < 9; ++m) acc4[m] += __shfl_xor(acc4[m], off);
       }
       s0 += __shfl_xor(s0, off);
       s1 += __shfl_xor(s1, off);
@@ -188,6 +202,12 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
         if (k == 0) {
 #pragma unroll
           for (int m = 0; m < 7; ++m) pw[P::Y3 + m] = acc3[m];
+        }
+      }
+      if constexpr (P::L >= 4) {
+        if (k == 0) {
+#pragma unroll
+          for (int m = 0; m < 9; ++m) pw[P::Y4 + m] = acc4[m];
         }
       }
       if (k == 0) {

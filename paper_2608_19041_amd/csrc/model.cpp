@@ -46,8 +46,9 @@ const char* stage_name(int s) {
 namespace {
 
 // ---------------------------------------------------------------------------
-// real Cartesian harmonics on the unit sphere (s = |u|^2 = 1), degrees 1..3,
-// Eq. (harmonics) and the degree-three block of the Supplementary Note
+// real Cartesian harmonics on the unit sphere (s = |u|^2 = 1), degrees 1..4,
+// Eq. (harmonics) and the degree-three and degree-four blocks of the
+// Supplementary Note
 // ---------------------------------------------------------------------------
 void harmonics_host(int l, double x, double y, double z, double* out) {
   const double r3 = std::sqrt(3.0);
@@ -59,7 +60,7 @@ void harmonics_host(int l, double x, double y, double z, double* out) {
     out[2] = 0.5 * (3 * z * z - 1.0);
     out[3] = r3 * x * z;
     out[4] = 0.5 * r3 * (x * x - y * y);
-  } else {
+  } else if (l == 3) {
     out[0] = std::sqrt(5.0 / 8.0) * y * (3 * x * x - y * y);
     out[1] = std::sqrt(15.0) * x * y * z;
     out[2] = std::sqrt(3.0 / 8.0) * y * (5 * z * z - 1.0);
@@ -67,6 +68,17 @@ void harmonics_host(int l, double x, double y, double z, double* out) {
     out[4] = std::sqrt(3.0 / 8.0) * x * (5 * z * z - 1.0);
     out[5] = 0.5 * std::sqrt(15.0) * z * (x * x - y * y);
     out[6] = std::sqrt(5.0 / 8.0) * x * (x * x - 3 * y * y);
+  } else {
+    const double x2 = x * x, y2 = y * y, z2 = z * z;
+    out[0] = 0.5 * std::sqrt(35.0) * x * y * (x2 - y2);
+    out[1] = 0.25 * std::sqrt(70.0) * y * z * (3 * x2 - y2);
+    out[2] = 0.5 * std::sqrt(5.0) * x * y * (7 * z2 - 1.0);
+    out[3] = 0.25 * std::sqrt(10.0) * y * z * (7 * z2 - 3.0);
+    out[4] = 0.125 * (35 * z2 * z2 - 30 * z2 + 3.0);
+    out[5] = 0.25 * std::sqrt(10.0) * x * z * (7 * z2 - 3.0);
+    out[6] = 0.25 * std::sqrt(5.0) * (x2 - y2) * (7 * z2 - 1.0);
+    out[7] = 0.25 * std::sqrt(70.0) * x * z * (x2 - 3 * y2);
+    out[8] = 0.125 * std::sqrt(35.0) * (x2 * x2 - 6 * x2 * y2 + y2 * y2);
   }
 }
 
@@ -358,20 +370,45 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     }
   }
 
-  // ---- coupling tensors; (2,3,3) symmetrised over its two degree-3 indices
+  // ---- coupling tensors, each symmetrised over the indices of equal degree
+  // (the exact integrals are; the quadrature sums are only up to rounding)
   std::vector<float> cpl;
   m->gaunt[0] = coupling(1, 1, 2);
   m->gaunt[2] = coupling(2, 2, 2);
+  auto push = [&](int l1, int l2, int l3) {
+    const std::vector<double> g = coupling(l1, l2, l3);
+    const int n1 = 2 * l1 + 1, n2 = 2 * l2 + 1, n3 = 2 * l3 + 1;
+    auto at = [&](int a, int b, int c) { return g[(a * n2 + b) * n3 + c]; };
+    for (int a = 0; a < n1; ++a)
+      for (int b = 0; b < n2; ++b)
+        for (int c = 0; c < n3; ++c) {
+          double v;
+          if (l1 == l2 && l2 == l3)
+            v = (at(a, b, c) + at(a, c, b) + at(b, a, c) + at(b, c, a) + at(c, a, b) + at(c, b, a)) / 6.0;
+          else if (l2 == l3)
+            v = 0.5 * (at(a, b, c) + at(a, c, b));
+          else if (l1 == l2)
+            v = 0.5 * (at(a, b, c) + at(b, a, c));
+          else
+            v = at(a, b, c);
+          cpl.push_back(static_cast<float>(v));
+        }
+  };
   if (L >= 3) {
-    m->gaunt[1] = coupling(1, 2, 3);
-    m->gaunt[3] = coupling(2, 3, 3);
-    cpl.reserve(kCouplings);
-    for (double v : m->gaunt[1]) cpl.push_back(static_cast<float>(v));
-    const auto& g = m->gaunt[3];
-    for (int a = 0; a < 5; ++a)
-      for (int b = 0; b < 7; ++b)
-        for (int c = 0; c < 7; ++c)
-          cpl.push_back(static_cast<float>(0.5 * (g[(a * 7 + b) * 7 + c] + g[(a * 7 + c) * 7 + b])));
+    cpl.reserve(couplings_for(L));
+    push(1, 2, 3);
+    push(2, 3, 3);
+  }
+  if (L >= 4) {
+    push(1, 3, 4);
+    push(2, 2, 4);
+    push(2, 4, 4);
+    push(3, 3, 4);
+    push(4, 4, 4);
+  }
+  if (cpl.size() != size_t(couplings_for(L))) {
+    set_error("dpa4c_model_create: coupling layout");
+    return DPA4C_ERR_INVALID_ARG;
   }
 
   // ---- one device block for every parameter array ---------------------

@@ -38,7 +38,7 @@ struct ReadoutParams {
   float A2[P::C2 * P::K2];
   float mu[P::DSTR];                       // calibration, zero padded
   float inv_sigma[P::DSTR];
-  float cpl[P::L >= 3 ? kCouplings : 1];   // C123 then C233
+  float cpl[P::L >= 3 ? couplings_for(P::L) : 1];   // C123, C233 (then the degree-four ones)
 };
 
 // Cooperative copy of the readout parameters by the ``nthreads`` threads of
@@ -56,7 +56,7 @@ __device__ void stage_readout_params(ReadoutParams<P>& rp, const ModelDev& md, i
     rp.inv_sigma[t] = t < P::DOUT ? md.inv_sigma[t] : 0.0f;
   }
   if constexpr (P::L >= 3)
-    for (int t = tid; t < kCouplings; t += nthreads) rp.cpl[t] = md.cpl[t];
+    for (int t = tid; t < couplings_for(P::L); t += nthreads) rp.cpl[t] = md.cpl[t];
 }
 
 template <class P>
@@ -70,6 +70,10 @@ struct ReadoutLds {
   float q[P::K2][9];              // STF matrices of the degree-two probes
   float qv[P::K2][P::K1][3];      // Q_eta v_kappa
   float t123[15], u123[3 * P::K2], w233[35], v233[5];
+  // degree four (one channel; Z4 = X~4): X~4, T134[m1] = C134 : Z3 Z4,
+  // T224[m1][m2] = C224 . Z4, T244[m1] = C244 : Z4 Z4
+  float xt4[P::L >= 4 ? 9 : 1], t134[P::L >= 4 ? 3 : 1], t224[P::L >= 4 ? 25 : 1],
+      t244[P::L >= 4 ? 5 : 1];
   // backward only
   float gxt1[3 * P::C1];
   float gxt2[5 * P::C2];
@@ -79,6 +83,8 @@ struct ReadoutLds {
   float gz3[8];
   float gq[P::K2][9];
   float ub123[3 * P::K2], tb123[15], vb233[5];
+  float gxt4[P::L >= 4 ? 9 : 1], tb134[P::L >= 4 ? 3 : 1], tb224[P::L >= 4 ? 25 : 1],
+      tb244[P::L >= 4 ? 5 : 1];
   float gy[P::NS];
 };
 
@@ -157,7 +163,8 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
   *M1 = m1;
   const float i1 = 1.0f / m1;
   constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
-  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
+  constexpr int n4 = (P::L >= 4 ? 9 : 0);
+  for (int o = lane; o < n1 + n2 + n3 + n4; o += kHalf) {
     if (o < n1) {
       int m = o / P::C1, cp = o % P::C1;
       const DPA4C_LDS float* x = s.y + P::Y1 + m * P::C1;
@@ -172,9 +179,12 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
 #pragma unroll
       for (int c = 0; c < P::C2; ++c) acc += x[c] * rp.W2[c * P::C2 + cp];
       s.xt2[t] = acc * i1;
-    } else {
+    } else if (o < n1 + n2 + n3) {
       int m = o - n1 - n2;
       s.xt3[m] = s.y[P::Y3 + m] * i1;
+    } else if constexpr (P::L >= 4) {
+      int m = o - n1 - n2 - n3;
+      s.xt4[m] = s.y[P::Y4 + m] * i1;
     }
   }
   wave_sync();
@@ -207,6 +217,39 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
       for (int m3 = 0; m3 < 7; ++m3) acc += c[m3] * s.xt3[m3];
       if (o < 15) s.t123[o] = acc;
       else s.w233[o - 15] = acc;
+    }
+  }
+  if constexpr (P::L >= 4) {
+    // T134[m1] = sum C134[m1][m3][m4] Z3 Z4, T224[m1][m2] = sum_m4 C224 Z4,
+    // T244[m1] = sum C244[m1][a][b] Z4 Z4 (33 entries, fixed order each)
+    for (int o = lane; o < 33; o += kHalf) {
+      float acc = 0.0f;
+      if (o < 3) {
+        const DPA4C_LDS float* c = cpl + kO134 + 63 * o;
+#pragma unroll
+        for (int m3 = 0; m3 < 7; ++m3) {
+          float r = 0.0f;
+#pragma unroll
+          for (int m4 = 0; m4 < 9; ++m4) r += c[9 * m3 + m4] * s.xt4[m4];
+          acc += r * s.xt3[m3];
+        }
+        s.t134[o] = acc;
+      } else if (o < 28) {
+        const DPA4C_LDS float* c = cpl + kO224 + 9 * (o - 3);
+#pragma unroll
+        for (int m4 = 0; m4 < 9; ++m4) acc += c[m4] * s.xt4[m4];
+        s.t224[o - 3] = acc;
+      } else {
+        const DPA4C_LDS float* c = cpl + kO244 + 81 * (o - 28);
+#pragma unroll
+        for (int a = 0; a < 9; ++a) {
+          float r = 0.0f;
+#pragma unroll
+          for (int b = 0; b < 9; ++b) r += c[9 * a + b] * s.xt4[b];
+          acc += r * s.xt4[a];
+        }
+        s.t244[o - 28] = acc;
+      }
     }
   }
   wave_sync();
@@ -251,6 +294,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
                                                           const float* __restrict__ x0,
                                                           DPA4C_LDS float* d) {
   const int lane = lane_of() & (kHalf - 1);
+  const DPA4C_LDS float* cpl = rp.cpl;
   float M0, M1;
   readout_intermediates<P>(s, rp, &M0, &M1);
   const float i0 = 1.0f / M0;
@@ -263,7 +307,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     d[P::oM1] = M1;
   }
   // Gram blocks, Eq. (gram), vech with sqrt(2) off the diagonal
-  for (int o = lane; o < P::nG1 + P::nG2 + P::nG3; o += kHalf) {
+  for (int o = lane; o < P::nG1 + P::nG2 + P::nG3 + P::nG4; o += kHalf) {
     float acc = 0.0f;
     if (o < P::nG1) {
       int c, cp;
@@ -277,9 +321,12 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
 #pragma unroll
       for (int m = 0; m < 5; ++m) acc += s.xt2[m * P::C2 + c] * s.xt2[m * P::C2 + cp];
       if (c != cp) acc *= kSqrt2;
-    } else {
+    } else if (o < P::nG1 + P::nG2 + P::nG3) {
 #pragma unroll
       for (int m = 0; m < 7; ++m) acc += s.xt3[m] * s.xt3[m];
+    } else if constexpr (P::L >= 4) {
+#pragma unroll
+      for (int m = 0; m < 9; ++m) acc += s.xt4[m] * s.xt4[m];
     }
     d[P::oG1 + o] = acc;
   }
@@ -323,6 +370,63 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
 #pragma unroll
         for (int m1 = 0; m1 < 5; ++m1) acc += s.z2[m1 * P::K2 + eta] * s.v233[m1];
         d[P::o233 + eta] = acc;
+      }
+    }
+  }
+  if constexpr (P::L >= 4) {
+    // (1,3,4) [K1], (2,2,4) [k1 <= k2], (2,4,4) [K2], (3,3,4), (4,4,4)
+    constexpr int n4 = P::n134 + P::n224 + P::n244 + 2;
+    for (int o = lane; o < n4; o += kHalf) {
+      float acc = 0.0f;
+      if (o < P::n134) {
+#pragma unroll
+        for (int m1 = 0; m1 < 3; ++m1) acc += s.z1[m1 * P::K1 + o] * s.t134[m1];
+        d[P::o134 + o] = acc;
+      } else if (o < P::n134 + P::n224) {
+        int k1, k2;
+        vech_pair(o - P::n134, P::K2, &k1, &k2);
+#pragma unroll
+        for (int m1 = 0; m1 < 5; ++m1) {
+          float r = 0.0f;
+#pragma unroll
+          for (int m2 = 0; m2 < 5; ++m2) r += s.t224[5 * m1 + m2] * s.z2[m2 * P::K2 + k2];
+          acc += s.z2[m1 * P::K2 + k1] * r;
+        }
+        d[P::o224 + o - P::n134] = (k1 == k2 ? 1.0f : kSqrt2) * acc;
+      } else if (o < P::n134 + P::n224 + P::n244) {
+        const int k1 = o - P::n134 - P::n224;
+#pragma unroll
+        for (int m1 = 0; m1 < 5; ++m1) acc += s.z2[m1 * P::K2 + k1] * s.t244[m1];
+        d[P::o244 + k1] = acc;
+      } else if (o == n4 - 2) {
+        const DPA4C_LDS float* c = cpl + kO334;
+#pragma unroll
+        for (int a = 0; a < 7; ++a) {
+          float r = 0.0f;
+#pragma unroll
+          for (int b = 0; b < 7; ++b) {
+            float q = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 9; ++e) q += c[(7 * a + b) * 9 + e] * s.xt4[e];
+            r += q * s.xt3[b];
+          }
+          acc += r * s.xt3[a];
+        }
+        d[P::o334] = acc;
+      } else {
+        const DPA4C_LDS float* c = cpl + kO444;
+        for (int a = 0; a < 9; ++a) {
+          float r = 0.0f;
+#pragma unroll
+          for (int b = 0; b < 9; ++b) {
+            float q = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 9; ++e) q += c[(9 * a + b) * 9 + e] * s.xt4[e];
+            r += q * s.xt4[b];
+          }
+          acc += r * s.xt4[a];
+        }
+        d[P::o444] = acc;
       }
     }
   }
@@ -422,7 +526,37 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
 #pragma unroll
       for (int k2 = 0; k2 < P::K2; ++k2) acc += d[P::o123 + k * P::K2 + k2] * s.u123[m * P::K2 + k2];
     }
+    if constexpr (P::L >= 4) acc += d[P::o134 + k] * s.t134[m];
     s.gz1[o] = acc;
+  }
+  if constexpr (P::L >= 4) {
+    // adjoints of the degree-four partial contractions:
+    // Tbar134[m1] = sum_k1 Jbar134[k1] Z1[m1][k1],
+    // Tbar224[m1][m2] = sum_(k1<=k2) w Jbar224 Z2[m1][k1] Z2[m2][k2],
+    // Tbar244[m1] = sum_k1 Jbar244[k1] Z2[m1][k1]
+    for (int o = lane; o < 33; o += kHalf) {
+      float acc = 0.0f;
+      if (o < 3) {
+#pragma unroll
+        for (int k1 = 0; k1 < P::K1; ++k1) acc += d[P::o134 + k1] * s.z1[o * P::K1 + k1];
+        s.tb134[o] = acc;
+      } else if (o < 28) {
+        const int m1 = (o - 3) / 5, m2 = (o - 3) % 5;
+#pragma unroll
+        for (int tt = 0; tt < P::n224; ++tt) {
+          int k1, k2;
+          vech_pair(tt, P::K2, &k1, &k2);
+          acc += (k1 == k2 ? 1.0f : kSqrt2) * d[P::o224 + tt] * s.z2[m1 * P::K2 + k1] *
+                 s.z2[m2 * P::K2 + k2];
+        }
+        s.tb224[o - 3] = acc;
+      } else {
+        const int m1 = o - 28;
+#pragma unroll
+        for (int k1 = 0; k1 < P::K2; ++k1) acc += d[P::o244 + k1] * s.z2[m1 * P::K2 + k1];
+        s.tb244[m1] = acc;
+      }
+    }
   }
   if constexpr (P::L >= 3) {
     // Ubar[m1][k2] = sum_k1 Jbar123[k1][k2] Z1[m1][k1],  Vbar[m1] = sum_e Jbar233[e] Z2[m1][e]
@@ -460,6 +594,28 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
       for (int m1 = 0; m1 < 3; ++m1) acc += s.ub123[m1 * P::K2 + eta] * s.t123[m1 * 5 + m];
       acc += d[P::o233 + eta] * s.v233[m];
     }
+    if constexpr (P::L >= 4) {
+      // (2,2,4): the pair (k1, k2) holding eta, through the symmetric T224
+#pragma unroll
+      for (int tt = 0; tt < P::n224; ++tt) {
+        int k1, k2;
+        vech_pair(tt, P::K2, &k1, &k2);
+        const float jb = (k1 == k2 ? 1.0f : kSqrt2) * d[P::o224 + tt];
+        if (k1 == eta) {
+          float r = 0.0f;
+#pragma unroll
+          for (int m2 = 0; m2 < 5; ++m2) r += s.t224[5 * m + m2] * s.z2[m2 * P::K2 + k2];
+          acc += jb * r;
+        }
+        if (k2 == eta) {
+          float r = 0.0f;
+#pragma unroll
+          for (int m1 = 0; m1 < 5; ++m1) r += s.z2[m1 * P::K2 + k1] * s.t224[5 * m1 + m];
+          acc += jb * r;
+        }
+      }
+      acc += d[P::o244 + eta] * s.t244[m];
+    }
     s.gz2[lane] = acc;
   }
   wave_sync();
@@ -472,7 +628,68 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
       for (int o = 0; o < 15; ++o) acc += s.tb123[o] * cpl[7 * o + m];
 #pragma unroll
       for (int m1 = 0; m1 < 5; ++m1) acc += 2.0f * s.vb233[m1] * s.w233[m1 * 7 + m];
+      if constexpr (P::L >= 4) {
+        // (1,3,4): sum Tbar134[m1] C134[m1][m][e] Z4[e]; (3,3,4): 2 Jbar C334[m][b][e] Z3 Z4
+#pragma unroll
+        for (int m1 = 0; m1 < 3; ++m1) {
+          float r = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 9; ++e) r += cpl[kO134 + (7 * m1 + m) * 9 + e] * s.xt4[e];
+          acc += s.tb134[m1] * r;
+        }
+        float r334 = 0.0f;
+#pragma unroll
+        for (int b = 0; b < 7; ++b) {
+          float q = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 9; ++e) q += cpl[kO334 + (7 * m + b) * 9 + e] * s.xt4[e];
+          r334 += q * s.xt3[b];
+        }
+        acc += 2.0f * d[P::o334] * r334;
+      }
       s.gz3[m] = acc;
+    }
+    if constexpr (P::L >= 4) {
+      // dE/dZ4[m] from (1,3,4), (2,2,4), (2,4,4), (3,3,4), (4,4,4), then
+      // dE/dX~4 = 2 Gbar4 X~4 + dE/dZ4
+      if (lane >= 7 && lane < 16) {
+        const int m = lane - 7;
+        float acc = 0.0f;
+#pragma unroll
+        for (int m1 = 0; m1 < 3; ++m1) {
+          float r = 0.0f;
+#pragma unroll
+          for (int a = 0; a < 7; ++a) r += cpl[kO134 + (7 * m1 + a) * 9 + m] * s.xt3[a];
+          acc += s.tb134[m1] * r;
+        }
+#pragma unroll
+        for (int o = 0; o < 25; ++o) acc += s.tb224[o] * cpl[kO224 + 9 * o + m];
+#pragma unroll
+        for (int m1 = 0; m1 < 5; ++m1) {
+          float r = 0.0f;
+#pragma unroll
+          for (int b = 0; b < 9; ++b) r += cpl[kO244 + (9 * m1 + m) * 9 + b] * s.xt4[b];
+          acc += 2.0f * s.tb244[m1] * r;
+        }
+        float r334 = 0.0f;
+#pragma unroll
+        for (int a = 0; a < 7; ++a) {
+          float q = 0.0f;
+#pragma unroll
+          for (int b = 0; b < 7; ++b) q += cpl[kO334 + (7 * a + b) * 9 + m] * s.xt3[b];
+          r334 += q * s.xt3[a];
+        }
+        acc += d[P::o334] * r334;
+        float r444 = 0.0f;
+        for (int b = 0; b < 9; ++b) {
+          float q = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 9; ++e) q += cpl[kO444 + (9 * m + b) * 9 + e] * s.xt4[e];
+          r444 += q * s.xt4[b];
+        }
+        acc += 3.0f * d[P::o444] * r444;
+        s.gxt4[m] = 2.0f * d[P::oG4] * s.xt4[m] + acc;
+      }
     }
     wave_sync();
   }
@@ -521,7 +738,8 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     s.gy[P::Y0 + c] = xb * i0;
     part0 += xb * s.y[P::Y0 + c];
   }
-  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
+  constexpr int n4 = (P::L >= 4 ? 9 : 0);
+  for (int o = lane; o < n1 + n2 + n3 + n4; o += kHalf) {
     float xb;
     int yi;
     if (o < n1) {
@@ -536,10 +754,14 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
 #pragma unroll
       for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * rp.W2[c * P::C2 + cp];
       yi = P::Y2 + t;
-    } else {
+    } else if (o < n1 + n2 + n3) {
       int m = o - n1 - n2;
       xb = s.gxt3[m];
       yi = P::Y3 + m;
+    } else {
+      int m = o - n1 - n2 - n3;
+      xb = P::L >= 4 ? s.gxt4[m < (P::L >= 4 ? 9 : 1) ? m : 0] : 0.0f;
+      yi = P::Y4 + m;
     }
     s.gy[yi] = xb * i1;
     part1 += xb * s.y[yi];

@@ -340,6 +340,8 @@ MODELS = {
     "plus": ModelSpec(C0=128, L=3, R=4, n_rbf=16, F=384, n_layers=3),
     # the full model with its calibration taken on diamond carbon
     "full_carbon": ModelSpec(C0=128, L=3, R=4, n_rbf=16, F=384, n_layers=3),
+    # the Plus widths with harmonics up to degree four (nine coupling triples)
+    "plus_l4": ModelSpec(C0=128, L=4, R=4, n_rbf=16, F=384, n_layers=3),
 }
 
 
