@@ -73,7 +73,8 @@ typedef struct dpa4c_model dpa4c_model;
  *     E_ref  [T+1]              Eq. (atomic-energy)
  *     mu [D_out], sigma [D_out] Eq. (calibration)
  * Supported (C0, L, R, F): the five variants of Supplementary Table S3,
- * (8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384), with
+ * (8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384), and the
+ * Plus widths with harmonics up to degree four, (128,4,4,384), each with
  * n_layers = 3 for the per-atom kernel; others fail with UNSUPPORTED, as
  * does n_types > 127 (the type table, padding row included, holds at most
  * 128 rows).

@@ -266,7 +266,7 @@ int read_header(const void* blob, size_t nbytes, dpa4c_model* m, int widths[2]) 
         return 0;
       }) == kNoProfile) {
     set_error("dpa4c_model_create: (C0, L, R, MLP width) is not one of the compiled variants "
-              "(8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384)");
+              "(8,2,0,96) (32,2,0,192) (64,2,0,256) (64,3,4,256) (128,3,4,384) (128,4,4,384)");
     return DPA4C_ERR_UNSUPPORTED;
   }
   if (m->n_rbf <= 0 || m->F <= 0 || m->F % 16 || m->n_layers < 1 || m->n_layers > 7 ||
