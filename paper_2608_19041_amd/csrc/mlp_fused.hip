@@ -317,8 +317,9 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       }
       __syncthreads();
     }
-    // ---- dE/dD = p1 Th1^T  (KP columns, tiles dealt round-robin) back into LDS;
-    // a wave with one tile fewer runs the shorter product
+    // ---- dE/dD = p1 Th1^T  (KP columns, tiles dealt round-robin) back into LDS,
+    // divided by the calibration scales; a wave with one tile fewer runs the
+    // shorter product
     {
       const int ntd = (DT - wave + kWavesPB - 1) / kWavesPB;
       v4f acc[NTD];
@@ -333,8 +334,9 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
       for (int t = 0; t < NTD; ++t) {
         if (t >= ntd) continue;
         const int col = (wave + kWavesPB * t) * 16 + col_in;
+        const float is = rpl.inv_sigma[col];   // dE/dD~ = dE/dD / sigma, Eq. (calibration)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) As[(4 * rgrp + r) * LDA + col] = acc[t][r];
+        for (int r = 0; r < 4; ++r) As[(4 * rgrp + r) * LDA + col] = acc[t][r] * is;
       }
       __syncthreads();
     }

@@ -295,17 +295,29 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
                                                           DPA4C_LDS float* d) {
   const int lane = lane_of() & (kHalf - 1);
   const DPA4C_LDS float* cpl = rp.cpl;
+  // the atom's row of the type table, requested before the LDS work
+  constexpr int NX = (P::C0 + kHalf - 1) / kHalf;
+  float x0r[NX];
+#pragma unroll
+  for (int q = 0; q < NX; ++q) x0r[q] = lane + q * kHalf < P::C0 ? x0[lane + q * kHalf] : 0.0f;
+  // every entry is calibrated (Eq. (calibration)) as it is written
+  auto put = [&](int o, float v) { d[o] = (v - rp.mu[o]) * rp.inv_sigma[o]; };
   float M0, M1;
   readout_intermediates<P>(s, rp, &M0, &M1);
   const float i0 = 1.0f / M0;
-  for (int c = lane; c < P::C0; c += kHalf) {
-    d[P::oX0 + c] = x0[c];
-    d[P::oX + c] = s.y[P::Y0 + c] * i0;
+#pragma unroll
+  for (int q = 0; q < NX; ++q) {
+    const int c = lane + q * kHalf;
+    if (c < P::C0) {
+      put(P::oX0 + c, x0r[q]);
+      put(P::oX + c, s.y[P::Y0 + c] * i0);
+    }
   }
   if (lane == 0) {
-    d[P::oM0] = M0;
-    d[P::oM1] = M1;
+    put(P::oM0, M0);
+    put(P::oM1, M1);
   }
+  if (lane < P::DSTR - P::DOUT) d[P::DOUT + lane] = 0.0f;   // zero padding
   // Gram blocks, Eq. (gram), vech with sqrt(2) off the diagonal
   for (int o = lane; o < P::nG1 + P::nG2 + P::nG3 + P::nG4; o += kHalf) {
     float acc = 0.0f;
@@ -328,7 +340,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
 #pragma unroll
       for (int m = 0; m < 9; ++m) acc += s.xt4[m] * s.xt4[m];
     }
-    d[P::oG1 + o] = acc;
+    put(P::oG1 + o, acc);
   }
   // (1,1,2): -(f/sqrt5) v_k1 . Q_eta v_k2, k1 <= k2
   for (int o = lane; o < P::n112; o += kHalf) {
@@ -337,7 +349,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     float acc = 0.0f;
 #pragma unroll
     for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];
-    d[P::o112 + o] = -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc;
+    put(P::o112 + o, -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc);
   }
   // (2,2,2): -sqrt(12/35) w tr(Q_a Q_b Q_c)
   if (lane < P::n222) {
@@ -354,7 +366,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
         for (int u = 0; u < 3; ++u) ab += s.q[a][r * 3 + u] * s.q[b][u * 3 + t];
         tr += ab * s.q[c][t * 3 + r];
       }
-    d[P::o222 + lane] = -kSqrt12_35 * w * tr;
+    put(P::o222 + lane, -kSqrt12_35 * w * tr);
   }
   if constexpr (P::L >= 3) {
     // (1,2,3) and (2,3,3): last contraction of the factored couplings
@@ -364,12 +376,12 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
         const int k1 = o / P::K2, k2 = o % P::K2;
 #pragma unroll
         for (int m1 = 0; m1 < 3; ++m1) acc += s.z1[m1 * P::K1 + k1] * s.u123[m1 * P::K2 + k2];
-        d[P::o123 + o] = acc;
+        put(P::o123 + o, acc);
       } else {
         const int eta = o - P::n123;
 #pragma unroll
         for (int m1 = 0; m1 < 5; ++m1) acc += s.z2[m1 * P::K2 + eta] * s.v233[m1];
-        d[P::o233 + eta] = acc;
+        put(P::o233 + eta, acc);
       }
     }
   }
@@ -381,7 +393,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
       if (o < P::n134) {
 #pragma unroll
         for (int m1 = 0; m1 < 3; ++m1) acc += s.z1[m1 * P::K1 + o] * s.t134[m1];
-        d[P::o134 + o] = acc;
+        put(P::o134 + o, acc);
       } else if (o < P::n134 + P::n224) {
         int k1, k2;
         vech_pair(o - P::n134, P::K2, &k1, &k2);
@@ -392,12 +404,12 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
           for (int m2 = 0; m2 < 5; ++m2) r += s.t224[5 * m1 + m2] * s.z2[m2 * P::K2 + k2];
           acc += s.z2[m1 * P::K2 + k1] * r;
         }
-        d[P::o224 + o - P::n134] = (k1 == k2 ? 1.0f : kSqrt2) * acc;
+        put(P::o224 + o - P::n134, (k1 == k2 ? 1.0f : kSqrt2) * acc);
       } else if (o < P::n134 + P::n224 + P::n244) {
         const int k1 = o - P::n134 - P::n224;
 #pragma unroll
         for (int m1 = 0; m1 < 5; ++m1) acc += s.z2[m1 * P::K2 + k1] * s.t244[m1];
-        d[P::o244 + k1] = acc;
+        put(P::o244 + k1, acc);
       } else if (o == n4 - 2) {
         const DPA4C_LDS float* c = cpl + kO334;
 #pragma unroll
@@ -412,7 +424,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
           }
           acc += r * s.xt3[a];
         }
-        d[P::o334] = acc;
+        put(P::o334, acc);
       } else {
         const DPA4C_LDS float* c = cpl + kO444;
         for (int a = 0; a < 9; ++a) {
@@ -426,7 +438,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
           }
           acc += r * s.xt4[a];
         }
-        d[P::o444] = acc;
+        put(P::o444, acc);
       }
     }
   }
@@ -436,16 +448,14 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     float acc = 0.0f;
 #pragma unroll
     for (int a = 0; a < 3; ++a) acc += s.qv[eta][k][a] * s.qv[eta][k][a];
-    d[P::oPi + o] = acc;
+    put(P::oPi + o, acc);
   }
-  wave_sync();
-  for (int o = lane; o < P::DSTR; o += kHalf)
-    d[o] = o < P::DOUT ? (d[o] - rp.mu[o]) * rp.inv_sigma[o] : 0.0f;
   wave_sync();
 }
 
-// Vector-Jacobian product of the readout: from dE/dD (LDS row ``d``, scaled
-// in place to dE/dD~) to dE/d(node state) in s.gy.  ``s`` must still hold
+// Vector-Jacobian product of the readout: from dE/dD~ = dE/dD / sigma (LDS
+// row ``d``; the producer of dE/dD applies the 1/sigma of Eq. (calibration))
+// to dE/d(node state) in s.gy.  ``s`` must still hold
 // what readout_forward left there for the same atom (node state and the
 // forward intermediates), which are reused rather than recomputed.
 template <class P>
@@ -456,8 +466,6 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
   const DPA4C_LDS float* cpl = rp.cpl;
   const float M0 = sqrtf(0.25f + s.y[0]);
   const float M1 = sqrtf(0.25f + s.y[1]);
-  for (int o = lane; o < P::DOUT; o += kHalf) d[o] *= rp.inv_sigma[o];
-  wave_sync();
   // --- dE/dQ_eta (3x3, not symmetrised) from (1,1,2), quartic and (2,2,2)
   if (lane < P::K2 * 9) {
     int eta = lane / 9, a = (lane % 9) / 3, b = lane % 3;
