@@ -42,7 +42,7 @@ extern "C" {
 
 #define DPA4C_OK 0
 #define DPA4C_ERR_INVALID_ARG (-1) /* bad pointer, size or value */
-#define DPA4C_ERR_UNSUPPORTED (-2) /* non-periodic cell, profile not built, row too long */
+#define DPA4C_ERR_UNSUPPORTED (-2) /* open axes of a non-diagonal cell, profile not built, row too long */
 #define DPA4C_ERR_CAPACITY (-3)    /* neighbour capacity too small; *n_pairs holds the need */
 #define DPA4C_ERR_HIP (-4)         /* a HIP runtime call failed */
 #define DPA4C_ERR_NONFINITE (-5)   /* a non-finite position was found */
@@ -99,7 +99,8 @@ int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
 
 /*
  * Neighbour list of Eq. (neighbor-set) at radius r_list (typically r_c plus
- * a skin), for a fully periodic cell, orthorhombic or triclinic.
+ * a skin), for a periodic cell (orthorhombic or triclinic) or an open or
+ * partly open system.  Along an open axis no periodic image is a neighbour.
  *
  * Membership uses the exact fixed-point predicate
  *     |Q(r_j) + sum_b n_b Q(h_b) - Q(r_i)|^2 < Q(r_list)^2,  Q(x) = rint(x * 2^20)
@@ -113,8 +114,12 @@ int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
  * pos       device float64 [N][3]
  * cell      host float64 [9], rows are the lattice vectors h_0, h_1, h_2
  *           (any non-singular matrix, entries below 1e6 A; a diagonal cell
- *           must have a positive diagonal)
- * pbc       host int [3]; must be {1, 1, 1}
+ *           must have a positive diagonal), or NULL for an open system
+ * pbc       host int [3] (ignored when cell is NULL): pbc[a] = 0 opens axis
+ *           a, which needs a diagonal cell (its length on open axes is not
+ *           used).  Internally an open axis is given the length
+ *           extent + 2 r_list + 1 A, read from the positions (one more
+ *           synchronisation), so no image can be within r_list
  * row_ptr   device int64 [N+1] out: CSR row offsets
  * nbr_j     device int32 [cap] out: neighbour index j
  * nbr_shift device int32 [cap] out: image n packed as
@@ -135,9 +140,10 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
  * Energy and forces for one configuration (Eqs. (energy-decomposition),
  * (atomic-energy), (forces)).
  *
- * The neighbour list passed in is a skin list from build_neighbors at any
- * radius r_list >= r_c built for positions from which no atom has moved by
- * more than (r_list - r_c)/2 (integer norm); the library keeps the edges with
+ * The neighbour list passed in is a skin list from build_neighbors (same
+ * cell and pbc) at any radius r_list >= r_c built for positions from which
+ * no atom has moved by more than (r_list - r_c)/2 (integer norm); the
+ * library keeps the edges with
  * the r_c predicate itself, in canonical order.  r_c must equal the model's.
  * n_pairs is the number of edges of that list (row_ptr[N], as returned by
  * build_neighbors); it sizes the library's edge workspace.

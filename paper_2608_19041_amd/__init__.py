@@ -112,6 +112,22 @@ def _host_f64(a, n):
     return a
 
 
+def _cell_arg(cell):
+    """Host float64 [9] (rows = lattice vectors) and its pointer; None (an
+    open system) passes a null pointer."""
+    if cell is None:
+        return None, None
+    a = _host_f64(cell, 9)
+    return a, a.ctypes.data
+
+
+def _pbc_arg(pbc):
+    if pbc is None:
+        return None, None
+    a = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+    return a, a.ctypes.data
+
+
 def _require(t, dtype, shape, name):
     import torch
     if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda or not t.is_contiguous():
@@ -129,8 +145,8 @@ def build_neighbors(pos, cell, pbc, r_list: float, cap: int | None = None, strea
     import torch
     _require(pos, torch.float64, None, "pos")
     n = pos.shape[0]
-    cellh = _host_f64(cell, 9)
-    pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+    cellh, cellp = _cell_arg(cell)
+    pbch, pbcp = _pbc_arg(pbc)
     dev = pos.device
     row_ptr = torch.empty(n + 1, dtype=torch.int64, device=dev)
     cap = int(cap if cap is not None else max(1024, 160 * n))
@@ -139,7 +155,7 @@ def build_neighbors(pos, cell, pbc, r_list: float, cap: int | None = None, strea
         nbr_j = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
         nbr_s = torch.empty(max(cap, 1), dtype=torch.int32, device=dev)
         npairs = ctypes.c_int64(0)
-        rc = lib.build_neighbors(_ptr(pos), n, cellh.ctypes.data, pbch.ctypes.data, float(r_list),
+        rc = lib.build_neighbors(_ptr(pos), n, cellp, pbcp, float(r_list),
                                  _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_s), cap, ctypes.byref(npairs),
                                  _stream(stream))
         if rc == ERR_CAPACITY:
@@ -208,10 +224,10 @@ class Model:
         e_atom = e_atom if e_atom is not None else torch.empty(n, dtype=torch.float64, device=dev)
         forces = forces if forces is not None else torch.empty(n, 3, dtype=torch.float64, device=dev)
         e_total = e_total if e_total is not None else torch.empty(1, dtype=torch.float64, device=dev)
-        cellh = _host_f64(cell, 9)
-        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        cellh, cellp = _cell_arg(cell)
+        pbch, pbcp = _pbc_arg(pbc)
         _check(library().compute_energy_forces(
-            self._h, _ptr(pos), _ptr(species), n, cellh.ctypes.data, pbch.ctypes.data, float(r_c),
+            self._h, _ptr(pos), _ptr(species), n, cellp, pbcp, float(r_c),
             _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
             _ptr(e_total), _stream(stream)))
         return e_atom, forces, e_total
@@ -229,10 +245,10 @@ class Model:
         e_total = torch.empty(1, dtype=torch.float64, device=dev)
         virial = torch.empty(3, 3, dtype=torch.float64, device=dev)
         w_atom = torch.empty(n, 3, 3, dtype=torch.float64, device=dev) if atom_virial else None
-        cellh = _host_f64(cell, 9)
-        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        cellh, cellp = _cell_arg(cell)
+        pbch, pbcp = _pbc_arg(pbc)
         _check(library().compute_energy_forces_virial(
-            self._h, _ptr(pos), _ptr(species), n, cellh.ctypes.data, pbch.ctypes.data, float(r_c),
+            self._h, _ptr(pos), _ptr(species), n, cellp, pbcp, float(r_c),
             _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
             _ptr(e_total), _ptr(virial), _ptr(w_atom), _stream(stream)))
         return e_atom, forces, e_total, virial, w_atom
@@ -270,12 +286,12 @@ class Model:
             e_th = torch.empty(k, dtype=torch.float64, device=dev)
             vir = torch.empty(k, 3, 3, dtype=torch.float64, device=dev) if virial else None
         masses = _host_f64(mass_by_species, self.info["n_types"] + 1)
-        cellh = _host_f64(cell, 9)
-        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        cellh, cellp = _cell_arg(cell)
+        pbch, pbcp = _pbc_arg(pbc)
         nreb = ctypes.c_int64(0)
         _check(library().nvt_step(
-            self._h, _ptr(pos), _ptr(vel), _ptr(species), masses.ctypes.data, n, cellh.ctypes.data,
-            pbch.ctypes.data, float(r_c), float(skin), float(dt_fs), int(nsteps), int(rebuild_every),
+            self._h, _ptr(pos), _ptr(vel), _ptr(species), masses.ctypes.data, n, cellp,
+            pbcp, float(r_c), float(skin), float(dt_fs), int(nsteps), int(rebuild_every),
             float(temperature), float(t_damp_fs), int(chain.shape[0] // 2), _ptr(chain),
             _ptr(e_pot), _ptr(e_kin), _ptr(e_th), _ptr(vir), _ptr(forces), ctypes.byref(nreb),
             _stream(stream)))
@@ -294,12 +310,12 @@ class Model:
         e_pot = e_pot if e_pot is not None else torch.empty(max(nsteps, 1), dtype=torch.float64, device=dev)
         e_kin = e_kin if e_kin is not None else torch.empty(max(nsteps, 1), dtype=torch.float64, device=dev)
         masses = _host_f64(mass_by_species, self.info["n_types"] + 1)
-        cellh = _host_f64(cell, 9)
-        pbch = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        cellh, cellp = _cell_arg(cell)
+        pbch, pbcp = _pbc_arg(pbc)
         nreb = ctypes.c_int64(0)
         _check(library().verlet_step(
-            self._h, _ptr(pos), _ptr(vel), _ptr(species), masses.ctypes.data, n, cellh.ctypes.data,
-            pbch.ctypes.data, float(r_c), float(skin), float(dt_fs), int(nsteps), int(rebuild_every),
+            self._h, _ptr(pos), _ptr(vel), _ptr(species), masses.ctypes.data, n, cellp,
+            pbcp, float(r_c), float(skin), float(dt_fs), int(nsteps), int(rebuild_every),
             _ptr(e_pot), _ptr(e_kin), _ptr(forces), ctypes.byref(nreb), _stream(stream)))
         return e_pot[:nsteps], e_kin[:nsteps], int(nreb.value)
 

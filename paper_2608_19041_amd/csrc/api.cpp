@@ -23,15 +23,75 @@ std::map<int, DevBuf*> g_nb_flags;
 
 constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8;
 
-int check_cell(const double* cell, const int* pbc) {
-  if (!cell || !pbc) {
-    set_error("cell and pbc must not be null");
+// Periodicity of a call.  A null cell is an open system (every axis open);
+// with a cell, pbc[a] = 0 opens axis a, which needs an orthorhombic
+// (diagonal) cell.
+struct CellSpec {
+  double cell[9];
+  bool open[3];
+  bool any_open;
+};
+
+int cell_spec(const double* cell, const int* pbc, CellSpec* cs) {
+  cs->any_open = false;
+  for (int k = 0; k < 9; ++k) cs->cell[k] = (k % 4 == 0) ? 1.0 : 0.0;
+  if (!cell) {
+    for (int a = 0; a < 3; ++a) cs->open[a] = true;
+    cs->any_open = true;
+    return 0;
+  }
+  if (!pbc) {
+    set_error("pbc must not be null when a cell is given");
     return DPA4C_ERR_INVALID_ARG;
   }
-  if (!pbc[0] || !pbc[1] || !pbc[2]) {
-    set_error("the GPU path needs a fully periodic cell");
-    return DPA4C_ERR_UNSUPPORTED;
+  for (int a = 0; a < 3; ++a) {
+    cs->open[a] = pbc[a] == 0;
+    cs->any_open = cs->any_open || cs->open[a];
   }
+  for (int k = 0; k < 9; ++k) cs->cell[k] = cell[k];
+  if (cs->any_open) {
+    for (int a = 0; a < 3; ++a)
+      for (int b = 0; b < 3; ++b)
+        if (a != b && cell[3 * a + b] != 0.0) {
+          set_error("open (non-periodic) axes need an orthorhombic cell");
+          return DPA4C_ERR_UNSUPPORTED;
+        }
+    for (int a = 0; a < 3; ++a)
+      if (cs->open[a]) cs->cell[4 * a] = 1.0;   // replaced by effective_cell
+  }
+  return 0;
+}
+
+// The lattice a build or an evaluation uses.  An open axis gets the virtual
+// length extent + 2 r + 1 A: no image of any atom then lies within r along
+// it, so the periodic machinery yields exactly the open-boundary neighbours
+// (image index 0 on that axis).  The extent (max - min of the positions
+// along the axis) is read from the device when ``pos`` is given; without it
+// the length is a placeholder, which compaction never uses (it multiplies
+// the lattice vector of an open axis by its image index, 0).
+int effective_cell(const CellSpec& cs, const double* pos, int64_t n, double r, NeighborScratch& nb,
+                   hipStream_t st, double out[9]) {
+  for (int k = 0; k < 9; ++k) out[k] = cs.cell[k];
+  if (!cs.any_open) return 0;
+  double ext[3] = {0.0, 0.0, 0.0};
+  if (pos && n > 0) {
+    if (nb.extent.ensure(6 * sizeof(int64_t))) return DPA4C_ERR_HIP;
+    if (!nb.host_extent)
+      DPA4C_HIP_TRY(hipHostMalloc((void**)&nb.host_extent, 6 * sizeof(int64_t), hipHostMallocDefault));
+    int rc = position_extent(pos, n, nb.extent.as<int64_t>(), nb.host_extent, st);
+    if (rc) return rc;
+    for (int a = 0; a < 3; ++a)
+      if (nb.host_extent[3 + a] >= nb.host_extent[a])
+        ext[a] = double(nb.host_extent[3 + a] - nb.host_extent[a]) / kQScale;
+  }
+  for (int a = 0; a < 3; ++a)
+    if (cs.open[a]) {
+      out[4 * a] = ext[a] + 2.0 * r + 1.0;
+      if (out[4 * a] > 1.0e6) {
+        set_error("an open system wider than 1e6 A");
+        return DPA4C_ERR_UNSUPPORTED;
+      }
+    }
   return 0;
 }
 
@@ -281,21 +341,25 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
     set_error("build_neighbors: at most 2^31 - 1 atoms");
     return DPA4C_ERR_INVALID_ARG;
   }
-  int rc = check_cell(cell, pbc);
+  CellSpec cs;
+  int rc = cell_spec(cell, pbc, &cs);
   if (rc) return rc;
   if (!(r_list > 0.0) || !(r_list < 1000.0)) {
     set_error("build_neighbors: r_list must be in (0, 1000) A");
     return DPA4C_ERR_INVALID_ARG;
   }
-  CellGrid g;
-  rc = make_grid(cell, qfix_host(r_list), &g);
-  if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
   int dev = 0;
   DPA4C_HIP_TRY(hipGetDevice(&dev));
   std::lock_guard<std::mutex> lock(g_nb_lock);
   NeighborScratch*& nb = g_nb_scratch[dev];
   if (!nb) nb = new NeighborScratch();
+  double ecell[9];
+  rc = effective_cell(cs, pos, N, r_list, *nb, st, ecell);
+  if (rc) return rc;
+  CellGrid g;
+  rc = make_grid(ecell, qfix_host(r_list), &g);
+  if (rc) return rc;
   DevBuf*& fl = g_nb_flags[dev];
   if (!fl) fl = new DevBuf();
   if (fl->ensure(8 * 8)) return DPA4C_ERR_HIP;
@@ -355,15 +419,19 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
     set_error("compute_energy_forces: r_c differs from the model's cutoff");
     return DPA4C_ERR_INVALID_ARG;
   }
-  int rc = check_cell(cell, pbc);
+  CellSpec cs;
+  int rc = cell_spec(cell, pbc, &cs);
   if (rc) return rc;
   DeviceGuard guard(m->device);
   dpa4c_model* mm = const_cast<dpa4c_model*>(m);
   std::lock_guard<std::mutex> lock(mm->mu_lock);
-  CellGrid g;
-  rc = make_grid(cell, qfix_host(m->r_c), &g);
-  if (rc) return rc;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  double ecell[9];   // open axes: a placeholder length (compaction does not use it)
+  rc = effective_cell(cs, nullptr, 0, m->r_c, mm->ws.nb, st, ecell);
+  if (rc) return rc;
+  CellGrid g;
+  rc = make_grid(ecell, qfix_host(m->r_c), &g);
+  if (rc) return rc;
   rc = ensure_workspace(mm, N, n_pairs);
   if (rc) return rc;
   if (N == 0) {
@@ -445,7 +513,8 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
       set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "masses must be positive and finite");
       return DPA4C_ERR_INVALID_ARG;
     }
-  int rc = check_cell(cell, pbc);
+  CellSpec cs;
+  int rc = cell_spec(cell, pbc, &cs);
   if (rc) return rc;
   DeviceGuard guard(m->device);
   dpa4c_model* mm = const_cast<dpa4c_model*>(m);
@@ -453,10 +522,18 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   Workspace& w = mm->ws;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t rcq = qfix_host(m->r_c), skq = qfix_host(skin);
+  // the grids of the skin list and of the compaction; with open axes they
+  // follow the extent of the atoms and are rebuilt with every list
   CellGrid g_list, g_cut;
-  rc = make_grid(cell, rcq + skq, &g_list);
-  if (rc) return rc;
-  rc = make_grid(cell, rcq, &g_cut);
+  auto make_grids = [&]() -> int {
+    double ec[9];
+    int r = effective_cell(cs, cs.any_open ? pos : nullptr, N, m->r_c + skin, w.nb, st, ec);
+    if (r) return r;
+    r = make_grid(ec, rcq + skq, &g_list);
+    if (r) return r;
+    return make_grid(ec, rcq, &g_cut);
+  };
+  rc = make_grids();
   if (rc) return rc;
 
   // masses on the device
@@ -508,6 +585,10 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   // if needed, fill, reverse index and the positions of the build
   auto initial_build = [&]() -> int {
     int r;
+    if (cs.any_open) {
+      r = make_grids();
+      if (r) return r;
+    }
     {
       StageScope t(m, kStNeighbor, st);
       r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,

@@ -21,6 +21,10 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
 int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
                    hipStream_t st);
+// per-axis min and max of the fixed-point positions Q(x) (finite ones):
+// host6 = [min x, y, z, max x, y, z]; dev6 is device scratch of 6 int64;
+// synchronises ``st``
+int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
 // skin_rev[s] = index of the reverse of skin edge s
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
                     int64_t n, int32_t* skin_rev, hipStream_t st);

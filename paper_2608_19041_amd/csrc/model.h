@@ -56,6 +56,8 @@ struct NeighborScratch {
   DevBuf counts;     // int64 [N]
   DevBuf partials;   // int64 scan partials
   DevBuf host_flag;  // pinned host int64 [4]
+  DevBuf extent;     // int64 [6]: min and max of the fixed-point positions
+  int64_t* host_extent = nullptr;   // pinned [6]
 };
 
 struct Workspace {

@@ -453,6 +453,50 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
   }
 }
 
+// per-axis minimum and maximum of the fixed-point positions (exact integer
+// min/max, so independent of the order of the atomics); out = [min x, y, z,
+// max x, y, z], initialised by the caller to (INT64_MAX, INT64_MIN)
+__global__ void __launch_bounds__(kBlock) extent_kernel(const double* __restrict__ pos, int64_t n,
+                                                        long long* __restrict__ out) {
+  __shared__ long long sh[6][kWavesPerBlock];
+  long long lo[3] = {INT64_MAX, INT64_MAX, INT64_MAX}, hi[3] = {INT64_MIN, INT64_MIN, INT64_MIN};
+  for (int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * kBlock) {
+    for (int a = 0; a < 3; ++a) {
+      const double x = pos[3 * i + a];
+      if (!isfinite(x) || fabs(x) > 1.0e12) continue;   // flagged by the build
+      const long long q = qfix(x);
+      lo[a] = q < lo[a] ? q : lo[a];
+      hi[a] = q > hi[a] ? q : hi[a];
+    }
+  }
+  for (int off = 1; off < kWave; off <<= 1)
+    for (int a = 0; a < 3; ++a) {
+      const long long l = __shfl_xor(lo[a], off), h = __shfl_xor(hi[a], off);
+      lo[a] = l < lo[a] ? l : lo[a];
+      hi[a] = h > hi[a] ? h : hi[a];
+    }
+  const int w = threadIdx.x / kWave;
+  if (lane_id() == 0)
+    for (int a = 0; a < 3; ++a) {
+      sh[a][w] = lo[a];
+      sh[3 + a][w] = hi[a];
+    }
+  __syncthreads();
+  if (threadIdx.x < 6) {
+    const int a = threadIdx.x;
+    long long v = sh[a][0];
+    for (int k = 1; k < kWavesPerBlock; ++k) v = a < 3 ? (sh[a][k] < v ? sh[a][k] : v)
+                                                       : (sh[a][k] > v ? sh[a][k] : v);
+    if (a < 3) atomicMin(out + a, v);
+    else atomicMax(out + a, v);
+  }
+}
+
+__global__ void extent_init_kernel(long long* out) {
+  if (threadIdx.x < 6) out[threadIdx.x] = threadIdx.x < 3 ? INT64_MAX : INT64_MIN;
+}
+
 int waves_grid(int64_t n) {
   int64_t blocks = (n + kWavesPerBlock - 1) / kWavesPerBlock;
   if (blocks > 4096) blocks = 4096;
@@ -602,6 +646,19 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
                        nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j,
                        nbr_shift, cap, flags);
   DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st) {
+  long long* d = reinterpret_cast<long long*>(dev6);
+  hipLaunchKernelGGL(extent_init_kernel, dim3(1), dim3(64), 0, st, d);
+  int64_t blocks = (n + kBlock - 1) / kBlock;
+  if (blocks > 1024) blocks = 1024;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(extent_kernel, dim3(blocks), dim3(kBlock), 0, st, pos, n, d);
+  DPA4C_HIP_TRY(hipGetLastError());
+  DPA4C_HIP_TRY(hipMemcpyAsync(host6, dev6, 6 * sizeof(int64_t), hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipStreamSynchronize(st));
   return 0;
 }
 

@@ -195,7 +195,7 @@ def test_triclinic_dynamics_match_oracle(dev, dp):
         assert np.abs(ek.cpu().numpy() - rek[1:]).max() < E_TOL * s.n
 
 
-def test_singular_and_open_cells_are_rejected(dev, dp):
+def test_singular_and_sheared_open_cells_are_rejected(dev, dp):
     model, _, _ = gpu_model(dp, "small")
     s = synth.fcc_copper(3, 0.05, seed=0)
     pos, species = on_dev(s, dev)
@@ -203,6 +203,9 @@ def test_singular_and_open_cells_are_rejected(dev, dp):
     with pytest.raises(dp.DPA4CError) as ei:
         dp.build_neighbors(pos, flat, s.pbc, 7.0)
     assert ei.value.code == -1
+    # an open axis is supported only with a diagonal cell
+    sheared = s.cell.copy()
+    sheared[1, 0] = 1.0
     with pytest.raises(dp.DPA4CError) as ei:
-        dp.build_neighbors(pos, s.cell, [1, 1, 0], 7.0)
+        dp.build_neighbors(pos, sheared, [1, 1, 0], 7.0)
     assert ei.value.code == -2
