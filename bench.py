@@ -13,6 +13,19 @@ nvt_step step: the same path plus the Nose-Hoover-chain half steps and the
 virial assembled at every step.  Inputs are synthetic (seeded lattice,
 random-init weights) and resident in HBM before timing starts.
 
+    python bench.py --capacity-scan [--scan-material diamond|copper] [--scan-model NAME]
+
+runs the paper's single-GPU capacity protocol instead (Methods, single-GPU
+crystal scans, and the Supplementary Note on the computational-reference
+benchmark): the requested atom count doubles from 128 until the first
+device out-of-memory failure, then three bisections in requested-count space
+refine the bracket; every request becomes a near-cubic conventional-cell
+supercell (edge counts differing by at most one) and runs NVT at 300 K, 1 fs,
+1 A skin, 10 warm-up and 100 timed steps.  Each point runs in a process of
+its own; only an out-of-memory error counts as a capacity boundary, any other
+failure stops the scan.  Prints one JSON line with the largest completed and
+the first failed system and every point's throughput.
+
 Prints one JSON line.  ``stage_ms_per_step`` comes from a short pass with
 HIP events around every stage; the timed region then records events only
 around the launches of the stage that took the most time, whose average
@@ -163,6 +176,177 @@ def cpu_baseline(spec, weights, system, budget_s=15.0):
                       f"the {system.n}-atom workload, {elapsed:.1f} s"}
 
 
+# capacity scans: material -> (atoms per conventional cell, structure builder,
+# default model); the NVT protocol of the paper's scans
+SCAN_MATERIALS = {
+    "diamond": (8, lambda reps: synth.diamond_carbon(reps, 0.03, seed=0), "full_carbon"),
+    "copper": (4, lambda reps: synth.fcc_copper(reps, 0.08, seed=0), "full"),
+}
+SCAN_TEMPERATURE, SCAN_DT, SCAN_SKIN, SCAN_TDAMP, SCAN_CHAIN = 300.0, 1.0, 1.0, 100.0, 3
+OOM_EXIT = 3
+# one call of nvt_step is kept below about a minute, so that a point at the
+# largest sizes prints progress; every call starts with a skin-list build
+SCAN_CALL_SECONDS = 60.0
+
+
+def capacity_point(args):
+    """One scan point in this process: prints progress and a final
+    ``capacity-point {json}`` line; exits OOM_EXIT on device out-of-memory."""
+    import torch
+    import paper_2608_19041_amd as dp
+    global synth
+    import synth
+
+    per_cell, build, default_model = SCAN_MATERIALS[args.scan_material]
+    model_name = args.scan_model or default_model
+    reps = synth.near_cubic_reps(args.capacity_point, per_cell)
+    n_atoms = per_cell * reps[0] * reps[1] * reps[2]
+    rec = {"requested": args.capacity_point, "atoms": n_atoms, "reps": list(reps)}
+    print(f"point: requested {args.capacity_point}, {reps} cells, {n_atoms} atoms", flush=True)
+
+    def oom(msg):
+        rec.update(status="oom", error=msg[-300:])
+        print("capacity-point " + json.dumps(rec), flush=True)
+        sys.exit(OOM_EXIT)
+
+    try:
+        system = build(reps)
+        dev = torch.device("cuda", 0)
+        spec, weights = synth.model_weights(model_name)
+        model = dp.Model(synth.pack_blob(spec, weights))
+        pos = torch.tensor(system.pos, dtype=torch.float64, device=dev)
+        vel = torch.tensor(synth.maxwell_boltzmann(system, SCAN_TEMPERATURE), dtype=torch.float64,
+                           device=dev)
+        species = torch.tensor(system.species, dtype=torch.int32, device=dev)
+        rp, nj, ns, npairs = dp.build_neighbors(pos, system.cell, system.pbc, spec.r_c + SCAN_SKIN)
+        _, forces, _ = model.compute_energy_forces(pos, species, system.cell, system.pbc,
+                                                   spec.r_c, rp, nj, ns, npairs)
+        del rp, nj, ns
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()      # the caller-side list goes back to the device
+        steps, warmup = args.scan_steps, args.scan_warmup
+        kmax = max(steps, warmup, 1)
+        e_pot = torch.empty(kmax, dtype=torch.float64, device=dev)
+        e_kin, e_th = torch.empty_like(e_pot), torch.empty_like(e_pot)
+        vir = torch.empty(kmax, 3, 3, dtype=torch.float64, device=dev)
+        chain = torch.zeros(2 * SCAN_CHAIN, dtype=torch.float64, device=dev)
+
+        def run(n):
+            return model.nvt_step(pos, vel, species, system.mass_by_type, system.cell, system.pbc,
+                                  spec.r_c, SCAN_SKIN, SCAN_DT, n, 0, forces, SCAN_TEMPERATURE,
+                                  SCAN_TDAMP, chain, out=(e_pot, e_kin, e_th, vir))
+
+        t0 = time.perf_counter()
+        run(warmup)
+        torch.cuda.synchronize()
+        per_step = (time.perf_counter() - t0) / max(warmup, 1)
+        print(f"point: {warmup} warm-up steps, {per_step * 1e3:.1f} ms/step", flush=True)
+        per_call = max(1, min(steps, int(SCAN_CALL_SECONDS / max(per_step, 1e-6))))
+        done, calls, rebuilds = 0, 0, 0
+        t0 = time.perf_counter()
+        while done < steps:
+            k = min(per_call, steps - done)
+            rebuilds += run(k)[4]
+            torch.cuda.synchronize()
+            done += k
+            calls += 1
+            if done < steps:
+                print(f"point: {done}/{steps} timed steps", flush=True)
+        wall = time.perf_counter() - t0
+        free_b, total_b = torch.cuda.mem_get_info(dev)
+    except dp.DPA4CError as e:
+        if e.code == dp.ERR_OOM:
+            oom(str(e))
+        raise
+    except torch.OutOfMemoryError as e:
+        oom(str(e))
+    rec.update(status="ok", model=model_name, steps=steps, warmup=warmup,
+               timed_calls=calls, neighbor_rebuilds=rebuilds,
+               ms_per_step=round(wall / steps * 1e3, 4),
+               atom_steps_per_s=round(n_atoms * steps / wall, 1),
+               hbm_in_use_gb=round((total_b - free_b) / 1e9, 3))
+    print("capacity-point " + json.dumps(rec), flush=True)
+
+
+def scan_bracket(point, start: int, bisections: int):
+    """The request sequence of the capacity protocol: ``point(requested)``
+    returns a record with "status" ("ok" or "oom"), "requested" and "atoms".
+    Doubles from ``start`` until the first "oom", then bisects the requested
+    interval between the last "ok" and the first "oom" ``bisections`` times.
+    Returns (points, last ok record or None, first oom record)."""
+    points, req, ok, fail = [], start, None, None
+    while fail is None:
+        r = point(req)
+        points.append(r)
+        if r["status"] == "ok":
+            ok = r
+            req *= 2
+        else:
+            fail = r
+    if ok is None:
+        return points, None, fail
+    for _ in range(bisections):
+        mid = (ok["requested"] + fail["requested"]) // 2
+        r = point(mid)
+        points.append(r)
+        if r["status"] == "ok":
+            ok = r
+        else:
+            fail = r
+    return points, ok, fail
+
+
+def capacity_scan(args):
+    """The scan driver: never touches the GPU itself, runs every point as a
+    child process and streams its output."""
+    import subprocess
+
+    def point(req):
+        cmd = [sys.executable, "-u", os.path.abspath(__file__), "--capacity-point", str(req),
+               "--scan-material", args.scan_material, "--scan-steps", str(args.scan_steps),
+               "--scan-warmup", str(args.scan_warmup)]
+        if args.scan_model:
+            cmd += ["--scan-model", args.scan_model]
+        proc = subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+        rec = None
+        for line in proc.stdout:
+            print(line.rstrip(), flush=True)
+            if line.startswith("capacity-point "):
+                rec = json.loads(line[len("capacity-point "):])
+        rc = proc.wait()
+        if rc == 0 and rec and rec["status"] == "ok":
+            return rec
+        if rc == OOM_EXIT and rec and rec["status"] == "oom":
+            return rec
+        print(f"scan stopped: point {req} failed with exit status {rc} and no out-of-memory "
+              "signature (not a capacity boundary)", file=sys.stderr, flush=True)
+        sys.exit(1)
+
+    points, ok, fail = scan_bracket(point, args.scan_start, args.scan_bisections)
+    if ok is None:
+        print("scan stopped: the first point already ran out of memory", file=sys.stderr)
+        sys.exit(1)
+    done = [p for p in points if p["status"] == "ok"]
+    best = max(done, key=lambda p: p["atom_steps_per_s"])
+    out = {
+        "metric": "capacity: largest completed NVT system on one MI355X",
+        "value": ok["atoms"],
+        "unit": "atoms",
+        "higher_is_better": True,
+        "first_failed": fail["atoms"],
+        "material": args.scan_material,
+        "model": done[-1]["model"],
+        "protocol": {"start": args.scan_start, "bisections": args.scan_bisections,
+                     "warmup": args.scan_warmup, "steps": args.scan_steps,
+                     "temperature_K": SCAN_TEMPERATURE, "dt_fs": SCAN_DT, "skin_A": SCAN_SKIN,
+                     "chain": [SCAN_TDAMP, SCAN_CHAIN]},
+        "saturated_atom_steps_per_s": best["atom_steps_per_s"],
+        "atoms_at_saturated": best["atoms"],
+        "points": points,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,12 +356,27 @@ def main():
     ap.add_argument("--workload", default="fcc4000_full", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--capacity-scan", action="store_true",
+                    help="run the capacity protocol instead of the throughput benchmark")
+    ap.add_argument("--capacity-point", type=int, default=None, help=argparse.SUPPRESS)
+    ap.add_argument("--scan-material", default="diamond", choices=sorted(SCAN_MATERIALS))
+    ap.add_argument("--scan-model", default=None)
+    ap.add_argument("--scan-start", type=int, default=128)
+    ap.add_argument("--scan-bisections", type=int, default=3)
+    ap.add_argument("--scan-steps", type=int, default=100)
+    ap.add_argument("--scan-warmup", type=int, default=10)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(spatial decomposition is designed but not built); run with --gpus 1",
               file=sys.stderr)
         sys.exit(2)
+    if args.capacity_point is not None:
+        capacity_point(args)
+        return
+    if args.capacity_scan:
+        capacity_scan(args)
+        return
 
     import torch
     import paper_2608_19041_amd as dp

@@ -47,6 +47,8 @@ extern "C" {
 #define DPA4C_ERR_HIP (-4)         /* a HIP runtime call failed */
 #define DPA4C_ERR_NONFINITE (-5)   /* a non-finite position was found */
 #define DPA4C_ERR_SKIN (-6)        /* an atom moved more than half the skin, rebuild disabled */
+#define DPA4C_ERR_OOM (-7)         /* device memory exhausted (hipErrorOutOfMemory); nothing was
+                                      computed, the model stays usable with a smaller input */
 
 typedef struct dpa4c_model dpa4c_model;
 

@@ -23,6 +23,7 @@ ERR_CAPACITY = -3
 ERR_HIP = -4
 ERR_NONFINITE = -5
 ERR_SKIN = -6
+ERR_OOM = -7
 
 _lib = None
 

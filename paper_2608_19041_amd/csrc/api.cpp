@@ -75,7 +75,7 @@ int effective_cell(const CellSpec& cs, const double* pos, int64_t n, double r, N
   if (!cs.any_open) return 0;
   double ext[3] = {0.0, 0.0, 0.0};
   if (pos && n > 0) {
-    if (nb.extent.ensure(6 * sizeof(int64_t))) return DPA4C_ERR_HIP;
+    DPA4C_TRY(nb.extent.ensure(6 * sizeof(int64_t)));
     if (!nb.host_extent)
       DPA4C_HIP_TRY(hipHostMalloc((void**)&nb.host_extent, 6 * sizeof(int64_t), hipHostMallocDefault));
     int rc = position_extent(pos, n, nb.extent.as<int64_t>(), nb.host_extent, st);
@@ -177,18 +177,23 @@ void collect_timing(dpa4c_model* m) {
 int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   Workspace& w = m->ws;
   const int64_t nn = n < 1 ? 1 : n, cc = cap < 1 ? 1 : cap;
-  if (w.ecount.ensure(4 * nn) || w.edge.ensure(16 * cc) || w.cidx.ensure(4 * cc) ||
-      w.sidx.ensure(4 * cc) || w.grad.ensure(16 * cc) ||
-      w.skin_rev.ensure(4 * cc) || w.node.ensure(4 * nn * (m->S + 2)) ||
-      w.node_grad.ensure(4 * nn * (m->S + 2)) || w.epart.ensure(8 * (partial_count(nn) + 8)) ||
-      w.flags.ensure(8 * 8) || w.eatom.ensure(8 * nn))
-    return DPA4C_ERR_HIP;
+  DPA4C_TRY(w.ecount.ensure(4 * nn));
+  DPA4C_TRY(w.edge.ensure(16 * cc));
+  DPA4C_TRY(w.cidx.ensure(4 * cc));
+  DPA4C_TRY(w.crev.ensure(4 * cc));
+  DPA4C_TRY(w.skin_rev.ensure(4 * cc));
+  DPA4C_TRY(w.node.ensure(4 * nn * (m->S + 2)));
+  DPA4C_TRY(w.node_grad.ensure(4 * nn * (m->S + 2)));
+  DPA4C_TRY(w.epart.ensure(8 * (partial_count(nn) + 8)));
+  DPA4C_TRY(w.flags.ensure(8 * 8));
+  DPA4C_TRY(w.eatom.ensure(8 * nn));
   return 0;
 }
 
 // the compaction inputs and outputs of a model evaluation
 CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nbr_j,
-                         const int32_t* nbr_shift, int64_t rcq, int64_t cap, Workspace& w) {
+                         const int32_t* nbr_shift, const int32_t* skin_rev, int64_t rcq,
+                         int64_t cap, Workspace& w) {
   CompactArgs ca{};
   ca.pos = pos;
   ca.nbr_j = nbr_j;
@@ -202,8 +207,9 @@ CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nb
   ca.cap = cap;
   ca.ecount = w.ecount.as<int32_t>();
   ca.edge = w.edge.as<float4>();
+  ca.skin_rev = skin_rev;
   ca.cidx = w.cidx.as<int32_t>();
-  ca.sidx = w.sidx.as<int32_t>();
+  ca.crev = w.crev.as<int32_t>();
   return ca;
 }
 
@@ -231,7 +237,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
   int rc;
-  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, rcq, cap, w);
+  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, skin_rev, rcq, cap, w);
   {
     StageScope t(m, kStForward, st);
     rc = launch_forward(m, n, species, row_ptr, ca, w.node.as<float>(), st);
@@ -246,14 +252,15 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStBackward, st);
     rc = launch_backward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                         w.node_grad.as<float>(), w.grad.as<float4>(), st);
+                         w.node_grad.as<float>(), vir ? const_cast<double*>(vir->atom) : nullptr,
+                         st);
     if (rc) return rc;
   }
   {
     StageScope t(m, kStForces, st);
-    rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.grad.as<float4>(),
-                       w.sidx.as<int32_t>(), skin_rev, w.cidx.as<int32_t>(), forces, tail, vir,
-                       st);
+    // the backward kernel has left dE/dr_ij in the edge records
+    rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
+                       w.crev.as<int32_t>(), w.cidx.as<int32_t>(), forces, tail, vir, st);
     if (rc) return rc;
     if (vir && virial) {
       rc = launch_sum_components(vir->part_v, tail_partial_count(n), 9, virial, st);
@@ -307,15 +314,18 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   m->params.release();
   Workspace& w = m->ws;
   DevBuf* bufs[] = {&w.skin_row, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
-                    &w.edge,     &w.cidx,   &w.sidx,       &w.grad,   &w.node,
+                    &w.edge,     &w.cidx,   &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
-                    &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials};
+                    &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials,
+                    &w.virpart,  &w.nvt,     &w.crev,     &w.watom,     &w.nb.extent};
   for (DevBuf* b : bufs) b->release();
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
   if (w.host_flags) hipHostFree(w.host_flags);
   if (w.fold_host) hipHostFree(w.fold_host);
+  if (w.nb.host_extent) hipHostFree(w.nb.host_extent);
+  if (w.nb.host_flag.p) hipHostFree(w.nb.host_flag.p);
   delete m;
 }
 
@@ -362,7 +372,7 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
   if (rc) return rc;
   DevBuf*& fl = g_nb_flags[dev];
   if (!fl) fl = new DevBuf();
-  if (fl->ensure(8 * 8)) return DPA4C_ERR_HIP;
+  DPA4C_TRY(fl->ensure(8 * 8));
   if (!nb->host_flag.p) {
     DPA4C_HIP_TRY(hipHostMalloc(&nb->host_flag.p, 64, hipHostMallocDefault));
     nb->host_flag.bytes = 64;
@@ -411,8 +421,8 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
     set_error("compute_energy_forces: bad pointer or size");
     return DPA4C_ERR_INVALID_ARG;
   }
-  if (N >= (int64_t(1) << 31) || n_pairs >= (int64_t(1) << 31)) {
-    set_error("compute_energy_forces: at most 2^31 - 1 atoms and edges");
+  if (N >= (int64_t(1) << 31)) {
+    set_error("compute_energy_forces: at most 2^31 - 1 atoms");
     return DPA4C_ERR_INVALID_ARG;
   }
   if (std::fabs(r_c - m->r_c) > 1e-12) {
@@ -443,13 +453,15 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
   if (rc) return rc;
   {
     StageScope t(m, kStSkinRev, st);
-    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, mm->ws.skin_rev.as<int32_t>(), st);
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, mm->ws.skin_rev.as<int32_t>(), st);
     if (rc) return rc;
   }
   VirialOut vo{};
   if (virial) {
-    if (mm->ws.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N)))) return DPA4C_ERR_HIP;
-    vo = VirialOut{mm->ws.edge.as<float4>(), mm->ws.virpart.as<double>(), atom_virial};
+    DPA4C_TRY(mm->ws.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N))));
+    if (!atom_virial) DPA4C_TRY(mm->ws.watom.ensure(9 * 8 * size_t(N)));
+    vo.part_v = mm->ws.virpart.as<double>();
+    vo.atom = atom_virial ? atom_virial : mm->ws.watom.as<double>();
   }
   return run_model(m, pos, species, N, g, row_ptr, nbr_j, nbr_shift, n_pairs,
                    mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr,
@@ -538,10 +550,12 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
 
   // masses on the device
   const int np_tail = tail_partial_count(N);
-  if (w.inv_mass.ensure(8 * T1) || w.mass.ensure(8 * T1) || w.flags.ensure(64) ||
-      w.tailpart.ensure(32 * size_t(np_tail)) ||
-      w.skin_row.ensure(8 * (N + 1)) || w.qbuild.ensure(8 * 3 * N))
-    return DPA4C_ERR_HIP;
+  DPA4C_TRY(w.inv_mass.ensure(8 * T1));
+  DPA4C_TRY(w.mass.ensure(8 * T1));
+  DPA4C_TRY(w.flags.ensure(64));
+  DPA4C_TRY(w.tailpart.ensure(32 * size_t(np_tail)));
+  DPA4C_TRY(w.skin_row.ensure(8 * (N + 1)));
+  DPA4C_TRY(w.qbuild.ensure(8 * 3 * N));
   if (!w.host_flags) DPA4C_HIP_TRY(hipHostMalloc((void**)&w.host_flags, 64, hipHostMallocDefault));
   {
     std::vector<double> im(T1);
@@ -564,9 +578,9 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   if (nvt) {
     const int M = nvt->length;
     const size_t S = 2 * size_t(M) + 1;
-    if (w.nvt.ensure(8 * (2 * S + size_t(npk))) ||
-        w.virpart.ensure(2 * 9 * 8 * size_t(np_tail)))
-      return DPA4C_ERR_HIP;
+    DPA4C_TRY(w.nvt.ensure(8 * (2 * S + size_t(npk))));
+    DPA4C_TRY(w.virpart.ensure(2 * 9 * 8 * size_t(np_tail)));
+    DPA4C_TRY(w.watom.ensure(9 * 8 * size_t(N)));
     nvt_state = w.nvt.as<double>();
     nvt_backup = nvt_state + S;
     kin_part = nvt_backup + S;
@@ -602,13 +616,11 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     if (w.host_flags[1]) return flags_to_error(w.host_flags[1]);
     const int64_t need = w.host_flags[0];
     if (need > w.cap || !w.skin_j.p) {
-      int64_t cap = need + need / 2 + 64 * N;
-      if (cap >= (int64_t(1) << 31)) cap = (int64_t(1) << 31) - 1;
-      if (cap < need) {
-        set_error(std::string(nvt ? "nvt_step: " : "verlet_step: ") + "more than 2^31 - 1 neighbour pairs");
-        return DPA4C_ERR_CAPACITY;
-      }
-      if (w.skin_j.ensure(4 * cap) || w.skin_shift.ensure(4 * cap)) return DPA4C_ERR_HIP;
+      // 1/8 headroom over the need (plus 16 per atom) before the next
+      // reallocation; the per-edge workspace is sized with it
+      const int64_t cap = need + need / 8 + 16 * N;
+      DPA4C_TRY(w.skin_j.ensure(4 * size_t(cap)));
+      DPA4C_TRY(w.skin_shift.ensure(4 * size_t(cap)));
       w.cap = cap;
     }
     r = ensure_workspace(mm, N, w.cap);
@@ -618,7 +630,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                        w.skin_shift.as<int32_t>(), w.cap, flags, st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.skin_rev.as<int32_t>(), st);
+                        N, w.cap, w.skin_rev.as<int32_t>(), st);
     if (r) return r;
     return launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
   };
@@ -689,7 +701,9 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                         part_e(step) + np_tail, nvt ? sums_of(-1) : sums_of(prev),
                         kick_next ? 1 : 0, check ? w.qbuild.as<int64_t>() : nullptr, skq, flags,
                         step + 1};
-    const VirialOut vo{w.edge.as<float4>(), nvt ? vir_part(step) : nullptr, nullptr};
+    VirialOut vo{};
+    vo.part_v = nvt ? vir_part(step) : nullptr;
+    vo.atom = w.watom.as<double>();
     return run_model(m, pos, species, N, g_cut, w.skin_row.as<int64_t>(),
                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
                      w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
@@ -721,7 +735,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     rc = finish(0);
     if (rc) return rc;
   }
-  if (w.backup.ensure(3 * 24 * size_t(N))) return DPA4C_ERR_HIP;
+  DPA4C_TRY(w.backup.ensure(3 * 24 * size_t(N)));
   double* bk = w.backup.as<double>();
   const size_t state = 24 * size_t(N);
   const double half_skin = 0.5 * skin;
@@ -855,10 +869,12 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   if (N == 0) return 0;
   // recompute node state and descriptor from the stored compacted edges
   const CompactArgs ca = compact_args(w.last_grid, w.last_pos, w.skin_j_used, w.skin_shift_used,
-                                      qfix_host(m->r_c), w.cap_used, mm->ws);
+                                      w.skin_rev.as<int32_t>(), qfix_host(m->r_c), w.cap_used,
+                                      mm->ws);
   int rc = launch_forward(m, N, w.last_species, w.skin_row_used, ca, w.node.as<float>(), st);
   if (rc) return rc;
-  if (w.desc.ensure(size_t(4) * N * m->D_out) || w.eatom.ensure(size_t(8) * N)) return DPA4C_ERR_HIP;
+  DPA4C_TRY(w.desc.ensure(size_t(4) * N * m->D_out));
+  DPA4C_TRY(w.eatom.ensure(size_t(8) * N));
   rc = launch_atoms(m, N, w.last_species, w.node.as<float>(), w.node_grad.as<float>(),
                     w.eatom.as<double>(), w.desc.as<float>(), st);
   if (rc) return rc;

@@ -189,9 +189,13 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
   if ((threadIdx.x & (kWave - 1)) == 0) record_check(c, flags, step);
 }
 
-// Force assembly.  The reverse of compact slot s is cidx[skin_rev[sidx[s]]]:
-// the compact slot of the reverse skin edge (every edge inside r_c has its
-// reverse inside r_c).  Sixteen lanes per atom, sixteen atoms per group.
+// Force assembly.  Compact slot s of row b = row_ptr[k] holds the gradient
+// g_e with the bits of j in its fourth component; the reverse edge sits in row
+// j at skin position crev[s], so its gradient is at
+// grad[row_ptr[j] + cidx[row_ptr[j] + crev[s]]] (every edge inside r_c has its
+// reverse inside r_c).  All these indices are row-local, so the list length
+// is not limited by 32-bit indexing.  Sixteen lanes per atom, sixteen atoms
+// per group.
 //
 // With TAIL (a velocity-Verlet step) the lane that holds F_k also applies
 // the second half kick v += dt/2 F/m, and the group's potential and kinetic
@@ -201,16 +205,14 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
 // half kick and the drift of the next step (drift_check): both use F_k, so
 // the arithmetic is that of separate kick kernels.
 //
-// With VIR the same lanes form the virial of Eq. (forces) from the atom's own
-// row: W_k = -sum_{e in row k} g_e (x) r_e (r_e from the compact edge
-// records, g_e and r_e promoted to float64), written per atom when asked and
-// summed per group in a fixed order into part_v[group][9].
+// With VIR the per-centre virial terms W_k of Eq. (forces), formed by the
+// backward kernel, are summed per group in a fixed order into
+// part_v[group][9].
 template <bool TAIL, bool VIR>
 __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
                                                         const float4* __restrict__ grad,
-                                                        const int32_t* __restrict__ sidx,
-                                                        const int32_t* __restrict__ skin_rev,
+                                                        const int32_t* __restrict__ crev,
                                                         const int32_t* __restrict__ cidx,
                                                         double* __restrict__ forces, StepTail tl,
                                                         VirialOut vo) {
@@ -247,36 +249,31 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
       }
     }
     double fx = 0.0, fy = 0.0, fz = 0.0;
-    double w[VIR ? 9 : 1];
+    double w[VIR ? 9 : 1];   // the centre's virial term, on the lane that sums it
     for (int c = 0; c < (VIR ? 9 : 1); ++c) w[c] = 0.0;
+    if (VIR && sub == 0 && k < n)
+      for (int c = 0; c < 9; ++c) w[c] = vo.atom[9 * k + c];
     if (k < n) {
       const int64_t b = row_ptr[k], e = b + ecount[k];
       for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
         const float4 g = grad[s];
-        const int32_t sr = skin_rev[sidx[s]];
-        const int32_t c = sr >= 0 ? cidx[sr] : -1;
-        const float4 r = c >= 0 ? grad[c] : g;   // a valid list always has the reverse
+        const int32_t j = __float_as_int(g.w), sr = crev[s];
+        int32_t cr = -1;
+        int64_t jb = 0;
+        if (sr >= 0) {
+          jb = row_ptr[j];
+          cr = cidx[jb + sr];
+        }
+        const float4 r = cr >= 0 ? grad[jb + cr] : g;   // a valid list always has the reverse
         fx += double(g.x) - double(r.x);
         fy += double(g.y) - double(r.y);
         fz += double(g.z) - double(r.z);
-        if (VIR) {
-          const float4 d = vo.edge[s];
-          const double ga[3] = {double(g.x), double(g.y), double(g.z)};
-          const double rb[3] = {double(d.x), double(d.y), double(d.z)};
-#pragma unroll
-          for (int a = 0; a < 3; ++a)
-#pragma unroll
-            for (int bb = 0; bb < 3; ++bb) w[3 * a + bb] -= ga[a] * rb[bb];
-        }
       }
     }
     for (int off = 1; off < kLanesPerAtom; off <<= 1) {
       fx += __shfl_xor(fx, off, kLanesPerAtom);
       fy += __shfl_xor(fy, off, kLanesPerAtom);
       fz += __shfl_xor(fz, off, kLanesPerAtom);
-      if (VIR)
-#pragma unroll
-        for (int c = 0; c < 9; ++c) w[c] += __shfl_xor(w[c], off, kLanesPerAtom);
     }
     double ep = 0.0, ek = 0.0;
     DriftCheck chk{0, 0, 0};
@@ -284,8 +281,6 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
       forces[3 * k] = fx;
       forces[3 * k + 1] = fy;
       forces[3 * k + 2] = fz;
-      if (VIR && vo.atom)
-        for (int c = 0; c < 9; ++c) vo.atom[9 * k + c] = w[c];
       if (TAIL) {
         const double f[3] = {fx, fy, fz};
         double v[3], v2 = 0.0;
@@ -474,26 +469,26 @@ int blocks_for(int64_t n) {
 }  // namespace
 
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
+                  const int32_t* crev, const int32_t* cidx,
                   double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st) {
   int64_t blocks = tail_partial_count(n);
   if (blocks > 8192) blocks = 8192;
   const StepTail tl = tail ? *tail : StepTail{};
   const VirialOut vo = vir ? *vir : VirialOut{};
-  if (vir && (!vir->edge || !vir->part_v)) return DPA4C_ERR_INVALID_ARG;
+  if (vir && (!vir->part_v || !vir->atom)) return DPA4C_ERR_INVALID_ARG;
   const dim3 grid(static_cast<unsigned>(blocks + (tail ? 1 : 0)));
   if (tail && vir)
     hipLaunchKernelGGL((forces_kernel<true, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+                       grad, crev, cidx, forces, tl, vo);
   else if (tail)
     hipLaunchKernelGGL((forces_kernel<true, false>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+                       grad, crev, cidx, forces, tl, vo);
   else if (vir)
     hipLaunchKernelGGL((forces_kernel<false, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, sidx, skin_rev, cidx, forces, tl, vo);
+                       grad, crev, cidx, forces, tl, vo);
   else
     hipLaunchKernelGGL((forces_kernel<false, false>), grid, dim3(kBlock), 0, st, n, row_ptr,
-                       ecount, grad, sidx, skin_rev, cidx, forces, tl, vo);
+                       ecount, grad, crev, cidx, forces, tl, vo);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

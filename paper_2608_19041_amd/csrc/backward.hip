@@ -20,6 +20,11 @@
 // one short polynomial and
 // its gradient instead of every harmonic.  The LPE partial sums of an edge
 // are combined with a fixed DPP butterfly.
+//
+// The gradient of an edge overwrites its record (r_ij, j) in place and keeps
+// j in the fourth component.  With VIR the lane that writes it also adds
+// -g_e (x) r_e (float64) to its group's slot in LDS; the slots are summed in
+// group order into the atom's term W_i of the virial of Eq. (forces).
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
@@ -32,16 +37,22 @@ namespace {
 
 constexpr int kTeam = 256;
 
-template <class P, bool FOLD>
-__global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
+// The virial's extra state would cost the widest degree-three variants one
+// wave per SIMD; those are held to four waves.
+template <class P>
+constexpr int backward_min_waves(bool vir) { return vir && P::L < 4 && P::C0 >= 64 ? 4 : 1; }
+
+template <class P, bool FOLD, bool VIR>
+__global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_kernel(ModelDev md, int64_t n,
                                                          const int32_t* __restrict__ typ,
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
-                                                         const float4* __restrict__ edge,
+                                                         float4* edge,
                                                          const float* __restrict__ node_grad,
-                                                         float4* __restrict__ grad) {
+                                                         double* __restrict__ w_atom) {
   static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
   constexpr int G = kTeam / P::LPE;
+  __shared__ double wv[VIR ? G : 1][9];
   const int tid = threadIdx.x;
   const int grp = tid / P::LPE;
   const int k = tid % P::LPE;
@@ -89,6 +100,8 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
 
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
+    if (VIR && k == 0)
+      for (int c = 0; c < 9; ++c) wv[grp][c] = 0.0;
     const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
     // Two-stage software pipeline, as in the forward kernel: the record of
@@ -224,24 +237,54 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
         const float gx = drho * x + (dux - udu * x) * g.inv_rho;
         const float gy_ = drho * y + (duy - udu * y) * g.inv_rho;
         const float gz = drho * z + (duz - udu * z) * g.inv_rho;
-        grad[b + el] = make_float4(gx, gy_, gz, 0.0f);
+        // in place: this record was read two rounds ago, and only records
+        // of later rounds are requested from here on
+        edge[b + el] = make_float4(gx, gy_, gz, rec.w);
+        if (VIR) {   // LDS adds to the group's own slot: one writer, program order
+          // r_e = rho u from values still live here (the record itself is
+          // not kept across the edge's work, which holds the register count)
+          const float rho = 1.0f / g.inv_rho;
+          const float ga[3] = {gx, gy_, gz};
+          const float rb[3] = {x * rho, y * rho, z * rho};
+#pragma unroll
+          for (int a = 0; a < 3; ++a)
+#pragma unroll
+            for (int c = 0; c < 3; ++c) atomicAdd(&wv[grp][3 * a + c], -(double(ga[a]) * double(rb[c])));
+        }
       }
+    }
+    if (VIR) {
+      __syncthreads();
+      if (tid < 9) {
+        double s = 0.0;
+        for (int q = 0; q < G; ++q) s += wv[q][tid];
+        w_atom[9 * i + tid] = s;
+      }
+      __syncthreads();   // the slots are cleared for the next row
     }
   }
 }
 
 template <class P>
 int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_t* row_ptr,
-           const int32_t* ecount, const float4* edge, const float* node_grad, float4* grad,
+           const int32_t* ecount, float4* edge, const float* node_grad, double* w_atom,
            hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
-  if (m->fold_n > 0)
-    hipLaunchKernelGGL((backward_kernel<P, true>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
-                       m->ws.fidx.as<int32_t>(), row_ptr, ecount, edge, node_grad, grad);
+  const int32_t* typ = m->fold_n > 0 ? m->ws.fidx.as<int32_t>() : species;
+  const dim3 grid(static_cast<unsigned>(blocks)), block(kTeam);
+  if (m->fold_n > 0 && w_atom)
+    hipLaunchKernelGGL((backward_kernel<P, true, true>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
+  else if (m->fold_n > 0)
+    hipLaunchKernelGGL((backward_kernel<P, true, false>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
+  else if (w_atom)
+    hipLaunchKernelGGL((backward_kernel<P, false, true>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
   else
-    hipLaunchKernelGGL((backward_kernel<P, false>), dim3(blocks), dim3(kTeam), 0, st, m->dev(),
-                       n, species, row_ptr, ecount, edge, node_grad, grad);
+    hipLaunchKernelGGL((backward_kernel<P, false, false>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -249,10 +292,10 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 }  // namespace
 
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
-                    const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                    const float* node_grad, float4* grad, hipStream_t st) {
+                    const int64_t* row_ptr, const int32_t* ecount, float4* edge,
+                    const float* node_grad, double* w_atom, hipStream_t st) {
   const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
-    return launch<decltype(p)>(m, n, species, row_ptr, ecount, edge, node_grad, grad, st);
+    return launch<decltype(p)>(m, n, species, row_ptr, ecount, edge, node_grad, w_atom, st);
   });
   if (rc == kNoProfile) {
     set_error("backward: profile not compiled");

@@ -150,13 +150,22 @@ struct ModelDev {
 // ---------------------------------------------------------------------------
 void set_error(const std::string& msg);
 
+// a failed HIP call returns DPA4C_ERR_OOM when the device (or pinned host)
+// memory is exhausted, DPA4C_ERR_HIP otherwise
 #define DPA4C_HIP_TRY(expr)                                                      \
   do {                                                                           \
     hipError_t _e = (expr);                                                      \
     if (_e != hipSuccess) {                                                      \
       ::dpa4c::set_error(std::string(#expr) + ": " + hipGetErrorString(_e));     \
-      return DPA4C_ERR_HIP;                                                      \
+      return _e == hipErrorOutOfMemory ? DPA4C_ERR_OOM : DPA4C_ERR_HIP;          \
     }                                                                            \
+  } while (0)
+
+// returns the (negative) code of a failed library call
+#define DPA4C_TRY(expr)        \
+  do {                         \
+    const int _r = (expr);     \
+    if (_r) return _r;         \
   } while (0)
 
 // packed image shift: ((nx+128) << 16) | ((ny+128) << 8) | (nz+128)

@@ -20,8 +20,10 @@ struct CompactArgs {
   int64_t cap;                // skin-list capacity
   int32_t* ecount;            // [N] out: edges kept per row
   float4* edge;               // [cap] out: (r_ij, bits of j) at the head of each skin row
-  int32_t* cidx;              // [cap] out: compact slot of each skin edge, or -1
-  int32_t* sidx;              // [cap] out: skin edge of each compact slot
+  const int32_t* skin_rev;    // [cap] position of the reverse of each skin edge in row j
+  int32_t* cidx;              // [cap] out: compact slot of each skin edge, or -1, counted
+                              // from the head of its row
+  int32_t* crev;              // [cap] out: skin_rev of the skin edge of each compact slot
 };
 
 __device__ inline int64_t qfix_dev(double x) {
@@ -37,7 +39,9 @@ __device__ inline bool within_q(int64_t dx, int64_t dy, int64_t dz, int64_t rq) 
 
 // Keeps the skin edges of row i inside r_c, in canonical order, and writes
 // their records r_ij = (r_j + sum_b n_b h_b) - r_i (float64 difference stored as
-// float32) to the first slots of the row.  All TEAM threads of the
+// float32) to the first slots of the row, and for every skin edge its
+// row-local compact slot (or -1) and, per compact slot, the reverse position
+// of its skin edge.  All TEAM threads of the
 // workgroup take part; ``wtot`` is LDS scratch of TEAM/64 ints.  Returns
 // the number kept (the same in every thread); the records are visible to
 // the whole workgroup on return.
@@ -89,7 +93,7 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
     }
     if (s < e) {
       if (pred) {
-        const int64_t slot = b + kept + off + pre;
+        const int slot = kept + off + pre;
         double rx, ry, rz;
         if (!a.tric) {
           rx = (a.pos[3 * j] + nx * a.h[0]) - xi;
@@ -100,10 +104,10 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
           ry = (a.pos[3 * j + 1] + (nx * a.h[1] + ny * a.h[4] + nz * a.h[7])) - yi;
           rz = (a.pos[3 * j + 2] + (nx * a.h[2] + ny * a.h[5] + nz * a.h[8])) - zi;
         }
-        a.edge[slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
+        a.edge[b + slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
                                    static_cast<float>(rz), __int_as_float(j));
-        a.sidx[slot] = static_cast<int32_t>(s);
-        a.cidx[s] = static_cast<int32_t>(slot);
+        a.cidx[s] = slot;
+        a.crev[b + slot] = a.skin_rev[s];
       } else {
         a.cidx[s] = -1;
       }

@@ -92,9 +92,9 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
   Workspace& w = m->ws;
   const int T1 = m->n_types + 1;
   if (n <= 0) return 0;
-  if (w.fold_mask.ensure(4 * sizeof(uint32_t)) || w.fidx.ensure(4 * size_t(n)) ||
-      w.fold_map.ensure(4 * size_t(T1)))
-    return DPA4C_ERR_HIP;
+  DPA4C_TRY(w.fold_mask.ensure(4 * sizeof(uint32_t)));
+  DPA4C_TRY(w.fidx.ensure(4 * size_t(n)));
+  DPA4C_TRY(w.fold_map.ensure(4 * size_t(T1)));
   // pinned host words: [0, 16) the presence mask, [64, 64 + 4 T1) the type map
   if (!w.fold_host)
     DPA4C_HIP_TRY(hipHostMalloc((void**)&w.fold_host, 64 + 4 * size_t(T1), hipHostMallocDefault));
@@ -126,7 +126,7 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
         4 * per_pair * size_t(n_used) * size_t(n_used) > kMaxFoldBytes) {
       m->fold_n = 0;   // the separable tables are used
     } else {
-      if (w.ftab.ensure(4 * per_pair * n_used * n_used)) return DPA4C_ERR_HIP;
+      DPA4C_TRY(w.ftab.ensure(4 * per_pair * n_used * n_used));
       int32_t* hmap = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(w.fold_host) + 64);
       std::memcpy(hmap, map.data(), 4 * size_t(T1));
       DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_map.p, hmap, 4 * size_t(T1), hipMemcpyHostToDevice, st));

@@ -25,9 +25,9 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
 // host6 = [min x, y, z, max x, y, z]; dev6 is device scratch of 6 int64;
 // synchronises ``st``
 int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
-// skin_rev[s] = index of the reverse of skin edge s
+// skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int32_t* skin_rev, hipStream_t st);
+                    int64_t n, int64_t cap, int32_t* skin_rev, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
 // index of every atom; synchronises ``st``
@@ -41,22 +41,24 @@ int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
 // desc_out (float [N][D_out]) receives D when not null
 int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
                  float* node_grad, double* e_atom, float* desc_out, hipStream_t st);
+// the gradients dE/dr_ij overwrite the compact edge records in ``edge``
+// (x, y, z = the gradient, w = the bits of j as before); with w_atom
+// ([N][9]) also the virial terms W_i = -sum_e g_e (x) r_e of every centre
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
-                    const int64_t* row_ptr, const int32_t* ecount, const float4* edge,
-                    const float* node_grad, float4* grad, hipStream_t st);
+                    const int64_t* row_ptr, const int32_t* ecount, float4* edge,
+                    const float* node_grad, double* w_atom, hipStream_t st);
 struct StepTail;
-// the virial of Eq. (forces) formed in the force assembly: edge = the compact
-// edge records (r_ij), part_v = [tail_partial_count(n)][9] group partials,
-// atom = [N][9] per-atom terms or null
+// the virial of Eq. (forces): atom = [N][9] per-centre terms W_i written by
+// the backward kernel, part_v = [tail_partial_count(n)][9] group partials of
+// them summed in a fixed order by the force assembly
 struct VirialOut {
-  const float4* edge;
   double* part_v;
-  double* atom;
+  const double* atom;
 };
 // force assembly; with ``tail`` also the velocity-Verlet work of the step
 // that needs only F_k (see StepTail), with ``vir`` the virial
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* sidx, const int32_t* skin_rev, const int32_t* cidx,
+                  const int32_t* crev, const int32_t* cidx,
                   double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st);
 // out[c] = fixed-order sum over p < np of part[ncomp p + c]
 int launch_sum_components(const double* part, int64_t np, int ncomp, double* out, hipStream_t st);

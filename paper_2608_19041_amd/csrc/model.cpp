@@ -21,11 +21,24 @@ int DevBuf::ensure(size_t want) {
     bytes = 0;
   }
   size_t b = want < 256 ? 256 : want;
+  // Large requests keep a reserve of device memory free for the runtime
+  // (kernel scratch, the caller's own allocations): running the device to the
+  // last byte can make a later, unrelated call fail.  Such a request reports
+  // out-of-memory like a failed hipMalloc.
+  constexpr size_t kReserve = size_t(512) << 20;
+  if (b > (size_t(64) << 20)) {
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess && b + kReserve > free_b) {
+      set_error("allocation of " + std::to_string(b) + " bytes would leave less than 512 MiB of " +
+                std::to_string(free_b) + " bytes of device memory free");
+      return DPA4C_ERR_OOM;
+    }
+  }
   hipError_t e = hipMalloc(&p, b);
   if (e != hipSuccess) {
     p = nullptr;
     set_error(std::string("hipMalloc of ") + std::to_string(b) + " bytes: " + hipGetErrorString(e));
-    return DPA4C_ERR_HIP;
+    return e == hipErrorOutOfMemory ? DPA4C_ERR_OOM : DPA4C_ERR_HIP;
   }
   bytes = b;
   return 0;
@@ -483,7 +496,7 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
   for (auto& pc : pieces) total += (pc.bytes + 255) / 256 * 256;
 
   DPA4C_HIP_TRY(hipSetDevice(device));
-  if (m->params.ensure(total)) return DPA4C_ERR_HIP;
+  DPA4C_TRY(m->params.ensure(total));
   std::vector<uint8_t> host(total - pair_bytes, 0);
   size_t off = 0;
   char* base = m->params.as<char>();

@@ -337,7 +337,7 @@ int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
                    hipStream_t st) {
   int64_t nb = (n + kScanTile - 1) / kScanTile;
   if (nb == 0) nb = 1;
-  if (partials.ensure(sizeof(int64_t) * nb)) return DPA4C_ERR_HIP;
+  DPA4C_TRY(partials.ensure(sizeof(int64_t) * nb));
   hipLaunchKernelGGL(scan_partials_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
                      partials.as<int64_t>());
   hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kBlock), 0, st, partials.as<int64_t>(), nb);
@@ -424,22 +424,28 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
 }
 
 // ---------------------------------------------------------------------------
+// A row outside [0, cap] (a malformed caller list) gets no reverse entries and
+// is nobody's reverse row, like the compaction, which keeps nothing of it.
+__device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0 && e >= b && e <= cap; }
+
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                           const int32_t* __restrict__ nbr_j,
                                                           const int32_t* __restrict__ nbr_shift,
-                                                          int32_t* __restrict__ rev) {
+                                                          int64_t cap, int32_t* __restrict__ rev) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
     int64_t b = row_ptr[i], e = row_ptr[i + 1];
+    if (!row_ok(b, e, cap)) continue;
     for (int64_t s = b + lane; s < e; s += kWave) {
       int32_t j = nbr_j[s];
       int64_t want = (int64_t(i) << 24) | int64_t(negate_shift(nbr_shift[s]) & 0xFFFFFF);
-      if (j < 0 || j >= n) {
+      if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) {
         rev[s] = -1;
         continue;
       }
-      int64_t lo = row_ptr[j], hi = row_ptr[j + 1];   // search [lo, hi)
+      const int64_t jb = row_ptr[j];
+      int64_t lo = jb, hi = row_ptr[j + 1];   // search [lo, hi)
       while (lo < hi) {
         int64_t mid = (lo + hi) >> 1;
         int64_t key = (int64_t(nbr_j[mid]) << 24) | int64_t(nbr_shift[mid] & 0xFFFFFF);
@@ -448,7 +454,7 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
       }
       bool found = lo < row_ptr[j + 1] &&
                    ((int64_t(nbr_j[lo]) << 24) | int64_t(nbr_shift[lo] & 0xFFFFFF)) == want;
-      rev[s] = found ? static_cast<int32_t>(lo) : -1;
+      rev[s] = found ? static_cast<int32_t>(lo - jb) : -1;
     }
   }
 }
@@ -582,12 +588,14 @@ int make_grid(const double cell[9], int64_t rq, CellGrid* g) {
 }
 
 int ensure_scratch(NeighborScratch& nb, int64_t n, const CellGrid& g) {
-  if (nb.qpos.ensure(sizeof(int64_t) * 3 * n) || nb.wrap.ensure(sizeof(int32_t) * 3 * n) ||
-      nb.cell_of.ensure(sizeof(int32_t) * n) || nb.cell_cnt.ensure(sizeof(int32_t) * g.ncell) ||
-      nb.cell_start.ensure(sizeof(int32_t) * (g.ncell + 1)) ||
-      nb.cell_fill.ensure(sizeof(int32_t) * g.ncell) || nb.cell_atoms.ensure(sizeof(int32_t) * n) ||
-      nb.counts.ensure(sizeof(int64_t) * n))
-    return DPA4C_ERR_HIP;
+  DPA4C_TRY(nb.qpos.ensure(sizeof(int64_t) * 3 * n));
+  DPA4C_TRY(nb.wrap.ensure(sizeof(int32_t) * 3 * n));
+  DPA4C_TRY(nb.cell_of.ensure(sizeof(int32_t) * n));
+  DPA4C_TRY(nb.cell_cnt.ensure(sizeof(int32_t) * g.ncell));
+  DPA4C_TRY(nb.cell_start.ensure(sizeof(int32_t) * (g.ncell + 1)));
+  DPA4C_TRY(nb.cell_fill.ensure(sizeof(int32_t) * g.ncell));
+  DPA4C_TRY(nb.cell_atoms.ensure(sizeof(int32_t) * n));
+  DPA4C_TRY(nb.counts.ensure(sizeof(int64_t) * n));
   return 0;
 }
 
@@ -663,9 +671,9 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int32_t* skin_rev, hipStream_t st) {
+                    int64_t n, int64_t cap, int32_t* skin_rev, hipStream_t st) {
   hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
-                     nbr_shift, skin_rev);
+                     nbr_shift, cap, skin_rev);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

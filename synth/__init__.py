@@ -100,9 +100,40 @@ def lattice(kind: str, a: float, reps: tuple[int, int, int]) -> tuple[np.ndarray
     return pos, cell
 
 
-def fcc_copper(reps: int, jitter: float, seed: int = 0, a: float = 3.615,
+def _reps3(reps) -> tuple[int, int, int]:
+    if np.ndim(reps) == 0:
+        return (int(reps),) * 3
+    nx, ny, nz = (int(r) for r in reps)
+    return nx, ny, nz
+
+
+def near_cubic_reps(atoms: int, per_cell: int) -> tuple[int, int, int]:
+    """Replication counts whose edges differ by at most one and whose product
+    of cells is nearest to atoms / per_cell (ties go to the smaller one): the
+    supercell rule of the paper's single-GPU capacity scans (Supplementary
+    Note on the computational-reference benchmark), which reproduces the
+    realised sizes of its scan tables, e.g. 2,370,192 = 8 * 66 * 67 * 67
+    for 2,359,296 requested diamond atoms."""
+    want = max(atoms / per_cell, 1.0)
+    k = max(int(round(want ** (1.0 / 3.0))), 1)
+    best = None
+    for base in (k - 1, k, k + 1):
+        if base < 1:
+            continue
+        for up in range(4):   # how many edges are base + 1
+            r = (base,) * (3 - up) + (base + 1,) * up
+            p = r[0] * r[1] * r[2]
+            key = (abs(p - want), p)
+            if best is None or key < best[0]:
+                best = (key, r)
+    return best[1]
+
+
+def fcc_copper(reps, jitter: float, seed: int = 0, a: float = 3.615,
                name: str | None = None) -> System:
-    pos, cell = lattice("fcc", a, (reps, reps, reps))
+    """FCC copper supercell (4-atom conventional cell); ``reps`` is an edge
+    count or a triple of them."""
+    pos, cell = lattice("fcc", a, _reps3(reps))
     rng = np.random.Generator(np.random.PCG64(seed))
     pos = pos + rng.normal(0.0, jitter, size=pos.shape)
     species = np.full(pos.shape[0], 28, dtype=np.int32)       # Cu, Z = 29
@@ -112,11 +143,11 @@ def fcc_copper(reps: int, jitter: float, seed: int = 0, a: float = 3.615,
                    "seed": seed})
 
 
-def diamond_carbon(reps: int, jitter: float, seed: int = 0, a: float = 3.567) -> System:
+def diamond_carbon(reps, jitter: float, seed: int = 0, a: float = 3.567) -> System:
     """Diamond-carbon supercell (8-atom conventional cell, lattice constant
     3.567 A) with Gaussian coordinate perturbations: the structure of the
-    paper's whole-step MD benchmark."""
-    pos, cell = lattice("diamond", a, (reps, reps, reps))
+    paper's whole-step MD benchmark.  ``reps`` is an edge count or a triple."""
+    pos, cell = lattice("diamond", a, _reps3(reps))
     rng = np.random.Generator(np.random.PCG64(seed))
     pos = pos + rng.normal(0.0, jitter, size=pos.shape)
     species = np.full(pos.shape[0], 5, dtype=np.int32)        # C, Z = 6
