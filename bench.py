@@ -86,8 +86,8 @@ def stage_work(name, spec, n_atoms, n_edges):
       per-atom kernel      - matrix cores: forward and input-gradient
         products of the MLP, 2 x 2 (D_out F + (L-1) F^2) flop per atom (the
         readout and its VJP add ~1% VALU work, not counted)
-      forces               - HBM: per edge 16 B gradient, 12 B for the
-        reverse slot (sidx, skin_rev, cidx) and 16 B gathered reverse
+      forces               - HBM: per edge 16 B gradient (with j), 16 B for
+        the reverse slot (crev, row_ptr[j], cidx) and 16 B gathered reverse
         gradient; per atom 12 B row bounds in, 24 B force out, and the
         velocity-Verlet work fused into it: species 4 B, E_i 8 B, velocity
         24 B in and out, position 24 B in and out, build snapshot 24 B
@@ -108,7 +108,7 @@ def stage_work(name, spec, n_atoms, n_edges):
         # per-atom kernel: forward and input-gradient products of the MLP
         return "mfma", 4 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "forces":
-        return "hbm", 44 * n_edges + (36 + 132) * n_atoms, "byte"
+        return "hbm", 48 * n_edges + (36 + 132) * n_atoms, "byte"
     return None
 
 
@@ -296,12 +296,58 @@ def scan_bracket(point, start: int, bisections: int):
     return points, ok, fail
 
 
+class ScanBudget(Exception):
+    """The next point would not finish within the scan's time budget."""
+
+
 def capacity_scan(args):
     """The scan driver: never touches the GPU itself, runs every point as a
-    child process and streams its output."""
+    child process and streams its output.  With ``--scan-log`` every finished
+    point is appended to that file (JSON lines) and points already in it are
+    not run again, so a scan can be split over several invocations;
+    ``--scan-max-seconds`` stops before a point that is predicted not to
+    finish in time (from the wall time per atom of the last point)."""
     import subprocess
 
+    key = {"material": args.scan_material, "model": args.scan_model, "steps": args.scan_steps,
+           "warmup": args.scan_warmup}
+    cache = {}
+    if args.scan_log and os.path.exists(args.scan_log):
+        with open(args.scan_log) as f:
+            for line in f:
+                r = json.loads(line)
+                if r.get("key") == key:
+                    cache[r["requested"]] = r
+    t_start = time.perf_counter()
+    pace = {"s_per_atom": None}
+
+    seen = []
+
     def point(req):
+        seen.append(req)
+        if req in cache:
+            print(f"point {req}: from the scan log ({cache[req]['status']})", flush=True)
+            return cache[req]
+        if args.scan_max_seconds and pace["s_per_atom"] is not None:
+            guess = pace["s_per_atom"] * synth_atoms(req) + 30.0
+            if time.perf_counter() - t_start + guess > args.scan_max_seconds:
+                raise ScanBudget(req)
+        t0 = time.perf_counter()
+        rec = run_point(req)
+        if rec["status"] == "ok":
+            pace["s_per_atom"] = (time.perf_counter() - t0) / rec["atoms"]
+        rec["key"] = key
+        if args.scan_log:
+            with open(args.scan_log, "a") as f:
+                f.write(json.dumps(rec) + "\n")
+        return rec
+
+    def synth_atoms(req):
+        per_cell = SCAN_MATERIALS[args.scan_material][0]
+        r = synth.near_cubic_reps(req, per_cell)
+        return per_cell * r[0] * r[1] * r[2]
+
+    def run_point(req):
         cmd = [sys.executable, "-u", os.path.abspath(__file__), "--capacity-point", str(req),
                "--scan-material", args.scan_material, "--scan-steps", str(args.scan_steps),
                "--scan-warmup", str(args.scan_warmup)]
@@ -322,7 +368,15 @@ def capacity_scan(args):
               "signature (not a capacity boundary)", file=sys.stderr, flush=True)
         sys.exit(1)
 
-    points, ok, fail = scan_bracket(point, args.scan_start, args.scan_bisections)
+    global synth
+    import synth
+    try:
+        points, ok, fail = scan_bracket(point, args.scan_start, args.scan_bisections)
+    except ScanBudget as e:
+        print(json.dumps({"metric": "capacity scan", "status": "incomplete",
+                          "next_request": e.args[0], "log": args.scan_log,
+                          "points_done": len(seen)}), flush=True)
+        return
     if ok is None:
         print("scan stopped: the first point already ran out of memory", file=sys.stderr)
         sys.exit(1)
@@ -365,6 +419,8 @@ def main():
     ap.add_argument("--scan-bisections", type=int, default=3)
     ap.add_argument("--scan-steps", type=int, default=100)
     ap.add_argument("--scan-warmup", type=int, default=10)
+    ap.add_argument("--scan-log", default=None)
+    ap.add_argument("--scan-max-seconds", type=float, default=None)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
