@@ -198,16 +198,17 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
 // per group.
 //
 // With TAIL (a velocity-Verlet step) the lane that holds F_k also applies
-// the second half kick v += dt/2 F/m, and the group's potential and kinetic
-// energies are summed in a fixed order into partial ``group`` of this step;
-// one extra block writes the totals of the previous step (a separate
-// partial buffer).  With kick_next the same lane goes on with the first
-// half kick and the drift of the next step (drift_check): both use F_k, so
-// the arithmetic is that of separate kick kernels.
+// the second half kick v += dt/2 F/m; the group's potential and kinetic
+// energies are summed in a fixed order, and each block adds its groups up in
+// the order it visits them into partial ``blockIdx.x`` of this step (at most
+// kMaxTailBlocks partials, so the step totals are short sums).  One extra
+// block writes the totals of the previous step (a separate partial buffer).
+// With kick_next the same lane goes on with the first half kick and the
+// drift of the next step (drift_check): both use F_k, so the arithmetic is
+// that of separate kick kernels.
 //
 // With VIR the per-centre virial terms W_k of Eq. (forces), formed by the
-// backward kernel, are summed per group in a fixed order into
-// part_v[group][9].
+// backward kernel, are summed the same way into part_v[block][9].
 template <bool TAIL, bool VIR>
 __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
@@ -229,6 +230,7 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
   }
   const int sub = threadIdx.x % kLanesPerAtom, slot = threadIdx.x / kLanesPerAtom;
   const int64_t groups = (n + APG - 1) / APG;
+  double blk_e = 0.0, blk_k = 0.0, blk_v = 0.0;   // the block's partials (threads 0, 0..8)
   for (int64_t grp = blockIdx.x; grp < groups; grp += nblk) {
     const int64_t k = grp * APG + slot;
     // the step's per-atom inputs, requested before the row so that their
@@ -317,19 +319,25 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
           sk += shk[q];
           c = merge(c, shc[q]);
         }
-        tl.part_e[grp] = se;
-        tl.part_k[grp] = sk;
+        blk_e += se;
+        blk_k += sk;
         if (tl.kick_next) record_check(c, tl.flags, tl.next_step);
       }
       if (VIR && threadIdx.x < 9) {
         const int c = threadIdx.x;
         double sv = shv[0][c];
         for (int q = 1; q < APG; ++q) sv += shv[q][c];
-        vo.part_v[9 * grp + c] = sv;
+        blk_v += sv;
       }
       __syncthreads();
     }
   }
+  // one partial per block: its groups in the order it visited them
+  if (TAIL && threadIdx.x == 0) {
+    tl.part_e[blockIdx.x] = blk_e;
+    tl.part_k[blockIdx.x] = blk_k;
+  }
+  if (VIR && threadIdx.x < 9) vo.part_v[9 * blockIdx.x + threadIdx.x] = blk_v;
 }
 
 // ---- Nose-Hoover chain (NVT) ------------------------------------------------
@@ -471,8 +479,7 @@ int blocks_for(int64_t n) {
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
                   const int32_t* crev, const int32_t* cidx,
                   double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st) {
-  int64_t blocks = tail_partial_count(n);
-  if (blocks > 8192) blocks = 8192;
+  const int64_t blocks = tail_partial_count(n);
   const StepTail tl = tail ? *tail : StepTail{};
   const VirialOut vo = vir ? *vir : VirialOut{};
   if (vir && (!vir->part_v || !vir->atom)) return DPA4C_ERR_INVALID_ARG;
@@ -559,9 +566,10 @@ int launch_final_step(StepSums prev, hipStream_t st) {
   return 0;
 }
 
+// blocks of the force assembly, one energy (and virial) partial each
 int tail_partial_count(int64_t n) {
   const int64_t g = (n + kBlock / kLanesPerAtom - 1) / (kBlock / kLanesPerAtom);
-  return static_cast<int>(g < 1 ? 1 : g);
+  return static_cast<int>(g < 1 ? 1 : (g > kMaxTailBlocks ? kMaxTailBlocks : g));
 }
 
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st) {

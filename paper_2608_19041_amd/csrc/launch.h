@@ -25,9 +25,10 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
 // host6 = [min x, y, z, max x, y, z]; dev6 is device scratch of 6 int64;
 // synchronises ``st``
 int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
-// skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1
+// skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1;
+// samples = scratch of (cap + 15) / 16 int64 (every 16th key of the list)
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int32_t* skin_rev, hipStream_t st);
+                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
 // index of every atom; synchronises ``st``
@@ -49,7 +50,7 @@ int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
                     const float* node_grad, double* w_atom, hipStream_t st);
 struct StepTail;
 // the virial of Eq. (forces): atom = [N][9] per-centre terms W_i written by
-// the backward kernel, part_v = [tail_partial_count(n)][9] group partials of
+// the backward kernel, part_v = [tail_partial_count(n)][9] block partials of
 // them summed in a fixed order by the force assembly
 struct VirialOut {
   double* part_v;
@@ -139,6 +140,9 @@ int launch_kinetic(const double* vel, const int32_t* species, const double* mass
 // vel *= *scale
 int launch_scale(double* vel, int64_t n, const double* scale, hipStream_t st);
 int launch_final_step(StepSums prev, hipStream_t st);
+// blocks of the force assembly, each writing one partial of the step's
+// E_pot and E_kin (and virial): min(ceil(n/16), kMaxTailBlocks)
+constexpr int kMaxTailBlocks = 8192;
 int tail_partial_count(int64_t n);
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st);
 // flags[idx] = value

@@ -68,6 +68,7 @@ struct Workspace {
   DevBuf skin_j;        // int32 [cap]
   DevBuf skin_shift;    // int32 [cap]
   DevBuf skin_rev;      // int32 [cap]: position of the reverse edge in row j, or -1
+  DevBuf rev_keys;      // int64 [(cap + 15) / 16]: every 16th key, for the reverse search
   DevBuf qbuild;        // int64 [N][3] fixed-point positions at the last build
   // compacted (r < r_c) edges, stored in the rows of the skin list
   DevBuf ecount;        // int32 [N]

@@ -424,37 +424,84 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
 }
 
 // ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(kBlock) fill_i32_kernel(int32_t* __restrict__ p, int64_t n,
+                                                          int32_t v) {
+  for (int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x; i < n; i += int64_t(gridDim.x) * kBlock)
+    p[i] = v;
+}
+
+// Canonical key of a list entry: rows are sorted by it.
+__device__ inline int64_t entry_key(int32_t j, int32_t sh) {
+  return (int64_t(j) << 24) | int64_t(sh & 0xFFFFFF);
+}
+
+// Every 16th key of the list, samples[g] = key of entry 16 g, so that a
+// search inside a row first narrows to 16 entries through the row's samples
+// (contiguous, one or two cache lines) instead of probing the row itself.
+__global__ void __launch_bounds__(kBlock) sample_keys_kernel(const int64_t* __restrict__ row_ptr,
+                                                             int64_t n,
+                                                             const int32_t* __restrict__ nbr_j,
+                                                             const int32_t* __restrict__ nbr_shift,
+                                                             int64_t cap,
+                                                             int64_t* __restrict__ samples) {
+  int64_t total = row_ptr[n];
+  total = total < cap ? total : cap;
+  const int64_t ng = (total + 15) >> 4;
+  for (int64_t g = blockIdx.x * int64_t(kBlock) + threadIdx.x; g < ng;
+       g += int64_t(gridDim.x) * kBlock)
+    samples[g] = entry_key(nbr_j[16 * g], nbr_shift[16 * g]);
+}
+
 // A row outside [0, cap] (a malformed caller list) gets no reverse entries and
 // is nobody's reverse row, like the compaction, which keeps nothing of it.
 __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0 && e >= b && e <= cap; }
 
+// skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
+// (i, -n), within row j, or -1.  One wave per row i.  A symmetric list pairs
+// every entry with its reverse, so only the canonical entry of a pair, the
+// one with key(j, n) > key(i, -n) (that is j > i, or a periodic self image
+// with the larger shift), searches; it writes both indices.  Entries whose
+// partner is missing (a malformed caller list) keep the -1 of the fill
+// before.  The search narrows [lo, hi) of row j with the samples at positions
+// 16 g inside it, then bisects at most 16 entries.
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                           const int32_t* __restrict__ nbr_j,
                                                           const int32_t* __restrict__ nbr_shift,
-                                                          int64_t cap, int32_t* __restrict__ rev) {
+                                                          int64_t cap,
+                                                          const int64_t* __restrict__ samples,
+                                                          int32_t* __restrict__ rev) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
     int64_t b = row_ptr[i], e = row_ptr[i + 1];
     if (!row_ok(b, e, cap)) continue;
     for (int64_t s = b + lane; s < e; s += kWave) {
-      int32_t j = nbr_j[s];
-      int64_t want = (int64_t(i) << 24) | int64_t(negate_shift(nbr_shift[s]) & 0xFFFFFF);
-      if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) {
-        rev[s] = -1;
-        continue;
+      const int32_t j = nbr_j[s], sh = nbr_shift[s];
+      const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(sh));
+      if (entry_key(j, sh) <= want) continue;   // the partner's row searches
+      if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) continue;
+      const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
+      int64_t lo = jb, hi = je;
+      const int64_t g0 = (jb + 15) >> 4, g1 = (je - 1) >> 4;   // samples inside the row
+      if (je > jb && g0 <= g1) {
+        int64_t l = g0, h = g1 + 1;   // first sample above ``want``
+        while (l < h) {
+          const int64_t m = (l + h) >> 1;
+          if (samples[m] <= want) l = m + 1;
+          else h = m;
+        }
+        if (l > g0) lo = 16 * (l - 1);
+        if (l <= g1) hi = 16 * l;
       }
-      const int64_t jb = row_ptr[j];
-      int64_t lo = jb, hi = row_ptr[j + 1];   // search [lo, hi)
       while (lo < hi) {
-        int64_t mid = (lo + hi) >> 1;
-        int64_t key = (int64_t(nbr_j[mid]) << 24) | int64_t(nbr_shift[mid] & 0xFFFFFF);
-        if (key < want) lo = mid + 1;
+        const int64_t mid = (lo + hi) >> 1;
+        if (entry_key(nbr_j[mid], nbr_shift[mid]) < want) lo = mid + 1;
         else hi = mid;
       }
-      bool found = lo < row_ptr[j + 1] &&
-                   ((int64_t(nbr_j[lo]) << 24) | int64_t(nbr_shift[lo] & 0xFFFFFF)) == want;
-      rev[s] = found ? static_cast<int32_t>(lo - jb) : -1;
+      if (lo < je && entry_key(nbr_j[lo], nbr_shift[lo]) == want) {
+        rev[s] = static_cast<int32_t>(lo - jb);
+        rev[lo] = static_cast<int32_t>(s - b);
+      }
     }
   }
 }
@@ -671,9 +718,16 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int32_t* skin_rev, hipStream_t st) {
+                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, hipStream_t st) {
+  if (n <= 0) return 0;
+  int64_t sb = ((cap + 15) / 16 + kBlock - 1) / kBlock;
+  sb = sb < 1 ? 1 : (sb > 8192 ? 8192 : sb);
+  hipLaunchKernelGGL(sample_keys_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st, row_ptr,
+                     n, nbr_j, nbr_shift, cap, samples);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb * 16 > 8192 ? 8192 : sb * 16)),
+                     dim3(kBlock), 0, st, skin_rev, cap, -1);
   hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
-                     nbr_shift, cap, skin_rev);
+                     nbr_shift, cap, samples, skin_rev);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
