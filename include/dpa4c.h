@@ -209,9 +209,11 @@ int compute_energy_forces_virial(const dpa4c_model* model, const double* pos,
  *                  after each step (eV)
  * n_rebuilds       host int64 out (may be NULL): rebuilds done in this call
  * Synchronises ``stream`` once per batch and at every rebuild (to size the
- * skin list: its capacity grows to 1.5x the pair count plus 64 per atom
- * whenever a build needs more).  The library holds 72 N bytes of device
- * memory for the batch start state.
+ * skin list: its capacity grows to the pair count plus 1/8 and 16 per atom
+ * whenever a build needs more).  The workspace holds 36 bytes per slot of
+ * that capacity, 72 N bytes for the batch start state and the node state;
+ * an allocation that would leave less than 512 MiB of device memory free
+ * returns DPA4C_ERR_OOM.
  */
 int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_t* species,
                 const double* mass_by_species, int64_t N, const double cell[9], const int pbc[3],
