@@ -190,7 +190,11 @@ int compute_energy_forces_virial(const dpa4c_model* model, const double* pos,
  * workspace.  It is rebuilt at the first step of a call, every
  * ``rebuild_every`` steps when that is > 0, and at every step where some
  * atom has moved by more than skin/2 since the last build (fixed-point
- * check on the device).  The steps between builds run in batches that the
+ * check on the device).  With rebuild_every == 0, a periodic cell and the
+ * list of the model's previous call still in place (same N, cell and
+ * radius, and no compute_energy_forces call since), the first step is
+ * checked like any other instead of rebuilt: results do not depend on which
+ * valid list is used, so a run split over several calls equals one call.  The steps between builds run in batches that the
  * host checks after the fact: a batch that contains such a step is rolled
  * back to its saved start (positions, velocities, forces), the steps before
  * the violation are replayed and the violating step rebuilds, so the

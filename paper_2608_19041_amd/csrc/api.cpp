@@ -452,6 +452,7 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
   }
   rc = prepare_species(mm, species, N, st);
   if (rc) return rc;
+  mm->ws.list_valid = false;   // the reverse index now describes the caller's list
   {
     StageScope t(m, kStSkinRev, st);
     rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, mm->ws.rev_keys.as<int64_t>(),
@@ -601,6 +602,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   // if needed, fill, reverse index and the positions of the build
   auto initial_build = [&]() -> int {
     int r;
+    w.list_valid = false;
     if (cs.any_open) {
       r = make_grids();
       if (r) return r;
@@ -634,8 +636,22 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
                         N, w.cap, w.rev_keys.as<int64_t>(), w.skin_rev.as<int32_t>(), st);
     if (r) return r;
-    return launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
+    r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
+    if (r) return r;
+    // open axes: the grid follows the atoms, so the list is not carried over
+    w.list_valid = !cs.any_open;
+    w.list_n = N;
+    w.list_rq = rcq + skq;
+    for (int k = 0; k < 9; ++k) w.list_cell[k] = cs.cell[k];
+    return 0;
   };
+  // a displacement-triggered call whose list is still the one of the last
+  // call starts with the displacement check instead of a build: any valid
+  // list gives the same edges in the same order, so the trajectory does not
+  // depend on it
+  bool reuse = rebuild_every == 0 && w.list_valid && w.list_n == N && w.list_rq == rcq + skq &&
+               !cs.any_open;
+  for (int k = 0; reuse && k < 9; ++k) reuse = w.list_cell[k] == cs.cell[k];
 
   int64_t rebuilds = 0;
   // energy partials of step s in buffer s % 2, so that a step can add up
@@ -731,7 +747,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   // steps before v are replayed (bit-identical) and step v rebuilds the
   // list, exactly as a per-step check would.  Forced rebuilds
   // (rebuild_every > 0) start batches of their own.
-  if (nsteps > 0) {
+  if (nsteps > 0 && !reuse) {
     rc = one_step(0, false, true, -1, false, false);
     if (rc) return rc;
     rc = finish(0);
@@ -741,9 +757,11 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   double* bk = w.backup.as<double>();
   const size_t state = 24 * size_t(N);
   const double half_skin = 0.5 * skin;
-  int64_t last_build = 0, batch = 8;
+  // step index of the last build (a carried-over list was built that many
+  // steps before this call's first)
+  int64_t last_build = reuse ? -1 - w.list_steps_since_build : 0, batch = 8;
   double growth = 0.0;   // A per step since the last build, from the last batch
-  for (int64_t s = 1; s < nsteps;) {
+  for (int64_t s = reuse ? 0 : 1; s < nsteps;) {
     if (rebuild_every > 0 && s % rebuild_every == 0) {
       rc = one_step(s, true, true, -1, false, false);
       if (rc) return rc;
@@ -824,6 +842,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
   DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, flags, 64, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
   if (n_rebuilds) *n_rebuilds = rebuilds;
+  if (nsteps > 0) w.list_steps_since_build = nsteps - 1 - last_build;
   return flags_to_error(w.host_flags[0]);
 }
 

@@ -104,6 +104,13 @@ struct Workspace {
   const int32_t* skin_shift_used = nullptr;
   int64_t cap_used = 0;
   CellGrid last_grid{};
+  // the dynamics' skin list as left by the last call (periodic cells only):
+  // valid for a call with the same atom count, cell and list radius (the
+  // displacement check against qbuild decides whether it still covers the
+  // positions); any other use of the reverse-index buffers clears it
+  bool list_valid = false;
+  int64_t list_n = 0, list_rq = 0, list_steps_since_build = 0;
+  double list_cell[9] = {};
   NeighborScratch nb;
 };
 
