@@ -182,7 +182,6 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   DPA4C_TRY(w.cidx.ensure(4 * cc));
   DPA4C_TRY(w.crev.ensure(4 * cc));
   DPA4C_TRY(w.skin_rev.ensure(4 * cc));
-  DPA4C_TRY(w.rev_keys.ensure(8 * ((cc + 15) / 16)));
   DPA4C_TRY(w.node.ensure(4 * nn * (m->S + 2)));
   DPA4C_TRY(w.node_grad.ensure(4 * nn * (m->S + 2)));
   DPA4C_TRY(w.epart.ensure(8 * (partial_count(nn) + 8)));
@@ -320,7 +319,7 @@ void dpa4c_model_destroy(dpa4c_model* m) {
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials,
-                    &w.virpart,  &w.nvt,     &w.crev,     &w.watom,    &w.rev_keys,     &w.nb.extent};
+                    &w.virpart,  &w.nvt,     &w.crev,     &w.watom,     &w.nb.extent};
   for (DevBuf* b : bufs) b->release();
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
   if (w.host_flags) hipHostFree(w.host_flags);
@@ -455,7 +454,9 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
   mm->ws.list_valid = false;   // the reverse index now describes the caller's list
   {
     StageScope t(m, kStSkinRev, st);
-    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, mm->ws.rev_keys.as<int64_t>(),
+    // the reverse search's key samples live in the edge records, which the
+    // forward kernel rewrites before reading them
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, mm->ws.edge.as<int64_t>(),
                          mm->ws.skin_rev.as<int32_t>(), st);
     if (rc) return rc;
   }
@@ -634,7 +635,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                        w.skin_shift.as<int32_t>(), w.cap, flags, st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.rev_keys.as<int64_t>(), w.skin_rev.as<int32_t>(), st);
+                        N, w.cap, w.edge.as<int64_t>(), w.skin_rev.as<int32_t>(), st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
     if (r) return r;

@@ -102,7 +102,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
     const int cnt = ecount[i];
     if (VIR && k == 0)
       for (int c = 0; c < 9; ++c) wv[grp][c] = 0.0;
-    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
+    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * kFoldWords)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
     // Two-stage software pipeline, as in the forward kernel: the record of
     // round r+2 and the neighbour species of round r+1 are requested while
@@ -136,11 +136,11 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j)
-        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * 6);
+        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           float c[6];
-          load6_planar<P::LPE>(ft + jj * P::LPE * 6, k, c);
+          load6_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, md.c45_inv[0], md.c45_inv[1], c);
           const float psi = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
           const float dpsi = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
           a0 += gy0[jj] * psi;

@@ -140,10 +140,16 @@ struct ModelDev {
   const float* cpl;         // [kCouplings]: C123 then C233 (symmetric in m2, m3), or null
   const float* E_ref;       // [T+1]
   // pair-folded tables (fold.hip), used when fold_n > 0:
-  // [fold_n^2 pairs][n_rows][CPL][LPE][6], pair (fa, fb) at fa * fold_n + fb
+  // [fold_n^2 pairs][n_rows][CPL] blocks of 5 LPE words, pair (fa, fb) at
+  // fa * fold_n + fb; c45_inv = the inverse scales of the fp16 c4 and c5
   const float* ftab;
   int fold_n;
+  float c45_inv[2];
 };
+
+// Words per channel of a folded table: c0..c3 as float32, c4 and c5 as a
+// scaled float16 pair in one word.
+constexpr int kFoldWords = 5;
 
 // ---------------------------------------------------------------------------
 // Error handling

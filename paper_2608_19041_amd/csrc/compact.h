@@ -59,6 +59,7 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
     bool pred = false;
     int32_t j = 0;
     int nx = 0, ny = 0, nz = 0;
+    double xj = 0.0, yj = 0.0, zj = 0.0;   // kept for the record (one gather each)
     if (s < e) {
       j = a.nbr_j[s];
       const int32_t sh = a.nbr_shift[s];
@@ -66,8 +67,10 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
       ny = unpack_y(sh);
       nz = unpack_z(sh);
       if (j >= 0 && j < n) {
-        int64_t dx = qfix_dev(a.pos[3 * j]) - qi0, dy = qfix_dev(a.pos[3 * j + 1]) - qi1,
-                dz = qfix_dev(a.pos[3 * j + 2]) - qi2;
+        xj = a.pos[3 * j];
+        yj = a.pos[3 * j + 1];
+        zj = a.pos[3 * j + 2];
+        int64_t dx = qfix_dev(xj) - qi0, dy = qfix_dev(yj) - qi1, dz = qfix_dev(zj) - qi2;
         if (!a.tric) {
           dx += nx * a.qh[0];
           dy += ny * a.qh[4];
@@ -96,13 +99,13 @@ __device__ inline int compact_row(const CompactArgs& a, int64_t n, int64_t i, in
         const int slot = kept + off + pre;
         double rx, ry, rz;
         if (!a.tric) {
-          rx = (a.pos[3 * j] + nx * a.h[0]) - xi;
-          ry = (a.pos[3 * j + 1] + ny * a.h[4]) - yi;
-          rz = (a.pos[3 * j + 2] + nz * a.h[8]) - zi;
+          rx = (xj + nx * a.h[0]) - xi;
+          ry = (yj + ny * a.h[4]) - yi;
+          rz = (zj + nz * a.h[8]) - zi;
         } else {   // (r_j + sum_b n_b h_b) - r_i
-          rx = (a.pos[3 * j] + (nx * a.h[0] + ny * a.h[3] + nz * a.h[6])) - xi;
-          ry = (a.pos[3 * j + 1] + (nx * a.h[1] + ny * a.h[4] + nz * a.h[7])) - yi;
-          rz = (a.pos[3 * j + 2] + (nx * a.h[2] + ny * a.h[5] + nz * a.h[8])) - zi;
+          rx = (xj + (nx * a.h[0] + ny * a.h[3] + nz * a.h[6])) - xi;
+          ry = (yj + (nx * a.h[1] + ny * a.h[4] + nz * a.h[7])) - yi;
+          rz = (zj + (nx * a.h[2] + ny * a.h[5] + nz * a.h[8])) - zi;
         }
         a.edge[b + slot] = make_float4(static_cast<float>(rx), static_cast<float>(ry),
                                    static_cast<float>(rz), __int_as_float(j));

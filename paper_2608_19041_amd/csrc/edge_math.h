@@ -286,4 +286,17 @@ __device__ inline void load6_planar(const float* __restrict__ blk, int k, float*
   c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w; c[4] = b.x; c[5] = b.y;
 }
 
+// the 6 coefficients of lane k from a folded block: [LPE][c0..c3] float32,
+// then [LPE] words holding c4 (low half) and c5 (high half) as float16
+// scaled by 1/inv4 and 1/inv5
+template <int LPE>
+__device__ inline void load6_folded(const float* __restrict__ blk, int k, float inv4, float inv5,
+                                    float* c) {
+  const float4 a = reinterpret_cast<const float4*>(blk)[k];
+  const uint32_t h = reinterpret_cast<const uint32_t*>(blk + 4 * LPE)[k];
+  c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
+  c[4] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu))) * inv4;
+  c[5] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h >> 16))) * inv5;
+}
+
 }  // namespace dpa4c

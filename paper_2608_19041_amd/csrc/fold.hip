@@ -10,6 +10,14 @@
 // Hermite interpolation of the radial table").  Its normalised coefficients
 // are that same linear combination of the tabulated ones.
 //
+// Storage: c0..c3 in float32, c4 and c5 as float16 scaled by fixed powers of
+// two (one per coefficient, from a bound over every pair: |gamma| < 2 and
+// |U| < 1 by their tanh forms, times the largest tabulated c4 or c5).  With
+// the normalised form c_n Delta^n the top two coefficients are orders of
+// magnitude below float32 resolution of the value, so their 2^-11 relative
+// rounding is far below the float32 rounding of the result and of its
+// derivative, and a channel takes 20 bytes instead of 24.
+//
 // For the few species of an MD system the library keeps one such table per
 // ordered pair present; the edge kernels then read one quintic per channel
 // instead of a g quintic, R q quintics and the pair coefficients.  Systems
@@ -61,8 +69,8 @@ struct FoldTypes {
 // one block per (table row, folded pair); thread = channel c
 __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* __restrict__ qtab,
                                   const float* __restrict__ pair, FoldTypes used, int n_used,
-                                  int n_types1, int C0, int R, int LPE, int rows,
-                                  float* __restrict__ ftab) {
+                                  int n_types1, int C0, int R, int LPE, int rows, float scale4,
+                                  float scale5, float* __restrict__ ftab) {
   const int s = blockIdx.x, p = blockIdx.y;
   const int a = used.t[p / n_used], b = used.t[p % n_used];
   const int PW = 2 + R, CPL = C0 / LPE;
@@ -70,14 +78,20 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
     const int k = c % LPE, j = c / LPE;
     const float* pc = pair + ((size_t(a * n_types1 + b) * CPL + j) * LPE + k) * PW;
     const float* g = gtab + ((size_t(s) * CPL + j) * LPE + k) * 6;
-    // coefficient-planar block of slot j: [LPE][c0..c3] then [LPE][c4, c5]
-    float* blk = ftab + ((size_t(p) * rows + s) * CPL + j) * LPE * 6;
+    // coefficient-planar block of slot j: [LPE][c0..c3] then [LPE] words of
+    // (c4, c5) in scaled float16
+    float* blk = ftab + ((size_t(p) * rows + s) * CPL + j) * LPE * kFoldWords;
+    double v[6];
     for (int q = 0; q < 6; ++q) {
-      double v = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
+      v[q] = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
       for (int mu = 0; mu < R; ++mu)
-        v += double(pc[2 + mu]) * double(qtab[(size_t(s) * R + mu) * 6 + q]);
-      blk[q < 4 ? 4 * k + q : 4 * LPE + 2 * k + (q - 4)] = static_cast<float>(v);
+        v[q] += double(pc[2 + mu]) * double(qtab[(size_t(s) * R + mu) * 6 + q]);
     }
+    for (int q = 0; q < 4; ++q) blk[4 * k + q] = static_cast<float>(v[q]);
+    const _Float16 h4 = static_cast<_Float16>(static_cast<float>(v[4] * scale4));
+    const _Float16 h5 = static_cast<_Float16>(static_cast<float>(v[5] * scale5));
+    reinterpret_cast<uint32_t*>(blk + 4 * LPE)[k] =
+        uint32_t(__builtin_bit_cast(uint16_t, h4)) | (uint32_t(__builtin_bit_cast(uint16_t, h5)) << 16);
   }
 }
 
@@ -121,8 +135,8 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
         ++n_used;
       }
     std::memcpy(m->fold_types_mask, mask, sizeof(mask));
-    const size_t per_pair = size_t(m->n_rows) * m->C0 * 6;
-    if (n_used > kMaxFoldTypes ||
+    const size_t per_pair = size_t(m->n_rows) * m->C0 * kFoldWords;
+    if (!m->fold_allowed || n_used > kMaxFoldTypes ||
         4 * per_pair * size_t(n_used) * size_t(n_used) > kMaxFoldBytes) {
       m->fold_n = 0;   // the separable tables are used
     } else {
@@ -132,7 +146,8 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
       DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_map.p, hmap, 4 * size_t(T1), hipMemcpyHostToDevice, st));
       hipLaunchKernelGGL(fold_build_kernel, dim3(m->n_rows, n_used * n_used),
                          dim3(m->C0 < 256 ? m->C0 : 256), 0, st, m->gtab, m->qtab, m->pair, used,
-                         n_used, T1, m->C0, m->R, m->C[1], m->n_rows, w.ftab.as<float>());
+                         n_used, T1, m->C0, m->R, m->C[1], m->n_rows, m->c45_scale[0],
+                         m->c45_scale[1], w.ftab.as<float>());
       DPA4C_HIP_TRY(hipGetLastError());
       m->fold_n = n_used;
     }

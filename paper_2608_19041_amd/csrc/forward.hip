@@ -66,7 +66,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 #pragma unroll
     for (int m = 0; m < (P::L >= 4 ? 9 : 1); ++m) acc4[m] = 0.0f;
     float s0 = 0.0f, s1 = 0.0f;
-    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * 6)
+    const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * kFoldWords)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
     const float w2mask = k < P::C2 ? 1.0f : 0.0f;
     const float w3mask = k == 0 ? 1.0f : 0.0f;
@@ -103,11 +103,11 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       float psi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j)
-        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * 6);
+        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           float c[6];
-          load6_planar<P::LPE>(ft + jj * P::LPE * 6, k, c);
+          load6_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, md.c45_inv[0], md.c45_inv[1], c);
           const float psi = quintic_val(c, tau);
           acc0[jj] += chi * psi;
           if (jj == 0) psi0 = psi;

@@ -68,7 +68,6 @@ struct Workspace {
   DevBuf skin_j;        // int32 [cap]
   DevBuf skin_shift;    // int32 [cap]
   DevBuf skin_rev;      // int32 [cap]: position of the reverse edge in row j, or -1
-  DevBuf rev_keys;      // int64 [(cap + 15) / 16]: every 16th key, for the reverse search
   DevBuf qbuild;        // int64 [N][3] fixed-point positions at the last build
   // compacted (r < r_c) edges, stored in the rows of the skin list
   DevBuf ecount;        // int32 [N]
@@ -91,7 +90,7 @@ struct Workspace {
   DevBuf mass;          // double [T+1]
   int64_t* host_flags = nullptr;          // pinned [8]
   // pair-folded tables of the species present (fold.hip)
-  DevBuf ftab;          // float [fold_n^2][n_rows][C0][6]
+  DevBuf ftab;          // float [fold_n^2][n_rows][C0 * kFoldWords]
   DevBuf fold_map;      // int32 [T+1]: type -> folded index, or -1
   DevBuf fold_mask;     // uint32 [4]: species present in the last call
   DevBuf fidx;          // int32 [N]: folded index of every atom
@@ -159,6 +158,8 @@ struct dpa4c_model {
   std::mutex mu_lock;
   int64_t last_n = 0;
   int fold_n = -1;                  // species with folded tables; 0 = separable path, -1 = unset
+  float c45_scale[2] = {1.0f, 1.0f};   // float16 scales of c4, c5 in the folded tables
+  bool fold_allowed = true;            // the float16 c4, c5 are below float32 rounding
   uint32_t fold_types_mask[4] = {};
 
   dpa4c::ModelDev dev() const;
