@@ -286,6 +286,16 @@ __device__ inline void load6_planar(const float* __restrict__ blk, int k, float*
   c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w; c[4] = b.x; c[5] = b.y;
 }
 
+// lane 0 of every group of W lanes to all lanes of its group
+template <int W>
+__device__ inline float4 group_bcast(float4 v) {
+  v.x = __shfl(v.x, 0, W);
+  v.y = __shfl(v.y, 0, W);
+  v.z = __shfl(v.z, 0, W);
+  v.w = __shfl(v.w, 0, W);
+  return v;
+}
+
 // the 6 coefficients of lane k from a folded block: [LPE][c0..c3] float32,
 // then [LPE] words holding c4 (low half) and c5 (high half) as float16
 // scaled by 1/inv4 and 1/inv5

@@ -75,24 +75,30 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
     // round r+2 and the neighbour species of round r+1 are requested while
     // round r computes, so a round waits only for its table and pair rows.
     // Records are read only inside [0, cnt) of the row.
+    // The lanes of a group share one edge, so only its lane 0 reads the
+    // record and the neighbour type; they reach the other lanes by a group
+    // broadcast when the round uses them (rec_nn and aj_n hold lane 0's
+    // values until then).
     const float4* erow = edge + b;
+    const bool lead = k == 0;
     float4 rec_n = make_float4(0.f, 0.f, 0.f, 0.f), rec_nn = rec_n;
     int aj_n = ai;
     if (cnt > 0) {
-      rec_n = erow[grp < cnt ? grp : 0];
-      aj_n = grp < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
-      if (G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
+      if (lead) rec_n = erow[grp < cnt ? grp : 0];
+      rec_n = group_bcast<P::LPE>(rec_n);
+      aj_n = (lead && grp < cnt) ? type_of(__float_as_int(rec_n.w)) : ai;
+      if (lead && G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
     }
     for (int base = 0; base < cnt; base += G) {
       const int el = base + grp;
       const bool valid = el < cnt;
       const float4 rec = rec_n;
-      const int aj = aj_n;
+      const int aj = __shfl(aj_n, 0, P::LPE);
       if (base + G < cnt) {
         const int el1 = el + G, el2 = el + 2 * G;
-        rec_n = rec_nn;
-        aj_n = el1 < cnt ? type_of(__float_as_int(rec_n.w)) : ai;
-        if (base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
+        rec_n = group_bcast<P::LPE>(rec_nn);
+        aj_n = (lead && el1 < cnt) ? type_of(__float_as_int(rec_n.w)) : ai;
+        if (lead && base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
       }
       const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
       float chi;
