@@ -142,13 +142,24 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j)
+        // power form; the float16 c4, c5 enter through their scaled weights
+        // (one mixed-precision FMA each), and d/drho's 1/Delta is applied
+        // once to the sums
         const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
+        const float e4 = md.c45_inv[0] * t4, e5 = md.c45_inv[1] * t5;
+        const float f4 = md.c45_inv[0] * d3, f5 = md.c45_inv[1] * d4;
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          float c[6];
-          load6_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, md.c45_inv[0], md.c45_inv[1], c);
-          const float psi = c[0] + c[1] * tau + c[2] * t2 + c[3] * t3 + c[4] * t4 + c[5] * t5;
-          const float dpsi = (c[1] + c[2] * d1 + c[3] * d2 + c[4] * d3 + c[5] * d4) * inv_delta;
+          float4 c;
+          uint32_t h;
+          load_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, &c, &h);
+          const float h4 = half_lo(h), h5 = half_hi(h);
+          float psi = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
+          psi = fmaf(h4, e4, psi);
+          psi = fmaf(h5, e5, psi);
+          float dpsi = fmaf(c.w, d2, fmaf(c.z, d1, c.y));
+          dpsi = fmaf(h4, f4, dpsi);
+          dpsi = fmaf(h5, f5, dpsi);
           a0 += gy0[jj] * psi;
           b0 += gy0[jj] * dpsi;
           if (jj == 0) {
@@ -156,6 +167,8 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
             dpsi0 = dpsi;
           }
         }
+        b0 *= inv_delta;
+        dpsi0 *= inv_delta;
       } else {
         float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (P::R > 0) {

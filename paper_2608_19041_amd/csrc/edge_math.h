@@ -296,6 +296,20 @@ __device__ inline float4 group_bcast(float4 v) {
   return v;
 }
 
+// the raw entries of lane k in a folded block: c0..c3 and the word of the
+// scaled float16 pair (c4 low, c5 high)
+template <int LPE>
+__device__ inline void load_folded(const float* __restrict__ blk, int k, float4* c03, uint32_t* h45) {
+  *c03 = reinterpret_cast<const float4*>(blk)[k];
+  *h45 = reinterpret_cast<const uint32_t*>(blk + 4 * LPE)[k];
+}
+__device__ inline float half_lo(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu)));
+}
+__device__ inline float half_hi(uint32_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h >> 16)));
+}
+
 // the 6 coefficients of lane k from a folded block: [LPE][c0..c3] float32,
 // then [LPE] words holding c4 (low half) and c5 (high half) as float16
 // scaled by 1/inv4 and 1/inv5

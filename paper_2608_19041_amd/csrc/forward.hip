@@ -109,12 +109,19 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       float psi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j)
+        // power form with the float16 c4, c5 scaled through their weights
+        // e4 = tau^4 / s4, e5 = tau^5 / s5 (one mixed-precision FMA each)
         const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
+        const float t2 = tau * tau, t3 = t2 * tau;
+        const float e4 = md.c45_inv[0] * (t2 * t2), e5 = md.c45_inv[1] * (t2 * t3);
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          float c[6];
-          load6_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, md.c45_inv[0], md.c45_inv[1], c);
-          const float psi = quintic_val(c, tau);
+          float4 c;
+          uint32_t h;
+          load_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, &c, &h);
+          float psi = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
+          psi = fmaf(half_lo(h), e4, psi);
+          psi = fmaf(half_hi(h), e5, psi);
           acc0[jj] += chi * psi;
           if (jj == 0) psi0 = psi;
         }
