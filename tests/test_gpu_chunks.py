@@ -79,3 +79,30 @@ def test_moved_atoms_between_calls_trigger_a_rebuild(dev, dp):
     assert carried[5] == fresh[5] >= 1
     for a, b in zip(carried[:5], fresh[:5]):
         assert np.array_equal(a, b)
+
+
+def test_chunked_nvt_is_close_to_one_call(dev, dp):
+    """NVT split over calls: a call boundary applies the chain's closing and
+    opening velocity scales one after the other instead of as one product,
+    so the run agrees with a single call to rounding, with the same rebuilds."""
+    s = synth.make_workload("fcc4000_full")[0]
+    model = new_model(dp)
+
+    def nvt(chunks):
+        pos, species, vel, F = start(dp, model, s, dev)
+        chain = torch.zeros(6, dtype=torch.float64, device=dev)
+        eps, nreb = [], 0
+        for k in chunks:
+            ep, ek, eth, _, nr = model.nvt_step(pos, vel, species, s.mass_by_type, s.cell, s.pbc,
+                                                6.0, 0.5, 1.0, k, 0, F, 300.0, 100.0, chain)
+            eps.append((ep + ek + eth).clone())
+            nreb += nr
+        torch.cuda.synchronize()
+        return pos.cpu().numpy(), torch.cat(eps).cpu().numpy(), chain.cpu().numpy(), nreb
+
+    one = nvt([30])
+    many = nvt([10, 10, 10])
+    assert one[3] >= 2 and many[3] == one[3]
+    assert np.abs(one[0] - many[0]).max() < 1e-9
+    assert np.abs(one[1] - many[1]).max() < 1e-7 * s.n
+    assert np.abs(one[2] - many[2]).max() < 1e-9
