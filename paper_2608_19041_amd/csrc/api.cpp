@@ -252,8 +252,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   {
     StageScope t(m, kStBackward, st);
     rc = launch_backward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                         w.node_grad.as<float>(), vir ? const_cast<double*>(vir->atom) : nullptr,
-                         st);
+                         w.node_grad.as<float>(), vir ? vir->atom : nullptr, st);
     if (rc) return rc;
   }
   {

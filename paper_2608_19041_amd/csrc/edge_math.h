@@ -263,27 +263,12 @@ __device__ inline int clamp_type(int a, int n_types1) {
 __device__ inline float quintic_val(const float* c, float t) {
   return c[0] + t * (c[1] + t * (c[2] + t * (c[3] + t * (c[4] + t * c[5]))));
 }
-// value and d/dtau
-__device__ inline void quintic_val_der(const float* c, float t, float* v, float* d) {
-  *v = c[0] + t * (c[1] + t * (c[2] + t * (c[3] + t * (c[4] + t * c[5]))));
-  *d = c[1] + t * (2.0f * c[2] + t * (3.0f * c[3] + t * (4.0f * c[4] + t * (5.0f * c[5]))));
-}
 
 // load 6 floats from an 8-byte aligned address as three float2
 __device__ inline void load6(const float* __restrict__ p, float* c) {
   const float2* q = reinterpret_cast<const float2*>(p);
   float2 a = q[0], b = q[1], d = q[2];
   c[0] = a.x; c[1] = a.y; c[2] = b.x; c[3] = b.y; c[4] = d.x; c[5] = d.y;
-}
-
-// the 6 coefficients of lane k from a coefficient-planar block of LPE
-// lanes: [LPE][c0..c3] then [LPE][c4, c5]; the lanes of one edge read 16-byte
-// and 8-byte words at unit stride, so each request covers whole cache lines
-template <int LPE>
-__device__ inline void load6_planar(const float* __restrict__ blk, int k, float* c) {
-  const float4 a = reinterpret_cast<const float4*>(blk)[k];
-  const float2 b = reinterpret_cast<const float2*>(blk + 4 * LPE)[k];
-  c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w; c[4] = b.x; c[5] = b.y;
 }
 
 // lane 0 of every group of W lanes to all lanes of its group
@@ -308,19 +293,6 @@ __device__ inline float half_lo(uint32_t h) {
 }
 __device__ inline float half_hi(uint32_t h) {
   return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h >> 16)));
-}
-
-// the 6 coefficients of lane k from a folded block: [LPE][c0..c3] float32,
-// then [LPE] words holding c4 (low half) and c5 (high half) as float16
-// scaled by 1/inv4 and 1/inv5
-template <int LPE>
-__device__ inline void load6_folded(const float* __restrict__ blk, int k, float inv4, float inv5,
-                                    float* c) {
-  const float4 a = reinterpret_cast<const float4*>(blk)[k];
-  const uint32_t h = reinterpret_cast<const uint32_t*>(blk + 4 * LPE)[k];
-  c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
-  c[4] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu))) * inv4;
-  c[5] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h >> 16))) * inv5;
 }
 
 }  // namespace dpa4c

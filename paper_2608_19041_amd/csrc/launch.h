@@ -54,7 +54,7 @@ struct StepTail;
 // them summed in a fixed order by the force assembly
 struct VirialOut {
   double* part_v;
-  const double* atom;
+  double* atom;
 };
 // force assembly; with ``tail`` also the velocity-Verlet work of the step
 // that needs only F_k (see StepTail), with ``vir`` the virial
