@@ -122,14 +122,24 @@ STAGE_KERNELS = {
 
 
 def kernel_source_hash(stage):
-    """sha256 over the kernel's .hip file and every header it can include."""
+    """sha256 over the kernel's .hip file and every file it includes with
+    #include "..." (followed transitively), in a fixed order."""
     import hashlib
+    import re
     csrc = os.path.join(HERE, "paper_2608_19041_amd", "csrc")
-    files = [STAGE_KERNELS[stage][1]] + sorted(f for f in os.listdir(csrc) if f.endswith(".h"))
+    todo, seen = [os.path.join(csrc, STAGE_KERNELS[stage][1])], []
+    while todo:
+        f = os.path.normpath(todo.pop())
+        if f in seen:
+            continue
+        seen.append(f)
+        with open(f) as fh:
+            for inc in re.findall(r'^#include "([^"]+)"', fh.read(), re.M):
+                todo.append(os.path.join(os.path.dirname(f), inc))
     h = hashlib.sha256()
-    for f in files:
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+    for f in sorted(seen):
+        with open(f, "rb") as fh:
+            h.update(os.path.relpath(f, HERE).encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
