@@ -19,6 +19,7 @@ pytestmark = pytest.mark.gpu
 
 E_TOL = 1e-5
 W_TOL = 2e-4
+F_TOL = 1e-4
 
 
 @pytest.fixture(scope="module")
@@ -235,3 +236,30 @@ def test_diamond_nvt_matches_oracle(dev, dp):
     assert np.abs(eth.cpu().numpy() - reth[1:]).max() < E_TOL * s.n
     _, _, ref_vir, _ = oracle.energy_forces(rpos, s.species, s.cell, s.pbc, virial=True)
     assert np.abs(vir[-1].cpu().numpy() - ref_vir).max() < E_TOL * s.n
+
+
+def test_diamond1m_sampled_full_size(dev, dp):
+    """The 1,000,000-atom diamond-carbon workload of the NVT benchmark at full
+    size, carbon-calibrated full model: E_i and the per-centre virial terms W_i
+    of sampled centres and the forces of sampled atoms, each against the
+    oracle evaluated on exactly the centres it needs; the total virial is
+    symmetric (rotation invariance) to the energy tolerance."""
+    model, oracle, _ = gpu_model(dp, "full_carbon")
+    s = synth.make_workload("diamond1m_nvt_full")[0]
+    pos, species = on_dev(s, dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 7.0)
+    ea, F, et, vir, w = model.compute_energy_forces_virial(pos, species, s.cell, s.pbc, 6.0, rp,
+                                                           nj, ns, e, atom_virial=True)
+    torch.cuda.synchronize()
+    ea, F, vir, w = ea.cpu().numpy(), F.cpu().numpy(), vir.cpu().numpy(), w.cpu().numpy()
+    del rp, nj, ns
+    rng = np.random.Generator(np.random.PCG64(23))
+    ks = np.unique(np.concatenate([[0, s.n - 1], rng.choice(s.n, 1, replace=False)])).astype(np.int64)
+    _, ej, _ = onb.neighbor_list(s.pos, s.cell, s.pbc, 6.0, centres=ks)
+    centres = np.unique(np.concatenate([ks, ej]))
+    ref_e, ref_f, _, ref_w = oracle.energy_forces(s.pos, s.species, s.cell, s.pbc,
+                                                  centres=centres, virial=True)
+    assert np.abs(ea[centres] - ref_e).max() < E_TOL
+    assert np.abs(w[centres] - ref_w).max() < W_TOL
+    assert np.abs(F[ks] - ref_f[ks]).max() < F_TOL
+    assert np.abs(vir - vir.T).max() < E_TOL * s.n
