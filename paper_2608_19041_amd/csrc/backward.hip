@@ -22,11 +22,9 @@
 // are combined with a fixed DPP butterfly.
 //
 // The gradient of an edge overwrites its record (r_ij, j) in place and keeps
-// j in the fourth component.  With w_atom the lane that writes it also adds
+// j in the fourth component.  With VIR the lane that writes it also adds
 // -g_e (x) r_e (float64) to its group's slot in LDS; the slots are summed in
-// group order into the atom's term W_i of the virial of Eq. (forces).  The
-// virial is a run-time switch of one kernel, so the gradients are the same
-// instructions, and the same bits, with and without it.
+// group order into the atom's term W_i of the virial of Eq. (forces).
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
@@ -42,10 +40,10 @@ constexpr int kTeam = 256;
 // The virial's extra state would cost the widest degree-three variants one
 // wave per SIMD; those are held to four waves.
 template <class P>
-constexpr int backward_min_waves() { return P::L < 4 && P::C0 >= 64 ? 4 : 1; }
+constexpr int backward_min_waves(bool vir) { return vir && P::L < 4 && P::C0 >= 64 ? 4 : 1; }
 
-template <class P, bool FOLD>
-__global__ void __launch_bounds__(kTeam, backward_min_waves<P>()) backward_kernel(ModelDev md, int64_t n,
+template <class P, bool FOLD, bool VIR>
+__global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_kernel(ModelDev md, int64_t n,
                                                          const int32_t* __restrict__ typ,
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
@@ -54,8 +52,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>()) backward_kerne
                                                          double* __restrict__ w_atom) {
   static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
   constexpr int G = kTeam / P::LPE;
-  __shared__ double wv[G][9];
-  const bool vir = w_atom != nullptr;
+  __shared__ double wv[VIR ? G : 1][9];
   const int tid = threadIdx.x;
   const int grp = tid / P::LPE;
   const int k = tid % P::LPE;
@@ -103,7 +100,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>()) backward_kerne
 
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
-    if (vir && k == 0)
+    if (VIR && k == 0)
       for (int c = 0; c < 9; ++c) wv[grp][c] = 0.0;
     const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * kFoldWords)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
@@ -262,7 +259,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>()) backward_kerne
         // in place: this record was read two rounds ago, and only records
         // of later rounds are requested from here on
         edge[b + el] = make_float4(gx, gy_, gz, rec.w);
-        if (vir) {   // LDS adds to the group's own slot: one writer, program order
+        if (VIR) {   // LDS adds to the group's own slot: one writer, program order
           // r_e = rho u from values still live here (the record itself is
           // not kept across the edge's work, which holds the register count)
           const float rho = 1.0f / g.inv_rho;
@@ -275,7 +272,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>()) backward_kerne
         }
       }
     }
-    if (vir) {
+    if (VIR) {
       __syncthreads();
       if (tid < 9) {
         double s = 0.0;
@@ -295,12 +292,18 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
   if (blocks < 1) return 0;
   const int32_t* typ = m->fold_n > 0 ? m->ws.fidx.as<int32_t>() : species;
   const dim3 grid(static_cast<unsigned>(blocks)), block(kTeam);
-  if (m->fold_n > 0)
-    hipLaunchKernelGGL((backward_kernel<P, true>), grid, block, 0, st, m->dev(), n, typ, row_ptr,
-                       ecount, edge, node_grad, w_atom);
+  if (m->fold_n > 0 && w_atom)
+    hipLaunchKernelGGL((backward_kernel<P, true, true>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
+  else if (m->fold_n > 0)
+    hipLaunchKernelGGL((backward_kernel<P, true, false>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
+  else if (w_atom)
+    hipLaunchKernelGGL((backward_kernel<P, false, true>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
   else
-    hipLaunchKernelGGL((backward_kernel<P, false>), grid, block, 0, st, m->dev(), n, typ, row_ptr,
-                       ecount, edge, node_grad, w_atom);
+    hipLaunchKernelGGL((backward_kernel<P, false, false>), grid, block, 0, st, m->dev(), n, typ,
+                       row_ptr, ecount, edge, node_grad, w_atom);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

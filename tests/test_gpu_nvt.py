@@ -90,6 +90,34 @@ def test_virial_config2_full_size(dev, dp):
     assert np.abs(vir - vir.T).max() < E_TOL * s.n
 
 
+def eight_species_bcc():
+    """A BCC cell of eight species, more than the library folds into per-pair
+    tables, so the edge kernels take the separable radial table."""
+    s = synth.bcc_hea(3, 0.06, seed=7)
+    types = np.array(sorted(set(s.meta["types"]) | {0, 7, 28}), dtype=np.int32)
+    rng = np.random.Generator(np.random.PCG64(3))
+    s.species = types[rng.integers(0, len(types), size=s.n)].astype(np.int32)
+    return s
+
+
+@pytest.mark.parametrize("name", ["small", "full"])
+@pytest.mark.parametrize("tables", ["folded", "separable"])
+def test_virial_leaves_energies_and_forces_bit_identical(dev, dp, name, tables):
+    """Asking for the virial changes no bit of E_i or F: NVE and NVT evaluate
+    the same gradients (one species: pair-folded tables; eight species: the
+    separable table and the pair cache)."""
+    model, _, _ = gpu_model(dp, name)
+    s = synth.fcc_copper(3, 0.08, seed=3) if tables == "folded" else eight_species_bcc()
+    pos, species = on_dev(s, dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, 7.0)
+    ea, F, et = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
+    ea2, F2, et2, vir, w = model.compute_energy_forces_virial(pos, species, s.cell, s.pbc, 6.0,
+                                                              rp, nj, ns, e, atom_virial=True)
+    torch.cuda.synchronize()
+    assert torch.equal(ea, ea2) and torch.equal(F, F2) and torch.equal(et, et2)
+    assert np.abs(vir.cpu().numpy()).max() > 0.0
+
+
 def start_state(dp, model, s, dev, temperature, list_radius=7.0):
     v0 = synth.maxwell_boltzmann(s, temperature)
     pos, species = on_dev(s, dev)
