@@ -141,33 +141,39 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
-        // one quintic per channel from the table of the pair (a_i, a_j)
+        // one quintic per channel from the table of the pair (a_i, a_j),
         // power form; the float16 c4, c5 enter through their scaled weights
-        // (one mixed-precision FMA each), and d/drho's 1/Delta is applied
-        // once to the sums
+        // (one mixed-precision FMA each).  The weighted sums a0 and b0 only
+        // need the lane's coefficients contracted with dE/dY0 first,
+        // A_p = sum_j Ybar0_j c_pj, and then one quintic in tau and its
+        // derivative; d/drho's 1/Delta is applied once to the sums.
         const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
         const float e4 = md.c45_inv[0] * t4, e5 = md.c45_inv[1] * t5;
         const float f4 = md.c45_inv[0] * d3, f5 = md.c45_inv[1] * d4;
+        float A[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           float4 c;
           uint32_t h;
           load_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, &c, &h);
           const float h4 = half_lo(h), h5 = half_hi(h);
-          float psi = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
-          psi = fmaf(h4, e4, psi);
-          psi = fmaf(h5, e5, psi);
-          float dpsi = fmaf(c.w, d2, fmaf(c.z, d1, c.y));
-          dpsi = fmaf(h4, f4, dpsi);
-          dpsi = fmaf(h5, f5, dpsi);
-          a0 += gy0[jj] * psi;
-          b0 += gy0[jj] * dpsi;
-          if (jj == 0) {
-            psi0 = psi;
-            dpsi0 = dpsi;
+          if (jj == 0) {   // the amplitude of the lane's first channel itself
+            psi0 = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
+            psi0 = fmaf(h4, e4, psi0);
+            psi0 = fmaf(h5, e5, psi0);
+            dpsi0 = fmaf(c.w, d2, fmaf(c.z, d1, c.y));
+            dpsi0 = fmaf(h4, f4, dpsi0);
+            dpsi0 = fmaf(h5, f5, dpsi0);
           }
+          A[0] = fmaf(gy0[jj], c.x, A[0]);
+          A[1] = fmaf(gy0[jj], c.y, A[1]);
+          A[2] = fmaf(gy0[jj], c.z, A[2]);
+          A[3] = fmaf(gy0[jj], c.w, A[3]);
+          A[4] = fmaf(gy0[jj], h4, A[4]);
+          A[5] = fmaf(gy0[jj], h5, A[5]);
         }
-        b0 *= inv_delta;
+        a0 = fmaf(A[5], e5, fmaf(A[4], e4, fmaf(A[3], t3, fmaf(A[2], t2, fmaf(A[1], tau, A[0])))));
+        b0 = fmaf(A[5], f5, fmaf(A[4], f4, fmaf(A[3], d2, fmaf(A[2], d1, A[1])))) * inv_delta;
         dpsi0 *= inv_delta;
       } else {
         float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
