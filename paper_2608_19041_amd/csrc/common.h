@@ -106,7 +106,7 @@ int with_profile(int C0, int L, int R, int F, Fn&& fn) {
 // ---------------------------------------------------------------------------
 constexpr int kMaxTypeRows = 128;        // type-table rows (species + padding) a model may have
 constexpr int kMaxFoldTypes = 5;         // species for which pair-folded tables are built
-constexpr size_t kMaxFoldBytes = size_t(64) << 20;   // and their largest total size
+constexpr size_t kMaxFoldBytes = size_t(256) << 20;  // and their largest total size
 constexpr int kC123 = 3 * 5 * 7;          // dense (1,2,3) coupling, [m1][m2][m3]
 constexpr int kC233 = 5 * 7 * 7;          // dense (2,3,3) coupling
 constexpr int kCouplings = kC123 + kC233;
