@@ -162,6 +162,18 @@ def measured_traffic(stage, workload):
     return float(kv["traffic_bytes_per_dispatch"])
 
 
+def cpu_model():
+    """The host CPU's model name from /proc/cpuinfo (None if unreadable)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(spec, weights, system, budget_s=15.0):
     """The float64 oracle on the host: E and F of a sample of centres."""
     import torch
@@ -180,7 +192,8 @@ def cpu_baseline(spec, weights, system, budget_s=15.0):
         done += len(cs)
         elapsed = time.perf_counter() - t0
     return {"value": done / elapsed, "unit": "atom-steps/s", "cores": torch.get_num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "host_nproc": os.cpu_count(),
+            "host_affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
             "sample": f"float64 torch-CPU oracle: energies and forces of {done} sampled centres "
                       f"(neighbour list, radial network per edge, readout, MLP, autograd) of "
                       f"the {system.n}-atom workload, {elapsed:.1f} s"}
@@ -417,7 +430,7 @@ def main():
     ap.add_argument("--steps", type=int, default=None,
                     help="timed steps (default: the workload's own step count)")
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="fcc4000_full", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--workload", default="fcc1m_full", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--capacity-scan", action="store_true",
