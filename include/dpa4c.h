@@ -155,7 +155,13 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
  * forces   device float64 [N][3] out
  * e_total  device float64 [1] out: sum of E_i (fixed-order two-pass sum)
  * All reductions run in a fixed order without floating-point atomics, so
- * repeated calls give bit-identical results.  Does not synchronise.
+ * repeated calls give bit-identical results.  Synchronises ``stream`` once,
+ * to read the species present and the list's size back.
+ *
+ * The list is checked on the device before anything is written: if
+ * row_ptr[N] exceeds n_pairs, or some entry (i -> j, n) has no reverse
+ * (j -> i, -n) (a list that is not symmetric), the call returns
+ * DPA4C_ERR_INVALID_ARG.
  */
 int compute_energy_forces(const dpa4c_model* model, const double* pos, const int32_t* species,
                           int64_t N, const double cell[9], const int pbc[3], double r_c,

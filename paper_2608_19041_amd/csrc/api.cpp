@@ -136,9 +136,9 @@ struct StageScope {
   hipStream_t st;
   int stage;
   size_t slot = SIZE_MAX;
-  StageScope(const dpa4c_model* mm, int s, hipStream_t stream)
+  StageScope(const dpa4c_model* mm, int s, hipStream_t stream, bool on = true)
       : m(const_cast<dpa4c_model*>(mm)), st(stream), stage(s) {
-    if (!m || !((m->timing.mask >> s) & 1)) return;
+    if (!on || !m || !((m->timing.mask >> s) & 1)) return;
     Timing& t = m->timing;
     if (t.used + 2 > t.pool.size()) {
       size_t grow = t.pool.size() < 256 ? 256 : t.pool.size();
@@ -187,13 +187,33 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   DPA4C_TRY(w.epart.ensure(8 * (partial_count(nn) + 8)));
   DPA4C_TRY(w.flags.ensure(8 * 8));
   DPA4C_TRY(w.eatom.ensure(8 * nn));
+  DPA4C_TRY(w.fidx.ensure(4 * nn));
+  DPA4C_TRY(w.fold_mask.ensure(4 * sizeof(uint32_t)));
+  DPA4C_TRY(w.check.ensure(2 * sizeof(int64_t)));
   return 0;
+}
+
+// the model workspace as the buffers of an evaluation
+EvalBufs ws_bufs(Workspace& w) {
+  EvalBufs b{};
+  b.ecount = w.ecount.as<int32_t>();
+  b.edge = w.edge.as<float4>();
+  b.cidx = w.cidx.as<int32_t>();
+  b.crev = w.crev.as<int32_t>();
+  b.skin_rev = w.skin_rev.as<int32_t>();
+  b.node = w.node.as<float>();
+  b.node_grad = w.node_grad.as<float>();
+  b.epart = w.epart.as<double>();
+  b.fidx = w.fidx.as<int32_t>();
+  b.fold_mask = w.fold_mask.as<uint32_t>();
+  b.check = w.check.as<int64_t>();
+  return b;
 }
 
 // the compaction inputs and outputs of a model evaluation
 CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nbr_j,
                          const int32_t* nbr_shift, const int32_t* skin_rev, int64_t rcq,
-                         int64_t cap, Workspace& w) {
+                         int64_t cap, const EvalBufs& w) {
   CompactArgs ca{};
   ca.pos = pos;
   ca.nbr_j = nbr_j;
@@ -205,11 +225,11 @@ CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nb
   ca.rcq = rcq;
   ca.tric = g.tric;
   ca.cap = cap;
-  ca.ecount = w.ecount.as<int32_t>();
-  ca.edge = w.edge.as<float4>();
+  ca.ecount = w.ecount;
+  ca.edge = w.edge;
   ca.skin_rev = skin_rev;
-  ca.cidx = w.cidx.as<int32_t>();
-  ca.crev = w.crev.as<int32_t>();
+  ca.cidx = w.cidx;
+  ca.crev = w.crev;
   return ca;
 }
 
@@ -224,12 +244,16 @@ struct NvtConfig {
 };
 
 // Everything after the skin list: forward (with the compaction of the skin
-// rows), per-atom kernel, backward, forces and the energy sum.
+// rows), per-atom kernel, backward, forces and the energy sum, on the
+// buffers ``B``; ``fidx`` is the folded index of every atom (null: the
+// separable tables).  ``record``: the buffers are the model's workspace, so
+// the stages may be timed and the inputs are kept for dpa4c_debug_stages.
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
               const CellGrid& g, const int64_t* row_ptr, const int32_t* nbr_j,
               const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
               double* forces, double* e_total, const StepTail* tail, const VirialOut* vir,
-              double* virial, hipStream_t st) {
+              double* virial, const EvalBufs& B, const int32_t* fidx, bool record,
+              hipStream_t st) {
   // e_total == nullptr: the caller sums the energy itself; ``tail``: the
   // velocity-Verlet work fused into the force assembly; ``vir``: the virial
   // partials (and per-atom terms), summed into virial[9] when that is given
@@ -237,29 +261,27 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
   int rc;
-  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, skin_rev, rcq, cap, w);
+  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, skin_rev, rcq, cap, B);
   {
-    StageScope t(m, kStForward, st);
-    rc = launch_forward(m, n, species, row_ptr, ca, w.node.as<float>(), st);
+    StageScope t(m, kStForward, st, record);
+    rc = launch_forward(m, n, species, fidx, row_ptr, ca, B.node, st);
     if (rc) return rc;
   }
   {
-    StageScope t(m, kStAtoms, st);
-    rc = launch_atoms(m, n, species, w.node.as<float>(), w.node_grad.as<float>(), e_atom, nullptr,
-                      st);
+    StageScope t(m, kStAtoms, st, record);
+    rc = launch_atoms(m, n, species, B.node, B.node_grad, e_atom, nullptr, st);
     if (rc) return rc;
   }
   {
-    StageScope t(m, kStBackward, st);
-    rc = launch_backward(m, n, species, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                         w.node_grad.as<float>(), vir ? vir->atom : nullptr, st);
+    StageScope t(m, kStBackward, st, record);
+    rc = launch_backward(m, n, species, fidx, row_ptr, B.ecount, B.edge, B.node_grad,
+                         vir ? vir->atom : nullptr, st);
     if (rc) return rc;
   }
   {
-    StageScope t(m, kStForces, st);
+    StageScope t(m, kStForces, st, record);
     // the backward kernel has left dE/dr_ij in the edge records
-    rc = launch_forces(n, row_ptr, w.ecount.as<int32_t>(), w.edge.as<float4>(),
-                       w.crev.as<int32_t>(), w.cidx.as<int32_t>(), forces, tail, vir, st);
+    rc = launch_forces(n, row_ptr, B.ecount, B.edge, B.crev, B.cidx, forces, tail, vir, st);
     if (rc) return rc;
     if (vir && virial) {
       rc = launch_sum_components(vir->part_v, tail_partial_count(n), 9, virial, st);
@@ -267,11 +289,13 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
     }
   }
   if (e_total) {
-    StageScope t(m, kStEnergy, st);
-    rc = launch_energy(n, e_atom, w.epart.as<double>(), e_total, st);
+    StageScope t(m, kStEnergy, st, record);
+    rc = launch_energy(n, e_atom, B.epart, e_total, st);
   }
+  if (!record) return rc;
   m->last_n = n;
   w.last_species = species;
+  w.last_fidx = fidx;
   w.last_pos = pos;
   w.last_grid = g;
   w.skin_row_used = row_ptr;
@@ -303,7 +327,21 @@ int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model*
     return DPA4C_ERR_INVALID_ARG;
   }
   DeviceGuard guard(device);
-  return create_model(blob, nbytes, device, out);
+  int rc = create_model(blob, nbytes, device, out);
+  if (rc) return rc;
+  // the species buffers every evaluation uses, allocated here so that the
+  // entry point without allocation finds them
+  Workspace& w = (*out)->ws;
+  const size_t T1 = size_t((*out)->n_types) + 1;
+  if (w.fold_map.ensure(4 * T1) != 0 ||
+      hipHostMalloc((void**)&w.fold_host, 64 + 4 * T1, hipHostMallocDefault) != hipSuccess) {
+    w.fold_host = nullptr;
+    set_error("dpa4c_model_create: allocation of the species buffers failed");
+    dpa4c_model_destroy(*out);
+    *out = nullptr;
+    return DPA4C_ERR_HIP;
+  }
+  return 0;
 }
 
 void dpa4c_model_destroy(dpa4c_model* m) {
@@ -316,6 +354,7 @@ void dpa4c_model_destroy(dpa4c_model* m) {
                     &w.edge,     &w.cidx,   &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
+                    &w.check,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials,
                     &w.virpart,  &w.nvt,     &w.crev,     &w.watom,     &w.nb.extent};
@@ -406,14 +445,24 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
 
 }  // extern "C"
 
-namespace {
+namespace dpa4c {
+
+void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[11]) {
+  const size_t nn = n < 1 ? 1 : size_t(n), cc = cap < 1 ? 1 : size_t(cap);
+  auto r256 = [](size_t b) { return (b + 255) / 256 * 256; };
+  const size_t raw[11] = {4 * nn,       16 * cc,      4 * cc,
+                          4 * cc,       4 * cc,       4 * nn * size_t(ns),
+                          4 * nn * size_t(ns),        8 * (size_t(partial_count(int64_t(nn))) + 8),
+                          4 * nn,       4 * sizeof(uint32_t), 2 * sizeof(int64_t)};
+  for (int k = 0; k < 11; ++k) sizes[k] = r256(raw[k]);
+}
 
 // compute_energy_forces with the optional virial (virial == nullptr: none)
-int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* species,
-                       int64_t N, const double cell[9], const int pbc[3], double r_c,
-                       const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                       int64_t n_pairs, double* e_atom, double* forces, double* e_total,
-                       double* virial, double* atom_virial, void* stream) {
+int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* species, int64_t N,
+                       const double cell[9], const int pbc[3], double r_c, const int64_t* row_ptr,
+                       const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
+                       double* e_atom, double* forces, double* e_total, double* virial,
+                       double* atom_virial, const EvalBufs* bufs, void* stream) {
   if (!m || N < 0 || n_pairs < 0 || !row_ptr || !e_total ||
       (N > 0 && (!pos || !species || !e_atom || !forces)) ||
       (n_pairs > 0 && (!nbr_j || !nbr_shift))) {
@@ -428,50 +477,80 @@ int energy_forces_impl(const dpa4c_model* m, const double* pos, const int32_t* s
     set_error("compute_energy_forces: r_c differs from the model's cutoff");
     return DPA4C_ERR_INVALID_ARG;
   }
+  if (bufs && virial) {
+    set_error("compute_energy_forces: no virial on caller-free buffers");
+    return DPA4C_ERR_INVALID_ARG;
+  }
   CellSpec cs;
   int rc = cell_spec(cell, pbc, &cs);
   if (rc) return rc;
   DeviceGuard guard(m->device);
   dpa4c_model* mm = const_cast<dpa4c_model*>(m);
   std::lock_guard<std::mutex> lock(mm->mu_lock);
+  Workspace& w = mm->ws;
   hipStream_t st = static_cast<hipStream_t>(stream);
   double ecell[9];   // open axes: a placeholder length (compaction does not use it)
-  rc = effective_cell(cs, nullptr, 0, m->r_c, mm->ws.nb, st, ecell);
+  rc = effective_cell(cs, nullptr, 0, m->r_c, w.nb, st, ecell);
   if (rc) return rc;
   CellGrid g;
   rc = make_grid(ecell, qfix_host(m->r_c), &g);
   if (rc) return rc;
-  rc = ensure_workspace(mm, N, n_pairs);
-  if (rc) return rc;
-  if (N == 0) {
-    DPA4C_HIP_TRY(hipMemsetAsync(e_total, 0, sizeof(double), st));
-    if (virial) DPA4C_HIP_TRY(hipMemsetAsync(virial, 0, 9 * sizeof(double), st));
-    return 0;
+  const bool own = bufs == nullptr;
+  if (own) {
+    rc = ensure_workspace(mm, N, n_pairs);
+    if (rc) return rc;
   }
-  rc = prepare_species(mm, species, N, st);
-  if (rc) return rc;
-  mm->ws.list_valid = false;   // the reverse index now describes the caller's list
+  const EvalBufs B = own ? ws_bufs(w) : *bufs;
+  if (N == 0) {
+    rc = launch_zero_i64(reinterpret_cast<int64_t*>(e_total), 1, st);
+    if (rc == 0 && virial) rc = launch_zero_i64(reinterpret_cast<int64_t*>(virial), 9, st);
+    return rc;
+  }
+  if (own) w.list_valid = false;   // the reverse index now describes the caller's list
   {
-    StageScope t(m, kStSkinRev, st);
+    StageScope t(m, kStSkinRev, st, own);
     // the reverse search's key samples live in the edge records, which the
     // forward kernel rewrites before reading them
-    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, mm->ws.edge.as<int64_t>(),
-                         mm->ws.skin_rev.as<int32_t>(), st);
+    rc = launch_zero_i64(B.check, 2, st);
     if (rc) return rc;
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, reinterpret_cast<int64_t*>(B.edge),
+                         B.skin_rev, B.check, st);
+    if (rc) return rc;
+  }
+  // the list's size and the pairs found come back with the species mask
+  // (prepare_species synchronises the stream)
+  int64_t* hcheck = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(w.fold_host) + 16);
+  DPA4C_HIP_TRY(hipMemcpyAsync(hcheck, row_ptr + N, sizeof(int64_t), hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipMemcpyAsync(hcheck + 1, B.check, sizeof(int64_t), hipMemcpyDeviceToHost, st));
+  bool use_fold = false;
+  rc = prepare_species(mm, species, N, B.fold_mask, B.fidx, own, &use_fold, st);
+  if (rc) return rc;
+  if (hcheck[0] > n_pairs || hcheck[0] < 0) {
+    set_error("compute_energy_forces: the list holds row_ptr[N] = " + std::to_string(hcheck[0]) +
+              " entries, outside [0, n_pairs = " + std::to_string(n_pairs) + "]");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  if (2 * hcheck[1] != hcheck[0]) {
+    set_error("compute_energy_forces: the neighbour list is not symmetric (" +
+              std::to_string(hcheck[0] - 2 * hcheck[1]) + " of " + std::to_string(hcheck[0]) +
+              " entries have no reverse (j -> i, -n))");
+    return DPA4C_ERR_INVALID_ARG;
   }
   VirialOut vo{};
   if (virial) {
-    DPA4C_TRY(mm->ws.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N))));
-    if (!atom_virial) DPA4C_TRY(mm->ws.watom.ensure(9 * 8 * size_t(N)));
-    vo.part_v = mm->ws.virpart.as<double>();
-    vo.atom = atom_virial ? atom_virial : mm->ws.watom.as<double>();
+    if (own) {
+      DPA4C_TRY(w.virpart.ensure(2 * 9 * 8 * size_t(tail_partial_count(N))));
+      if (!atom_virial) DPA4C_TRY(w.watom.ensure(9 * 8 * size_t(N)));
+    }
+    vo.part_v = w.virpart.as<double>();
+    vo.atom = atom_virial ? atom_virial : w.watom.as<double>();
   }
-  return run_model(m, pos, species, N, g, row_ptr, nbr_j, nbr_shift, n_pairs,
-                   mm->ws.skin_rev.as<int32_t>(), e_atom, forces, e_total, nullptr,
-                   virial ? &vo : nullptr, virial, st);
+  return run_model(m, pos, species, N, g, row_ptr, nbr_j, nbr_shift, n_pairs, B.skin_rev, e_atom,
+                   forces, e_total, nullptr, virial ? &vo : nullptr, virial, B,
+                   use_fold ? B.fidx : nullptr, own, st);
 }
 
-}  // namespace
+}  // namespace dpa4c
 
 extern "C" {
 
@@ -480,8 +559,8 @@ int compute_energy_forces(const dpa4c_model* m, const double* pos, const int32_t
                           const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
                           int64_t n_pairs, double* e_atom, double* forces, double* e_total,
                           void* stream) {
-  return energy_forces_impl(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
-                            e_atom, forces, e_total, nullptr, nullptr, stream);
+  return energy_forces_core(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
+                            e_atom, forces, e_total, nullptr, nullptr, nullptr, stream);
 }
 
 int compute_energy_forces_virial(const dpa4c_model* m, const double* pos,
@@ -494,8 +573,8 @@ int compute_energy_forces_virial(const dpa4c_model* m, const double* pos,
     set_error("compute_energy_forces_virial: null virial");
     return DPA4C_ERR_INVALID_ARG;
   }
-  return energy_forces_impl(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
-                            e_atom, forces, e_total, virial, atom_virial, stream);
+  return energy_forces_core(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
+                            e_atom, forces, e_total, virial, atom_virial, nullptr, stream);
 }
 
 }  // extern "C"
@@ -566,8 +645,13 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     DPA4C_HIP_TRY(hipMemcpyAsync(w.inv_mass.p, im.data(), 8 * T1, hipMemcpyHostToDevice, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(w.mass.p, mass_by_species, 8 * T1, hipMemcpyHostToDevice, st));
   }
-  rc = prepare_species(mm, species, N, st);
+  DPA4C_TRY(w.fidx.ensure(4 * size_t(N)));
+  DPA4C_TRY(w.fold_mask.ensure(4 * sizeof(uint32_t)));
+  bool use_fold = false;
+  rc = prepare_species(mm, species, N, w.fold_mask.as<uint32_t>(), w.fidx.as<int32_t>(), true,
+                       &use_fold, st);
   if (rc) return rc;
+  const int32_t* fidx = use_fold ? w.fidx.as<int32_t>() : nullptr;
   int64_t* flags = w.flags.as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
 
@@ -634,7 +718,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                        w.skin_shift.as<int32_t>(), w.cap, flags, st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.edge.as<int64_t>(), w.skin_rev.as<int32_t>(), st);
+                        N, w.cap, w.edge.as<int64_t>(), w.skin_rev.as<int32_t>(), nullptr, st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
     if (r) return r;
@@ -725,7 +809,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     return run_model(m, pos, species, N, g_cut, w.skin_row.as<int64_t>(),
                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
                      w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
-                     nvt ? &vo : nullptr, nullptr, st);
+                     nvt ? &vo : nullptr, nullptr, ws_bufs(w), fidx, true, st);
   };
   // the end of a batch: the totals of step ``last`` (NVT: its closing chain
   // half step and velocity scaling)
@@ -891,8 +975,9 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   // recompute node state and descriptor from the stored compacted edges
   const CompactArgs ca = compact_args(w.last_grid, w.last_pos, w.skin_j_used, w.skin_shift_used,
                                       w.skin_rev.as<int32_t>(), qfix_host(m->r_c), w.cap_used,
-                                      mm->ws);
-  int rc = launch_forward(m, N, w.last_species, w.skin_row_used, ca, w.node.as<float>(), st);
+                                      ws_bufs(w));
+  int rc = launch_forward(m, N, w.last_species, w.last_fidx, w.skin_row_used, ca,
+                          w.node.as<float>(), st);
   if (rc) return rc;
   DPA4C_TRY(w.desc.ensure(size_t(4) * N * m->D_out));
   DPA4C_TRY(w.eatom.ensure(size_t(8) * N));

@@ -469,6 +469,11 @@ __global__ void set_flag_kernel(int64_t* flags, int idx, int64_t value) {
   if (threadIdx.x == 0) flags[idx] = value;
 }
 
+__global__ void __launch_bounds__(kBlock) zero_i64_kernel(int64_t* __restrict__ p, int64_t n) {
+  for (int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x; i < n; i += int64_t(gridDim.x) * kBlock)
+    p[i] = 0;
+}
+
 int blocks_for(int64_t n) {
   int64_t b = (n + kBlock - 1) / kBlock;
   return static_cast<int>(b < 1 ? 1 : b);
@@ -580,6 +585,14 @@ int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t
 
 int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st) {
   hipLaunchKernelGGL(set_flag_kernel, dim3(1), dim3(64), 0, st, flags, idx, value);
+  DPA4C_HIP_TRY(hipGetLastError());
+  return 0;
+}
+
+int launch_zero_i64(int64_t* p, int64_t n, hipStream_t st) {
+  if (n <= 0) return 0;
+  int b = blocks_for(n);
+  hipLaunchKernelGGL(zero_i64_kernel, dim3(b < 1024 ? b : 1024), dim3(kBlock), 0, st, p, n);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

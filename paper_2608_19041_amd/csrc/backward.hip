@@ -291,17 +291,17 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
 }
 
 template <class P>
-int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_t* row_ptr,
-           const int32_t* ecount, float4* edge, const float* node_grad, double* w_atom,
-           hipStream_t st) {
+int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
+           const int64_t* row_ptr, const int32_t* ecount, float4* edge, const float* node_grad,
+           double* w_atom, hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
-  const int32_t* typ = m->fold_n > 0 ? m->ws.fidx.as<int32_t>() : species;
+  const int32_t* typ = fidx ? fidx : species;
   const dim3 grid(static_cast<unsigned>(blocks)), block(kTeam);
-  if (m->fold_n > 0 && w_atom)
+  if (fidx && w_atom)
     hipLaunchKernelGGL((backward_kernel<P, true, true>), grid, block, 0, st, m->dev(), n, typ,
                        row_ptr, ecount, edge, node_grad, w_atom);
-  else if (m->fold_n > 0)
+  else if (fidx)
     hipLaunchKernelGGL((backward_kernel<P, true, false>), grid, block, 0, st, m->dev(), n, typ,
                        row_ptr, ecount, edge, node_grad, w_atom);
   else if (w_atom)
@@ -316,11 +316,11 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 
 }  // namespace
 
-int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
+int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                     const int64_t* row_ptr, const int32_t* ecount, float4* edge,
                     const float* node_grad, double* w_atom, hipStream_t st) {
   const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
-    return launch<decltype(p)>(m, n, species, row_ptr, ecount, edge, node_grad, w_atom, st);
+    return launch<decltype(p)>(m, n, species, fidx, row_ptr, ecount, edge, node_grad, w_atom, st);
   });
   if (rc == kNoProfile) {
     set_error("backward: profile not compiled");

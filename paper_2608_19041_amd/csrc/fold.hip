@@ -22,9 +22,11 @@
 // ordered pair present; the edge kernels then read one quintic per channel
 // instead of a g quintic, R q quintics and the pair coefficients.  Systems
 // with more than kMaxFoldTypes species, or whose folded tables would exceed
-// kMaxFoldBytes (beyond that the tables fall out of the caches and the
-// separable path is faster: five species at full width need 230 MB), use the
-// separable tables directly.
+// kMaxFoldBytes, use the separable tables directly.  Five species at full
+// width fold into 25 tables of 7.7 MB (192 MB, most of the last-level cache);
+// on the 5-species alloy that measured faster than the separable tables
+// (backward 0.94 -> 0.70 ms at 31,250 atoms), since every edge then reads
+// 20 B per channel from one table instead of 48 B from two.
 #include <hip/hip_runtime.h>
 
 #include <cstring>
@@ -95,6 +97,10 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
   }
 }
 
+__global__ void zero_u32_kernel(uint32_t* p, int n) {
+  if (static_cast<int>(threadIdx.x) < n) p[threadIdx.x] = 0u;
+}
+
 int grid_for(int64_t n) {
   int64_t b = (n + 255) / 256;
   return static_cast<int>(b < 4096 ? (b < 1 ? 1 : b) : 4096);
@@ -102,22 +108,23 @@ int grid_for(int64_t n) {
 
 }  // namespace
 
-int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream_t st) {
+int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, uint32_t* mask_dev,
+                    int32_t* fidx, bool may_alloc, bool* use_fold, hipStream_t st) {
   Workspace& w = m->ws;
   const int T1 = m->n_types + 1;
+  *use_fold = false;
   if (n <= 0) return 0;
-  DPA4C_TRY(w.fold_mask.ensure(4 * sizeof(uint32_t)));
-  DPA4C_TRY(w.fidx.ensure(4 * size_t(n)));
-  DPA4C_TRY(w.fold_map.ensure(4 * size_t(T1)));
-  // pinned host words: [0, 16) the presence mask, [64, 64 + 4 T1) the type map
-  if (!w.fold_host)
-    DPA4C_HIP_TRY(hipHostMalloc((void**)&w.fold_host, 64 + 4 * size_t(T1), hipHostMallocDefault));
-  DPA4C_HIP_TRY(hipMemsetAsync(w.fold_mask.p, 0, 4 * sizeof(uint32_t), st));
-  hipLaunchKernelGGL(presence_kernel, dim3(grid_for(n)), dim3(256), 0, st, species, n, T1,
-                     w.fold_mask.as<uint32_t>());
+  // the type map and the pinned host words ([0, 16) the presence mask,
+  // [64, 64 + 4 T1) the type map) are allocated with the model
+  if (!w.fold_host || !w.fold_map.p) {
+    set_error("prepare_species: the model's species buffers are missing");
+    return DPA4C_ERR_INVALID_ARG;
+  }
+  hipLaunchKernelGGL(zero_u32_kernel, dim3(1), dim3(64), 0, st, mask_dev, 4);
+  hipLaunchKernelGGL(presence_kernel, dim3(grid_for(n)), dim3(256), 0, st, species, n, T1, mask_dev);
   DPA4C_HIP_TRY(hipGetLastError());
-  DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_host, w.fold_mask.p, 4 * sizeof(uint32_t),
-                               hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_host, mask_dev, 4 * sizeof(uint32_t), hipMemcpyDeviceToHost,
+                               st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
   uint32_t mask[4];
   std::memcpy(mask, w.fold_host, sizeof(mask));
@@ -134,13 +141,16 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
         }
         ++n_used;
       }
-    std::memcpy(m->fold_types_mask, mask, sizeof(mask));
     const size_t per_pair = size_t(m->n_rows) * m->C0 * kFoldWords;
-    if (!m->fold_allowed || n_used > kMaxFoldTypes ||
-        4 * per_pair * size_t(n_used) * size_t(n_used) > kMaxFoldBytes) {
+    const size_t need = 4 * per_pair * size_t(n_used) * size_t(n_used);
+    if (!m->fold_allowed || n_used > kMaxFoldTypes || need > kMaxFoldBytes) {
+      std::memcpy(m->fold_types_mask, mask, sizeof(mask));
       m->fold_n = 0;   // the separable tables are used
+    } else if (!may_alloc && need > w.ftab.bytes) {
+      return 0;        // this call only: separable tables, the folded state kept
     } else {
-      DPA4C_TRY(w.ftab.ensure(4 * per_pair * n_used * n_used));
+      DPA4C_TRY(w.ftab.ensure(need));
+      std::memcpy(m->fold_types_mask, mask, sizeof(mask));
       int32_t* hmap = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(w.fold_host) + 64);
       std::memcpy(hmap, map.data(), 4 * size_t(T1));
       DPA4C_HIP_TRY(hipMemcpyAsync(w.fold_map.p, hmap, 4 * size_t(T1), hipMemcpyHostToDevice, st));
@@ -154,8 +164,9 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream
   }
   if (m->fold_n > 0) {
     hipLaunchKernelGGL(fold_index_kernel, dim3(grid_for(n)), dim3(256), 0, st, species, n, T1,
-                       w.fold_map.as<int32_t>(), w.fidx.as<int32_t>());
+                       w.fold_map.as<int32_t>(), fidx);
     DPA4C_HIP_TRY(hipGetLastError());
+    *use_fold = true;
   }
   return 0;
 }

@@ -242,13 +242,13 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 }
 
 template <class P>
-int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_t* row_ptr,
-           const CompactArgs& ca, float* node, hipStream_t st) {
+int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
+           const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st) {
   int64_t blocks = n < 16384 ? n : 16384;
   if (blocks < 1) return 0;
-  if (m->fold_n > 0)
+  if (fidx)
     hipLaunchKernelGGL((forward_kernel<P, true>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
-                       m->ws.fidx.as<int32_t>(), row_ptr, ca, node);
+                       fidx, row_ptr, ca, node);
   else
     hipLaunchKernelGGL((forward_kernel<P, false>), dim3(blocks), dim3(kTeam), 0, st, m->dev(), n,
                        species, row_ptr, ca, node);
@@ -258,10 +258,10 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int64_
 
 }  // namespace
 
-int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
+int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                    const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st) {
   const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
-    return launch<decltype(p)>(m, n, species, row_ptr, ca, node, st);
+    return launch<decltype(p)>(m, n, species, fidx, row_ptr, ca, node, st);
   });
   if (rc == kNoProfile) {
     set_error("forward: profile not compiled");

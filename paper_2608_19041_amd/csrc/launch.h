@@ -26,17 +26,26 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
 // synchronises ``st``
 int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
 // skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1;
-// samples = scratch of (cap + 15) / 16 int64 (every 16th key of the list)
+// samples = scratch of (cap + 15) / 16 int64 (every 16th key of the list);
+// with ``paired`` (device int64, zeroed by the caller) also the number of
+// reverse pairs found, so a symmetric list of E entries gives E / 2
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, hipStream_t st);
+                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, int64_t* paired,
+                    hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
-// index of every atom; synchronises ``st``
-int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, hipStream_t st);
+// index of every atom into ``fidx`` [n]; ``mask_dev`` is device scratch of 4
+// uint32.  Without ``may_alloc`` the tables are rebuilt only inside the
+// allocation they already have; a species set that needs more runs this call
+// on the separable tables and leaves the model's folded state as it was.
+// *use_fold tells the edge kernels which tables to read.  Synchronises ``st``.
+int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, uint32_t* mask_dev,
+                    int32_t* fidx, bool may_alloc, bool* use_fold, hipStream_t st);
 
-// model stages (the edge kernels read ws.fidx when the model has folded tables)
+// model stages: the edge kernels read the pair-folded tables with the
+// folded index ``fidx`` of every atom, or the separable tables when fidx is null
 // compaction of every skin row (compact.h) and the forward pass
-int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species,
+int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                    const int64_t* row_ptr, const CompactArgs& ca, float* node, hipStream_t st);
 // readout + MLP + head + MLP gradient + readout VJP on 16-atom tiles;
 // desc_out (float [N][D_out]) receives D when not null
@@ -45,7 +54,7 @@ int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const 
 // the gradients dE/dr_ij overwrite the compact edge records in ``edge``
 // (x, y, z = the gradient, w = the bits of j as before); with w_atom
 // ([N][9]) also the virial terms W_i = -sum_e g_e (x) r_e of every centre
-int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species,
+int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                     const int64_t* row_ptr, const int32_t* ecount, float4* edge,
                     const float* node_grad, double* w_atom, hipStream_t st);
 struct StepTail;
@@ -145,6 +154,35 @@ int launch_final_step(StepSums prev, hipStream_t st);
 constexpr int kMaxTailBlocks = 8192;
 int tail_partial_count(int64_t n);
 int launch_snapshot_q(const double* pos, int64_t n, int64_t* qbuild, hipStream_t st);
+// p[0, n) = 0 (a fill kernel, not a memset node)
+int launch_zero_i64(int64_t* p, int64_t n, hipStream_t st);
+
+// The per-call device buffers of an energy-and-force evaluation: the
+// model's workspace, or a caller-free scratch area (noalloc.hip).
+struct EvalBufs {
+  int32_t* ecount;      // int32 [N]
+  float4* edge;         // float4 [cap]
+  int32_t* cidx;        // int32 [cap]
+  int32_t* crev;        // int32 [cap]
+  int32_t* skin_rev;    // int32 [cap]
+  float* node;          // float [N][S+2]
+  float* node_grad;     // float [N][S+2]
+  double* epart;        // double [partial_count(N) + 8]
+  int32_t* fidx;        // int32 [N]
+  uint32_t* fold_mask;  // uint32 [4]
+  int64_t* check;       // int64 [2]: reverse pairs found
+};
+// bytes of each EvalBufs array for N atoms, a list of cap entries and a node
+// state of ns floats per atom, each rounded up to 256 (in struct order)
+void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[11]);
+// compute_energy_forces(_virial) on the given buffers (null: the model's
+// workspace, grown as needed); ``bufs`` given means no allocation, no timing
+// events and no memset nodes on the stream
+int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* species, int64_t N,
+                       const double cell[9], const int pbc[3], double r_c, const int64_t* row_ptr,
+                       const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
+                       double* e_atom, double* forces, double* e_total, double* virial,
+                       double* atom_virial, const EvalBufs* bufs, void* stream);
 // flags[idx] = value
 int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st);
 int partial_count(int64_t n);

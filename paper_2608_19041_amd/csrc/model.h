@@ -94,9 +94,14 @@ struct Workspace {
   DevBuf fold_map;      // int32 [T+1]: type -> folded index, or -1
   DevBuf fold_mask;     // uint32 [4]: species present in the last call
   DevBuf fidx;          // int32 [N]: folded index of every atom
-  uint32_t* fold_host = nullptr;          // pinned
+  DevBuf check;         // int64 [2]: reverse pairs found in a caller's list
+  // pinned host words, allocated with the model: [0, 16) the species
+  // presence mask, [16, 32) row_ptr[N] and the reverse pairs of a caller's
+  // list, [64, 64 + 4 (T+1)) the type map of the folded tables
+  uint32_t* fold_host = nullptr;
   // inputs of the last evaluation (the stage-check entry point re-runs it)
   const int32_t* last_species = nullptr;
+  const int32_t* last_fidx = nullptr;     // folded index of that call, or null (separable)
   const double* last_pos = nullptr;
   const int64_t* skin_row_used = nullptr;
   const int32_t* skin_j_used = nullptr;

@@ -456,53 +456,75 @@ __global__ void __launch_bounds__(kBlock) sample_keys_kernel(const int64_t* __re
 // is nobody's reverse row, like the compaction, which keeps nothing of it.
 __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0 && e >= b && e <= cap; }
 
-// skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
-// (i, -n), within row j, or -1.  One wave per row i.  A symmetric list pairs
+// The reverse search of entry s = (i -> j, n) of row i (which begins at
+// b): the position of the key (i, -n) within row j.  A symmetric list pairs
 // every entry with its reverse, so only the canonical entry of a pair, the
 // one with key(j, n) > key(i, -n) (that is j > i, or a periodic self image
-// with the larger shift), searches; it writes both indices.  Entries whose
-// partner is missing (a malformed caller list) keep the -1 of the fill
-// before.  The search narrows [lo, hi) of row j with the samples at positions
-// 16 g inside it, then bisects at most 16 entries.
+// with the larger shift), searches; it writes both indices and returns true.
+// The search narrows [lo, hi) of row j with the samples at positions 16 g
+// inside it, then bisects at most 16 entries.
+__device__ inline bool reverse_search(int64_t n, int64_t i, int64_t s, int64_t b,
+                                      const int64_t* __restrict__ row_ptr,
+                                      const int32_t* __restrict__ nbr_j,
+                                      const int32_t* __restrict__ nbr_shift, int64_t cap,
+                                      const int64_t* __restrict__ samples,
+                                      int32_t* __restrict__ rev) {
+  const int32_t j = nbr_j[s], sh = nbr_shift[s];
+  const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(sh));
+  if (entry_key(j, sh) <= want) return false;   // the partner's row searches
+  if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) return false;
+  const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
+  int64_t lo = jb, hi = je;
+  const int64_t g0 = (jb + 15) >> 4, g1 = (je - 1) >> 4;   // samples inside the row
+  if (je > jb && g0 <= g1) {
+    int64_t l = g0, h = g1 + 1;   // first sample above ``want``
+    while (l < h) {
+      const int64_t m = (l + h) >> 1;
+      if (samples[m] <= want) l = m + 1;
+      else h = m;
+    }
+    if (l > g0) lo = 16 * (l - 1);
+    if (l <= g1) hi = 16 * l;
+  }
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (entry_key(nbr_j[mid], nbr_shift[mid]) < want) lo = mid + 1;
+    else hi = mid;
+  }
+  if (lo < je && entry_key(nbr_j[lo], nbr_shift[lo]) == want) {
+    rev[s] = static_cast<int32_t>(lo - jb);
+    rev[lo] = static_cast<int32_t>(s - b);
+    return true;
+  }
+  return false;
+}
+
+// skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
+// (i, -n), within row j, or -1.  One wave per row i.  Entries whose partner
+// is missing (a malformed caller list) keep the -1 of the fill before.  With
+// ``paired`` the pairs found are counted (one atomic per wave and row), so
+// the caller can tell a symmetric list (2 x pairs = entries) from one that
+// is not.
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                           const int32_t* __restrict__ nbr_j,
                                                           const int32_t* __restrict__ nbr_shift,
                                                           int64_t cap,
                                                           const int64_t* __restrict__ samples,
-                                                          int32_t* __restrict__ rev) {
+                                                          int32_t* __restrict__ rev,
+                                                          unsigned long long* __restrict__ paired) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
   for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
-    int64_t b = row_ptr[i], e = row_ptr[i + 1];
+    const int64_t b = row_ptr[i], e = row_ptr[i + 1];
     if (!row_ok(b, e, cap)) continue;
-    for (int64_t s = b + lane; s < e; s += kWave) {
-      const int32_t j = nbr_j[s], sh = nbr_shift[s];
-      const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(sh));
-      if (entry_key(j, sh) <= want) continue;   // the partner's row searches
-      if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) continue;
-      const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
-      int64_t lo = jb, hi = je;
-      const int64_t g0 = (jb + 15) >> 4, g1 = (je - 1) >> 4;   // samples inside the row
-      if (je > jb && g0 <= g1) {
-        int64_t l = g0, h = g1 + 1;   // first sample above ``want``
-        while (l < h) {
-          const int64_t m = (l + h) >> 1;
-          if (samples[m] <= want) l = m + 1;
-          else h = m;
-        }
-        if (l > g0) lo = 16 * (l - 1);
-        if (l <= g1) hi = 16 * l;
-      }
-      while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (entry_key(nbr_j[mid], nbr_shift[mid]) < want) lo = mid + 1;
-        else hi = mid;
-      }
-      if (lo < je && entry_key(nbr_j[lo], nbr_shift[lo]) == want) {
-        rev[s] = static_cast<int32_t>(lo - jb);
-        rev[lo] = static_cast<int32_t>(s - b);
-      }
+    unsigned long long found = 0;
+    for (int64_t s0 = b; s0 < e; s0 += kWave) {
+      const int64_t s = s0 + lane;
+      const bool hit =
+          s < e && reverse_search(n, i, s, b, row_ptr, nbr_j, nbr_shift, cap, samples, rev);
+      found += __popcll(__ballot(hit));
     }
+    if (paired && lane == 0 && found) atomicAdd(paired, found);
   }
 }
 
@@ -718,7 +740,8 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, hipStream_t st) {
+                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, int64_t* paired,
+                    hipStream_t st) {
   if (n <= 0) return 0;
   int64_t sb = ((cap + 15) / 16 + kBlock - 1) / kBlock;
   sb = sb < 1 ? 1 : (sb > 8192 ? 8192 : sb);
@@ -727,7 +750,8 @@ int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t*
   hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb * 16 > 8192 ? 8192 : sb * 16)),
                      dim3(kBlock), 0, st, skin_rev, cap, -1);
   hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
-                     nbr_shift, cap, samples, skin_rev);
+                     nbr_shift, cap, samples, skin_rev,
+                     reinterpret_cast<unsigned long long*>(paired));
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

@@ -113,3 +113,41 @@ def test_workspace_beyond_device_memory_is_out_of_memory(dev, dp):
     ea, F, et = model.compute_energy_forces(pos, species, s.cell, s.pbc, 6.0, rp, nj, ns, e)
     torch.cuda.synchronize()
     assert np.isfinite(F.cpu().numpy()).all() and abs(float(F.sum(0).abs().max())) < 1e-9
+
+
+def test_malformed_caller_lists_are_refused(dev, dp):
+    """A list with more entries than n_pairs, and a list where one entry lost
+    its reverse, are refused with INVALID_ARG before any output is written;
+    the intact list then evaluates normally."""
+    spec, w = synth.model_weights("small")
+    model = dp.Model(synth.pack_blob(spec, w))
+    s = synth.fcc_copper(3, 0.05, seed=4)
+    pos = torch.tensor(s.pos, dtype=torch.float64, device=dev)
+    species = torch.tensor(s.species, dtype=torch.int32, device=dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, spec.r_c + 1.0)
+    e_atom = torch.full((s.n,), 7.0, dtype=torch.float64, device=dev)
+    F = torch.full((s.n, 3), 7.0, dtype=torch.float64, device=dev)
+    et = torch.full((1,), 7.0, dtype=torch.float64, device=dev)
+    # row_ptr[N] beyond n_pairs
+    with pytest.raises(dp.DPA4CError) as ex:
+        model.compute_energy_forces(pos, species, s.cell, s.pbc, spec.r_c, rp, nj, ns, e - 5,
+                                    e_atom, F, et)
+    assert ex.value.code == dp.ERR_INVALID_ARG and "n_pairs" in str(ex.value)
+    # drop the first entry of row 5: its partner in the other row has no reverse
+    rph = rp.cpu().numpy().copy()
+    k = int(rph[5])
+    keep = np.ones(e, bool)
+    keep[k] = False
+    rph[6:] -= 1
+    rp2 = torch.tensor(rph, device=dev)
+    nj2 = nj[torch.tensor(keep, device=dev)].contiguous()
+    ns2 = ns[torch.tensor(keep, device=dev)].contiguous()
+    with pytest.raises(dp.DPA4CError) as ex:
+        model.compute_energy_forces(pos, species, s.cell, s.pbc, spec.r_c, rp2, nj2, ns2, e - 1,
+                                    e_atom, F, et)
+    assert ex.value.code == dp.ERR_INVALID_ARG and "not symmetric" in str(ex.value)
+    torch.cuda.synchronize()
+    assert bool((e_atom == 7.0).all()) and bool((F == 7.0).all()) and float(et[0]) == 7.0
+    ea, F, et = model.compute_energy_forces(pos, species, s.cell, s.pbc, spec.r_c, rp, nj, ns, e)
+    torch.cuda.synchronize()
+    assert np.isfinite(ea.cpu().numpy()).all() and abs(float(et[0]) - float(ea.sum())) < 1e-9
