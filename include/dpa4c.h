@@ -189,6 +189,36 @@ int compute_energy_forces_virial(const dpa4c_model* model, const double* pos,
                                  double* atom_virial, void* stream);
 
 /*
+ * compute_energy_forces without any device allocation, for callers that
+ * cannot allocate while they run: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same arguments, outputs,
+ * determinism and errors as compute_energy_forces; the library calls no
+ * hipMalloc, hipFree or allocating routine and records no memset.
+ *
+ * The per-call buffers live in a fixed 64 MiB device array (one per device,
+ * held until the process ends) instead of the model's workspace.  They take
+ * 28 bytes per list entry (n_pairs), 8 (S+2) + 8 bytes per atom and about
+ * 1 KB more (each array rounded up to 256 bytes): about 12,000 atoms of a
+ * dense metal at the full width with a 1 A skin.  A larger input returns
+ * DPA4C_ERR_INVALID_ARG before any device work.  Every call on a device
+ * shares that device's array, so calls that overlap on one device (other
+ * streams, other threads, other models) race; calls on one stream do not.
+ *
+ * The pair-folded radial tables are built only inside the allocation a
+ * previous call on the model left: with a species set whose tables do not
+ * fit it, this call reads the separable tables (the same model, results
+ * equal to float32 rounding).  One compute_energy_forces call with the same
+ * species beforehand gives this entry point the folded tables.  The model's
+ * own workspace, and so the list that verlet_step carries between calls, is
+ * untouched.  Synchronises ``stream`` once (the species present).
+ */
+int compute_energy_forces_noalloc(const dpa4c_model* model, const double* pos,
+                                  const int32_t* species, int64_t N, const double cell[9],
+                                  const int pbc[3], double r_c, const int64_t* row_ptr,
+                                  const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
+                                  double* e_atom, double* forces, double* e_total, void* stream);
+
+/*
  * ``nsteps`` velocity-Verlet NVE steps (Supplementary Note on the MD
  * protocol: full neighbour list with a skin, checked every step):
  *     v += dt/2 F/m;  r += dt v;  [rebuild];  F = F(r);  v += dt/2 F/m.

@@ -53,6 +53,8 @@ def library():
                                             vp, vp, vp, vp]),
             "compute_energy_forces_virial": (i32, [vp, vp, vp, i64, vp, vp, dbl, vp, vp, vp,
                                                    i64, vp, vp, vp, vp, vp, vp]),
+            "compute_energy_forces_noalloc": (i32, [vp, vp, vp, i64, vp, vp, dbl, vp, vp, vp, i64,
+                                                    vp, vp, vp, vp]),
             "verlet_step": (i32, [vp, vp, vp, vp, vp, i64, vp, vp, dbl, dbl, dbl, i32, i32,
                                   vp, vp, vp, ctypes.POINTER(i64), vp]),
             "nvt_step": (i32, [vp, vp, vp, vp, vp, i64, vp, vp, dbl, dbl, dbl, i32, i32, dbl, dbl,
@@ -74,7 +76,8 @@ def library():
 
 def exported_symbols() -> list[str]:
     return ["dpa4c_model_create", "dpa4c_model_destroy", "dpa4c_model_info", "build_neighbors",
-            "compute_energy_forces", "compute_energy_forces_virial", "verlet_step", "nvt_step",
+            "compute_energy_forces", "compute_energy_forces_virial",
+            "compute_energy_forces_noalloc", "verlet_step", "nvt_step",
             "dpa4c_debug_stages", "dpa4c_set_timing",
             "dpa4c_get_timings", "dpa4c_stage_name", "dpa4c_debug_gemm", "dpa4c_last_error"]
 
@@ -228,6 +231,25 @@ class Model:
         cellh, cellp = _cell_arg(cell)
         pbch, pbcp = _pbc_arg(pbc)
         _check(library().compute_energy_forces(
+            self._h, _ptr(pos), _ptr(species), n, cellp, pbcp, float(r_c),
+            _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
+            _ptr(e_total), _stream(stream)))
+        return e_atom, forces, e_total
+
+    def compute_energy_forces_noalloc(self, pos, species, cell, pbc, r_c, row_ptr, nbr_j,
+                                      nbr_shift, n_pairs, e_atom, forces, e_total, stream=None):
+        """compute_energy_forces into caller buffers, with no device allocation
+        in the library (its per-call buffers are a fixed device array)."""
+        import torch
+        n = pos.shape[0]
+        _require(pos, torch.float64, (n, 3), "pos")
+        _require(species, torch.int32, (n,), "species")
+        _require(e_atom, torch.float64, (n,), "e_atom")
+        _require(forces, torch.float64, (n, 3), "forces")
+        _require(e_total, torch.float64, (1,), "e_total")
+        cellh, cellp = _cell_arg(cell)
+        pbch, pbcp = _pbc_arg(pbc)
+        _check(library().compute_energy_forces_noalloc(
             self._h, _ptr(pos), _ptr(species), n, cellp, pbcp, float(r_c),
             _ptr(row_ptr), _ptr(nbr_j), _ptr(nbr_shift), int(n_pairs), _ptr(e_atom), _ptr(forces),
             _ptr(e_total), _stream(stream)))

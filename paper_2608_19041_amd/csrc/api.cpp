@@ -341,7 +341,12 @@ int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model*
     *out = nullptr;
     return DPA4C_ERR_HIP;
   }
-  return 0;
+  rc = noalloc_setup(device);
+  if (rc) {
+    dpa4c_model_destroy(*out);
+    *out = nullptr;
+  }
+  return rc;
 }
 
 void dpa4c_model_destroy(dpa4c_model* m) {

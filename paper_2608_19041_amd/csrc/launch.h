@@ -183,6 +183,9 @@ int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* s
                        const int32_t* nbr_j, const int32_t* nbr_shift, int64_t n_pairs,
                        double* e_atom, double* forces, double* e_total, double* virial,
                        double* atom_virial, const EvalBufs* bufs, void* stream);
+// per-device set-up of the no-allocation entry point (noalloc.hip); called
+// with ``device`` current by dpa4c_model_create
+int noalloc_setup(int device);
 // flags[idx] = value
 int launch_set_flag(int64_t* flags, int idx, int64_t value, hipStream_t st);
 int partial_count(int64_t n);
