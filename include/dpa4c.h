@@ -129,10 +129,11 @@ int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
  * n_pairs   host out: number of edges; always set when the count succeeded.
  * If the edge count exceeds cap, returns DPA4C_ERR_CAPACITY with *n_pairs
  * set and row_ptr written, but nbr_j / nbr_shift untouched; call again with
- * cap >= *n_pairs.  A non-finite position gives DPA4C_ERR_NONFINITE; a row
- * longer than 1024 or an image index beyond +-127 gives
- * DPA4C_ERR_UNSUPPORTED.  Synchronises ``stream`` twice (to read the count
- * and the error flags).
+ * cap >= *n_pairs.  A non-finite position gives DPA4C_ERR_NONFINITE; an
+ * image index beyond +-127 gives DPA4C_ERR_UNSUPPORTED.  Rows have no length
+ * limit (rows beyond 512 entries are ordered through a device scratch of
+ * 8 bytes per entry, allocated when the count finds one).  Synchronises
+ * ``stream`` twice (to read the count and the error flags).
  */
 int build_neighbors(const double* pos, int64_t N, const double cell[9], const int pbc[3],
                     double r_list, int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift,

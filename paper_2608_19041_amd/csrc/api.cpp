@@ -103,7 +103,7 @@ int flags_to_error(int64_t f) {
     return DPA4C_ERR_NONFINITE;
   }
   if (f & kFlagRowTooLong) {
-    set_error("a neighbour row is longer than 1024 entries");
+    set_error("a neighbour row is longer than the fill kernel's row buffer and no scratch was given");
     return DPA4C_ERR_UNSUPPORTED;
   }
   if (f & kFlagShift) {
@@ -361,7 +361,8 @@ void dpa4c_model_destroy(dpa4c_model* m) {
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.check,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
-                    &w.nb.cell_fill, &w.nb.cell_atoms, &w.nb.counts, &w.nb.partials,
+                    &w.nb.cell_fill, &w.nb.cell_rec, &w.nb.long_keys, &w.nb.counts,
+                    &w.nb.partials,
                     &w.virpart,  &w.nvt,     &w.crev,     &w.watom,     &w.nb.extent};
   for (DevBuf* b : bufs) b->release();
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
@@ -429,10 +430,11 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
   }
   int64_t* flags = fl->as<int64_t>();
   DPA4C_HIP_TRY(hipMemsetAsync(flags, 0, 64, st));
-  rc = build_skin_list(*nb, pos, N, g, row_ptr, nullptr, nullptr, cap, flags, false, st);
+  rc = build_skin_list(*nb, pos, N, g, row_ptr, flags, st);
   if (rc) return rc;
   DPA4C_HIP_TRY(hipMemcpyAsync(hflag, row_ptr + N, 8, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 1, flags, 8, hipMemcpyDeviceToHost, st));
+  DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 2, flags + 3, 8, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
   if (hflag[1] & kFlagNonFinite) return flags_to_error(hflag[1]);
   *n_pairs = hflag[0];
@@ -441,7 +443,7 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
               " edges");
     return DPA4C_ERR_CAPACITY;
   }
-  rc = fill_skin_list(*nb, N, g, row_ptr, nbr_j, nbr_shift, cap, flags, st);
+  rc = fill_skin_list(*nb, N, g, row_ptr, nbr_j, nbr_shift, cap, flags, hflag[2], nullptr, st);
   if (rc) return rc;
   DPA4C_HIP_TRY(hipMemcpyAsync(hflag + 1, flags, 8, hipMemcpyDeviceToHost, st));
   DPA4C_HIP_TRY(hipStreamSynchronize(st));
@@ -519,7 +521,7 @@ int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* s
     rc = launch_zero_i64(B.check, 2, st);
     if (rc) return rc;
     rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, reinterpret_cast<int64_t*>(B.edge),
-                         B.skin_rev, B.check, st);
+                         false, B.skin_rev, B.check, st);
     if (rc) return rc;
   }
   // the list's size and the pairs found come back with the species mask
@@ -698,13 +700,13 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     }
     {
       StageScope t(m, kStNeighbor, st);
-      r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), nullptr, nullptr, 0,
-                          flags, false, st);
+      r = build_skin_list(w.nb, pos, N, g_list, w.skin_row.as<int64_t>(), flags, st);
       if (r) return r;
     }
     DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags, w.skin_row.as<int64_t>() + N, 8,
                                  hipMemcpyDeviceToHost, st));
     DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags + 1, flags, 8, hipMemcpyDeviceToHost, st));
+    DPA4C_HIP_TRY(hipMemcpyAsync(w.host_flags + 2, flags + 3, 8, hipMemcpyDeviceToHost, st));
     DPA4C_HIP_TRY(hipStreamSynchronize(st));
     if (w.host_flags[1]) return flags_to_error(w.host_flags[1]);
     const int64_t need = w.host_flags[0];
@@ -719,11 +721,14 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     r = ensure_workspace(mm, N, w.cap);
     if (r) return r;
     StageScope t(m, kStNeighbor, st);
+    // the keys for the reverse search go to the edge records, which the
+    // forward kernel rewrites before reading them
     r = fill_skin_list(w.nb, N, g_list, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
-                       w.skin_shift.as<int32_t>(), w.cap, flags, st);
+                       w.skin_shift.as<int32_t>(), w.cap, flags, w.host_flags[2],
+                       w.edge.as<int64_t>(), st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.edge.as<int64_t>(), w.skin_rev.as<int32_t>(), nullptr, st);
+                        N, w.cap, w.edge.as<int64_t>(), true, w.skin_rev.as<int32_t>(), nullptr, st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
     if (r) return r;

@@ -231,7 +231,7 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
   const int sub = threadIdx.x % kLanesPerAtom, slot = threadIdx.x / kLanesPerAtom;
   const int64_t groups = (n + APG - 1) / APG;
   double blk_e = 0.0, blk_k = 0.0, blk_v = 0.0;   // the block's partials (threads 0, 0..8)
-  for (int64_t grp = blockIdx.x; grp < groups; grp += nblk) {
+  for (int64_t grp = xcd_block(blockIdx.x, nblk); grp < groups; grp += nblk) {
     const int64_t k = grp * APG + slot;
     // the step's per-atom inputs, requested before the row so that their
     // latency overlaps the gathers

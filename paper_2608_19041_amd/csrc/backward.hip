@@ -63,7 +63,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
   // index of every atom
   auto type_of = [&](int64_t a) { return FOLD ? typ[a] : clamp_type(typ[a], T1); };
 
-  for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x); i < n; i += gridDim.x) {
     const int ai = type_of(i);
     const float* gyr = node_grad + size_t(i) * P::NS;
     // per-centre coefficients in the lane's channel layout

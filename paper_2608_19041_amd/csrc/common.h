@@ -13,6 +13,19 @@ constexpr double kEps = 1.0e-7;          // Eq. (edge-geometry) regulariser
 constexpr double kQScale = 1048576.0;    // 2^20: fixed-point resolution of positions
 constexpr int kWave = 64;
 
+// Workgroups are handed to the 8 XCDs of the chip in turn (dispatch index b
+// runs on XCD b % 8), and each XCD has its own L2.  xcd_block maps b to a
+// work index so that every XCD takes one contiguous eighth of [0, nblocks):
+// kernels whose rows gather the data of neighbouring atoms (positions,
+// reverse rows, reverse gradients) then find most of it in their own L2.  A
+// bijection on [0, nblocks).
+__device__ inline int64_t xcd_block(int64_t b, int64_t nblocks) {
+  constexpr int64_t kXcd = 8;
+  const int64_t per = nblocks / kXcd, rem = nblocks % kXcd;
+  const int64_t x = b % kXcd, k = b / kXcd;
+  return x * per + (x < rem ? x : rem) + k;
+}
+
 // ---------------------------------------------------------------------------
 // Compile-time profile (C0, L, R): every width of the model follows from it
 // (Eqs. (degree-channels), (probe-ranks), (moment-width), (dim-out)).

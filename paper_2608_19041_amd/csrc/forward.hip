@@ -51,7 +51,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
   // index of every atom
   auto type_of = [&](int64_t a) { return FOLD ? typ[a] : clamp_type(typ[a], T1); };
 
-  for (int64_t i = blockIdx.x; i < n; i += gridDim.x) {
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x); i < n; i += gridDim.x) {
     const int ai = type_of(i);
     const int64_t b = row_ptr[i];
     // the row's edges inside r_c, compacted to the head of its skin row

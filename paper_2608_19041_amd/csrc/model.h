@@ -52,7 +52,8 @@ struct NeighborScratch {
   DevBuf cell_cnt;   // int32 [ncell]
   DevBuf cell_start; // int32 [ncell+1]
   DevBuf cell_fill;  // int32 [ncell]
-  DevBuf cell_atoms; // int32 [N]
+  DevBuf cell_rec;   // 32-byte records [N] in bin order: fixed-point position and atom index
+  DevBuf long_keys;  // int64 [cap] keys of rows longer than the fill kernel's LDS row
   DevBuf counts;     // int64 [N]
   DevBuf partials;   // int64 scan partials
   DevBuf host_flag;  // pinned host int64 [4]

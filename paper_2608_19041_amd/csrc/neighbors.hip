@@ -1,5 +1,5 @@
-// Cell-list neighbour search and per-step edge compaction, Methods Eq.
-// (neighbor-set), integer arithmetic only.
+// Cell-list neighbour search and the reverse index of a skin list, Methods
+// Eq. (neighbor-set), integer arithmetic only.
 //
 // Positions are mapped to fixed point Q(x) = rint(x * 2^20) (int64) and the
 // membership test |Q(r_j) + sum_b n_b Q(h_b) - Q(r_i)|^2 < Q(r)^2 is exact, so
@@ -13,9 +13,19 @@
 // margin, far above the rounding of the fractional coordinates, so every
 // pair within the radius is visited and the integer test decides.
 //
+// Bins are about half the radius wide (reach 2), so a centre's stencil
+// covers ~15.6 r^3 instead of 27 r^3 with radius-wide bins.  After binning,
+// each atom's fixed-point position and index are copied into a record in bin
+// order, so the atoms of consecutive bins along the third axis are one
+// contiguous run: the stencil of a centre is a few dozen such runs, which a
+// wave reads with coalesced loads as one list of candidates, 64 at a time.
+//
 // Work mapping: one 64-lane wavefront per centre atom, waves striding over
-// centres; candidate atoms of a stencil cell are spread over the lanes and
-// compacted with a wave ballot, which keeps their relative order.
+// centres.  The count kernel counts a row; the fill kernel collects the
+// accepted keys (j, packed n) of a row in LDS and writes each at its rank,
+// the number of smaller keys in the row: canonical order without a sort
+// network.  Rows longer than kMaxRow are ranked the same way from a global
+// scratch the host provides once the count has shown them.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -30,9 +40,10 @@ namespace {
 
 constexpr int kBlock = 256;            // 4 waves
 constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kMaxRow = 1024;          // longest row the fill kernel sorts in LDS
-constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8,
-                  kFlagRev = 16;
+constexpr int kMaxRow = 512;           // longest row the fill kernel ranks in LDS
+constexpr int kMaxSeg = kWave;         // stencil runs a wave holds at once
+constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8;
+constexpr int kFlagMaxRow = 3;         // flags[3]: the longest row of the last count
 
 __device__ inline int64_t floor_div(int64_t a, int64_t b) {
   int64_t q = a / b;
@@ -176,92 +187,161 @@ __global__ void __launch_bounds__(1024) cell_scan_kernel(const int32_t* __restri
   }
 }
 
+// One candidate record per atom, in bin order: the wrapped fixed-point
+// position and the atom index (32 bytes, read by two 16-byte loads).
+struct alignas(16) CellRec {
+  int64_t q[3];
+  int32_t j;
+  int32_t pad;
+};
+
+// the atom's record at a free slot of its bin (slot order inside a bin does
+// not matter: rows are ranked by key afterwards)
 __global__ void __launch_bounds__(kBlock) place_kernel(int64_t n, const int32_t* __restrict__ cell_of,
+                                                       const int64_t* __restrict__ qpos,
                                                        const int32_t* __restrict__ start,
                                                        int32_t* __restrict__ fill,
-                                                       int32_t* __restrict__ atoms) {
+                                                       CellRec* __restrict__ rec) {
   int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x;
   if (i >= n) return;
   int cid = cell_of[i];
   int slot = atomicAdd(&fill[cid], 1);
-  atoms[start[cid] + slot] = static_cast<int32_t>(i);
+  CellRec r;
+  r.q[0] = qpos[3 * i];
+  r.q[1] = qpos[3 * i + 1];
+  r.q[2] = qpos[3 * i + 2];
+  r.j = static_cast<int32_t>(i);
+  r.pad = 0;
+  rec[start[cid] + slot] = r;
 }
 
-// Visits every (cell, image) of the stencil of centre i and calls
-// f(j, nx, ny, nz, pred) on chunks of candidates (one per lane, pred false on
-// idle lanes).  Wave-uniform control flow.
+// exclusive-to-inclusive prefix sum over the 64 lanes of a wave
+__device__ inline int wave_inclusive_scan(int v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int t = __shfl_up(v, off);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+// The stencil of one centre as runs of bins: a run is the bins of one
+// (axis-0, axis-1) offset whose axis-2 bins are consecutive with one image
+// index, so its atoms are one contiguous range of the bin-ordered records.
+struct SegLds {
+  int64_t off[3][kMaxSeg];   // image displacement sum_b s_b Q(h_b) minus Q(r_i)
+  int32_t begin[kMaxSeg];    // first record of the run
+  int32_t vend[kMaxSeg];     // end of the run in the centre's list of candidates
+  int32_t s[3][kMaxSeg];     // image indices of the run
+};
+
+// Visits every candidate (record, image) of the stencil of centre i and
+// calls f(j, s0, s1, s2, pred) on chunks of 64 (one per lane, pred false on
+// idle lanes); pred is the exact membership test with the centre itself
+// (j = i, n = 0) excluded.  The image index of a pair is n = s - m_j + m_i
+// with m the wrap counts of binning.  Wave-uniform control flow.
 template <bool TRIC, class Fn>
-__device__ inline void for_candidates(const GridDev& g, int64_t i, const int64_t* __restrict__ qpos,
-                                      const int32_t* __restrict__ wrap,
-                                      const int32_t* __restrict__ cell_of,
-                                      const int32_t* __restrict__ start,
-                                      const int32_t* __restrict__ atoms, Fn&& f) {
+__device__ inline void for_stencil(const GridDev& g, int64_t i, const int64_t* __restrict__ qpos,
+                                   const int32_t* __restrict__ cell_of,
+                                   const int32_t* __restrict__ start,
+                                   const CellRec* __restrict__ rec, SegLds& sg, Fn&& f) {
+  const int lane = lane_id();
   const int64_t qi0 = qpos[3 * i], qi1 = qpos[3 * i + 1], qi2 = qpos[3 * i + 2];
-  const int mi0 = wrap[3 * i], mi1 = wrap[3 * i + 1], mi2 = wrap[3 * i + 2];
   const int cid_i = cell_of[i];
   const int ci0 = cid_i / (g.nc1 * g.nc2);
   const int ci1 = (cid_i / g.nc2) % g.nc1;
   const int ci2 = cid_i % g.nc2;
-  const int lane = lane_id();
-  for (int d0 = -g.re0; d0 <= g.re0; ++d0) {
-    int t0 = ci0 + d0;
-    int s0 = static_cast<int>(floor_div(t0, g.nc0));
-    int w0 = t0 - s0 * g.nc0;
-    for (int d1 = -g.re1; d1 <= g.re1; ++d1) {
-      int t1 = ci1 + d1;
-      int s1 = static_cast<int>(floor_div(t1, g.nc1));
-      int w1 = t1 - s1 * g.nc1;
-      for (int d2 = -g.re2; d2 <= g.re2; ++d2) {
-        int t2 = ci2 + d2;
-        int s2 = static_cast<int>(floor_div(t2, g.nc2));
-        int w2 = t2 - s2 * g.nc2;
-        int cid = (w0 * g.nc1 + w1) * g.nc2 + w2;
-        int cb = start[cid], ce = start[cid + 1];
-        for (int base = cb; base < ce; base += kWave) {
-          int idx = base + lane;
-          bool pred = false;
-          int32_t j = 0;
-          int nx = 0, ny = 0, nz = 0;
-          if (idx < ce) {
-            j = atoms[idx];
-            int64_t dx, dy, dz;
-            if (!TRIC) {
-              dx = qpos[3 * j] + s0 * g.qh[0] - qi0;
-              dy = qpos[3 * j + 1] + s1 * g.qh[4] - qi1;
-              dz = qpos[3 * j + 2] + s2 * g.qh[8] - qi2;
-            } else {   // image displacement sum_b s_b Q(h_b)
-              dx = qpos[3 * j] + s0 * g.qh[0] + s1 * g.qh[3] + s2 * g.qh[6] - qi0;
-              dy = qpos[3 * j + 1] + s0 * g.qh[1] + s1 * g.qh[4] + s2 * g.qh[7] - qi1;
-              dz = qpos[3 * j + 2] + s0 * g.qh[2] + s1 * g.qh[5] + s2 * g.qh[8] - qi2;
-            }
-            nx = s0 - wrap[3 * j] + mi0;
-            ny = s1 - wrap[3 * j + 1] + mi1;
-            nz = s2 - wrap[3 * j + 2] + mi2;
-            pred = within(dx, dy, dz, g.rq) && !(j == i && nx == 0 && ny == 0 && nz == 0);
-          }
-          f(j, nx, ny, nz, pred);
-        }
+  const int lo2 = ci2 - g.re2, hi2 = ci2 + g.re2;
+  const int s2lo = static_cast<int>(floor_div(lo2, g.nc2));
+  const int nr = static_cast<int>(floor_div(hi2, g.nc2)) - s2lo + 1;   // image runs along axis 2
+  const int n1 = 2 * g.re1 + 1;
+  const int nseg = (2 * g.re0 + 1) * n1 * nr;
+  for (int sb = 0; sb < nseg; sb += kMaxSeg) {
+    const int q = sb + lane;
+    int len = 0;
+    if (q < nseg) {
+      const int r = q % nr, p = q / nr;
+      const int t0 = ci0 + p / n1 - g.re0, t1 = ci1 + p % n1 - g.re1;
+      const int s0 = static_cast<int>(floor_div(t0, g.nc0));
+      const int s1 = static_cast<int>(floor_div(t1, g.nc1));
+      const int s2 = s2lo + r;
+      const int w0 = t0 - s0 * g.nc0, w1 = t1 - s1 * g.nc1;
+      const int a = max(lo2, s2 * g.nc2) - s2 * g.nc2;
+      const int b = min(hi2, s2 * g.nc2 + g.nc2 - 1) - s2 * g.nc2;
+      const int base = (w0 * g.nc1 + w1) * g.nc2;
+      const int beg = start[base + a];
+      len = start[base + b + 1] - beg;
+      int64_t ox, oy, oz;
+      if (!TRIC) {
+        ox = s0 * g.qh[0] - qi0;
+        oy = s1 * g.qh[4] - qi1;
+        oz = s2 * g.qh[8] - qi2;
+      } else {
+        ox = s0 * g.qh[0] + s1 * g.qh[3] + s2 * g.qh[6] - qi0;
+        oy = s0 * g.qh[1] + s1 * g.qh[4] + s2 * g.qh[7] - qi1;
+        oz = s0 * g.qh[2] + s1 * g.qh[5] + s2 * g.qh[8] - qi2;
       }
+      sg.off[0][lane] = ox;
+      sg.off[1][lane] = oy;
+      sg.off[2][lane] = oz;
+      sg.begin[lane] = beg;
+      sg.s[0][lane] = s0;
+      sg.s[1][lane] = s1;
+      sg.s[2][lane] = s2;
     }
+    const int vend = wave_inclusive_scan(len);
+    sg.vend[lane] = vend;
+    const int total = __shfl(vend, kWave - 1);
+    wave_lds_sync();
+    int seg = 0;   // the run of this lane's candidate (candidates advance, so does the run)
+    for (int k0 = 0; k0 < total; k0 += kWave) {
+      const int k = k0 + lane;
+      bool pred = false;
+      int32_t j = 0;
+      int sx = 0, sy = 0, sz = 0;
+      if (k < total) {
+        while (sg.vend[seg] <= k) ++seg;
+        const int first = seg > 0 ? sg.vend[seg - 1] : 0;
+        const CellRec c = rec[sg.begin[seg] + (k - first)];
+        j = c.j;
+        sx = sg.s[0][seg];
+        sy = sg.s[1][seg];
+        sz = sg.s[2][seg];
+        pred = within(c.q[0] + sg.off[0][seg], c.q[1] + sg.off[1][seg], c.q[2] + sg.off[2][seg],
+                      g.rq) &&
+               !(j == i && sx == 0 && sy == 0 && sz == 0);
+      }
+      f(j, sx, sy, sz, pred);
+    }
+    wave_lds_sync();   // the next batch of runs overwrites the table
   }
 }
 
 template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) count_kernel(int64_t n, GridDev g,
                                                        const int64_t* __restrict__ qpos,
-                                                       const int32_t* __restrict__ wrap,
                                                        const int32_t* __restrict__ cell_of,
                                                        const int32_t* __restrict__ start,
-                                                       const int32_t* __restrict__ atoms,
-                                                       int64_t* __restrict__ counts) {
+                                                       const CellRec* __restrict__ rec,
+                                                       int64_t* __restrict__ counts,
+                                                       int64_t* __restrict__ flags) {
+  __shared__ SegLds segs[kWavesPerBlock];
+  SegLds& sg = segs[threadIdx.x / kWave];
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
-  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+  int64_t longest = 0;
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave; i < n;
+       i += nwaves) {
     int64_t total = 0;
-    for_candidates<TRIC>(g, i, qpos, wrap, cell_of, start, atoms, [&](int32_t, int, int, int, bool pred) {
+    for_stencil<TRIC>(g, i, qpos, cell_of, start, rec, sg, [&](int32_t, int, int, int, bool pred) {
       total += __popcll(__ballot(pred));
     });
     if (lane_id() == 0) counts[i] = total;
+    longest = total > longest ? total : longest;
   }
+  if (lane_id() == 0 && longest > 0)
+    atomicMax(reinterpret_cast<unsigned long long*>(flags + kFlagMaxRow),
+              static_cast<unsigned long long>(longest));
 }
 
 // ---------------------------------------------------------------------------
@@ -348,17 +428,104 @@ int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
 }
 
 // ---------------------------------------------------------------------------
+// Canonical key of a list entry: rows are sorted by it.
+__device__ inline int64_t entry_key(int32_t j, int32_t sh) {
+  return (int64_t(j) << 24) | int64_t(sh & 0xFFFFFF);
+}
+
+// Rows of the skin list: the accepted candidates of centre i as keys
+// (j, packed n), each written at its rank in the row (the number of smaller
+// keys; keys of a row are distinct), so rows come out in canonical order.
+// With ``keys`` the keys are also written to keys[row_ptr[i] + rank], and
+// every 16th of them (absolute position 16 g) to samples[g], for the
+// reverse search.  Rows longer than kMaxRow collect their keys in
+// long_keys[row_ptr[i] ...] instead of LDS (the host passes it when the
+// count found such rows; without it they are flagged).
+// One row: the accepted keys into kb[0, len) in candidate order, then
+// each written at its rank.  ``kb`` is the wave's LDS row or, for a row
+// longer than kMaxRow, a global scratch row (inlined for each, so LDS rows
+// use LDS instructions).
+template <bool TRIC, class KB>
+__device__ __forceinline__ void fill_row(const GridDev& g, int64_t i, int64_t r0, int len, KB* kb,
+                                         const int64_t* __restrict__ qpos,
+                                         const int32_t* __restrict__ wrap,
+                                         const int32_t* __restrict__ cell_of,
+                                         const int32_t* __restrict__ start,
+                                         const CellRec* __restrict__ rec, SegLds& sg,
+                                         int32_t* __restrict__ nbr_j,
+                                         int32_t* __restrict__ nbr_shift,
+                                         int64_t* __restrict__ keys, int64_t* __restrict__ samples,
+                                         int64_t* __restrict__ flags) {
+  const int lane = lane_id();
+  const int mi0 = wrap[3 * i], mi1 = wrap[3 * i + 1], mi2 = wrap[3 * i + 2];
+  int fill = 0;
+  bool shift_bad = false;
+  for_stencil<TRIC>(g, i, qpos, cell_of, start, rec, sg, [&](int32_t j, int s0, int s1, int s2,
+                                                             bool pred) {
+    uint64_t m;
+    const int pre = ballot_prefix(pred, &m);
+    if (pred) {
+      const int nx = s0 - wrap[3 * j] + mi0;
+      const int ny = s1 - wrap[3 * j + 1] + mi1;
+      const int nz = s2 - wrap[3 * j + 2] + mi2;
+      if (nx < -127 || nx > 127 || ny < -127 || ny > 127 || nz < -127 || nz > 127) shift_bad = true;
+      const int slot = fill + pre;
+      if (slot < len) kb[slot] = entry_key(j, pack_shift(nx, ny, nz));
+    }
+    fill += __popcll(m);
+  });
+  if (shift_bad)
+    atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagShift);
+  wave_lds_sync();
+  // rank of each key: the keys of the row smaller than it, up to kPer keys
+  // per lane at a time against one broadcast read of every key
+  constexpr int kPer = 8;
+  for (int t0 = 0; t0 < len; t0 += kWave * kPer) {
+    int64_t mine[kPer];
+    int rank[kPer];
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int t = t0 + lane + kWave * r;
+      mine[r] = t < len ? kb[t] : INT64_MAX;
+      rank[r] = 0;
+    }
+    for (int u = 0; u < len; ++u) {
+      const int64_t ku = kb[u];
+#pragma unroll
+      for (int r = 0; r < kPer; ++r) rank[r] += ku < mine[r] ? 1 : 0;
+    }
+#pragma unroll
+    for (int r = 0; r < kPer; ++r) {
+      const int t = t0 + lane + kWave * r;
+      if (t < len) {
+        const int64_t at = r0 + rank[r];
+        nbr_j[at] = static_cast<int32_t>(mine[r] >> 24);
+        nbr_shift[at] = static_cast<int32_t>(mine[r] & 0xFFFFFF);
+        if (keys) {
+          keys[at] = mine[r];
+          if ((at & 15) == 0) samples[at >> 4] = mine[r];
+        }
+      }
+    }
+  }
+  wave_lds_sync();   // the row's keys are read before the next row overwrites them
+}
+
 template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       const int64_t* __restrict__ qpos,
                                                       const int32_t* __restrict__ wrap,
                                                       const int32_t* __restrict__ cell_of,
                                                       const int32_t* __restrict__ start,
-                                                      const int32_t* __restrict__ atoms,
+                                                      const CellRec* __restrict__ rec,
                                                       const int64_t* __restrict__ row_ptr,
                                                       int32_t* __restrict__ nbr_j,
                                                       int32_t* __restrict__ nbr_shift, int64_t cap,
+                                                      int64_t* __restrict__ keys,
+                                                      int64_t* __restrict__ samples,
+                                                      int64_t* __restrict__ long_keys,
                                                       int64_t* __restrict__ flags) {
+  __shared__ SegLds segs[kWavesPerBlock];
   __shared__ int64_t keys_all[kWavesPerBlock][kMaxRow];
   if (row_ptr[n] > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -367,59 +534,21 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
     }
     return;
   }
-  int64_t* keys = keys_all[threadIdx.x / kWave];
-  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  SegLds& sg = segs[w];
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
-  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + w; i < n; i += nwaves) {
     const int64_t r0 = row_ptr[i];
     const int len = static_cast<int>(row_ptr[i + 1] - r0);
-    if (len > kMaxRow) {
-      if (lane == 0)
-        atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagRowTooLong);
-      continue;
+    if (len <= kMaxRow) {
+      fill_row<TRIC>(g, i, r0, len, keys_all[w], qpos, wrap, cell_of, start, rec, sg, nbr_j,
+                     nbr_shift, keys, samples, flags);
+    } else if (long_keys) {
+      fill_row<TRIC>(g, i, r0, len, long_keys + r0, qpos, wrap, cell_of, start, rec, sg, nbr_j,
+                     nbr_shift, keys, samples, flags);
+    } else if (lane_id() == 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagRowTooLong);
     }
-    int fill = 0;
-    bool shift_bad = false;
-    for_candidates<TRIC>(g, i, qpos, wrap, cell_of, start, atoms, [&](int32_t j, int nx, int ny, int nz, bool pred) {
-      uint64_t m;
-      int pre = ballot_prefix(pred, &m);
-      if (pred) {
-        if (nx < -127 || nx > 127 || ny < -127 || ny > 127 || nz < -127 || nz > 127) shift_bad = true;
-        int slot = fill + pre;
-        if (slot < kMaxRow)
-          keys[slot] = (int64_t(j) << 24) | int64_t(pack_shift(nx, ny, nz) & 0xFFFFFF);
-      }
-      fill += __popcll(m);
-    });
-    if (shift_bad)
-      atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagShift);
-    int np = 1;
-    while (np < len) np <<= 1;
-    for (int t = len + lane; t < np; t += kWave) keys[t] = INT64_MAX;
-    wave_lds_sync();
-    // bitonic sort of keys[0, np)
-    for (int k = 2; k <= np; k <<= 1) {
-      for (int jj = k >> 1; jj > 0; jj >>= 1) {
-        for (int t = lane; t < np; t += kWave) {
-          int p = t ^ jj;
-          if (p > t) {
-            int64_t a = keys[t], b = keys[p];
-            bool up = (t & k) == 0;
-            if ((a > b) == up) {
-              keys[t] = b;
-              keys[p] = a;
-            }
-          }
-        }
-        wave_lds_sync();
-      }
-    }
-    for (int t = lane; t < len; t += kWave) {
-      int64_t key = keys[t];
-      nbr_j[r0 + t] = static_cast<int32_t>(key >> 24);
-      nbr_shift[r0 + t] = static_cast<int32_t>(key & 0xFFFFFF);
-    }
-    wave_lds_sync();
   }
 }
 
@@ -430,26 +559,21 @@ __global__ void __launch_bounds__(kBlock) fill_i32_kernel(int32_t* __restrict__ 
     p[i] = v;
 }
 
-// Canonical key of a list entry: rows are sorted by it.
-__device__ inline int64_t entry_key(int32_t j, int32_t sh) {
-  return (int64_t(j) << 24) | int64_t(sh & 0xFFFFFF);
-}
-
-// Every 16th key of the list, samples[g] = key of entry 16 g, so that a
-// search inside a row first narrows to 16 entries through the row's samples
-// (contiguous, one or two cache lines) instead of probing the row itself.
-__global__ void __launch_bounds__(kBlock) sample_keys_kernel(const int64_t* __restrict__ row_ptr,
-                                                             int64_t n,
-                                                             const int32_t* __restrict__ nbr_j,
-                                                             const int32_t* __restrict__ nbr_shift,
-                                                             int64_t cap,
-                                                             int64_t* __restrict__ samples) {
+// keys[s] = key of entry s and samples[g] = keys[16 g], for a list built
+// elsewhere (a caller's)
+__global__ void __launch_bounds__(kBlock) key_kernel(const int64_t* __restrict__ row_ptr, int64_t n,
+                                                     const int32_t* __restrict__ nbr_j,
+                                                     const int32_t* __restrict__ nbr_shift,
+                                                     int64_t cap, int64_t* __restrict__ keys,
+                                                     int64_t* __restrict__ samples) {
   int64_t total = row_ptr[n];
-  total = total < cap ? total : cap;
-  const int64_t ng = (total + 15) >> 4;
-  for (int64_t g = blockIdx.x * int64_t(kBlock) + threadIdx.x; g < ng;
-       g += int64_t(gridDim.x) * kBlock)
-    samples[g] = entry_key(nbr_j[16 * g], nbr_shift[16 * g]);
+  total = total < cap ? (total < 0 ? 0 : total) : cap;
+  for (int64_t s = blockIdx.x * int64_t(kBlock) + threadIdx.x; s < total;
+       s += int64_t(gridDim.x) * kBlock) {
+    const int64_t k = entry_key(nbr_j[s], nbr_shift[s]);
+    keys[s] = k;
+    if ((s & 15) == 0) samples[s >> 4] = k;
+  }
 }
 
 // A row outside [0, cap] (a malformed caller list) gets no reverse entries and
@@ -461,42 +585,57 @@ __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0
 // every entry with its reverse, so only the canonical entry of a pair, the
 // one with key(j, n) > key(i, -n) (that is j > i, or a periodic self image
 // with the larger shift), searches; it writes both indices and returns true.
-// The search narrows [lo, hi) of row j with the samples at positions 16 g
-// inside it, then bisects at most 16 entries.
+// The samples inside row j (every 16th key of the list) are compared all at
+// once, which leaves a block of at most 16 keys; the position is the start
+// of that block plus the number of its keys below the one sought.  Rows with
+// more than 32 samples bisect them instead.
 __device__ inline bool reverse_search(int64_t n, int64_t i, int64_t s, int64_t b,
                                       const int64_t* __restrict__ row_ptr,
-                                      const int32_t* __restrict__ nbr_j,
-                                      const int32_t* __restrict__ nbr_shift, int64_t cap,
+                                      const int64_t* __restrict__ keys, int64_t cap,
                                       const int64_t* __restrict__ samples,
                                       int32_t* __restrict__ rev) {
-  const int32_t j = nbr_j[s], sh = nbr_shift[s];
-  const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(sh));
-  if (entry_key(j, sh) <= want) return false;   // the partner's row searches
-  if (j < 0 || j >= n || !row_ok(row_ptr[j], row_ptr[j + 1], cap)) return false;
+  const int64_t key = keys[s];
+  const int32_t j = static_cast<int32_t>(key >> 24);
+  const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(static_cast<int32_t>(key & 0xFFFFFF)));
+  if (key <= want) return false;   // the partner's row searches
+  if (j < 0 || j >= n) return false;
   const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
+  if (!row_ok(jb, je, cap) || je == jb) return false;
   int64_t lo = jb, hi = je;
   const int64_t g0 = (jb + 15) >> 4, g1 = (je - 1) >> 4;   // samples inside the row
-  if (je > jb && g0 <= g1) {
-    int64_t l = g0, h = g1 + 1;   // first sample above ``want``
-    while (l < h) {
-      const int64_t m = (l + h) >> 1;
-      if (samples[m] <= want) l = m + 1;
-      else h = m;
+  if (g0 <= g1) {
+    int64_t below;   // samples of the row not above ``want``
+    if (g1 - g0 < 32) {
+      below = 0;
+#pragma unroll 8
+      for (int64_t t = g0; t <= g1; ++t) below += samples[t] <= want ? 1 : 0;
+    } else {
+      int64_t l = g0, h = g1 + 1;
+      while (l < h) {
+        const int64_t m = (l + h) >> 1;
+        if (samples[m] <= want) l = m + 1;
+        else h = m;
+      }
+      below = l - g0;
     }
-    if (l > g0) lo = 16 * (l - 1);
-    if (l <= g1) hi = 16 * l;
+    if (below > 0) lo = 16 * (g0 + below - 1);
+    if (g0 + below <= g1) hi = 16 * (g0 + below);
   }
-  while (lo < hi) {
-    const int64_t mid = (lo + hi) >> 1;
-    if (entry_key(nbr_j[mid], nbr_shift[mid]) < want) lo = mid + 1;
-    else hi = mid;
+  // [lo, hi) holds at most 16 keys and the first key >= want of the row
+  int64_t pos = lo;
+  bool eq = false;
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    if (lo + t < hi) {
+      const int64_t k = keys[lo + t];
+      pos += k < want ? 1 : 0;
+      eq = eq || k == want;
+    }
   }
-  if (lo < je && entry_key(nbr_j[lo], nbr_shift[lo]) == want) {
-    rev[s] = static_cast<int32_t>(lo - jb);
-    rev[lo] = static_cast<int32_t>(s - b);
-    return true;
-  }
-  return false;
+  if (!eq) return false;
+  rev[s] = static_cast<int32_t>(pos - jb);
+  rev[pos] = static_cast<int32_t>(s - b);
+  return true;
 }
 
 // skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
@@ -506,22 +645,20 @@ __device__ inline bool reverse_search(int64_t n, int64_t i, int64_t s, int64_t b
 // the caller can tell a symmetric list (2 x pairs = entries) from one that
 // is not.
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
-                                                          const int32_t* __restrict__ nbr_j,
-                                                          const int32_t* __restrict__ nbr_shift,
-                                                          int64_t cap,
+                                                          const int64_t* __restrict__ keys, int64_t cap,
                                                           const int64_t* __restrict__ samples,
                                                           int32_t* __restrict__ rev,
                                                           unsigned long long* __restrict__ paired) {
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
-  for (int64_t i = blockIdx.x * int64_t(kWavesPerBlock) + threadIdx.x / kWave; i < n; i += nwaves) {
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave; i < n;
+       i += nwaves) {
     const int64_t b = row_ptr[i], e = row_ptr[i + 1];
     if (!row_ok(b, e, cap)) continue;
     unsigned long long found = 0;
     for (int64_t s0 = b; s0 < e; s0 += kWave) {
       const int64_t s = s0 + lane;
-      const bool hit =
-          s < e && reverse_search(n, i, s, b, row_ptr, nbr_j, nbr_shift, cap, samples, rev);
+      const bool hit = s < e && reverse_search(n, i, s, b, row_ptr, keys, cap, samples, rev);
       found += __popcll(__ballot(hit));
     }
     if (paired && lane == 0 && found) atomicAdd(paired, found);
@@ -625,33 +762,41 @@ int make_grid(const double cell[9], int64_t rq, CellGrid* g) {
                          h[0] * h[4] - h[1] * h[3]};
   for (int k = 0; k < 9; ++k) g->inv[k] = cof[k] / det;
   const double r = double(rq) / kQScale;
-  for (int a = 0; a < 3; ++a) {
-    int64_t nc;
-    if (!g->tric) {
-      const int64_t L = g->qh[4 * a];
-      nc = L / g->rq;
-      if (nc < 1) nc = 1;
-      if (nc > 1024) nc = 1024;
-      g->reach[a] = static_cast<int>((g->rq * nc + L - 1) / L);
-    } else {
-      // distance between the lattice planes of axis a: V / |h_b x h_c|
-      const double* u = h + 3 * ((a + 1) % 3);
-      const double* v = h + 3 * ((a + 2) % 3);
-      const double cx = u[1] * v[2] - u[2] * v[1], cy = u[2] * v[0] - u[0] * v[2],
-                   cz = u[0] * v[1] - u[1] * v[0];
-      const double d = vol / std::sqrt(cx * cx + cy * cy + cz * cz);
-      nc = static_cast<int64_t>(std::floor(d / r));
-      if (nc < 1) nc = 1;
-      if (nc > 1024) nc = 1024;
-      const double re = std::ceil((r + 1e-6) * double(nc) / d);
-      if (re > 1024.0) {
-        set_error("the cell is too thin for the neighbour radius");
-        return DPA4C_ERR_UNSUPPORTED;
+  // bins of about half the radius (sub = 2 per radius, stencil reach 2); a
+  // grid of more than kMaxFineBins bins (a sparse system in a large cell)
+  // falls back to radius-wide bins
+  constexpr int64_t kMaxFineBins = int64_t(1) << 24;
+  for (int sub = 2; sub >= 1; --sub) {
+    g->ncell = 1;
+    for (int a = 0; a < 3; ++a) {
+      int64_t nc;
+      if (!g->tric) {
+        const int64_t L = g->qh[4 * a];
+        nc = sub * L / g->rq;
+        if (nc < 1) nc = 1;
+        if (nc > 1024) nc = 1024;
+        g->reach[a] = static_cast<int>((g->rq * nc + L - 1) / L);
+      } else {
+        // distance between the lattice planes of axis a: V / |h_b x h_c|
+        const double* u = h + 3 * ((a + 1) % 3);
+        const double* v = h + 3 * ((a + 2) % 3);
+        const double cx = u[1] * v[2] - u[2] * v[1], cy = u[2] * v[0] - u[0] * v[2],
+                     cz = u[0] * v[1] - u[1] * v[0];
+        const double d = vol / std::sqrt(cx * cx + cy * cy + cz * cz);
+        nc = static_cast<int64_t>(std::floor(sub * d / r));
+        if (nc < 1) nc = 1;
+        if (nc > 1024) nc = 1024;
+        const double re = std::ceil((r + 1e-6) * double(nc) / d);
+        if (re > 1024.0) {
+          set_error("the cell is too thin for the neighbour radius");
+          return DPA4C_ERR_UNSUPPORTED;
+        }
+        g->reach[a] = static_cast<int>(re);
       }
-      g->reach[a] = static_cast<int>(re);
+      g->nc[a] = static_cast<int>(nc);
+      g->ncell *= nc;
     }
-    g->nc[a] = static_cast<int>(nc);
-    g->ncell *= nc;
+    if (g->ncell <= kMaxFineBins) break;
   }
   return 0;
 }
@@ -663,14 +808,13 @@ int ensure_scratch(NeighborScratch& nb, int64_t n, const CellGrid& g) {
   DPA4C_TRY(nb.cell_cnt.ensure(sizeof(int32_t) * g.ncell));
   DPA4C_TRY(nb.cell_start.ensure(sizeof(int32_t) * (g.ncell + 1)));
   DPA4C_TRY(nb.cell_fill.ensure(sizeof(int32_t) * g.ncell));
-  DPA4C_TRY(nb.cell_atoms.ensure(sizeof(int32_t) * n));
+  DPA4C_TRY(nb.cell_rec.ensure(sizeof(CellRec) * n));
   DPA4C_TRY(nb.counts.ensure(sizeof(int64_t) * n));
   return 0;
 }
 
 int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const CellGrid& g,
-                    int64_t* row_ptr, int32_t* nbr_j, int32_t* nbr_shift, int64_t cap,
-                    int64_t* flags, bool fill, hipStream_t st) {
+                    int64_t* row_ptr, int64_t* flags, hipStream_t st) {
   int rc = ensure_scratch(nb, n, g);
   if (rc) return rc;
   GridDev gd = to_dev(g);
@@ -689,39 +833,42 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
   hipLaunchKernelGGL(cell_scan_kernel, dim3(1), dim3(1024), 0, st, nb.cell_cnt.as<int32_t>(),
                      g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>());
   hipLaunchKernelGGL(place_kernel, dim3(blocks), dim3(kBlock), 0, st, n, nb.cell_of.as<int32_t>(),
-                     nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>(),
-                     nb.cell_atoms.as<int32_t>());
+                     nb.qpos.as<int64_t>(), nb.cell_start.as<int32_t>(),
+                     nb.cell_fill.as<int32_t>(), nb.cell_rec.as<CellRec>());
   if (g.tric)
     hipLaunchKernelGGL(count_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
-                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(),
-                       nb.counts.as<int64_t>());
+                       nb.qpos.as<int64_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(),
+                       nb.counts.as<int64_t>(), flags);
   else
     hipLaunchKernelGGL(count_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
-                       nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(),
-                       nb.counts.as<int64_t>());
+                       nb.qpos.as<int64_t>(), nb.cell_of.as<int32_t>(),
+                       nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(),
+                       nb.counts.as<int64_t>(), flags);
   DPA4C_HIP_TRY(hipGetLastError());
-  rc = exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, st);
-  if (rc) return rc;
-  if (fill) return fill_skin_list(nb, n, g, row_ptr, nbr_j, nbr_shift, cap, flags, st);
-  return 0;
+  return exclusive_scan(nb.counts.as<int64_t>(), n, row_ptr, nb.partials, st);
 }
 
 int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
-                   hipStream_t st) {
+                   int64_t max_row, int64_t* keys, hipStream_t st) {
   GridDev gd = to_dev(g);
+  int64_t* long_keys = nullptr;
+  if (max_row > kMaxRow) {
+    DPA4C_TRY(nb.long_keys.ensure(sizeof(int64_t) * size_t(cap < 1 ? 1 : cap)));
+    long_keys = nb.long_keys.as<int64_t>();
+  }
+  int64_t* samples = keys ? keys + cap : nullptr;
   if (g.tric)
     hipLaunchKernelGGL(fill_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j,
-                       nbr_shift, cap, flags);
+                       nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(), row_ptr, nbr_j,
+                       nbr_shift, cap, keys, samples, long_keys, flags);
   else
     hipLaunchKernelGGL(fill_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
-                       nb.cell_start.as<int32_t>(), nb.cell_atoms.as<int32_t>(), row_ptr, nbr_j,
-                       nbr_shift, cap, flags);
+                       nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(), row_ptr, nbr_j,
+                       nbr_shift, cap, keys, samples, long_keys, flags);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -740,18 +887,19 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int64_t* samples, int32_t* skin_rev, int64_t* paired,
-                    hipStream_t st) {
+                    int64_t n, int64_t cap, int64_t* keys, bool keys_ready, int32_t* skin_rev,
+                    int64_t* paired, hipStream_t st) {
   if (n <= 0) return 0;
-  int64_t sb = ((cap + 15) / 16 + kBlock - 1) / kBlock;
+  int64_t* samples = keys + cap;
+  int64_t sb = (cap + kBlock - 1) / kBlock;
   sb = sb < 1 ? 1 : (sb > 8192 ? 8192 : sb);
-  hipLaunchKernelGGL(sample_keys_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st, row_ptr,
-                     n, nbr_j, nbr_shift, cap, samples);
-  hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb * 16 > 8192 ? 8192 : sb * 16)),
-                     dim3(kBlock), 0, st, skin_rev, cap, -1);
-  hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, nbr_j,
-                     nbr_shift, cap, samples, skin_rev,
-                     reinterpret_cast<unsigned long long*>(paired));
+  if (!keys_ready)
+    hipLaunchKernelGGL(key_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st, row_ptr, n,
+                       nbr_j, nbr_shift, cap, keys, samples);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st,
+                     skin_rev, cap, -1);
+  hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, keys,
+                     cap, samples, skin_rev, reinterpret_cast<unsigned long long*>(paired));
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
