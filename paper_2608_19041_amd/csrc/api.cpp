@@ -516,11 +516,11 @@ int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* s
   if (own) w.list_valid = false;   // the reverse index now describes the caller's list
   {
     StageScope t(m, kStSkinRev, st, own);
-    // the reverse search's key samples live in the edge records, which the
+    // the reverse search's samples live in the edge records, which the
     // forward kernel rewrites before reading them
     rc = launch_zero_i64(B.check, 2, st);
     if (rc) return rc;
-    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, reinterpret_cast<int64_t*>(B.edge),
+    rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, reinterpret_cast<int32_t*>(B.edge),
                          false, B.skin_rev, B.check, st);
     if (rc) return rc;
   }
@@ -721,14 +721,14 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     r = ensure_workspace(mm, N, w.cap);
     if (r) return r;
     StageScope t(m, kStNeighbor, st);
-    // the keys for the reverse search go to the edge records, which the
+    // the samples for the reverse search go to the edge records, which the
     // forward kernel rewrites before reading them
     r = fill_skin_list(w.nb, N, g_list, w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(),
                        w.skin_shift.as<int32_t>(), w.cap, flags, w.host_flags[2],
-                       w.edge.as<int64_t>(), st);
+                       w.edge.as<int32_t>(), st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.edge.as<int64_t>(), true, w.skin_rev.as<int32_t>(), nullptr, st);
+                        N, w.cap, w.edge.as<int32_t>(), true, w.skin_rev.as<int32_t>(), nullptr, st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
     if (r) return r;

@@ -20,22 +20,22 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
                     int64_t* row_ptr, int64_t* flags, hipStream_t st);
 // the sorted rows of a counted list; ``max_row`` (the longest row, from the
 // count) above the LDS row size makes the fill use a global scratch for
-// those rows.  With ``keys`` (int64 [cap + cap / 16 + 1]) the rows' keys and
-// every 16th of them are also written there for launch_skin_rev.
+// those rows.  With ``jsamp`` (int32 [cap / 16 + 1]) the neighbour index at
+// every 16th position of the list also goes there for launch_skin_rev.
 int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
-                   int64_t max_row, int64_t* keys, hipStream_t st);
+                   int64_t max_row, int32_t* jsamp, hipStream_t st);
 // per-axis min and max of the fixed-point positions Q(x) (finite ones):
 // host6 = [min x, y, z, max x, y, z]; dev6 is device scratch of 6 int64;
 // synchronises ``st``
 int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
 // skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1;
-// keys = scratch of cap + cap / 16 + 1 int64: the list's keys and every 16th
-// of them, computed here unless ``keys_ready`` (fill_skin_list wrote them);
+// jsamp = scratch of cap / 16 + 1 int32: nbr_j at every 16th position of the
+// list, computed here unless ``jsamp_ready`` (fill_skin_list wrote it);
 // with ``paired`` (device int64, zeroed by the caller) also the number of
 // reverse pairs found, so a symmetric list of E entries gives E / 2
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int64_t* keys, bool keys_ready, int32_t* skin_rev,
+                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
                     int64_t* paired, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded

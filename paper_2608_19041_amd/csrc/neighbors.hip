@@ -158,35 +158,6 @@ __global__ void __launch_bounds__(kBlock) bin_kernel(const double* __restrict__ 
   atomicAdd(&cell_cnt[cid], 1);
 }
 
-// exclusive scan of the (few thousand) cell counts in one block
-__global__ void __launch_bounds__(1024) cell_scan_kernel(const int32_t* __restrict__ cnt,
-                                                         int64_t ncell, int32_t* __restrict__ start,
-                                                         int32_t* __restrict__ fill) {
-  __shared__ int32_t part[1024];
-  int64_t per = (ncell + 1023) / 1024;
-  int64_t b = threadIdx.x * per, e = b + per < ncell ? b + per : ncell;
-  int32_t s = 0;
-  for (int64_t k = b; k < e; ++k) s += cnt[k];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int32_t run = 0;
-    for (int t = 0; t < 1024; ++t) {
-      int32_t v = part[t];
-      part[t] = run;
-      run += v;
-    }
-    start[ncell] = run;
-  }
-  __syncthreads();
-  int32_t run = part[threadIdx.x];
-  for (int64_t k = b; k < e; ++k) {
-    start[k] = run;
-    fill[k] = 0;
-    run += cnt[k];
-  }
-}
-
 // One candidate record per atom, in bin order: the wrapped fixed-point
 // position and the atom index (32 bytes, read by two 16-byte loads).
 struct alignas(16) CellRec {
@@ -365,8 +336,8 @@ __device__ inline int64_t block_exclusive_scan(int64_t v, int64_t* sh, int64_t* 
   return incl - v;
 }
 
-__global__ void __launch_bounds__(kBlock) scan_partials_kernel(const int64_t* __restrict__ in,
-                                                               int64_t n,
+template <class T>
+__global__ void __launch_bounds__(kBlock) scan_partials_kernel(const T* __restrict__ in, int64_t n,
                                                                int64_t* __restrict__ partials) {
   __shared__ int64_t sh[kBlock];
   int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
@@ -392,36 +363,37 @@ __global__ void __launch_bounds__(kBlock) scan_top_kernel(int64_t* __restrict__ 
   }
 }
 
-__global__ void __launch_bounds__(kBlock) scan_apply_kernel(const int64_t* __restrict__ in,
-                                                            int64_t n,
+template <class T>
+__global__ void __launch_bounds__(kBlock) scan_apply_kernel(const T* __restrict__ in, int64_t n,
                                                             const int64_t* __restrict__ partials,
-                                                            int64_t* __restrict__ out) {
+                                                            T* __restrict__ out) {
   __shared__ int64_t sh[kBlock];
   int64_t base = blockIdx.x * int64_t(kScanTile) + threadIdx.x * kScanPer;
   int64_t v[kScanPer];
   int64_t s = 0;
   for (int k = 0; k < kScanPer; ++k) {
-    v[k] = base + k < n ? in[base + k] : 0;
+    v[k] = base + k < n ? int64_t(in[base + k]) : 0;
     s += v[k];
   }
   int64_t tot;
   int64_t run = block_exclusive_scan(s, sh, &tot) + partials[blockIdx.x];
   for (int k = 0; k < kScanPer; ++k) {
-    if (base + k < n) out[base + k] = run;
+    if (base + k < n) out[base + k] = static_cast<T>(run);
     run += v[k];
   }
-  if (base <= n - 1 && n - 1 < base + kScanPer) out[n] = run;  // thread holding the last element
+  if (base <= n - 1 && n - 1 < base + kScanPer) out[n] = static_cast<T>(run);  // thread holding the last element
 }
 
-int exclusive_scan(const int64_t* in, int64_t n, int64_t* out, DevBuf& partials,
-                   hipStream_t st) {
+// exclusive scan out[0..n] of in[0..n) with out[n] = the total (int32 or int64)
+template <class T>
+int exclusive_scan(const T* in, int64_t n, T* out, DevBuf& partials, hipStream_t st) {
   int64_t nb = (n + kScanTile - 1) / kScanTile;
   if (nb == 0) nb = 1;
   DPA4C_TRY(partials.ensure(sizeof(int64_t) * nb));
-  hipLaunchKernelGGL(scan_partials_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
+  hipLaunchKernelGGL(scan_partials_kernel<T>, dim3(nb), dim3(kBlock), 0, st, in, n,
                      partials.as<int64_t>());
   hipLaunchKernelGGL(scan_top_kernel, dim3(1), dim3(kBlock), 0, st, partials.as<int64_t>(), nb);
-  hipLaunchKernelGGL(scan_apply_kernel, dim3(nb), dim3(kBlock), 0, st, in, n,
+  hipLaunchKernelGGL(scan_apply_kernel<T>, dim3(nb), dim3(kBlock), 0, st, in, n,
                      partials.as<int64_t>(), out);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
@@ -433,14 +405,43 @@ __device__ inline int64_t entry_key(int32_t j, int32_t sh) {
   return (int64_t(j) << 24) | int64_t(sh & 0xFFFFFF);
 }
 
-// Rows of the skin list: the accepted candidates of centre i as keys
-// (j, packed n), each written at its rank in the row (the number of smaller
-// keys; keys of a row are distinct), so rows come out in canonical order.
-// With ``keys`` the keys are also written to keys[row_ptr[i] + rank], and
-// every 16th of them (absolute position 16 g) to samples[g], for the
-// reverse search.  Rows longer than kMaxRow collect their keys in
-// long_keys[row_ptr[i] ...] instead of LDS (the host passes it when the
-// count found such rows; without it they are flagged).
+// Writes the keys kb[0, len) of a row at their ranks, the number of smaller
+// keys in the row (keys of a row are distinct), PER keys per lane at a time
+// against one broadcast read of every key; with ``jsamp`` also j of every
+// entry at an absolute position 16 g, to jsamp[g].
+template <int PER, class KB>
+__device__ __forceinline__ void rank_row(int len, int64_t r0, KB* kb, int32_t* __restrict__ nbr_j,
+                                         int32_t* __restrict__ nbr_shift,
+                                         int32_t* __restrict__ jsamp) {
+  const int lane = lane_id();
+  for (int t0 = 0; t0 < len; t0 += kWave * PER) {
+    int64_t mine[PER];
+    int rank[PER];
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int t = t0 + lane + kWave * r;
+      mine[r] = t < len ? kb[t] : INT64_MAX;
+      rank[r] = 0;
+    }
+    for (int u = 0; u < len; ++u) {
+      const int64_t ku = kb[u];
+#pragma unroll
+      for (int r = 0; r < PER; ++r) rank[r] += ku < mine[r] ? 1 : 0;
+    }
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int t = t0 + lane + kWave * r;
+      if (t < len) {
+        const int64_t at = r0 + rank[r];
+        const int32_t j = static_cast<int32_t>(mine[r] >> 24);
+        nbr_j[at] = j;
+        nbr_shift[at] = static_cast<int32_t>(mine[r] & 0xFFFFFF);
+        if (jsamp && (at & 15) == 0) jsamp[at >> 4] = j;
+      }
+    }
+  }
+}
+
 // One row: the accepted keys into kb[0, len) in candidate order, then
 // each written at its rank.  ``kb`` is the wave's LDS row or, for a row
 // longer than kMaxRow, a global scratch row (inlined for each, so LDS rows
@@ -454,9 +455,7 @@ __device__ __forceinline__ void fill_row(const GridDev& g, int64_t i, int64_t r0
                                          const CellRec* __restrict__ rec, SegLds& sg,
                                          int32_t* __restrict__ nbr_j,
                                          int32_t* __restrict__ nbr_shift,
-                                         int64_t* __restrict__ keys, int64_t* __restrict__ samples,
-                                         int64_t* __restrict__ flags) {
-  const int lane = lane_id();
+                                         int32_t* __restrict__ jsamp, int64_t* __restrict__ flags) {
   const int mi0 = wrap[3 * i], mi1 = wrap[3 * i + 1], mi2 = wrap[3 * i + 2];
   int fill = 0;
   bool shift_bad = false;
@@ -477,40 +476,20 @@ __device__ __forceinline__ void fill_row(const GridDev& g, int64_t i, int64_t r0
   if (shift_bad)
     atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagShift);
   wave_lds_sync();
-  // rank of each key: the keys of the row smaller than it, up to kPer keys
-  // per lane at a time against one broadcast read of every key
-  constexpr int kPer = 8;
-  for (int t0 = 0; t0 < len; t0 += kWave * kPer) {
-    int64_t mine[kPer];
-    int rank[kPer];
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int t = t0 + lane + kWave * r;
-      mine[r] = t < len ? kb[t] : INT64_MAX;
-      rank[r] = 0;
-    }
-    for (int u = 0; u < len; ++u) {
-      const int64_t ku = kb[u];
-#pragma unroll
-      for (int r = 0; r < kPer; ++r) rank[r] += ku < mine[r] ? 1 : 0;
-    }
-#pragma unroll
-    for (int r = 0; r < kPer; ++r) {
-      const int t = t0 + lane + kWave * r;
-      if (t < len) {
-        const int64_t at = r0 + rank[r];
-        nbr_j[at] = static_cast<int32_t>(mine[r] >> 24);
-        nbr_shift[at] = static_cast<int32_t>(mine[r] & 0xFFFFFF);
-        if (keys) {
-          keys[at] = mine[r];
-          if ((at & 15) == 0) samples[at >> 4] = mine[r];
-        }
-      }
-    }
-  }
+  if (len <= kWave) rank_row<1>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+  else if (len <= 2 * kWave) rank_row<2>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+  else if (len <= 4 * kWave) rank_row<4>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+  else rank_row<8>(len, r0, kb, nbr_j, nbr_shift, jsamp);
   wave_lds_sync();   // the row's keys are read before the next row overwrites them
 }
 
+// Rows of the skin list: the accepted candidates of centre i as keys
+// (j, packed n), each written at its rank in the row, so rows come out in
+// canonical order.  With ``jsamp`` the neighbour index of every entry at an
+// absolute position 16 g also goes to jsamp[g], for the reverse search.
+// Rows longer than kMaxRow collect their keys in long_keys[row_ptr[i] ...]
+// instead of LDS (the host passes it when the count found such rows;
+// without it they are flagged).
 template <bool TRIC>
 __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       const int64_t* __restrict__ qpos,
@@ -521,8 +500,7 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       const int64_t* __restrict__ row_ptr,
                                                       int32_t* __restrict__ nbr_j,
                                                       int32_t* __restrict__ nbr_shift, int64_t cap,
-                                                      int64_t* __restrict__ keys,
-                                                      int64_t* __restrict__ samples,
+                                                      int32_t* __restrict__ jsamp,
                                                       int64_t* __restrict__ long_keys,
                                                       int64_t* __restrict__ flags) {
   __shared__ SegLds segs[kWavesPerBlock];
@@ -542,10 +520,10 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
     const int len = static_cast<int>(row_ptr[i + 1] - r0);
     if (len <= kMaxRow) {
       fill_row<TRIC>(g, i, r0, len, keys_all[w], qpos, wrap, cell_of, start, rec, sg, nbr_j,
-                     nbr_shift, keys, samples, flags);
+                     nbr_shift, jsamp, flags);
     } else if (long_keys) {
       fill_row<TRIC>(g, i, r0, len, long_keys + r0, qpos, wrap, cell_of, start, rec, sg, nbr_j,
-                     nbr_shift, keys, samples, flags);
+                     nbr_shift, jsamp, flags);
     } else if (lane_id() == 0) {
       atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagRowTooLong);
     }
@@ -559,110 +537,153 @@ __global__ void __launch_bounds__(kBlock) fill_i32_kernel(int32_t* __restrict__ 
     p[i] = v;
 }
 
-// keys[s] = key of entry s and samples[g] = keys[16 g], for a list built
-// elsewhere (a caller's)
-__global__ void __launch_bounds__(kBlock) key_kernel(const int64_t* __restrict__ row_ptr, int64_t n,
-                                                     const int32_t* __restrict__ nbr_j,
-                                                     const int32_t* __restrict__ nbr_shift,
-                                                     int64_t cap, int64_t* __restrict__ keys,
-                                                     int64_t* __restrict__ samples) {
+// jsamp[g] = nbr_j[16 g], for a list built elsewhere (a caller's)
+__global__ void __launch_bounds__(kBlock) jsamp_kernel(const int64_t* __restrict__ row_ptr, int64_t n,
+                                                       const int32_t* __restrict__ nbr_j, int64_t cap,
+                                                       int32_t* __restrict__ jsamp) {
   int64_t total = row_ptr[n];
   total = total < cap ? (total < 0 ? 0 : total) : cap;
-  for (int64_t s = blockIdx.x * int64_t(kBlock) + threadIdx.x; s < total;
-       s += int64_t(gridDim.x) * kBlock) {
-    const int64_t k = entry_key(nbr_j[s], nbr_shift[s]);
-    keys[s] = k;
-    if ((s & 15) == 0) samples[s >> 4] = k;
-  }
+  for (int64_t g = blockIdx.x * int64_t(kBlock) + threadIdx.x; 16 * g < total;
+       g += int64_t(gridDim.x) * kBlock)
+    jsamp[g] = nbr_j[16 * g];
 }
 
 // A row outside [0, cap] (a malformed caller list) gets no reverse entries and
 // is nobody's reverse row, like the compaction, which keeps nothing of it.
 __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0 && e >= b && e <= cap; }
 
-// The reverse search of entry s = (i -> j, n) of row i (which begins at
-// b): the position of the key (i, -n) within row j.  A symmetric list pairs
-// every entry with its reverse, so only the canonical entry of a pair, the
-// one with key(j, n) > key(i, -n) (that is j > i, or a periodic self image
-// with the larger shift), searches; it writes both indices and returns true.
-// The samples inside row j (every 16th key of the list) are compared all at
-// once, which leaves a block of at most 16 keys; the position is the start
-// of that block plus the number of its keys below the one sought.  Rows with
-// more than 32 samples bisect them instead.
-__device__ inline bool reverse_search(int64_t n, int64_t i, int64_t s, int64_t b,
+// The reverse search of entry s = (i -> j, n): the position of the entry
+// (i, -n) within row j, written to rev[s] (row-local) and the position of s
+// within row i to rev of that entry.  Row j is ordered by neighbour index,
+// so the entries (i, m) of row j are consecutive and begin at the first
+// entry with neighbour index >= i: the samples of row j (the neighbour
+// index at every absolute position 16 g inside it) are bisected for the
+// aligned block of 16 entries that holds it, that block is compared at once
+// (four 16-byte loads with VEC, one load per entry without), and the entries
+// (i, m) from there are matched on the image.
+template <bool VEC>
+__device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s,
                                       const int64_t* __restrict__ row_ptr,
-                                      const int64_t* __restrict__ keys, int64_t cap,
-                                      const int64_t* __restrict__ samples,
+                                      const int32_t* __restrict__ nbr_j,
+                                      const int32_t* __restrict__ nbr_shift, int64_t cap,
+                                      const int32_t* __restrict__ jsamp,
                                       int32_t* __restrict__ rev) {
-  const int64_t key = keys[s];
-  const int32_t j = static_cast<int32_t>(key >> 24);
-  const int64_t want = entry_key(static_cast<int32_t>(i), negate_shift(static_cast<int32_t>(key & 0xFFFFFF)));
-  if (key <= want) return false;   // the partner's row searches
+  const int32_t j = nbr_j[s];
+  const int32_t want_sh = negate_shift(nbr_shift[s]);
   if (j < 0 || j >= n) return false;
   const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
   if (!row_ok(jb, je, cap) || je == jb) return false;
-  int64_t lo = jb, hi = je;
   const int64_t g0 = (jb + 15) >> 4, g1 = (je - 1) >> 4;   // samples inside the row
+  int64_t l = g0;                                           // first sample >= i
   if (g0 <= g1) {
-    int64_t below;   // samples of the row not above ``want``
-    if (g1 - g0 < 32) {
-      below = 0;
-#pragma unroll 8
-      for (int64_t t = g0; t <= g1; ++t) below += samples[t] <= want ? 1 : 0;
-    } else {
-      int64_t l = g0, h = g1 + 1;
-      while (l < h) {
-        const int64_t m = (l + h) >> 1;
-        if (samples[m] <= want) l = m + 1;
-        else h = m;
-      }
-      below = l - g0;
+    int64_t h = g1 + 1;
+    while (l < h) {
+      const int64_t m = (l + h) >> 1;
+      if (jsamp[m] < i) l = m + 1;
+      else h = m;
     }
-    if (below > 0) lo = 16 * (g0 + below - 1);
-    if (g0 + below <= g1) hi = 16 * (g0 + below);
   }
-  // [lo, hi) holds at most 16 keys and the first key >= want of the row
-  int64_t pos = lo;
-  bool eq = false;
+  // the first entry >= i lies in [lo, hi), inside the aligned block [16 q, 16 q + 16)
+  const int64_t lo = l > g0 ? 16 * (l - 1) : jb;
+  const int64_t hi = l <= g1 ? 16 * l : je;
+  const int64_t q16 = l > g0 ? 16 * (l - 1) : 16 * (g0 - 1);
+  int64_t p = lo;
+  if (VEC) {
+    const int4* blk = reinterpret_cast<const int4*>(nbr_j + q16);
 #pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    if (lo + t < hi) {
-      const int64_t k = keys[lo + t];
-      pos += k < want ? 1 : 0;
-      eq = eq || k == want;
+    for (int v = 0; v < 4; ++v) {
+      const int64_t t = q16 + 4 * v;
+      if (t + 3 >= lo && t < hi) {
+        const int4 x = blk[v];
+        p += (t >= lo && t < hi && x.x < i) + (t + 1 >= lo && t + 1 < hi && x.y < i) +
+             (t + 2 >= lo && t + 2 < hi && x.z < i) + (t + 3 >= lo && t + 3 < hi && x.w < i);
+      }
     }
+  } else {
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      if (lo + t < hi && nbr_j[lo + t] < i) ++p;
   }
-  if (!eq) return false;
-  rev[s] = static_cast<int32_t>(pos - jb);
-  rev[pos] = static_cast<int32_t>(s - b);
-  return true;
+  for (int64_t t = p; t < je && nbr_j[t] == i; ++t)
+    if (nbr_shift[t] == want_sh) {
+      rev[s] = static_cast<int32_t>(t - jb);
+      rev[t] = static_cast<int32_t>(s - row_ptr[i]);
+      return true;
+    }
+  return false;
 }
 
 // skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
-// (i, -n), within row j, or -1.  One wave per row i.  Entries whose partner
-// is missing (a malformed caller list) keep the -1 of the fill before.  With
-// ``paired`` the pairs found are counted (one atomic per wave and row), so
-// the caller can tell a symmetric list (2 x pairs = entries) from one that
-// is not.
+// (i, -n), within row j, or -1.  A symmetric list pairs every entry with its
+// reverse, so only the canonical entry of a pair, the one with
+// key(j, n) > key(i, -n) (that is j > i, or a periodic self image with the
+// larger shift), searches and writes both indices.  One wave takes rows in
+// turn and queues their canonical entries in LDS, so every search round
+// runs 64 searches.  Entries whose partner is missing (a malformed caller
+// list) keep the -1 of the fill before.  With ``paired`` the pairs found
+// are counted (one atomic per wave), so the caller can tell a symmetric list
+// (2 x pairs = entries) from one that is not.
+template <bool VEC>
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
-                                                          const int64_t* __restrict__ keys, int64_t cap,
-                                                          const int64_t* __restrict__ samples,
+                                                          const int32_t* __restrict__ nbr_j,
+                                                          const int32_t* __restrict__ nbr_shift,
+                                                          int64_t cap,
+                                                          const int32_t* __restrict__ jsamp,
                                                           int32_t* __restrict__ rev,
                                                           unsigned long long* __restrict__ paired) {
+  __shared__ int64_t qs_all[kWavesPerBlock][2 * kWave];
+  __shared__ int32_t qi_all[kWavesPerBlock][2 * kWave];
+  const int w = threadIdx.x / kWave;
+  int64_t* qs = qs_all[w];
+  int32_t* qi = qi_all[w];
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
-  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + threadIdx.x / kWave; i < n;
-       i += nwaves) {
+  unsigned long long found = 0;
+  int qn = 0;   // queued searches (wave-uniform)
+  // runs the first ``count`` (<= 64) queued searches and moves the rest down
+  auto run = [&](int count) {
+    const bool hit = lane < count &&
+                     reverse_search<VEC>(n, qi[lane], qs[lane], row_ptr, nbr_j, nbr_shift, cap,
+                                         jsamp, rev);
+    found += __popcll(__ballot(hit));
+    const int rest = qn - count;
+    int64_t ks = 0;
+    int32_t ki = 0;
+    if (lane < rest) {
+      ks = qs[count + lane];
+      ki = qi[count + lane];
+    }
+    wave_lds_sync();
+    if (lane < rest) {
+      qs[lane] = ks;
+      qi[lane] = ki;
+    }
+    wave_lds_sync();
+    qn = rest;
+  };
+  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + w; i < n; i += nwaves) {
     const int64_t b = row_ptr[i], e = row_ptr[i + 1];
     if (!row_ok(b, e, cap)) continue;
-    unsigned long long found = 0;
     for (int64_t s0 = b; s0 < e; s0 += kWave) {
       const int64_t s = s0 + lane;
-      const bool hit = s < e && reverse_search(n, i, s, b, row_ptr, keys, cap, samples, rev);
-      found += __popcll(__ballot(hit));
+      bool canon = false;
+      if (s < e) {
+        const int32_t sh = nbr_shift[s];
+        canon = entry_key(nbr_j[s], sh) > entry_key(static_cast<int32_t>(i), negate_shift(sh));
+      }
+      uint64_t m;
+      const int pre = ballot_prefix(canon, &m);
+      if (canon) {
+        qs[qn + pre] = s;
+        qi[qn + pre] = static_cast<int32_t>(i);
+      }
+      qn += __popcll(m);
+      wave_lds_sync();
+      if (qn >= kWave) run(kWave);
     }
-    if (paired && lane == 0 && found) atomicAdd(paired, found);
   }
+  if (qn > 0) run(qn);
+  if (paired && lane == 0 && found) atomicAdd(paired, found);
 }
 
 // per-axis minimum and maximum of the fixed-point positions (exact integer
@@ -810,6 +831,9 @@ int ensure_scratch(NeighborScratch& nb, int64_t n, const CellGrid& g) {
   DPA4C_TRY(nb.cell_fill.ensure(sizeof(int32_t) * g.ncell));
   DPA4C_TRY(nb.cell_rec.ensure(sizeof(CellRec) * n));
   DPA4C_TRY(nb.counts.ensure(sizeof(int64_t) * n));
+  // the bin counts and the row counts are scanned with the same partials
+  const int64_t most = std::max<int64_t>(n, g.ncell);
+  DPA4C_TRY(nb.partials.ensure(sizeof(int64_t) * size_t((most + kScanTile - 1) / kScanTile + 1)));
   return 0;
 }
 
@@ -830,8 +854,11 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
     hipLaunchKernelGGL(bin_kernel<false>, dim3(blocks), dim3(kBlock), 0, st, pos, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
                        nb.cell_cnt.as<int32_t>(), flags);
-  hipLaunchKernelGGL(cell_scan_kernel, dim3(1), dim3(1024), 0, st, nb.cell_cnt.as<int32_t>(),
-                     g.ncell, nb.cell_start.as<int32_t>(), nb.cell_fill.as<int32_t>());
+  rc = exclusive_scan(nb.cell_cnt.as<int32_t>(), g.ncell, nb.cell_start.as<int32_t>(), nb.partials,
+                      st);
+  if (rc) return rc;
+  hipLaunchKernelGGL(zero_i32_kernel, dim3(cblocks), dim3(kBlock), 0, st,
+                     nb.cell_fill.as<int32_t>(), g.ncell);
   hipLaunchKernelGGL(place_kernel, dim3(blocks), dim3(kBlock), 0, st, n, nb.cell_of.as<int32_t>(),
                      nb.qpos.as<int64_t>(), nb.cell_start.as<int32_t>(),
                      nb.cell_fill.as<int32_t>(), nb.cell_rec.as<CellRec>());
@@ -851,24 +878,23 @@ int build_skin_list(NeighborScratch& nb, const double* pos, int64_t n, const Cel
 
 int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int64_t* row_ptr,
                    int32_t* nbr_j, int32_t* nbr_shift, int64_t cap, int64_t* flags,
-                   int64_t max_row, int64_t* keys, hipStream_t st) {
+                   int64_t max_row, int32_t* jsamp, hipStream_t st) {
   GridDev gd = to_dev(g);
   int64_t* long_keys = nullptr;
   if (max_row > kMaxRow) {
     DPA4C_TRY(nb.long_keys.ensure(sizeof(int64_t) * size_t(cap < 1 ? 1 : cap)));
     long_keys = nb.long_keys.as<int64_t>();
   }
-  int64_t* samples = keys ? keys + cap : nullptr;
   if (g.tric)
     hipLaunchKernelGGL(fill_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
                        nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(), row_ptr, nbr_j,
-                       nbr_shift, cap, keys, samples, long_keys, flags);
+                       nbr_shift, cap, jsamp, long_keys, flags);
   else
     hipLaunchKernelGGL(fill_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, gd,
                        nb.qpos.as<int64_t>(), nb.wrap.as<int32_t>(), nb.cell_of.as<int32_t>(),
                        nb.cell_start.as<int32_t>(), nb.cell_rec.as<CellRec>(), row_ptr, nbr_j,
-                       nbr_shift, cap, keys, samples, long_keys, flags);
+                       nbr_shift, cap, jsamp, long_keys, flags);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -887,19 +913,30 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int64_t* keys, bool keys_ready, int32_t* skin_rev,
+                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
                     int64_t* paired, hipStream_t st) {
   if (n <= 0) return 0;
-  int64_t* samples = keys + cap;
   int64_t sb = (cap + kBlock - 1) / kBlock;
   sb = sb < 1 ? 1 : (sb > 8192 ? 8192 : sb);
-  if (!keys_ready)
-    hipLaunchKernelGGL(key_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st, row_ptr, n,
-                       nbr_j, nbr_shift, cap, keys, samples);
+  if (!jsamp_ready) {
+    int64_t jb = (cap / 16 + kBlock) / kBlock;
+    jb = jb < 1 ? 1 : (jb > 4096 ? 4096 : jb);
+    hipLaunchKernelGGL(jsamp_kernel, dim3(static_cast<unsigned>(jb)), dim3(kBlock), 0, st, row_ptr,
+                       n, nbr_j, cap, jsamp);
+  }
   hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st,
                      skin_rev, cap, -1);
-  hipLaunchKernelGGL(skin_rev_kernel, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr, keys,
-                     cap, samples, skin_rev, reinterpret_cast<unsigned long long*>(paired));
+  // the block compare reads 16-byte groups of nbr_j: a list that is not
+  // 16-byte aligned takes one load per entry
+  const bool vec = (reinterpret_cast<uintptr_t>(nbr_j) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(skin_rev_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr,
+                       nbr_j, nbr_shift, cap, jsamp, skin_rev,
+                       reinterpret_cast<unsigned long long*>(paired));
+  else
+    hipLaunchKernelGGL(skin_rev_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr,
+                       nbr_j, nbr_shift, cap, jsamp, skin_rev,
+                       reinterpret_cast<unsigned long long*>(paired));
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
