@@ -142,38 +142,43 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j),
-        // power form; the float16 c4, c5 enter through their scaled weights
+        // power form; the float16 c2 .. c5 enter through their scaled weights
         // (one mixed-precision FMA each).  The weighted sums a0 and b0 only
         // need the lane's coefficients contracted with dE/dY0 first,
         // A_p = sum_j Ybar0_j c_pj, and then one quintic in tau and its
         // derivative; d/drho's 1/Delta is applied once to the sums.
         const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
-        const float e4 = md.c45_inv[0] * t4, e5 = md.c45_inv[1] * t5;
-        const float f4 = md.c45_inv[0] * d3, f5 = md.c45_inv[1] * d4;
+        const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
+        const float e4 = md.c_inv[2] * t4, e5 = md.c_inv[3] * t5;
+        const float f2 = md.c_inv[0] * d1, f3 = md.c_inv[1] * d2;
+        const float f4 = md.c_inv[2] * d3, f5 = md.c_inv[3] * d4;
         float A[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          float4 c;
-          uint32_t h;
-          load_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, &c, &h);
-          const float h4 = half_lo(h), h5 = half_hi(h);
+          float c0, c1;
+          uint32_t h23, h45;
+          load_folded(ft + jj * P::LPE * kFoldWords, k, &c0, &c1, &h23, &h45);
+          const float h2 = half_lo(h23), h3 = half_hi(h23), h4 = half_lo(h45), h5 = half_hi(h45);
           if (jj == 0) {   // the amplitude of the lane's first channel itself
-            psi0 = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
+            psi0 = fmaf(c1, tau, c0);
+            psi0 = fmaf(h2, e2, psi0);
+            psi0 = fmaf(h3, e3, psi0);
             psi0 = fmaf(h4, e4, psi0);
             psi0 = fmaf(h5, e5, psi0);
-            dpsi0 = fmaf(c.w, d2, fmaf(c.z, d1, c.y));
+            dpsi0 = fmaf(h2, f2, c1);
+            dpsi0 = fmaf(h3, f3, dpsi0);
             dpsi0 = fmaf(h4, f4, dpsi0);
             dpsi0 = fmaf(h5, f5, dpsi0);
           }
-          A[0] = fmaf(gy0[jj], c.x, A[0]);
-          A[1] = fmaf(gy0[jj], c.y, A[1]);
-          A[2] = fmaf(gy0[jj], c.z, A[2]);
-          A[3] = fmaf(gy0[jj], c.w, A[3]);
+          A[0] = fmaf(gy0[jj], c0, A[0]);
+          A[1] = fmaf(gy0[jj], c1, A[1]);
+          A[2] = fmaf(gy0[jj], h2, A[2]);
+          A[3] = fmaf(gy0[jj], h3, A[3]);
           A[4] = fmaf(gy0[jj], h4, A[4]);
           A[5] = fmaf(gy0[jj], h5, A[5]);
         }
-        a0 = fmaf(A[5], e5, fmaf(A[4], e4, fmaf(A[3], t3, fmaf(A[2], t2, fmaf(A[1], tau, A[0])))));
-        b0 = fmaf(A[5], f5, fmaf(A[4], f4, fmaf(A[3], d2, fmaf(A[2], d1, A[1])))) * inv_delta;
+        a0 = fmaf(A[5], e5, fmaf(A[4], e4, fmaf(A[3], e3, fmaf(A[2], e2, fmaf(A[1], tau, A[0])))));
+        b0 = fmaf(A[5], f5, fmaf(A[4], f4, fmaf(A[3], f3, fmaf(A[2], f2, A[1])))) * inv_delta;
         dpsi0 *= inv_delta;
       } else {
         float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};

@@ -153,16 +153,16 @@ struct ModelDev {
   const float* cpl;         // [kCouplings]: C123 then C233 (symmetric in m2, m3), or null
   const float* E_ref;       // [T+1]
   // pair-folded tables (fold.hip), used when fold_n > 0:
-  // [fold_n^2 pairs][n_rows][CPL] blocks of 5 LPE words, pair (fa, fb) at
-  // fa * fold_n + fb; c45_inv = the inverse scales of the fp16 c4 and c5
+  // [fold_n^2 pairs][n_rows][CPL] blocks of 4 LPE words, pair (fa, fb) at
+  // fa * fold_n + fb; c_inv = the inverse scales of the float16 c2 .. c5
   const float* ftab;
   int fold_n;
-  float c45_inv[2];
+  float c_inv[4];
 };
 
-// Words per channel of a folded table: c0..c3 as float32, c4 and c5 as a
-// scaled float16 pair in one word.
-constexpr int kFoldWords = 5;
+// Words per channel of a folded table: c0 and c1 as float32, then (c2, c3)
+// and (c4, c5) as scaled float16 pairs, one word each: one 16-byte load.
+constexpr int kFoldWords = 4;
 
 // ---------------------------------------------------------------------------
 // Error handling

@@ -281,12 +281,15 @@ __device__ inline float4 group_bcast(float4 v) {
   return v;
 }
 
-// the raw entries of lane k in a folded block: c0..c3 and the word of the
-// scaled float16 pair (c4 low, c5 high)
-template <int LPE>
-__device__ inline void load_folded(const float* __restrict__ blk, int k, float4* c03, uint32_t* h45) {
-  *c03 = reinterpret_cast<const float4*>(blk)[k];
-  *h45 = reinterpret_cast<const uint32_t*>(blk + 4 * LPE)[k];
+// the raw entries of lane k in a folded block: c0, c1 and the words of the
+// scaled float16 pairs (c2 low, c3 high) and (c4 low, c5 high)
+__device__ inline void load_folded(const float* __restrict__ blk, int k, float* c0, float* c1,
+                                   uint32_t* h23, uint32_t* h45) {
+  const float4 v = reinterpret_cast<const float4*>(blk)[k];
+  *c0 = v.x;
+  *c1 = v.y;
+  *h23 = __float_as_uint(v.z);
+  *h45 = __float_as_uint(v.w);
 }
 __device__ inline float half_lo(uint32_t h) {
   return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu)));

@@ -109,19 +109,22 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       float psi0 = 0.0f;
       if constexpr (FOLD) {
         // one quintic per channel from the table of the pair (a_i, a_j)
-        // power form with the float16 c4, c5 scaled through their weights
-        // e4 = tau^4 / s4, e5 = tau^5 / s5 (one mixed-precision FMA each)
+        // power form with the float16 c2 .. c5 scaled through their weights
+        // e_n = tau^n / s_n (one mixed-precision FMA each)
         const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
         const float t2 = tau * tau, t3 = t2 * tau;
-        const float e4 = md.c45_inv[0] * (t2 * t2), e5 = md.c45_inv[1] * (t2 * t3);
+        const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
+        const float e4 = md.c_inv[2] * (t2 * t2), e5 = md.c_inv[3] * (t2 * t3);
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          float4 c;
-          uint32_t h;
-          load_folded<P::LPE>(ft + jj * P::LPE * kFoldWords, k, &c, &h);
-          float psi = fmaf(c.w, t3, fmaf(c.z, t2, fmaf(c.y, tau, c.x)));
-          psi = fmaf(half_lo(h), e4, psi);
-          psi = fmaf(half_hi(h), e5, psi);
+          float c0, c1;
+          uint32_t h23, h45;
+          load_folded(ft + jj * P::LPE * kFoldWords, k, &c0, &c1, &h23, &h45);
+          float psi = fmaf(c1, tau, c0);
+          psi = fmaf(half_lo(h23), e2, psi);
+          psi = fmaf(half_hi(h23), e3, psi);
+          psi = fmaf(half_lo(h45), e4, psi);
+          psi = fmaf(half_hi(h45), e5, psi);
           acc0[jj] += chi * psi;
           if (jj == 0) psi0 = psi;
         }

@@ -382,12 +382,14 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
       std::swap(a0, b0); std::swap(a1, b1); std::swap(a2, b2);
     }
   }
-  // float16 scales of the folded tables' c4 and c5: a power of two that maps
+  // float16 scales of the folded tables' c2 .. c5: a power of two that maps
   // the bound 2 max|g_n| + R max|q_n| (gamma = 1 + tanh < 2, |U| = |tanh| < 1)
   // to at most 2^14, half of the float16 range.  Their rounding (at most
-  // 2^-11 of the bound) enters d/dtau with weights 4 and 5; the tables are
-  // folded only while that stays below the float32 rounding of the slope
-  // term c1, else the separable float32 tables are used.
+  // 2^-11 of each bound) enters the value with weight 1 and d/dtau with
+  // weights 2 .. 5; the tables are folded only while the value error stays
+  // below the float32 rounding of the value term c0 and the slope error
+  // below 2^-14 of the slope term c1, else the separable float32 tables are
+  // used.
   double bnd[6] = {};
   for (int q = 0; q < 6; ++q) {
     double gmax = 0.0, qmax = 0.0;
@@ -395,14 +397,16 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     for (size_t e = q; e < qtab.size(); e += 6) qmax = std::max(qmax, double(std::fabs(qtab[e])));
     bnd[q] = 2.0 * gmax + double(R) * qmax;
   }
-  for (int q = 4; q < 6; ++q) {
+  for (int q = 2; q < 6; ++q) {
     int ex = 0;
     if (bnd[q] > 0.0) ex = static_cast<int>(std::floor(std::log2(16384.0 / bnd[q])));
     ex = std::max(-100, std::min(100, ex));
-    m->c45_scale[q - 4] = static_cast<float>(std::ldexp(1.0, ex));
+    m->c_scale[q - 2] = static_cast<float>(std::ldexp(1.0, ex));
   }
-  m->fold_allowed = (4.0 * bnd[4] + 5.0 * bnd[5]) * std::ldexp(1.0, -11) <=
-                    bnd[1] * std::ldexp(1.0, -24);
+  const double f16 = std::ldexp(1.0, -11);
+  m->fold_allowed = (bnd[2] + bnd[3] + bnd[4] + bnd[5]) * f16 <= bnd[0] * std::ldexp(1.0, -24) &&
+                    (2.0 * bnd[2] + 3.0 * bnd[3] + 4.0 * bnd[4] + 5.0 * bnd[5]) * f16 <=
+                        bnd[1] * std::ldexp(1.0, -14);
 
   // ---- coupling tensors, each symmetrised over the indices of equal degree
   // (the exact integrals are; the quadrature sums are only up to rounding)
@@ -563,7 +567,6 @@ dpa4c::ModelDev dpa4c_model::dev() const {
   d.E_ref = E_ref;
   d.ftab = ws.ftab.as<float>();
   d.fold_n = fold_n > 0 ? fold_n : 0;
-  d.c45_inv[0] = 1.0f / c45_scale[0];
-  d.c45_inv[1] = 1.0f / c45_scale[1];
+  for (int q = 0; q < 4; ++q) d.c_inv[q] = 1.0f / c_scale[q];
   return d;
 }

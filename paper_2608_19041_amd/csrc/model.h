@@ -164,8 +164,8 @@ struct dpa4c_model {
   std::mutex mu_lock;
   int64_t last_n = 0;
   int fold_n = -1;                  // species with folded tables; 0 = separable path, -1 = unset
-  float c45_scale[2] = {1.0f, 1.0f};   // float16 scales of c4, c5 in the folded tables
-  bool fold_allowed = true;            // the float16 c4, c5 are below float32 rounding
+  float c_scale[4] = {1.0f, 1.0f, 1.0f, 1.0f};   // float16 scales of c2 .. c5 in the folded tables
+  bool fold_allowed = true;            // the float16 rounding of c2 .. c5 is within bounds
   uint32_t fold_types_mask[4] = {};
 
   dpa4c::ModelDev dev() const;
