@@ -377,3 +377,20 @@ def test_verlet_is_bit_reproducible(dev, dp, every):
     assert a[5] == b[5] and a[5] >= 2
     for x, y in zip(a[:5], b[:5]):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("n,box,r", [(30, 6.0, 9.58), (20, 5.0, 13.0)])
+def test_neighbors_long_rows(dev, dp, n, box, r):
+    """Rows beyond the fill kernel's LDS row (512 entries) are ordered through
+    the device scratch: lists still bit-identical to the oracle, whether some
+    rows or all rows are long (many periodic images of a small cell)."""
+    s = synth.random_periodic(n, seed=31, cell=np.diag([box, box * 1.05, box * 0.95]), d_min=0.8)
+    pos, _ = on_dev(s, dev)
+    rp, nj, ns, e = dp.build_neighbors(pos, s.cell, s.pbc, r)
+    counts = np.diff(rp.cpu().numpy())
+    print(f"rows {counts.min()}..{counts.max()}, {int((counts > 512).sum())} of {n} above 512",
+          flush=True)
+    assert counts.max() > 512
+    ref = onb.neighbor_list(s.pos, s.cell, s.pbc, r)
+    assert e == len(ref[0])
+    assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref)
