@@ -2,7 +2,8 @@
 // the edge recomputation of Methods "Fused execution and backward
 // recomputation".
 //
-// For centre i the workgroup reads the node-state gradient
+// One wavefront per centre (four per 256-thread workgroup, never waiting for
+// each other).  For centre i the wave reads the node-state gradient
 // [dE/dS0, dE/dS1, dE/dY] (from the per-atom kernel), revisits the edges of
 // row i, recomputes the tabulated radial maps (value and derivative), the
 // pair coefficients and the envelope, and writes
@@ -21,6 +22,11 @@
 // its gradient instead of every harmonic.  The LPE partial sums of an edge
 // are combined with a fixed DPP butterfly.
 //
+// The row is taken in passes of 64 edges: each lane first forms one edge's
+// geometry, envelope and table row into the wave's LDS slice, so the groups
+// do not repeat that work per lane; with folded tables a group requests the
+// table entries of its next edge before it evaluates the current one.
+//
 // The gradient of an edge overwrites its record (r_ij, j) in place and keeps
 // j in the fourth component.  With VIR the lane that writes it also adds
 // -g_e (x) r_e (float64) to its group's slot in LDS; the slots are summed in
@@ -36,14 +42,10 @@ namespace dpa4c {
 namespace {
 
 constexpr int kTeam = 256;
-
-// The virial's extra state would cost the widest degree-three variants one
-// wave per SIMD; those are held to four waves.
-template <class P>
-constexpr int backward_min_waves(bool vir) { return vir && P::L < 4 && P::C0 >= 64 ? 4 : 1; }
+constexpr int kWaves = kTeam / kWave;
 
 template <class P, bool FOLD, bool VIR>
-__global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_kernel(ModelDev md, int64_t n,
+__global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
                                                          const int32_t* __restrict__ typ,
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
@@ -51,11 +53,20 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
                                                          const float* __restrict__ node_grad,
                                                          double* __restrict__ w_atom) {
   static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
-  constexpr int G = kTeam / P::LPE;
-  __shared__ double wv[VIR ? G : 1][9];
-  const int tid = threadIdx.x;
-  const int grp = tid / P::LPE;
-  const int k = tid % P::LPE;
+  constexpr int G = kWave / P::LPE;   // edge groups in a wave
+  __shared__ double wv_all[kWaves][VIR ? G : 1][9];
+  // per edge of a pass: (u, 1/rho), (tau, chi, dchi, table row), (j, a_j)
+  __shared__ float4 geo_all[kWaves][kWave];
+  __shared__ float4 rad_all[kWaves][kWave];
+  __shared__ int2 ids_all[kWaves][kWave];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int grp = lane / P::LPE;
+  const int k = lane % P::LPE;
+  double (*wv)[9] = wv_all[wave];
+  float4* geo = geo_all[wave];
+  float4* rad = rad_all[wave];
+  int2* ids = ids_all[wave];
   const int T1 = md.n_types1;
   const float inv_delta = md.inv_delta;
   const int nf = md.fold_n;
@@ -63,7 +74,9 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
   // index of every atom
   auto type_of = [&](int64_t a) { return FOLD ? typ[a] : clamp_type(typ[a], T1); };
 
-  for (int64_t i = xcd_block(blockIdx.x, gridDim.x); i < n; i += gridDim.x) {
+  for (int64_t blk = xcd_block(blockIdx.x, gridDim.x); blk * kWaves < n; blk += gridDim.x) {
+    const int64_t i = blk * kWaves + wave;
+    if (i >= n) break;
     const int ai = type_of(i);
     const float* gyr = node_grad + size_t(i) * P::NS;
     // per-centre coefficients in the lane's channel layout
@@ -104,39 +117,15 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       for (int c = 0; c < 9; ++c) wv[grp][c] = 0.0;
     const float* pair_base = FOLD ? md.ftab + size_t(ai) * nf * md.n_rows * (P::C0 * kFoldWords)
                                   : md.pair + size_t(ai) * T1 * (P::C0 * P::PW);
-    // Two-stage software pipeline, as in the forward kernel: the record of
-    // round r+2 and the neighbour species of round r+1 are requested while
-    // round r computes.  Records are read only inside [0, cnt) of the row.
-    // The lanes of a group share one edge, so only its lane 0 reads the
-    // record and the neighbour type; they reach the other lanes by a group
-    // broadcast when the round uses them (rec_nn and aj_n hold lane 0's
-    // values until then).
-    const float4* erow = edge + b;
-    const bool lead = k == 0;
-    float4 rec_n = make_float4(0.f, 0.f, 0.f, 0.f), rec_nn = rec_n;
-    int aj_n = ai;
-    if (cnt > 0) {
-      if (lead) rec_n = erow[grp < cnt ? grp : 0];
-      rec_n = group_bcast<P::LPE>(rec_n);
-      aj_n = (lead && grp < cnt) ? type_of(__float_as_int(rec_n.w)) : ai;
-      if (lead && G < cnt) rec_nn = erow[grp + G < cnt ? grp + G : 0];
-    }
-    for (int base = 0; base < cnt; base += G) {
-      const int el = base + grp;
-      const bool valid = el < cnt;
-      const float4 rec = rec_n;
-      const int aj = __shfl(aj_n, 0, P::LPE);
-      if (base + G < cnt) {
-        const int el1 = el + G, el2 = el + 2 * G;
-        rec_n = group_bcast<P::LPE>(rec_nn);
-        aj_n = (lead && el1 < cnt) ? type_of(__float_as_int(rec_n.w)) : ai;
-        if (lead && base + 2 * G < cnt) rec_nn = erow[el2 < cnt ? el2 : 0];
-      }
-      const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
-      float chi, dchi;
-      envelope(g.rho, md.inv_rc, &chi, &dchi);
-      float tau;
-      const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
+
+    // Entry x of the pass (compact slot c0 + x of the row): the edge
+    // gradient from its LDS entry and, with folded tables, the lane's table
+    // entries ``T`` of that edge.
+    auto edge_work = [&](int x, int c0, const float4* T) {
+      const float4 ge = geo[x], ra = rad[x];
+      const float x_ = ge.x, y = ge.y, z = ge.z, inv_rho = ge.w;
+      const float tau = ra.x, chi = ra.y, dchi = ra.z;
+      const bool valid = c0 + x < cnt;
       const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;
       const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
@@ -147,7 +136,6 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
         // need the lane's coefficients contracted with dE/dY0 first,
         // A_p = sum_j Ybar0_j c_pj, and then one quintic in tau and its
         // derivative; d/drho's 1/Delta is applied once to the sums.
-        const float* ft = pair_base + (size_t(aj) * md.n_rows + row) * (P::C0 * kFoldWords);
         const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
         const float e4 = md.c_inv[2] * t4, e5 = md.c_inv[3] * t5;
         const float f2 = md.c_inv[0] * d1, f3 = md.c_inv[1] * d2;
@@ -155,12 +143,11 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
         float A[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          float c0, c1;
-          uint32_t h23, h45;
-          load_folded(ft + jj * P::LPE * kFoldWords, k, &c0, &c1, &h23, &h45);
+          const float c0f = T[jj].x, c1 = T[jj].y;
+          const uint32_t h23 = __float_as_uint(T[jj].z), h45 = __float_as_uint(T[jj].w);
           const float h2 = half_lo(h23), h3 = half_hi(h23), h4 = half_lo(h45), h5 = half_hi(h45);
           if (jj == 0) {   // the amplitude of the lane's first channel itself
-            psi0 = fmaf(c1, tau, c0);
+            psi0 = fmaf(c1, tau, c0f);
             psi0 = fmaf(h2, e2, psi0);
             psi0 = fmaf(h3, e3, psi0);
             psi0 = fmaf(h4, e4, psi0);
@@ -170,7 +157,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
             dpsi0 = fmaf(h4, f4, dpsi0);
             dpsi0 = fmaf(h5, f5, dpsi0);
           }
-          A[0] = fmaf(gy0[jj], c0, A[0]);
+          A[0] = fmaf(gy0[jj], c0f, A[0]);
           A[1] = fmaf(gy0[jj], c1, A[1]);
           A[2] = fmaf(gy0[jj], h2, A[2]);
           A[3] = fmaf(gy0[jj], h3, A[3]);
@@ -181,6 +168,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
         b0 = fmaf(A[5], f5, fmaf(A[4], f4, fmaf(A[3], f3, fmaf(A[2], f2, A[1])))) * inv_delta;
         dpsi0 *= inv_delta;
       } else {
+        const int row = __float_as_int(ra.w), aj = ids[x].y;
         float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (P::R > 0) {
           float c[6];
@@ -220,12 +208,11 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
         }
       }
       // Q_k(u) and its gradient
-      const float x = g.ux, y = g.uy, z = g.uz;
-      const float mono[6] = {x * x, x * y, x * z, y * y, y * z, z * z};
+      const float mono[6] = {x_ * x_, x_ * y, x_ * z, y * y, y * z, z * z};
       float gq[3];
-      gq[0] = M2[0] * x + M2[3] * y + M2[5] * z;
-      gq[1] = M2[3] * x + M2[1] * y + M2[4] * z;
-      gq[2] = M2[5] * x + M2[4] * y + M2[2] * z;
+      gq[0] = M2[0] * x_ + M2[3] * y + M2[5] * z;
+      gq[1] = M2[3] * x_ + M2[1] * y + M2[4] * z;
+      gq[2] = M2[5] * x_ + M2[4] * y + M2[2] * z;
       float c3[3] = {0.f, 0.f, 0.f};
       if constexpr (P::L >= 3) {
 #pragma unroll
@@ -237,7 +224,7 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       float c4[3] = {0.f, 0.f, 0.f};   // grad P4
       if constexpr (P::L >= 4) {
         float mono3[10];
-        cubic_monomials(x, y, z, mono3);
+        cubic_monomials(x_, y, z, mono3);
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
 #pragma unroll
@@ -246,10 +233,10 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       }
       // Q = v.u + (1/2) u.M u + (1/3) u.grad P3 + (1/4) u.grad P4 (Euler's
       // relation per degree)
-      float Q = (v1[0] * x + v1[1] * y + v1[2] * z) +
-                0.5f * (gq[0] * x + gq[1] * y + gq[2] * z) +
-                (1.0f / 3.0f) * (c3[0] * x + c3[1] * y + c3[2] * z);
-      if constexpr (P::L >= 4) Q += 0.25f * (c4[0] * x + c4[1] * y + c4[2] * z);
+      float Q = (v1[0] * x_ + v1[1] * y + v1[2] * z) +
+                0.5f * (gq[0] * x_ + gq[1] * y + gq[2] * z) +
+                (1.0f / 3.0f) * (c3[0] * x_ + c3[1] * y + c3[2] * z);
+      if constexpr (P::L >= 4) Q += 0.25f * (c4[0] * x_ + c4[1] * y + c4[2] * z);
       const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
       float drho = dchi * a0 + chi * b0 + Q * (dchi2 * psi0 + chi2 * dpsi0) +
                    gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2;
@@ -263,34 +250,82 @@ __global__ void __launch_bounds__(kTeam, backward_min_waves<P>(VIR)) backward_ke
       duy = group_sum<P::LPE>(duy);
       duz = group_sum<P::LPE>(duz);
       if (valid && k == 0) {
-        const float udu = x * dux + y * duy + z * duz;
-        const float gx = drho * x + (dux - udu * x) * g.inv_rho;
-        const float gy_ = drho * y + (duy - udu * y) * g.inv_rho;
-        const float gz = drho * z + (duz - udu * z) * g.inv_rho;
-        // in place: this record was read two rounds ago, and only records
-        // of later rounds are requested from here on
-        edge[b + el] = make_float4(gx, gy_, gz, rec.w);
+        const float udu = x_ * dux + y * duy + z * duz;
+        const float gx = drho * x_ + (dux - udu * x_) * inv_rho;
+        const float gy_ = drho * y + (duy - udu * y) * inv_rho;
+        const float gz = drho * z + (duz - udu * z) * inv_rho;
+        // in place: every record of the pass was read before its edges run
+        edge[b + c0 + x] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
         if (VIR) {   // LDS adds to the group's own slot: one writer, program order
-          // r_e = rho u from values still live here (the record itself is
-          // not kept across the edge's work, which holds the register count)
-          const float rho = 1.0f / g.inv_rho;
+          const float rho = 1.0f / inv_rho;
           const float ga[3] = {gx, gy_, gz};
-          const float rb[3] = {x * rho, y * rho, z * rho};
+          const float rb[3] = {x_ * rho, y * rho, z * rho};
 #pragma unroll
           for (int a = 0; a < 3; ++a)
 #pragma unroll
             for (int c = 0; c < 3; ++c) atomicAdd(&wv[grp][3 * a + c], -(double(ga[a]) * double(rb[c])));
         }
       }
+    };
+    // the lane's folded table entries of entry x of the pass
+    auto load_rows = [&](int x, float4* T) {
+      const float* ft = pair_base + size_t(__float_as_int(rad[x].w)) * (P::C0 * kFoldWords);
+#pragma unroll
+      for (int jj = 0; jj < P::CPL; ++jj)
+        T[jj] = reinterpret_cast<const float4*>(ft + jj * P::LPE * kFoldWords)[k];
+    };
+
+    // The row in passes of 64 edges: each lane first reads one record and
+    // forms its edge's geometry, envelope and table row into the wave's LDS
+    // slice (entries past the row get chi = 0 and table row 0), then the
+    // groups take the pass's edges.
+    for (int c0 = 0; c0 < cnt; c0 += kWave) {
+      const int np = cnt - c0 < kWave ? cnt - c0 : kWave;
+      {
+        float4 ge = make_float4(0.f, 0.f, 0.f, 1.0f), ra = make_float4(0.f, 0.f, 0.f, 0.f);
+        int2 id = make_int2(0, 0);
+        if (lane < np) {
+          const float4 rec = edge[b + c0 + lane];
+          const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
+          float chi, dchi, tau;
+          envelope(g.rho, md.inv_rc, &chi, &dchi);
+          const int row = table_row(g.rho, inv_delta, md.n_rows, &tau);
+          const int j = __float_as_int(rec.w);
+          const int aj = type_of(j);
+          ge = make_float4(g.ux, g.uy, g.uz, g.inv_rho);
+          ra = make_float4(tau, chi, dchi, __int_as_float(FOLD ? aj * md.n_rows + row : row));
+          id = make_int2(j, aj);
+        }
+        geo[lane] = ge;
+        rad[lane] = ra;
+        ids[lane] = id;
+      }
+      wave_sync();
+      if constexpr (FOLD) {
+        // the table entries of a group's next edge are requested before its
+        // current edge is evaluated (two register sets, used in turn)
+        float4 TA[P::CPL], TB[P::CPL];
+        load_rows(grp, TA);
+        for (int base = 0; base < np; base += 2 * G) {
+          if (base + G < np) load_rows(base + G + grp, TB);
+          edge_work(base + grp, c0, TA);
+          if (base + G >= np) break;
+          if (base + 2 * G < np) load_rows(base + 2 * G + grp, TA);
+          edge_work(base + G + grp, c0, TB);
+        }
+      } else {
+        for (int base = 0; base < np; base += G) edge_work(base + grp, c0, nullptr);
+      }
+      wave_sync();   // the LDS entries are rewritten by the next pass
     }
     if (VIR) {
-      __syncthreads();
-      if (tid < 9) {
+      wave_sync();
+      if (lane < 9) {
         double s = 0.0;
-        for (int q = 0; q < G; ++q) s += wv[q][tid];
-        w_atom[9 * i + tid] = s;
+        for (int q = 0; q < G; ++q) s += wv[q][lane];
+        w_atom[9 * i + lane] = s;
       }
-      __syncthreads();   // the slots are cleared for the next row
+      wave_sync();   // the slots are cleared for the next row
     }
   }
 }
@@ -299,7 +334,8 @@ template <class P>
 int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
            const int64_t* row_ptr, const int32_t* ecount, float4* edge, const float* node_grad,
            double* w_atom, hipStream_t st) {
-  int64_t blocks = n < 16384 ? n : 16384;
+  int64_t blocks = (n + kWaves - 1) / kWaves;   // a wave per centre
+  blocks = blocks < 65536 ? blocks : 65536;
   if (blocks < 1) return 0;
   const int32_t* typ = fidx ? fidx : species;
   const dim3 grid(static_cast<unsigned>(blocks)), block(kTeam);
