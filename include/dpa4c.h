@@ -93,9 +93,12 @@ int dpa4c_model_create(const void* blob, size_t nbytes, int device, dpa4c_model*
 void dpa4c_model_destroy(dpa4c_model* model);
 
 /*
- * Integer widths of a model, written to ``info`` (host, 12 int64):
+ * Integer widths of a model, written to ``info`` (host, 13 int64):
  * C0, L, R, S (Eq. (moment-width)), D_out (Eq. (dim-out)), F, n_layers,
- * n_types, table rows, C1, C2, K1.
+ * n_types, table rows, C1, C2, K1, and the words per channel of its folded
+ * radial tables (3: c0, c1 in float32 and c2, c3 in scaled float16, the
+ * quintic's c4, c5 being below float32 resolution for this model; 0: the
+ * model runs on the separable float32 tables only).
  */
 int dpa4c_model_info(const dpa4c_model* model, int64_t* info);
 

@@ -194,7 +194,7 @@ class Model:
     """A model handle on one device (weights, radial table, pair cache)."""
 
     INFO_KEYS = ("C0", "L", "R", "S", "D_out", "F", "n_layers", "n_types", "table_rows", "C1",
-                 "C2", "K1")
+                 "C2", "K1", "fold_words")
 
     def __init__(self, blob: bytes, device: int = 0):
         lib = library()
@@ -203,7 +203,7 @@ class Model:
         _check(lib.dpa4c_model_create(buf, len(blob), int(device), ctypes.byref(h)))
         self._h = h
         self.device = device
-        info = (ctypes.c_int64 * 12)()
+        info = (ctypes.c_int64 * 13)()
         _check(lib.dpa4c_model_info(self._h, info))
         self.info = dict(zip(self.INFO_KEYS, list(info)))
 

@@ -378,8 +378,8 @@ int dpa4c_model_info(const dpa4c_model* m, int64_t* info) {
     set_error("dpa4c_model_info: null argument");
     return DPA4C_ERR_INVALID_ARG;
   }
-  int64_t v[12] = {m->C0, m->L, m->R, m->S, m->D_out, m->F, m->n_layers, m->n_types,
-                   m->n_rows, m->C[1], m->C[2], m->K[1]};
+  int64_t v[13] = {m->C0, m->L, m->R, m->S, m->D_out, m->F, m->n_layers, m->n_types,
+                   m->n_rows, m->C[1], m->C[2], m->K[1], m->fold_allowed ? kFoldWords : 0};
   std::memcpy(info, v, sizeof(v));
   return 0;
 }

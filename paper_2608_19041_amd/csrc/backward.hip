@@ -121,7 +121,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
     // Entry x of the pass (compact slot c0 + x of the row): the edge
     // gradient from its LDS entry and, with folded tables, the lane's table
     // entries ``T`` of that edge.
-    auto edge_work = [&](int x, int c0, const float4* T) {
+    auto edge_work = [&](int x, int c0, const float3* T) {
       const float4 ge = geo[x], ra = rad[x];
       const float x_ = ge.x, y = ge.y, z = ge.z, inv_rho = ge.w;
       const float tau = ra.x, chi = ra.y, dchi = ra.z;
@@ -130,42 +130,35 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
-        // one quintic per channel from the table of the pair (a_i, a_j),
-        // power form; the float16 c2 .. c5 enter through their scaled weights
-        // (one mixed-precision FMA each).  The weighted sums a0 and b0 only
+        // the quintic of each channel from the table of the pair (a_i, a_j)
+        // (c4 and c5 below float32 resolution, not stored), power form; the
+        // float16 c2, c3 enter through their scaled weights (one
+        // mixed-precision FMA each).  The weighted sums a0 and b0 only
         // need the lane's coefficients contracted with dE/dY0 first,
         // A_p = sum_j Ybar0_j c_pj, and then one quintic in tau and its
         // derivative; d/drho's 1/Delta is applied once to the sums.
         const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
-        const float e4 = md.c_inv[2] * t4, e5 = md.c_inv[3] * t5;
         const float f2 = md.c_inv[0] * d1, f3 = md.c_inv[1] * d2;
-        const float f4 = md.c_inv[2] * d3, f5 = md.c_inv[3] * d4;
-        float A[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        float A[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
           const float c0f = T[jj].x, c1 = T[jj].y;
-          const uint32_t h23 = __float_as_uint(T[jj].z), h45 = __float_as_uint(T[jj].w);
-          const float h2 = half_lo(h23), h3 = half_hi(h23), h4 = half_lo(h45), h5 = half_hi(h45);
+          const uint32_t h23 = __float_as_uint(T[jj].z);
+          const float h2 = half_lo(h23), h3 = half_hi(h23);
           if (jj == 0) {   // the amplitude of the lane's first channel itself
             psi0 = fmaf(c1, tau, c0f);
             psi0 = fmaf(h2, e2, psi0);
             psi0 = fmaf(h3, e3, psi0);
-            psi0 = fmaf(h4, e4, psi0);
-            psi0 = fmaf(h5, e5, psi0);
             dpsi0 = fmaf(h2, f2, c1);
             dpsi0 = fmaf(h3, f3, dpsi0);
-            dpsi0 = fmaf(h4, f4, dpsi0);
-            dpsi0 = fmaf(h5, f5, dpsi0);
           }
           A[0] = fmaf(gy0[jj], c0f, A[0]);
           A[1] = fmaf(gy0[jj], c1, A[1]);
           A[2] = fmaf(gy0[jj], h2, A[2]);
           A[3] = fmaf(gy0[jj], h3, A[3]);
-          A[4] = fmaf(gy0[jj], h4, A[4]);
-          A[5] = fmaf(gy0[jj], h5, A[5]);
         }
-        a0 = fmaf(A[5], e5, fmaf(A[4], e4, fmaf(A[3], e3, fmaf(A[2], e2, fmaf(A[1], tau, A[0])))));
-        b0 = fmaf(A[5], f5, fmaf(A[4], f4, fmaf(A[3], f3, fmaf(A[2], f2, A[1])))) * inv_delta;
+        a0 = fmaf(A[3], e3, fmaf(A[2], e2, fmaf(A[1], tau, A[0])));
+        b0 = fmaf(A[3], f3, fmaf(A[2], f2, A[1])) * inv_delta;
         dpsi0 *= inv_delta;
       } else {
         const int row = __float_as_int(ra.w), aj = ids[x].y;
@@ -268,11 +261,10 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       }
     };
     // the lane's folded table entries of entry x of the pass
-    auto load_rows = [&](int x, float4* T) {
+    auto load_rows = [&](int x, float3* T) {
       const float* ft = pair_base + size_t(__float_as_int(rad[x].w)) * (P::C0 * kFoldWords);
 #pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj)
-        T[jj] = reinterpret_cast<const float4*>(ft + jj * P::LPE * kFoldWords)[k];
+      for (int jj = 0; jj < P::CPL; ++jj) T[jj] = load_fold_entry(ft + (jj * P::LPE + k) * kFoldWords);
     };
 
     // The row in passes of 64 edges: each lane first reads one record and
@@ -304,7 +296,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       if constexpr (FOLD) {
         // the table entries of a group's next edge are requested before its
         // current edge is evaluated (two register sets, used in turn)
-        float4 TA[P::CPL], TB[P::CPL];
+        float3 TA[P::CPL], TB[P::CPL];
         load_rows(grp, TA);
         for (int base = 0; base < np; base += 2 * G) {
           if (base + G < np) load_rows(base + G + grp, TB);

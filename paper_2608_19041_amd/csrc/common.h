@@ -154,15 +154,15 @@ struct ModelDev {
   const float* E_ref;       // [T+1]
   // pair-folded tables (fold.hip), used when fold_n > 0:
   // [fold_n^2 pairs][n_rows][CPL] blocks of 4 LPE words, pair (fa, fb) at
-  // fa * fold_n + fb; c_inv = the inverse scales of the float16 c2 .. c5
+  // fa * fold_n + fb; c_inv = the inverse scales of the float16 c2, c3
   const float* ftab;
   int fold_n;
   float c_inv[4];
 };
 
 // Words per channel of a folded table: c0 and c1 as float32, then (c2, c3)
-// and (c4, c5) as scaled float16 pairs, one word each: one 16-byte load.
-constexpr int kFoldWords = 4;
+// as a scaled float16 pair: one 12-byte load.
+constexpr int kFoldWords = 3;
 
 // ---------------------------------------------------------------------------
 // Error handling

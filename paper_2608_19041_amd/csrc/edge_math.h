@@ -10,10 +10,13 @@ namespace dpa4c {
 
 __device__ inline int lane_of() { return threadIdx.x & (kWave - 1); }
 
+// Orders the LDS accesses of a wavefront: what its lanes wrote before is
+// visible to its lanes after.  The fences cover LDS only, so outstanding
+// global loads and stores of the wave are not waited for.
 __device__ inline void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // Eq. (edge-geometry) in float32: rho = sqrt(|r|^2 + eps^2) and u = r / rho
@@ -281,15 +284,10 @@ __device__ inline float4 group_bcast(float4 v) {
   return v;
 }
 
-// the raw entries of lane k in a folded block: c0, c1 and the words of the
-// scaled float16 pairs (c2 low, c3 high) and (c4 low, c5 high)
-__device__ inline void load_folded(const float* __restrict__ blk, int k, float* c0, float* c1,
-                                   uint32_t* h23, uint32_t* h45) {
-  const float4 v = reinterpret_cast<const float4*>(blk)[k];
-  *c0 = v.x;
-  *c1 = v.y;
-  *h23 = __float_as_uint(v.z);
-  *h45 = __float_as_uint(v.w);
+// The lane's entry of a folded table row: c0 and c1 (float32) and the word
+// of scaled float16 (c2, c3).
+__device__ inline float3 load_fold_entry(const float* __restrict__ p) {
+  return *reinterpret_cast<const float3*>(p);
 }
 __device__ inline float half_lo(uint32_t h) {
   return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu)));

@@ -10,21 +10,23 @@
 // Hermite interpolation of the radial table").  Its normalised coefficients
 // are that same linear combination of the tabulated ones.
 //
-// Storage: c0 and c1 in float32, c2 .. c5 as float16 scaled by fixed powers
+// Storage: c0 and c1 in float32, c2 and c3 as float16 scaled by fixed powers
 // of two (one per coefficient, from a bound over every pair: |gamma| < 2 and
-// |U| < 1 by their tanh forms, times the largest tabulated coefficient).
-// With the normalised form c_n Delta^n the coefficients fall by about two
-// orders of magnitude per power at Delta = 0.002 A, so the 2^-11 relative
-// rounding of c2 .. c5 stays below the float32 rounding of the value and
-// near 1e-5 of the slope (checked per model at set-up), and a channel takes
-// one 16-byte load instead of 24 bytes.
+// |U| < 1 by their tanh forms, times the largest tabulated coefficient); c4
+// and c5 are not stored.  With the normalised form c_n Delta^n the
+// coefficients fall by about two orders of magnitude per power at
+// Delta = 0.002 A, so the whole contribution of c4 and c5 together with the
+// 2^-11 relative rounding of c2 and c3 stays below the float32 rounding of
+// the value and below 2^-14 of the slope term (checked per model at set-up;
+// a model that fails the check runs on the separable float32 tables), and a
+// channel takes one 12-byte load instead of 24 bytes.
 //
 // For the few species of an MD system the library keeps one such table per
 // ordered pair present; the edge kernels then read one quintic per channel
 // instead of a g quintic, R q quintics and the pair coefficients.  Systems
 // with more than kMaxFoldTypes species, or whose folded tables would exceed
 // kMaxFoldBytes, use the separable tables directly.  Five species at full
-// width fold into 25 tables of 7.7 MB (192 MB, most of the last-level cache);
+// width fold into 25 tables of 5.8 MB (144 MB, most of the last-level cache);
 // on the 5-species alloy that measured faster than the separable tables
 // (backward 0.94 -> 0.70 ms at 31,250 atoms), since every edge then reads
 // 20 B per channel from one table instead of 48 B from two.
@@ -73,7 +75,7 @@ struct FoldTypes {
 __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* __restrict__ qtab,
                                   const float* __restrict__ pair, FoldTypes used, int n_used,
                                   int n_types1, int C0, int R, int LPE, int rows,
-                                  const float4 scale, float* __restrict__ ftab) {
+                                  const float2 scale, float* __restrict__ ftab) {
   const int s = blockIdx.x, p = blockIdx.y;
   const int a = used.t[p / n_used], b = used.t[p % n_used];
   const int PW = 2 + R, CPL = C0 / LPE;
@@ -81,24 +83,23 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
     const int k = c % LPE, j = c / LPE;
     const float* pc = pair + ((size_t(a * n_types1 + b) * CPL + j) * LPE + k) * PW;
     const float* g = gtab + ((size_t(s) * CPL + j) * LPE + k) * 6;
-    // block of slot j: lane k's 16 bytes are c0, c1 (float32) and the words
-    // (c2, c3) and (c4, c5) in scaled float16
+    // block of slot j: lane k's three words are c0, c1 (float32) and the word
+    // (c2, c3) in scaled float16
     float* blk = ftab + ((size_t(p) * rows + s) * CPL + j) * LPE * kFoldWords;
-    double v[6];
-    for (int q = 0; q < 6; ++q) {
+    double v[4];
+    for (int q = 0; q < 4; ++q) {
       v[q] = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
       for (int mu = 0; mu < R; ++mu)
         v[q] += double(pc[2 + mu]) * double(qtab[(size_t(s) * R + mu) * 6 + q]);
     }
-    const float sc[4] = {scale.x, scale.y, scale.z, scale.w};
-    uint16_t hb[4];
-    for (int q = 0; q < 4; ++q)
+    const float sc[2] = {scale.x, scale.y};
+    uint16_t hb[2];
+    for (int q = 0; q < 2; ++q)
       hb[q] = __builtin_bit_cast(uint16_t,
                                  static_cast<_Float16>(static_cast<float>(v[2 + q] * sc[q])));
-    blk[4 * k] = static_cast<float>(v[0]);
-    blk[4 * k + 1] = static_cast<float>(v[1]);
-    reinterpret_cast<uint32_t*>(blk)[4 * k + 2] = uint32_t(hb[0]) | (uint32_t(hb[1]) << 16);
-    reinterpret_cast<uint32_t*>(blk)[4 * k + 3] = uint32_t(hb[2]) | (uint32_t(hb[3]) << 16);
+    blk[kFoldWords * k] = static_cast<float>(v[0]);
+    blk[kFoldWords * k + 1] = static_cast<float>(v[1]);
+    reinterpret_cast<uint32_t*>(blk)[kFoldWords * k + 2] = uint32_t(hb[0]) | (uint32_t(hb[1]) << 16);
   }
 }
 
@@ -162,7 +163,7 @@ int prepare_species(dpa4c_model* m, const int32_t* species, int64_t n, uint32_t*
       hipLaunchKernelGGL(fold_build_kernel, dim3(m->n_rows, n_used * n_used),
                          dim3(m->C0 < 256 ? m->C0 : 256), 0, st, m->gtab, m->qtab, m->pair, used,
                          n_used, T1, m->C0, m->R, m->C[1], m->n_rows,
-                         make_float4(m->c_scale[0], m->c_scale[1], m->c_scale[2], m->c_scale[3]),
+                         make_float2(m->c_scale[0], m->c_scale[1]),
                          w.ftab.as<float>());
       DPA4C_HIP_TRY(hipGetLastError());
       m->fold_n = n_used;

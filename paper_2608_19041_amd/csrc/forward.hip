@@ -35,8 +35,13 @@ namespace {
 constexpr int kTeam = 256;
 constexpr int kWaves = kTeam / kWave;
 
+// Four waves per SIMD fit every degree-three profile without spilling; the
+// degree-four one needs more registers per lane.
+template <class P>
+constexpr int forward_min_waves() { return P::L >= 4 ? 1 : 4; }
+
 template <class P, bool FOLD>
-__global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
+__global__ void __launch_bounds__(kTeam, forward_min_waves<P>()) forward_kernel(ModelDev md, int64_t n,
                                                         const int32_t* __restrict__ typ,
                                                         const int64_t* __restrict__ row_ptr,
                                                         CompactArgs ca,
@@ -86,25 +91,23 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
 
     // One edge's contribution from its LDS entry and, with folded tables,
     // the lane's table entries ``T`` of that edge.
-    auto edge_work = [&](int x, const float4* T) {
+    auto edge_work = [&](int x, const float3* T) {
       const float4 pr = pre[x];
       const float tau = pr.x, chi = pr.y;
       float psi0 = 0.0f;
       if constexpr (FOLD) {
-        // one quintic per channel from the table of the pair (a_i, a_j),
-        // power form with the float16 c2 .. c5 scaled through their weights
-        // e_n = tau^n / s_n (one mixed-precision FMA each)
+        // the quintic of each channel from the table of the pair (a_i, a_j)
+        // (c4 and c5 below float32 resolution, not stored), power form with
+        // the float16 c2, c3 scaled through their weights e_n = tau^n / s_n
+        // (one mixed-precision FMA each)
         const float t2 = tau * tau, t3 = t2 * tau;
         const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
-        const float e4 = md.c_inv[2] * (t2 * t2), e5 = md.c_inv[3] * (t2 * t3);
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
-          const uint32_t h23 = __float_as_uint(T[jj].z), h45 = __float_as_uint(T[jj].w);
+          const uint32_t h23 = __float_as_uint(T[jj].z);
           float psi = fmaf(T[jj].y, tau, T[jj].x);
           psi = fmaf(half_lo(h23), e2, psi);
           psi = fmaf(half_hi(h23), e3, psi);
-          psi = fmaf(half_lo(h45), e4, psi);
-          psi = fmaf(half_hi(h45), e5, psi);
           acc0[jj] += chi * psi;
           if (jj == 0) psi0 = psi;
         }
@@ -161,11 +164,10 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       }
     };
     // the lane's folded table entries of entry x of the pass
-    auto load_rows = [&](int x, float4* T) {
+    auto load_rows = [&](int x, float3* T) {
       const float* ft = pair_base + size_t(__float_as_int(pre[x].z)) * (P::C0 * kFoldWords);
 #pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj)
-        T[jj] = reinterpret_cast<const float4*>(ft + jj * P::LPE * kFoldWords)[k];
+      for (int jj = 0; jj < P::CPL; ++jj) T[jj] = load_fold_entry(ft + (jj * P::LPE + k) * kFoldWords);
     };
 
     int kept = 0;
@@ -208,7 +210,7 @@ __global__ void __launch_bounds__(kTeam) forward_kernel(ModelDev md, int64_t n,
       if constexpr (FOLD) {
         // the table entries of a group's next edge are requested before its
         // current edge is evaluated (two register sets, used in turn)
-        float4 TA[P::CPL], TB[P::CPL];
+        float3 TA[P::CPL], TB[P::CPL];
         if (np > 0) load_rows(grp, TA);
         for (int base = 0; base < np; base += 2 * G) {
           if (base + G < np) load_rows(base + G + grp, TB);

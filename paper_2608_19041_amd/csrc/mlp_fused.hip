@@ -186,6 +186,24 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
   const DPA4C_LDS ReadoutParams<P>& rpl = *(DPA4C_LDS ReadoutParams<P>*)(&rp);
   DPA4C_LDS float* arow = (DPA4C_LDS float*)(As + ra * LDA);
   stage_readout_params<P>(rp, md, threadIdx.x, kThreads);
+  // The half-wave's share of its atom's node state (zero past n) and the
+  // atom's species, requested one tile ahead: the loads for the next tile are
+  // issued after the current tile's readout and complete during its MLP.
+  constexpr int NY = (P::NS + kHalf - 1) / kHalf;
+  float ynext[NY];
+  int snext = 0;
+  auto fetch_node = [&](int64_t tl) {
+    const int64_t i = tl * kRows + ra;
+    const bool ok = i < n;
+    const float* ny = node + size_t(ok ? i : 0) * P::NS;
+#pragma unroll
+    for (int q = 0; q < NY; ++q) {
+      const int t = hl + q * kHalf;
+      ynext[q] = (ok && t < P::NS) ? ny[t] : 0.0f;
+    }
+    snext = ok ? species[i] : 0;
+  };
+  fetch_node(blockIdx.x);
   __syncthreads();
 
   for (int64_t tile = blockIdx.x; tile * kRows < n; tile += gridDim.x) {
@@ -195,10 +213,12 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
     {
       const int64_t i = row0 + ra;
       const bool ok = i < n;
-      const float* ny = node + size_t(ok ? i : 0) * P::NS;
-      for (int t = hl; t < P::NS; t += kHalf) rl.y[t] = ok ? ny[t] : 0.0f;
-      const float* x0 =
-          md.type_embed + size_t(ok ? clamp_type(species[i], md.n_types1) : 0) * P::C0;
+#pragma unroll
+      for (int q = 0; q < NY; ++q) {
+        const int t = hl + q * kHalf;
+        if (t < P::NS) rl.y[t] = ynext[q];
+      }
+      const float* x0 = md.type_embed + size_t(ok ? clamp_type(snext, md.n_types1) : 0) * P::C0;
       wave_sync();
       readout_forward<P>(rl, rpl, x0, arow);
       if (ok && desc_out)
@@ -208,6 +228,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
     }
     BStream<NT> bs;    // the B stream of the next hidden-width product
     bstream_open(bs, p.W[0], KP / 16, wave, kWavesPB, FT, lane16);
+    fetch_node(tile + gridDim.x);
     __syncthreads();
 
     float s[3][NT][4];   // SiLU'(pre) of the three layers

@@ -382,14 +382,15 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
       std::swap(a0, b0); std::swap(a1, b1); std::swap(a2, b2);
     }
   }
-  // float16 scales of the folded tables' c2 .. c5: a power of two that maps
-  // the bound 2 max|g_n| + R max|q_n| (gamma = 1 + tanh < 2, |U| = |tanh| < 1)
-  // to at most 2^14, half of the float16 range.  Their rounding (at most
-  // 2^-11 of each bound) enters the value with weight 1 and d/dtau with
-  // weights 2 .. 5; the tables are folded only while the value error stays
-  // below the float32 rounding of the value term c0 and the slope error
-  // below 2^-14 of the slope term c1, else the separable float32 tables are
-  // used.
+  // float16 scales of the folded tables' c2, c3 (and of c4, c5, for the
+  // bound): a power of two that maps the bound 2 max|g_n| + R max|q_n|
+  // (gamma = 1 + tanh < 2, |U| = |tanh| < 1) to at most 2^14, half of the
+  // float16 range.  The rounding of c2, c3 (at most 2^-11 of each bound)
+  // enters the value with weight 1 and d/dtau with weights 2, 3; c4 and c5
+  // are dropped, so their whole bounds enter with weights 1 and 4, 5.  The
+  // tables are folded only while the value error stays below the float32
+  // rounding of the value term c0 and the slope error below 2^-14 of the
+  // slope term c1, else the separable float32 tables are used.
   double bnd[6] = {};
   for (int q = 0; q < 6; ++q) {
     double gmax = 0.0, qmax = 0.0;
@@ -404,9 +405,9 @@ int create_model(const void* blob, size_t nbytes, int device, dpa4c_model** out)
     m->c_scale[q - 2] = static_cast<float>(std::ldexp(1.0, ex));
   }
   const double f16 = std::ldexp(1.0, -11);
-  m->fold_allowed = (bnd[2] + bnd[3] + bnd[4] + bnd[5]) * f16 <= bnd[0] * std::ldexp(1.0, -24) &&
-                    (2.0 * bnd[2] + 3.0 * bnd[3] + 4.0 * bnd[4] + 5.0 * bnd[5]) * f16 <=
-                        bnd[1] * std::ldexp(1.0, -14);
+  const double val_lim = bnd[0] * std::ldexp(1.0, -24), slope_lim = bnd[1] * std::ldexp(1.0, -14);
+  m->fold_allowed = (bnd[2] + bnd[3]) * f16 + bnd[4] + bnd[5] <= val_lim &&
+                    (2.0 * bnd[2] + 3.0 * bnd[3]) * f16 + 4.0 * bnd[4] + 5.0 * bnd[5] <= slope_lim;
 
   // ---- coupling tensors, each symmetrised over the indices of equal degree
   // (the exact integrals are; the quadrature sums are only up to rounding)

@@ -164,8 +164,10 @@ struct dpa4c_model {
   std::mutex mu_lock;
   int64_t last_n = 0;
   int fold_n = -1;                  // species with folded tables; 0 = separable path, -1 = unset
-  float c_scale[4] = {1.0f, 1.0f, 1.0f, 1.0f};   // float16 scales of c2 .. c5 in the folded tables
-  bool fold_allowed = true;            // the float16 rounding of c2 .. c5 is within bounds
+  float c_scale[4] = {1.0f, 1.0f, 1.0f, 1.0f};   // float16 scales of c2 .. c5 (folded tables use c2, c3)
+  // the folded tables hold c0, c1, c2, c3: the float16 rounding of c2, c3
+  // and the dropped c4, c5 are within bounds (else separable tables only)
+  bool fold_allowed = true;
   uint32_t fold_types_mask[4] = {};
 
   dpa4c::ModelDev dev() const;

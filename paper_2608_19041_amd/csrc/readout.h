@@ -28,6 +28,17 @@ namespace dpa4c {
 
 constexpr int kHalf = 32;   // lanes per atom
 
+// vech index t -> (c, c') with c <= c', row-major over the upper triangle
+__device__ inline void vech_pair(int t, int C, int* c, int* cp) {
+  int r = 0;
+  while (t >= C - r) {
+    t -= C - r;
+    ++r;
+  }
+  *c = r;
+  *cp = r + t;
+}
+
 // Readout parameters staged once per workgroup into LDS (the readout reads
 // each of them many times per atom).
 template <class P>
@@ -39,6 +50,10 @@ struct ReadoutParams {
   float mu[P::DSTR];                       // calibration, zero padded
   float inv_sigma[P::DSTR];
   float cpl[P::L >= 3 ? couplings_for(P::L) : 1];   // C123, C233 (then the degree-four ones)
+  // (c, c') of every vech index, c | c' << 8: degree one (C1) and degree two
+  // (C2, which is also K1)
+  uint16_t vp1[P::nG1];
+  uint16_t vp2[P::nG2];
 };
 
 // Cooperative copy of the readout parameters by the ``nthreads`` threads of
@@ -57,6 +72,12 @@ __device__ void stage_readout_params(ReadoutParams<P>& rp, const ModelDev& md, i
   }
   if constexpr (P::L >= 3)
     for (int t = tid; t < couplings_for(P::L); t += nthreads) rp.cpl[t] = md.cpl[t];
+  for (int t = tid; t < P::nG1 + P::nG2; t += nthreads) {
+    const bool one = t < P::nG1;
+    int c, cp;
+    vech_pair(one ? t : t - P::nG1, one ? P::C1 : P::C2, &c, &cp);
+    (one ? rp.vp1[t] : rp.vp2[t - P::nG1]) = static_cast<uint16_t>(c | (cp << 8));
+  }
 }
 
 template <class P>
@@ -94,16 +115,6 @@ constexpr float kInvSqrt6 = 0.4082482904638631f;
 constexpr float kInvSqrt5 = 0.4472135954999579f;
 constexpr float kSqrt12_35 = 0.5855400437691199f;
 
-// vech index t -> (c, c') with c <= c', row-major over the upper triangle
-__device__ inline void vech_pair(int t, int C, int* c, int* cp) {
-  int r = 0;
-  while (t >= C - r) {
-    t -= C - r;
-    ++r;
-  }
-  *c = r;
-  *cp = r + t;
-}
 
 // STF(z) of Eq. (stf) in the basis order (xy, yz, z^2, xz, x^2 - y^2):
 // entry (a, b) of the symmetric trace-free matrix
@@ -322,14 +333,12 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
   for (int o = lane; o < P::nG1 + P::nG2 + P::nG3 + P::nG4; o += kHalf) {
     float acc = 0.0f;
     if (o < P::nG1) {
-      int c, cp;
-      vech_pair(o, P::C1, &c, &cp);
+      const int c = rp.vp1[o] & 0xFF, cp = rp.vp1[o] >> 8;
 #pragma unroll
       for (int m = 0; m < 3; ++m) acc += s.xt1[m * P::C1 + c] * s.xt1[m * P::C1 + cp];
       if (c != cp) acc *= kSqrt2;
     } else if (o < P::nG1 + P::nG2) {
-      int c, cp;
-      vech_pair(o - P::nG1, P::C2, &c, &cp);
+      const int c = rp.vp2[o - P::nG1] & 0xFF, cp = rp.vp2[o - P::nG1] >> 8;
 #pragma unroll
       for (int m = 0; m < 5; ++m) acc += s.xt2[m * P::C2 + c] * s.xt2[m * P::C2 + cp];
       if (c != cp) acc *= kSqrt2;
@@ -344,8 +353,9 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
   }
   // (1,1,2): -(f/sqrt5) v_k1 . Q_eta v_k2, k1 <= k2
   for (int o = lane; o < P::n112; o += kHalf) {
-    int eta = o % P::K2, pr = o / P::K2, k1, k2;
-    vech_pair(pr, P::K1, &k1, &k2);
+    static_assert(P::K1 == P::C2, "the degree-two vech table serves the probes");
+    const int eta = o % P::K2, pr = o / P::K2;
+    const int k1 = rp.vp2[pr] & 0xFF, k2 = rp.vp2[pr] >> 8;
     float acc = 0.0f;
 #pragma unroll
     for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];

@@ -120,14 +120,17 @@ def test_feature_vector_at_the_tabulation_class(dev, dp, name, key):
 
 @pytest.mark.parametrize("key", ["fcc108", "hea54"])
 def test_folded_tables_equal_separable_tables(dev, dp, key):
-    """The same system on the pair-folded tables (float16 c4, c5) and on the
-    separable float32 tables (a fresh model's first call without allocation
-    has no folded tables): E_i and F agree to float32 rounding, and each is
-    within the stated tolerance of the oracle."""
+    """The same system on the pair-folded tables (c0, c1 in float32, c2, c3
+    in scaled float16, c4 and c5 not stored, their bound being below float32
+    resolution for this model) and on the separable float32 tables of the
+    full quintic (a fresh model's first call without allocation has no
+    folded tables): E_i and F agree to float32 rounding, and each is within
+    the stated tolerance of the oracle."""
     spec, w = synth.model_weights("full")
     blob = synth.pack_blob(spec, w)
     s = system_of(key)
     folded = dp.Model(blob)
+    assert folded.info["fold_words"] == 3
     e_f, f_f = run(dp, folded, s, dev)
     e_s, f_s = run(dp, dp.Model(blob), s, dev, noalloc=True)
     ref_e, ref_f = om.Oracle(spec, w).energy_forces(s.pos, s.species, s.cell, s.pbc)
