@@ -44,8 +44,14 @@ namespace {
 constexpr int kTeam = 256;
 constexpr int kWaves = kTeam / kWave;
 
+// Four waves per SIMD for the degree-three variants without the virial
+// (measured faster than three, despite a few spilled registers); the virial
+// and degree-four variants would spill more and keep their natural count.
+template <class P, bool VIR>
+constexpr int backward_min_waves() { return P::L < 4 && !VIR ? 4 : 1; }
+
 template <class P, bool FOLD, bool VIR>
-__global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
+__global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backward_kernel(ModelDev md, int64_t n,
                                                          const int32_t* __restrict__ typ,
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
@@ -55,10 +61,17 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
   static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
   constexpr int G = kWave / P::LPE;   // edge groups in a wave
   __shared__ double wv_all[kWaves][VIR ? G : 1][9];
-  // per edge of a pass: (u, 1/rho), (tau, chi, dchi, table row), (j, a_j)
+  // per edge of a pass: (u, 1/rho), (tau, chi, dchi, table row), (j, a_j);
+  // the per-edge terms that do not depend on the lane's channel: (chi^2,
+  // d chi^2/drho, the S0/S1 term, the degree-three/four part of Q_0), the
+  // gradient of that part, and with folded tables the quintic weights
+  // (e2, e3, f2, f3)
   __shared__ float4 geo_all[kWaves][kWave];
   __shared__ float4 rad_all[kWaves][kWave];
   __shared__ int2 ids_all[kWaves][kWave];
+  __shared__ float4 sc_all[kWaves][kWave];
+  __shared__ float4 cb_all[kWaves][kWave];
+  __shared__ float4 wt_all[kWaves][FOLD ? kWave : 1];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int grp = lane / P::LPE;
@@ -67,6 +80,9 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
   float4* geo = geo_all[wave];
   float4* rad = rad_all[wave];
   int2* ids = ids_all[wave];
+  float4* scl = sc_all[wave];
+  float4* cub = cb_all[wave];
+  float4* wts = wt_all[wave];
   const int T1 = md.n_types1;
   const float inv_delta = md.inv_delta;
   const int nf = md.fold_n;
@@ -93,23 +109,34 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       for (int m = 0; m < 5; ++m) w[m] = k < P::C2 ? gyr[P::Y2 + m * P::C2 + k] : 0.0f;
       quad_form2(w, M2);
     }
+    // channel 0's degree-three (and four) polynomial and the normaliser
+    // gradients, in every lane: the per-edge pass evaluates them once per
+    // edge, and only lane 0 of a group adds them
     float G3[3][6];
     {
       float w[7];
 #pragma unroll
-      for (int m = 0; m < 7; ++m) w[m] = (P::L >= 3 && k == 0) ? gyr[P::Y3 + m] : 0.0f;
+      for (int m = 0; m < 7; ++m) w[m] = P::L >= 3 ? gyr[P::Y3 + m] : 0.0f;
       cubic_form3(w, G3);
+#pragma unroll
+      for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int qq = 0; qq < 6; ++qq) G3[a][qq] = wave_uniform(G3[a][qq]);
     }
     float G4[P::L >= 4 ? 3 : 1][10];   // gradient of the degree-four polynomial
     if constexpr (P::L >= 4) {
       float w[9], pc[15];
 #pragma unroll
-      for (int m = 0; m < 9; ++m) w[m] = k == 0 ? gyr[P::Y4 + m] : 0.0f;
+      for (int m = 0; m < 9; ++m) w[m] = gyr[P::Y4 + m];
       quartic_coeffs4(w, pc);
       quartic_grad4(pc, G4);
+#pragma unroll
+      for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int qq = 0; qq < 10; ++qq) G4[a][qq] = wave_uniform(G4[a][qq]);
     }
-    const float gs0 = k == 0 ? gyr[0] : 0.0f;
-    const float gs1 = k == 0 ? gyr[1] : 0.0f;
+    const float gs0 = wave_uniform(gyr[0]), gs1 = wave_uniform(gyr[1]);
+    const float m0 = k == 0 ? 1.0f : 0.0f;
 
     const int64_t b = row_ptr[i];
     const int cnt = ecount[i];
@@ -126,8 +153,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       const float x_ = ge.x, y = ge.y, z = ge.z, inv_rho = ge.w;
       const float tau = ra.x, chi = ra.y, dchi = ra.z;
       const bool valid = c0 + x < cnt;
-      const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;
-      const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
+      const float4 sc = scl[x];
       float a0 = 0.0f, b0 = 0.0f, psi0 = 0.0f, dpsi0 = 0.0f;
       if constexpr (FOLD) {
         // the quintic of each channel from the table of the pair (a_i, a_j)
@@ -137,8 +163,8 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
         // need the lane's coefficients contracted with dE/dY0 first,
         // A_p = sum_j Ybar0_j c_pj, and then one quintic in tau and its
         // derivative; d/drho's 1/Delta is applied once to the sums.
-        const float e2 = md.c_inv[0] * t2, e3 = md.c_inv[1] * t3;
-        const float f2 = md.c_inv[0] * d1, f3 = md.c_inv[1] * d2;
+        const float4 wt = wts[x];
+        const float e2 = wt.x, e3 = wt.y, f2 = wt.z, f3 = wt.w;
         float A[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jj = 0; jj < P::CPL; ++jj) {
@@ -161,6 +187,8 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
         b0 = fmaf(A[3], f3, fmaf(A[2], f2, A[1])) * inv_delta;
         dpsi0 *= inv_delta;
       } else {
+        const float t2 = tau * tau, t3 = t2 * tau, t4 = t2 * t2, t5 = t4 * tau;
+        const float d1 = 2.0f * tau, d2 = 3.0f * t2, d3 = 4.0f * t3, d4 = 5.0f * t4;
         const int row = __float_as_int(ra.w), aj = ids[x].y;
         float q[4] = {0.f, 0.f, 0.f, 0.f}, dq[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (P::R > 0) {
@@ -200,43 +228,23 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
           }
         }
       }
-      // Q_k(u) and its gradient
-      const float mono[6] = {x_ * x_, x_ * y, x_ * z, y * y, y * z, z * z};
+      // Q_k(u) and its gradient: the lane's degree-one and degree-two parts
+      // here, channel 0's degree-three (and four) part from the pass
       float gq[3];
       gq[0] = M2[0] * x_ + M2[3] * y + M2[5] * z;
       gq[1] = M2[3] * x_ + M2[1] * y + M2[4] * z;
       gq[2] = M2[5] * x_ + M2[4] * y + M2[2] * z;
-      float c3[3] = {0.f, 0.f, 0.f};
-      if constexpr (P::L >= 3) {
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-#pragma unroll
-          for (int qq = 0; qq < 6; ++qq) c3[a] += G3[a][qq] * mono[qq];
-        }
-      }
-      float c4[3] = {0.f, 0.f, 0.f};   // grad P4
-      if constexpr (P::L >= 4) {
-        float mono3[10];
-        cubic_monomials(x_, y, z, mono3);
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-#pragma unroll
-          for (int qq = 0; qq < 10; ++qq) c4[a] += G4[a][qq] * mono3[qq];
-        }
-      }
+      const float4 cb = cub[x];
       // Q = v.u + (1/2) u.M u + (1/3) u.grad P3 + (1/4) u.grad P4 (Euler's
       // relation per degree)
-      float Q = (v1[0] * x_ + v1[1] * y + v1[2] * z) +
-                0.5f * (gq[0] * x_ + gq[1] * y + gq[2] * z) +
-                (1.0f / 3.0f) * (c3[0] * x_ + c3[1] * y + c3[2] * z);
-      if constexpr (P::L >= 4) Q += 0.25f * (c4[0] * x_ + c4[1] * y + c4[2] * z);
-      const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
-      float drho = dchi * a0 + chi * b0 + Q * (dchi2 * psi0 + chi2 * dpsi0) +
-                   gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2;
+      const float Q = (v1[0] * x_ + v1[1] * y + v1[2] * z) +
+                      0.5f * (gq[0] * x_ + gq[1] * y + gq[2] * z) + m0 * sc.w;
+      const float chi2 = sc.x, dchi2 = sc.y;
+      float drho = dchi * a0 + chi * b0 + Q * (dchi2 * psi0 + chi2 * dpsi0) + m0 * sc.z;
       const float wu = chi2 * psi0;
-      float dux = wu * (v1[0] + gq[0] + c3[0] + c4[0]);
-      float duy = wu * (v1[1] + gq[1] + c3[1] + c4[1]);
-      float duz = wu * (v1[2] + gq[2] + c3[2] + c4[2]);
+      float dux = wu * (v1[0] + gq[0] + m0 * cb.x);
+      float duy = wu * (v1[1] + gq[1] + m0 * cb.y);
+      float duz = wu * (v1[2] + gq[2] + m0 * cb.z);
       if (!valid) drho = dux = duy = duz = 0.0f;
       drho = group_sum<P::LPE>(drho);
       dux = group_sum<P::LPE>(dux);
@@ -275,6 +283,7 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
       const int np = cnt - c0 < kWave ? cnt - c0 : kWave;
       {
         float4 ge = make_float4(0.f, 0.f, 0.f, 1.0f), ra = make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 sc = make_float4(0.f, 0.f, 0.f, 0.f), cb = sc, wt = sc;
         int2 id = make_int2(0, 0);
         if (lane < np) {
           const float4 rec = edge[b + c0 + lane];
@@ -287,10 +296,43 @@ __global__ void __launch_bounds__(kTeam) backward_kernel(ModelDev md, int64_t n,
           ge = make_float4(g.ux, g.uy, g.uz, g.inv_rho);
           ra = make_float4(tau, chi, dchi, __int_as_float(FOLD ? aj * md.n_rows + row : row));
           id = make_int2(j, aj);
+          const float x_ = g.ux, y = g.uy, z = g.uz;
+          const float chi2 = chi * chi, dchi2 = 2.0f * chi * dchi;
+          float c3[3] = {0.f, 0.f, 0.f};
+          if constexpr (P::L >= 3) {
+            const float mono[6] = {x_ * x_, x_ * y, x_ * z, y * y, y * z, z * z};
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+#pragma unroll
+              for (int qq = 0; qq < 6; ++qq) c3[a] += G3[a][qq] * mono[qq];
+            }
+          }
+          float c4[3] = {0.f, 0.f, 0.f};   // grad P4
+          if constexpr (P::L >= 4) {
+            float mono3[10];
+            cubic_monomials(x_, y, z, mono3);
+#pragma unroll
+            for (int a = 0; a < 3; ++a) {
+#pragma unroll
+              for (int qq = 0; qq < 10; ++qq) c4[a] += G4[a][qq] * mono3[qq];
+            }
+          }
+          float q0 = (1.0f / 3.0f) * (c3[0] * x_ + c3[1] * y + c3[2] * z);
+          if constexpr (P::L >= 4) q0 += 0.25f * (c4[0] * x_ + c4[1] * y + c4[2] * z);
+          sc = make_float4(chi2, dchi2, gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2, q0);
+          cb = make_float4(c3[0] + c4[0], c3[1] + c4[1], c3[2] + c4[2], 0.0f);
+          if constexpr (FOLD) {
+            const float t2 = tau * tau, t3 = t2 * tau;
+            wt = make_float4(md.c_inv[0] * t2, md.c_inv[1] * t3, md.c_inv[0] * (2.0f * tau),
+                             md.c_inv[1] * (3.0f * t2));
+          }
         }
         geo[lane] = ge;
         rad[lane] = ra;
         ids[lane] = id;
+        scl[lane] = sc;
+        cub[lane] = cb;
+        if constexpr (FOLD) wts[lane] = wt;
       }
       wave_sync();
       if constexpr (FOLD) {

@@ -10,6 +10,12 @@ namespace dpa4c {
 
 __device__ inline int lane_of() { return threadIdx.x & (kWave - 1); }
 
+// A value that is the same in every lane of the wave, moved to a scalar
+// register (out of the vector register budget).
+__device__ inline float wave_uniform(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+
 // Orders the LDS accesses of a wavefront: what its lanes wrote before is
 // visible to its lanes after.  The fences cover LDS only, so outstanding
 // global loads and stores of the wave are not waited for.
