@@ -270,9 +270,8 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
     };
     // the lane's folded table entries of entry x of the pass
     auto load_rows = [&](int x, float3* T) {
-      const float* ft = pair_base + size_t(__float_as_int(rad[x].w)) * (P::C0 * kFoldWords);
-#pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj) T[jj] = load_fold_entry(ft + (jj * P::LPE + k) * kFoldWords);
+      load_fold_row<P::LPE, P::CPL>(
+          pair_base + size_t(__float_as_int(rad[x].w)) * (P::C0 * kFoldWords), k, T);
     };
 
     // The row in passes of 64 edges: each lane first reads one record and

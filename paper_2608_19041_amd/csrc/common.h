@@ -153,8 +153,9 @@ struct ModelDev {
   const float* cpl;         // [kCouplings]: C123 then C233 (symmetric in m2, m3), or null
   const float* E_ref;       // [T+1]
   // pair-folded tables (fold.hip), used when fold_n > 0:
-  // [fold_n^2 pairs][n_rows][CPL] blocks of 4 LPE words, pair (fa, fb) at
-  // fa * fold_n + fb; c_inv = the inverse scales of the float16 c2, c3
+  // [fold_n^2 pairs][n_rows] rows of kFoldWords C0 words in the order of
+  // load_fold_row, pair (fa, fb) at fa * fold_n + fb; c_inv = the inverse
+  // scales of the float16 c2, c3
   const float* ftab;
   int fold_n;
   float c_inv[4];

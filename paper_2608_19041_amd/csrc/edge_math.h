@@ -290,10 +290,42 @@ __device__ inline float4 group_bcast(float4 v) {
   return v;
 }
 
-// The lane's entry of a folded table row: c0 and c1 (float32) and the word
-// of scaled float16 (c2, c3).
-__device__ inline float3 load_fold_entry(const float* __restrict__ p) {
-  return *reinterpret_cast<const float3*>(p);
+// The lane's entries of a folded table row (kFoldWords * C0 words) for its
+// CPL channels c = k + LPE j.  The row holds first the (c0, c1) float32 pairs
+// and then the words of scaled float16 (c2, c3), each permuted so that a
+// lane's values are adjacent: the pairs of its channels j = 2q, 2q + 1 form
+// the 16 bytes at (q LPE + k) * 4, and the words of j = 4q .. 4q + 3 the 16
+// bytes at 2 C0 + (q LPE + k) * 4 (8 bytes at 2 C0 + 2 k when CPL = 2).  A
+// lane thus reads its 12 CPL bytes with 16-byte loads, the group at unit
+// stride.  T[j] = (c0, c1, word) of channel j.
+template <int LPE, int CPL>
+__device__ inline void load_fold_row(const float* __restrict__ row, int k, float3* T) {
+  static_assert(CPL == 2 || CPL % 4 == 0, "folded row layout");
+  float4 a[CPL / 2];
+#pragma unroll
+  for (int q = 0; q < CPL / 2; ++q) a[q] = *reinterpret_cast<const float4*>(row + (q * LPE + k) * 4);
+  uint32_t w[CPL];
+  const float* wrow = row + 2 * LPE * CPL;
+  if constexpr (CPL == 2) {
+    const uint2 v = *reinterpret_cast<const uint2*>(wrow + 2 * k);
+    w[0] = v.x;
+    w[1] = v.y;
+  } else {
+#pragma unroll
+    for (int q = 0; q < CPL / 4; ++q) {
+      const uint4 v = *reinterpret_cast<const uint4*>(wrow + (q * LPE + k) * 4);
+      w[4 * q] = v.x;
+      w[4 * q + 1] = v.y;
+      w[4 * q + 2] = v.z;
+      w[4 * q + 3] = v.w;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < CPL; ++j) {
+    const float4& p = a[j / 2];
+    T[j] = (j & 1) ? make_float3(p.z, p.w, __uint_as_float(w[j]))
+                   : make_float3(p.x, p.y, __uint_as_float(w[j]));
+  }
 }
 __device__ inline float half_lo(uint32_t h) {
   return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h & 0xFFFFu)));

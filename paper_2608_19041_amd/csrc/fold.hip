@@ -83,9 +83,13 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
     const int k = c % LPE, j = c / LPE;
     const float* pc = pair + ((size_t(a * n_types1 + b) * CPL + j) * LPE + k) * PW;
     const float* g = gtab + ((size_t(s) * CPL + j) * LPE + k) * 6;
-    // block of slot j: lane k's three words are c0, c1 (float32) and the word
-    // (c2, c3) in scaled float16
-    float* blk = ftab + ((size_t(p) * rows + s) * CPL + j) * LPE * kFoldWords;
+    // row s of pair p: the (c0, c1) pairs, then the (c2, c3) words, each
+    // permuted so that lane k's values for its channels are adjacent (the
+    // order the edge kernels read, load_fold_row)
+    float* row = ftab + (size_t(p) * rows + s) * C0 * kFoldWords;
+    float* pr = row + ((j / 2) * LPE + k) * 4 + 2 * (j % 2);
+    uint32_t* wd = reinterpret_cast<uint32_t*>(row + 2 * C0) +
+                   (CPL == 2 ? 2 * k + j : ((j / 4) * LPE + k) * 4 + j % 4);
     double v[4];
     for (int q = 0; q < 4; ++q) {
       v[q] = double(pc[0]) * double(g[q]) + (q == 0 ? double(pc[1]) : 0.0);
@@ -97,9 +101,9 @@ __global__ void fold_build_kernel(const float* __restrict__ gtab, const float* _
     for (int q = 0; q < 2; ++q)
       hb[q] = __builtin_bit_cast(uint16_t,
                                  static_cast<_Float16>(static_cast<float>(v[2 + q] * sc[q])));
-    blk[kFoldWords * k] = static_cast<float>(v[0]);
-    blk[kFoldWords * k + 1] = static_cast<float>(v[1]);
-    reinterpret_cast<uint32_t*>(blk)[kFoldWords * k + 2] = uint32_t(hb[0]) | (uint32_t(hb[1]) << 16);
+    pr[0] = static_cast<float>(v[0]);
+    pr[1] = static_cast<float>(v[1]);
+    *wd = uint32_t(hb[0]) | (uint32_t(hb[1]) << 16);
   }
 }
 

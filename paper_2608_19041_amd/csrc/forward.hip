@@ -165,9 +165,8 @@ __global__ void __launch_bounds__(kTeam, forward_min_waves<P>()) forward_kernel(
     };
     // the lane's folded table entries of entry x of the pass
     auto load_rows = [&](int x, float3* T) {
-      const float* ft = pair_base + size_t(__float_as_int(pre[x].z)) * (P::C0 * kFoldWords);
-#pragma unroll
-      for (int jj = 0; jj < P::CPL; ++jj) T[jj] = load_fold_entry(ft + (jj * P::LPE + k) * kFoldWords);
+      load_fold_row<P::LPE, P::CPL>(
+          pair_base + size_t(__float_as_int(pre[x].z)) * (P::C0 * kFoldWords), k, T);
     };
 
     int kept = 0;
