@@ -28,6 +28,25 @@ namespace dpa4c {
 
 constexpr int kHalf = 32;   // lanes per atom
 
+// sum_q a[q] b[q] over N (a multiple of 4) values of two 16-byte aligned LDS
+// rows, four at a time
+typedef float lds_f4 __attribute__((ext_vector_type(4)));
+template <int N>
+__device__ inline float lds_dot(const DPA4C_LDS float* a, const DPA4C_LDS float* b) {
+  static_assert(N % 4 == 0, "rows of whole 16-byte vectors");
+  float acc = 0.0f;
+#pragma unroll
+  for (int q = 0; q < N / 4; ++q) {
+    const lds_f4 x = *reinterpret_cast<const DPA4C_LDS lds_f4*>(a + 4 * q);
+    const lds_f4 y = *reinterpret_cast<const DPA4C_LDS lds_f4*>(b + 4 * q);
+    acc = fmaf(x.x, y.x, acc);
+    acc = fmaf(x.y, y.y, acc);
+    acc = fmaf(x.z, y.z, acc);
+    acc = fmaf(x.w, y.w, acc);
+  }
+  return acc;
+}
+
 // vech index t -> (c, c') with c <= c', row-major over the upper triangle
 __device__ inline void vech_pair(int t, int C, int* c, int* cp) {
   int r = 0;
@@ -41,12 +60,18 @@ __device__ inline void vech_pair(int t, int C, int* c, int* cp) {
 
 // Readout parameters staged once per workgroup into LDS (the readout reads
 // each of them many times per atom).
+// The matrices are also kept transposed (W1T[c'][c] = W1[c][c'], ...) so that
+// both the products and their adjoints read contiguous 16-byte rows.
 template <class P>
 struct ReadoutParams {
-  float W1[P::C1 * P::C1];                 // alignment, degree 1 (I + W applied in-kernel)
-  float W2[P::C2 * P::C2];
-  float A1[P::kHasA1 ? P::C1 * P::K1 : 1]; // probes, degree 1 (identity when K1 = C1)
-  float A2[P::C2 * P::K2];
+  alignas(16) float W1[P::C1 * P::C1];     // alignment, degree 1 (I + W applied in-kernel)
+  alignas(16) float W2[P::C2 * P::C2];
+  alignas(16) float A1[P::kHasA1 ? P::C1 * P::K1 : 1]; // probes, degree 1 (identity when K1 = C1)
+  alignas(16) float A2[P::C2 * P::K2];
+  alignas(16) float W1T[P::C1 * P::C1];
+  alignas(16) float W2T[P::C2 * P::C2];
+  alignas(16) float A1T[P::kHasA1 ? P::C1 * P::K1 : 1];
+  alignas(16) float A2T[P::C2 * P::K2];
   float mu[P::DSTR];                       // calibration, zero padded
   float inv_sigma[P::DSTR];
   float cpl[P::L >= 3 ? couplings_for(P::L) : 1];   // C123, C233 (then the degree-four ones)
@@ -61,11 +86,23 @@ struct ReadoutParams {
 template <class P>
 __device__ void stage_readout_params(ReadoutParams<P>& rp, const ModelDev& md, int tid,
                                      int nthreads) {
-  for (int t = tid; t < P::C1 * P::C1; t += nthreads) rp.W1[t] = md.W1[t];
-  for (int t = tid; t < P::C2 * P::C2; t += nthreads) rp.W2[t] = md.W2[t];
+  for (int t = tid; t < P::C1 * P::C1; t += nthreads) {
+    rp.W1[t] = md.W1[t];
+    rp.W1T[(t % P::C1) * P::C1 + t / P::C1] = md.W1[t];
+  }
+  for (int t = tid; t < P::C2 * P::C2; t += nthreads) {
+    rp.W2[t] = md.W2[t];
+    rp.W2T[(t % P::C2) * P::C2 + t / P::C2] = md.W2[t];
+  }
   if constexpr (P::kHasA1)
-    for (int t = tid; t < P::C1 * P::K1; t += nthreads) rp.A1[t] = md.A1[t];
-  for (int t = tid; t < P::C2 * P::K2; t += nthreads) rp.A2[t] = md.A2[t];
+    for (int t = tid; t < P::C1 * P::K1; t += nthreads) {
+      rp.A1[t] = md.A1[t];
+      rp.A1T[(t % P::K1) * P::C1 + t / P::K1] = md.A1[t];
+    }
+  for (int t = tid; t < P::C2 * P::K2; t += nthreads) {
+    rp.A2[t] = md.A2[t];
+    rp.A2T[(t % P::K2) * P::C2 + t / P::K2] = md.A2[t];
+  }
   for (int t = tid; t < P::DSTR; t += nthreads) {
     rp.mu[t] = t < P::DOUT ? md.mu[t] : 0.0f;
     rp.inv_sigma[t] = t < P::DOUT ? md.inv_sigma[t] : 0.0f;
@@ -80,26 +117,38 @@ __device__ void stage_readout_params(ReadoutParams<P>& rp, const ModelDev& md, i
   }
 }
 
+// Rows that are read as 16-byte vectors are 16-byte aligned: the node state
+// starts 8 bytes into the (aligned) block, so that its Y blocks are.
 template <class P>
-struct ReadoutLds {
+struct alignas(16) ReadoutLds {
+  float ypad_[2];
   float y[P::NS];                 // [S0, S1, Y]
-  float xt1[3 * P::C1];           // aligned features, Eq. (alignment)
-  float xt2[5 * P::C2];
+  alignas(16) float xt1[3 * P::C1];   // aligned features, Eq. (alignment)
+  alignas(16) float xt2[5 * P::C2];
   float xt3[8];                   // degree three (identity probe: Z3 = X~3)
-  float z1[3 * P::K1];            // probes, Eq. (probes)
+  alignas(16) float z1[3 * P::K1];    // probes, Eq. (probes)
+  // channel-major copies, the degree index padded with zeros to 4 (8):
+  // xt1c[c][m] = xt1[m][c], xt2c[c][m] = xt2[m][c], z1c[k][a] = z1[a][k]
+  alignas(16) float xt1c[P::C1 * 4];
+  alignas(16) float xt2c[P::C2 * 8];
+  alignas(16) float z1c[P::K1 * 4];
   float z2[5 * P::K2];
   float q[P::K2][9];              // STF matrices of the degree-two probes
-  float qv[P::K2][P::K1][3];      // Q_eta v_kappa
+  alignas(16) float qv[P::K2][P::K1][4];   // Q_eta v_kappa (fourth entry zero)
   float t123[15], u123[3 * P::K2], w233[35], v233[5];
   // degree four (one channel; Z4 = X~4): X~4, T134[m1] = C134 : Z3 Z4,
   // T224[m1][m2] = C224 . Z4, T244[m1] = C244 : Z4 Z4
   float xt4[P::L >= 4 ? 9 : 1], t134[P::L >= 4 ? 3 : 1], t224[P::L >= 4 ? 25 : 1],
       t244[P::L >= 4 ? 5 : 1];
   // backward only
-  float gxt1[3 * P::C1];
-  float gxt2[5 * P::C2];
+  alignas(16) float gxt1[3 * P::C1];
+  alignas(16) float gxt2[5 * P::C2];
+  // the Gram adjoints as full symmetric matrices, weights included:
+  // Gbar[c][c'] = dE/dG_cc' times 2 (c = c') or sqrt(2)
+  alignas(16) float gb1[P::C1 * P::C1];
+  alignas(16) float gb2[P::C2 * P::C2];
   float gxt3[8];
-  float gz1[3 * P::K1];
+  alignas(16) float gz1[3 * P::K1];
   float gz2[5 * P::K2];
   float gz3[8];
   float gq[P::K2][9];
@@ -179,17 +228,17 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
     if (o < n1) {
       int m = o / P::C1, cp = o % P::C1;
       const DPA4C_LDS float* x = s.y + P::Y1 + m * P::C1;
-      float acc = x[cp];
-#pragma unroll
-      for (int c = 0; c < P::C1; ++c) acc += x[c] * rp.W1[c * P::C1 + cp];
-      s.xt1[o] = acc * i1;
+      const float v = (x[cp] + lds_dot<P::C1>(x, rp.W1T + cp * P::C1)) * i1;
+      s.xt1[o] = v;
+      s.xt1c[cp * 4 + m] = v;
+      if (m == 0) s.xt1c[cp * 4 + 3] = 0.0f;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, cp = t % P::C2;
       const DPA4C_LDS float* x = s.y + P::Y2 + m * P::C2;
-      float acc = x[cp];
-#pragma unroll
-      for (int c = 0; c < P::C2; ++c) acc += x[c] * rp.W2[c * P::C2 + cp];
-      s.xt2[t] = acc * i1;
+      const float v = (x[cp] + lds_dot<P::C2>(x, rp.W2T + cp * P::C2)) * i1;
+      s.xt2[t] = v;
+      s.xt2c[cp * 8 + m] = v;
+      if (m == 0) s.xt2c[cp * 8 + 5] = s.xt2c[cp * 8 + 6] = s.xt2c[cp * 8 + 7] = 0.0f;
     } else if (o < n1 + n2 + n3) {
       int m = o - n1 - n2;
       s.xt3[m] = s.y[P::Y3 + m] * i1;
@@ -204,19 +253,16 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
       int m = o / P::K1, k = o % P::K1;
       float acc;
       if constexpr (P::kHasA1) {
-        acc = 0.0f;
-#pragma unroll
-        for (int c = 0; c < P::C1; ++c) acc += s.xt1[m * P::C1 + c] * rp.A1[c * P::K1 + k];
+        acc = lds_dot<P::C1>(s.xt1 + m * P::C1, rp.A1T + k * P::C1);
       } else {
         acc = s.xt1[m * P::C1 + k];
       }
       s.z1[o] = acc;
+      s.z1c[k * 4 + m] = acc;
+      if (m == 0) s.z1c[k * 4 + 3] = 0.0f;
     } else {
       int t = o - 3 * P::K1, m = t / P::K2, k = t % P::K2;
-      float acc = 0.0f;
-#pragma unroll
-      for (int c = 0; c < P::C2; ++c) acc += s.xt2[m * P::C2 + c] * rp.A2[c * P::K2 + k];
-      s.z2[t] = acc;
+      s.z2[t] = lds_dot<P::C2>(s.xt2 + m * P::C2, rp.A2T + k * P::C2);
     }
   }
   if constexpr (P::L >= 3) {
@@ -292,6 +338,7 @@ __device__ inline void readout_intermediates(DPA4C_LDS ReadoutLds<P>& s,
 #pragma unroll
     for (int b = 0; b < 3; ++b) acc += s.q[eta][a * 3 + b] * s.z1[b * P::K1 + k];
     s.qv[eta][k][a] = acc;
+    if (a == 0) s.qv[eta][k][3] = 0.0f;
   }
   wave_sync();
 }
@@ -334,13 +381,11 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     float acc = 0.0f;
     if (o < P::nG1) {
       const int c = rp.vp1[o] & 0xFF, cp = rp.vp1[o] >> 8;
-#pragma unroll
-      for (int m = 0; m < 3; ++m) acc += s.xt1[m * P::C1 + c] * s.xt1[m * P::C1 + cp];
+      acc = lds_dot<4>(s.xt1c + 4 * c, s.xt1c + 4 * cp);
       if (c != cp) acc *= kSqrt2;
     } else if (o < P::nG1 + P::nG2) {
       const int c = rp.vp2[o - P::nG1] & 0xFF, cp = rp.vp2[o - P::nG1] >> 8;
-#pragma unroll
-      for (int m = 0; m < 5; ++m) acc += s.xt2[m * P::C2 + c] * s.xt2[m * P::C2 + cp];
+      acc = lds_dot<8>(s.xt2c + 8 * c, s.xt2c + 8 * cp);
       if (c != cp) acc *= kSqrt2;
     } else if (o < P::nG1 + P::nG2 + P::nG3) {
 #pragma unroll
@@ -356,9 +401,7 @@ __device__ __attribute__((noinline)) void readout_forward(DPA4C_LDS ReadoutLds<P
     static_assert(P::K1 == P::C2, "the degree-two vech table serves the probes");
     const int eta = o % P::K2, pr = o / P::K2;
     const int k1 = rp.vp2[pr] & 0xFF, k2 = rp.vp2[pr] >> 8;
-    float acc = 0.0f;
-#pragma unroll
-    for (int a = 0; a < 3; ++a) acc += s.z1[a * P::K1 + k1] * s.qv[eta][k2][a];
+    const float acc = lds_dot<4>(s.z1c + 4 * k1, &s.qv[eta][k2][0]);
     put(P::o112 + o, -kInvSqrt5 * (k1 == k2 ? 1.0f : kSqrt2) * acc);
   }
   // (2,2,2): -sqrt(12/35) w tr(Q_a Q_b Q_c)
@@ -711,39 +754,41 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     }
     wave_sync();
   }
-  // --- dE/dX~ from the Gram blocks and the probes
+  // --- dE/dX~ from the Gram blocks and the probes: the Gram adjoints are
+  // first expanded to full symmetric matrices (vech weights included), so
+  // that each output reads two contiguous rows
+  for (int o = lane; o < P::C1 * P::C1 + P::C2 * P::C2; o += kHalf) {
+    if (o < P::C1 * P::C1) {
+      const int c = o / P::C1, cp = o % P::C1;
+      const int a = c < cp ? c : cp, b = c < cp ? cp : c;
+      s.gb1[o] = d[P::oG1 + tri_index(a, b, P::C1)] * (c == cp ? 2.0f : kSqrt2);
+    } else {
+      const int u = o - P::C1 * P::C1, c = u / P::C2, cp = u % P::C2;
+      const int a = c < cp ? c : cp, b = c < cp ? cp : c;
+      s.gb2[u] = d[P::oG2 + tri_index(a, b, P::C2)] * (c == cp ? 2.0f : kSqrt2);
+    }
+  }
+  wave_sync();
   constexpr int n1 = 3 * P::C1, n2 = 5 * P::C2, n3 = (P::L >= 3 ? 7 : 0);
-  for (int o = lane; o < n1 + n2 + n3; o += kHalf) {
-    if (o < n1) {
-      int m = o / P::C1, c = o % P::C1;
-      float acc = 0.0f;
-#pragma unroll
-      for (int cp = 0; cp < P::C1; ++cp) {
-        int a = c < cp ? c : cp, b = c < cp ? cp : c;
-        float gb = d[P::oG1 + tri_index(a, b, P::C1)];
-        acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt1[m * P::C1 + cp];
-      }
-      if constexpr (P::kHasA1) {
-#pragma unroll
-        for (int k = 0; k < P::K1; ++k) acc += s.gz1[m * P::K1 + k] * rp.A1[c * P::K1 + k];
-      } else {
-        acc += s.gz1[m * P::K1 + c];
-      }
-      s.gxt1[o] = acc;
-    } else if (o < n1 + n2) {
-      int t = o - n1, m = t / P::C2, c = t % P::C2;
-      float acc = 0.0f;
-#pragma unroll
-      for (int cp = 0; cp < P::C2; ++cp) {
-        int a = c < cp ? c : cp, b = c < cp ? cp : c;
-        float gb = d[P::oG2 + tri_index(a, b, P::C2)];
-        acc += gb * (c == cp ? 2.0f : kSqrt2) * s.xt2[m * P::C2 + cp];
-      }
+  for (int o = lane; o < n1; o += kHalf) {
+    const int m = o / P::C1, c = o % P::C1;
+    float acc = lds_dot<P::C1>(s.gb1 + c * P::C1, s.xt1 + m * P::C1);
+    if constexpr (P::kHasA1) {
+      acc += lds_dot<P::K1>(s.gz1 + m * P::K1, rp.A1 + c * P::K1);
+    } else {
+      acc += s.gz1[m * P::K1 + c];
+    }
+    s.gxt1[o] = acc;
+  }
+  for (int o = lane; o < n2 + n3; o += kHalf) {
+    if (o < n2) {
+      const int m = o / P::C2, c = o % P::C2;
+      float acc = lds_dot<P::C2>(s.gb2 + c * P::C2, s.xt2 + m * P::C2);
 #pragma unroll
       for (int k = 0; k < P::K2; ++k) acc += s.gz2[m * P::K2 + k] * rp.A2[c * P::K2 + k];
-      s.gxt2[t] = acc;
+      s.gxt2[o] = acc;
     } else {
-      int m = o - n1 - n2;
+      const int m = o - n2;
       s.gxt3[m] = 2.0f * d[P::oG3] * s.xt3[m] + s.gz3[m];
     }
   }
@@ -762,15 +807,11 @@ __device__ __attribute__((noinline)) void readout_backward(DPA4C_LDS ReadoutLds<
     int yi;
     if (o < n1) {
       int m = o / P::C1, c = o % P::C1;
-      xb = s.gxt1[o];
-#pragma unroll
-      for (int cp = 0; cp < P::C1; ++cp) xb += s.gxt1[m * P::C1 + cp] * rp.W1[c * P::C1 + cp];
+      xb = s.gxt1[o] + lds_dot<P::C1>(s.gxt1 + m * P::C1, rp.W1 + c * P::C1);
       yi = P::Y1 + o;
     } else if (o < n1 + n2) {
       int t = o - n1, m = t / P::C2, c = t % P::C2;
-      xb = s.gxt2[t];
-#pragma unroll
-      for (int cp = 0; cp < P::C2; ++cp) xb += s.gxt2[m * P::C2 + cp] * rp.W2[c * P::C2 + cp];
+      xb = s.gxt2[t] + lds_dot<P::C2>(s.gxt2 + m * P::C2, rp.W2 + c * P::C2);
       yi = P::Y2 + t;
     } else if (o < n1 + n2 + n3) {
       int m = o - n1 - n2;
