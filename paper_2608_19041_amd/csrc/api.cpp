@@ -521,7 +521,7 @@ int energy_forces_core(const dpa4c_model* m, const double* pos, const int32_t* s
     rc = launch_zero_i64(B.check, 2, st);
     if (rc) return rc;
     rc = launch_skin_rev(row_ptr, nbr_j, nbr_shift, N, n_pairs, reinterpret_cast<int32_t*>(B.edge),
-                         false, B.skin_rev, B.check, st);
+                         false, B.skin_rev, B.check, nullptr, st);
     if (rc) return rc;
   }
   // the list's size and the pairs found come back with the species mask
@@ -728,7 +728,8 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                        w.edge.as<int32_t>(), st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.edge.as<int32_t>(), true, w.skin_rev.as<int32_t>(), nullptr, st);
+                        N, w.cap, w.edge.as<int32_t>(), true, w.skin_rev.as<int32_t>(), nullptr,
+                        &w.nb, st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
     if (r) return r;

@@ -33,10 +33,13 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 // jsamp = scratch of cap / 16 + 1 int32: nbr_j at every 16th position of the
 // list, computed here unless ``jsamp_ready`` (fill_skin_list wrote it);
 // with ``paired`` (device int64, zeroed by the caller) also the number of
-// reverse pairs found, so a symmetric list of E entries gives E / 2
+// reverse pairs found, so a symmetric list of E entries gives E / 2; with
+// ``order_of`` (the scratch of the build that made this list) the rows are
+// taken in the build's spatial bin order
+struct NeighborScratch;
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
                     int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
-                    int64_t* paired, hipStream_t st);
+                    int64_t* paired, const NeighborScratch* order_of, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
 // index of every atom into ``fidx`` [n]; ``mask_dev`` is device scratch of 4

@@ -622,7 +622,10 @@ __device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s,
 // runs 64 searches.  Entries whose partner is missing (a malformed caller
 // list) keep the -1 of the fill before.  With ``paired`` the pairs found
 // are counted (one atomic per wave), so the caller can tell a symmetric list
-// (2 x pairs = entries) from one that is not.
+// (2 x pairs = entries) from one that is not.  With ``order`` (the
+// neighbour build's atom records in bin order) the rows are taken in that
+// spatial order, so that centres searched close in time share their rows j
+// in L2; the results do not depend on the order.
 template <bool VEC>
 __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                           const int32_t* __restrict__ nbr_j,
@@ -630,7 +633,8 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
                                                           int64_t cap,
                                                           const int32_t* __restrict__ jsamp,
                                                           int32_t* __restrict__ rev,
-                                                          unsigned long long* __restrict__ paired) {
+                                                          unsigned long long* __restrict__ paired,
+                                                          const CellRec* __restrict__ order) {
   __shared__ int64_t qs_all[kWavesPerBlock][2 * kWave];
   __shared__ int32_t qi_all[kWavesPerBlock][2 * kWave];
   const int w = threadIdx.x / kWave;
@@ -661,7 +665,8 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
     wave_lds_sync();
     qn = rest;
   };
-  for (int64_t i = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + w; i < n; i += nwaves) {
+  for (int64_t r = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + w; r < n; r += nwaves) {
+    const int64_t i = order ? order[r].j : r;
     const int64_t b = row_ptr[i], e = row_ptr[i + 1];
     if (!row_ok(b, e, cap)) continue;
     for (int64_t s0 = b; s0 < e; s0 += kWave) {
@@ -914,7 +919,8 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
                     int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
-                    int64_t* paired, hipStream_t st) {
+                    int64_t* paired, const NeighborScratch* order_of, hipStream_t st) {
+  const CellRec* order = order_of ? order_of->cell_rec.as<CellRec>() : nullptr;
   if (n <= 0) return 0;
   int64_t sb = (cap + kBlock - 1) / kBlock;
   sb = sb < 1 ? 1 : (sb > 8192 ? 8192 : sb);
@@ -932,11 +938,11 @@ int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t*
   if (vec)
     hipLaunchKernelGGL(skin_rev_kernel<true>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr,
                        nbr_j, nbr_shift, cap, jsamp, skin_rev,
-                       reinterpret_cast<unsigned long long*>(paired));
+                       reinterpret_cast<unsigned long long*>(paired), order);
   else
     hipLaunchKernelGGL(skin_rev_kernel<false>, dim3(waves_grid(n)), dim3(kBlock), 0, st, n, row_ptr,
                        nbr_j, nbr_shift, cap, jsamp, skin_rev,
-                       reinterpret_cast<unsigned long long*>(paired));
+                       reinterpret_cast<unsigned long long*>(paired), order);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
