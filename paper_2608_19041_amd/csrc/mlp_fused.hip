@@ -168,7 +168,22 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
   constexpr int NTD = (DT + kWavesPB - 1) / kWavesPB;
   constexpr int NTD1 = NTD > 1 ? NTD - 1 : 1;         // the shorter dE/dD product
   constexpr int APW = kRows / kWavesPB;               // atoms per wave in the readouts
+  // Two activation tiles: a product reads one and its epilogue writes the
+  // other, so a wave that has finished its share of a product goes on to its
+  // epilogue while the others still read (one barrier per layer).  As (row
+  // stride LDA) holds D, h2, p3, p1 and dE/dD; Bs (LDB) holds h1 and p2.
+  // Only where the workgroup already has a CU to itself and the second tile
+  // still fits in LDS; otherwise both are As, with a barrier between a
+  // product and its epilogue.
+  constexpr int LDB = F + 4;
+  constexpr size_t kBase = sizeof(float) * kRows * LDA + sizeof(ReadoutLds<P>) * kRows +
+                           sizeof(ReadoutParams<P>) + sizeof(float) * kWavesPB * kRows;
+  constexpr bool kTwo =
+      kBase > 80 * 1024 && kBase + sizeof(float) * kRows * LDB + 1024 <= 160 * 1024;
   __shared__ float As[kRows * LDA];
+  __shared__ float Bs_buf[kTwo ? kRows * LDB : 1];
+  float* const Bs = kTwo ? Bs_buf : As;
+  constexpr int LDBv = kTwo ? LDB : LDA;
   __shared__ float epart[kWavesPB][kRows];
   __shared__ ReadoutLds<P> rl_all[kRows];   // one per atom of the tile
   __shared__ ReadoutParams<P> rp;
@@ -236,12 +251,18 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
     float wh[NT];        // head weights of the wave's columns
 #pragma unroll
     for (int layer = 0; layer < 3; ++layer) {
+      // layer 0 reads D from As and writes h1 to Bs, layer 1 reads Bs and
+      // writes h2 to As, layer 2 reads As; h3 stays in registers (head)
+      const float* src = layer == 1 ? Bs : As;
+      const int lds = layer == 1 ? LDBv : LDA;
+      float* dst = layer == 0 ? Bs : As;
+      const int ldd = layer == 0 ? LDBv : LDA;
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
       float bias[NT];
       BStream<NT> bsn;
-      mfma_tiles<NT>(acc, As, LDA, (layer == 0 ? KP : F) / 16, bs, lane, lane16, [&] {
+      mfma_tiles<NT>(acc, src, lds, (layer == 0 ? KP : F) / 16, bs, lane, lane16, [&] {
 #pragma unroll
         for (int t = 0; t < NT; ++t)
           bias[t] = t < nt ? p.bias[layer][(wave + kWavesPB * t) * 16 + col_in] : 0.0f;
@@ -255,7 +276,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
         }
       });
       bs = bsn;
-      __syncthreads();   // everyone has read the A tile
+      if constexpr (!kTwo) __syncthreads();   // everyone has read the A tile
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if (t >= nt) continue;
@@ -267,10 +288,10 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
           const float act = pre * sg;
           s[layer][t][r] = sg * (1.0f + pre * (1.0f - sg));
           h[t][r] = layer == 0 ? act : act + h[t][r];   // identity residual for equal widths
-          As[(4 * rgrp + r) * LDA + col] = h[t][r];
+          if (layer < 2) dst[(4 * rgrp + r) * ldd + col] = h[t][r];
         }
       }
-      __syncthreads();
+      __syncthreads();   // the next A tile is complete, and this one is read
     }
     // ---- head: E_i = h3 . w + b + E_ref, fixed-order reduction
     float part[4] = {0.f, 0.f, 0.f, 0.f};
@@ -314,18 +335,24 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
     BStream<NTD> bsd;   // the B stream of dE/dD
 #pragma unroll
     for (int layer = 2; layer >= 1; --layer) {
+      // layer 2 reads p3 from As and writes p2 to Bs, layer 1 reads Bs and
+      // writes p1 to As
+      const float* src = layer == 2 ? As : Bs;
+      const int lds = layer == 2 ? LDA : LDBv;
+      float* dst = layer == 2 ? Bs : As;
+      const int ldd = layer == 2 ? LDBv : LDA;
       v4f acc[NT];
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
       BStream<NT> bsn;
-      mfma_tiles<NT>(acc, As, LDA, F / 16, bs, lane, lane16, [&] {
+      mfma_tiles<NT>(acc, src, lds, F / 16, bs, lane, lane16, [&] {
         if (layer == 2)
           bstream_open(bsn, p.WT[1], F / 16, wave, kWavesPB, FT, lane16);
         else
           bstream_open(bsd, p.WT[0], F / 16, wave, kWavesPB, DT, lane16);
       });
       if (layer == 2) bs = bsn;
-      __syncthreads();
+      if constexpr (!kTwo) __syncthreads();   // everyone has read the A tile
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         if (t >= nt) continue;
@@ -333,7 +360,7 @@ __global__ void __launch_bounds__(kThreads) atom_kernel(MlpArgs p, ModelDev md, 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           h[t][r] += acc[t][r];
-          As[(4 * rgrp + r) * LDA + col] = h[t][r] * s[layer - 1][t][r];
+          dst[(4 * rgrp + r) * ldd + col] = h[t][r] * s[layer - 1][t][r];
         }
       }
       __syncthreads();
