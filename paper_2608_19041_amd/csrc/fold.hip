@@ -26,10 +26,13 @@
 // instead of a g quintic, R q quintics and the pair coefficients.  Systems
 // with more than kMaxFoldTypes species, or whose folded tables would exceed
 // kMaxFoldBytes, use the separable tables directly.  Five species at full
-// width fold into 25 tables of 5.8 MB (144 MB, most of the last-level cache);
-// on the 5-species alloy that measured faster than the separable tables
-// (backward 0.94 -> 0.70 ms at 31,250 atoms), since every edge then reads
-// 20 B per channel from one table instead of 48 B from two.
+// width (128 channels, 3,000 rows at r_c = 6 A and Delta = 0.002 A) fold into
+// 25 tables of 4.6 MB (115 MB, within the last-level cache); on the 5-species
+// alloy the folded tables measured faster than the separable ones (backward
+// 0.94 -> 0.70 ms at 31,250 atoms, when a folded channel still took 16 B),
+// since every edge then reads one 12-byte entry per channel from one table
+// instead of 24 B of g coefficients per channel plus the q rows and the pair
+// coefficients.
 #include <hip/hip_runtime.h>
 
 #include <cstring>

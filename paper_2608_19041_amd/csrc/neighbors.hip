@@ -41,6 +41,7 @@ namespace {
 constexpr int kBlock = 256;            // 4 waves
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kMaxRow = 512;           // longest row the fill kernel ranks in LDS
+constexpr int kRankBlock = 8;          // keys compared per step of the bucketed rank
 constexpr int kMaxSeg = kWave;         // stencil runs a wave holds at once
 constexpr int64_t kFlagCapacity = 1, kFlagRowTooLong = 2, kFlagShift = 4, kFlagNonFinite = 8;
 constexpr int kFlagMaxRow = 3;         // flags[3]: the longest row of the last count
@@ -65,6 +66,14 @@ __device__ inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// The same for LDS alone: outstanding global loads and stores of the wave
+// are not waited for.
+__device__ inline void wave_local_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 struct GridDev {
@@ -442,11 +451,105 @@ __device__ __forceinline__ void rank_row(int len, int64_t r0, KB* kb, int32_t* _
   }
 }
 
+typedef long long i64x2 __attribute__((ext_vector_type(2)));
+
+// The same ranks for a row held in LDS, counted inside buckets: the keys
+// are grouped by j into at most 64 buckets of one power-of-two width over
+// the row's range of j, so a key's bucket never decreases as the key grows
+// and its rank is the number of keys in lower buckets plus the number of
+// smaller keys in its own bucket.  The keys are regrouped in place by bucket
+// (in any order inside one); each lane then takes grouped keys and compares
+// only with its bucket.  ``boff`` and ``bend`` are 64 ints of the wave's LDS;
+// kb (16-byte aligned) has room for kRankBlock keys past the row.
+template <int PER, class KB>
+__device__ __forceinline__ void rank_row_lds(int len, int64_t r0, KB* kb, int32_t* boff,
+                                             int32_t* bend, int32_t* __restrict__ nbr_j,
+                                             int32_t* __restrict__ nbr_shift,
+                                             int32_t* __restrict__ jsamp) {
+  const int lane = lane_id();
+  int64_t key[PER];
+  int32_t jlo = INT32_MAX, jhi = INT32_MIN;
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int t = lane + kWave * r;
+    key[r] = t < len ? kb[t] : 0;
+    if (t < len) {
+      const int32_t j = static_cast<int32_t>(key[r] >> 24);
+      jlo = j < jlo ? j : jlo;
+      jhi = j > jhi ? j : jhi;
+    }
+  }
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) {
+    const int32_t lo = __shfl_xor(jlo, off), hi = __shfl_xor(jhi, off);
+    jlo = lo < jlo ? lo : jlo;
+    jhi = hi > jhi ? hi : jhi;
+  }
+  jlo = __builtin_amdgcn_readfirstlane(jlo);
+  jhi = __builtin_amdgcn_readfirstlane(jhi);
+  // width 2^sh with (jhi - jlo) >> sh < 64
+  const uint32_t span = static_cast<uint32_t>(jhi - jlo);
+  const int sh = span < 64u ? 0 : 26 - __clz(span);
+  auto bucket = [&](int64_t k) {
+    return static_cast<int>(static_cast<uint32_t>(static_cast<int32_t>(k >> 24) - jlo) >> sh);
+  };
+  boff[lane] = 0;
+  wave_local_sync();
+  int bk[PER], slot[PER];
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    bk[r] = 0;
+    slot[r] = 0;
+    if (lane + kWave * r < len) {
+      bk[r] = bucket(key[r]);
+      slot[r] = atomicAdd(&boff[bk[r]], 1);
+    }
+  }
+  wave_local_sync();
+  const int cnt = boff[lane];
+  const int incl = wave_inclusive_scan(cnt);
+  wave_local_sync();
+  boff[lane] = incl - cnt;
+  bend[lane] = incl;
+  wave_local_sync();
+#pragma unroll
+  for (int r = 0; r < PER; ++r)
+    if (lane + kWave * r < len) kb[boff[bk[r]] + slot[r]] = key[r];
+  if (lane < kRankBlock) kb[len + lane] = INT64_MAX;   // sentinels past the row
+  wave_local_sync();
+  // Every key before a bucket is smaller than the bucket's keys and every
+  // key after it larger (or a sentinel), so a key's rank is counted over
+  // whole aligned blocks of kRankBlock keys around its bucket.
+#pragma unroll
+  for (int r = 0; r < PER; ++r) {
+    const int t = lane + kWave * r;
+    if (t < len) {
+      const int64_t k = kb[t];
+      const int b = bucket(k);
+      const int lo = boff[b] & ~(kRankBlock - 1), hi = bend[b];
+      int rank = lo;
+      for (int u = lo; u < hi; u += kRankBlock) {
+        const i64x2* q = reinterpret_cast<const i64x2*>(kb + u);
+#pragma unroll
+        for (int v = 0; v < kRankBlock / 2; ++v) {
+          const i64x2 x = q[v];
+          rank += (x.x < k ? 1 : 0) + (x.y < k ? 1 : 0);
+        }
+      }
+      const int64_t at = r0 + rank;
+      const int32_t j = static_cast<int32_t>(k >> 24);
+      nbr_j[at] = j;
+      nbr_shift[at] = static_cast<int32_t>(k & 0xFFFFFF);
+      if (jsamp && (at & 15) == 0) jsamp[at >> 4] = j;
+    }
+  }
+}
+
 // One row: the accepted keys into kb[0, len) in candidate order, then
-// each written at its rank.  ``kb`` is the wave's LDS row or, for a row
-// longer than kMaxRow, a global scratch row (inlined for each, so LDS rows
-// use LDS instructions).
-template <bool TRIC, class KB>
+// each written at its rank.  ``kb`` is the wave's LDS row (LDS_ROW) or, for
+// a row longer than kMaxRow, a global scratch row (inlined for each, so LDS
+// rows use LDS instructions).
+template <bool TRIC, bool LDS_ROW, class KB>
 __device__ __forceinline__ void fill_row(const GridDev& g, int64_t i, int64_t r0, int len, KB* kb,
                                          const int64_t* __restrict__ qpos,
                                          const int32_t* __restrict__ wrap,
@@ -475,12 +578,21 @@ __device__ __forceinline__ void fill_row(const GridDev& g, int64_t i, int64_t r0
   });
   if (shift_bad)
     atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagShift);
-  wave_lds_sync();
-  if (len <= kWave) rank_row<1>(len, r0, kb, nbr_j, nbr_shift, jsamp);
-  else if (len <= 2 * kWave) rank_row<2>(len, r0, kb, nbr_j, nbr_shift, jsamp);
-  else if (len <= 4 * kWave) rank_row<4>(len, r0, kb, nbr_j, nbr_shift, jsamp);
-  else rank_row<8>(len, r0, kb, nbr_j, nbr_shift, jsamp);
-  wave_lds_sync();   // the row's keys are read before the next row overwrites them
+  if constexpr (LDS_ROW) {
+    wave_local_sync();
+    if (len <= kWave) rank_row<1>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+    else if (len <= 2 * kWave) rank_row_lds<2>(len, r0, kb, sg.begin, sg.vend, nbr_j, nbr_shift, jsamp);
+    else if (len <= 4 * kWave) rank_row_lds<4>(len, r0, kb, sg.begin, sg.vend, nbr_j, nbr_shift, jsamp);
+    else rank_row_lds<8>(len, r0, kb, sg.begin, sg.vend, nbr_j, nbr_shift, jsamp);
+    wave_local_sync();   // the row's keys are read before the next row overwrites them
+  } else {
+    wave_lds_sync();     // the keys are global memory here: the stores are waited for
+    if (len <= kWave) rank_row<1>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+    else if (len <= 2 * kWave) rank_row<2>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+    else if (len <= 4 * kWave) rank_row<4>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+    else rank_row<8>(len, r0, kb, nbr_j, nbr_shift, jsamp);
+    wave_lds_sync();
+  }
 }
 
 // Rows of the skin list: the accepted candidates of centre i as keys
@@ -504,7 +616,7 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
                                                       int64_t* __restrict__ long_keys,
                                                       int64_t* __restrict__ flags) {
   __shared__ SegLds segs[kWavesPerBlock];
-  __shared__ int64_t keys_all[kWavesPerBlock][kMaxRow];
+  __shared__ alignas(16) int64_t keys_all[kWavesPerBlock][kMaxRow + kRankBlock];
   if (row_ptr[n] > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagCapacity);
@@ -519,10 +631,10 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
     const int64_t r0 = row_ptr[i];
     const int len = static_cast<int>(row_ptr[i + 1] - r0);
     if (len <= kMaxRow) {
-      fill_row<TRIC>(g, i, r0, len, keys_all[w], qpos, wrap, cell_of, start, rec, sg, nbr_j,
+      fill_row<TRIC, true>(g, i, r0, len, keys_all[w], qpos, wrap, cell_of, start, rec, sg, nbr_j,
                      nbr_shift, jsamp, flags);
     } else if (long_keys) {
-      fill_row<TRIC>(g, i, r0, len, long_keys + r0, qpos, wrap, cell_of, start, rec, sg, nbr_j,
+      fill_row<TRIC, false>(g, i, r0, len, long_keys + r0, qpos, wrap, cell_of, start, rec, sg, nbr_j,
                      nbr_shift, jsamp, flags);
     } else if (lane_id() == 0) {
       atomicOr(reinterpret_cast<unsigned long long*>(flags), (unsigned long long)kFlagRowTooLong);
