@@ -86,9 +86,9 @@ def stage_work(name, spec, n_atoms, n_edges):
       per-atom kernel      - matrix cores: forward and input-gradient
         products of the MLP, 2 x 2 (D_out F + (L-1) F^2) flop per atom (the
         readout and its VJP add ~1% VALU work, not counted)
-      forces               - HBM: per edge 16 B gradient (with j), 16 B for
-        the reverse slot (crev, row_ptr[j], cidx) and 16 B gathered reverse
-        gradient; per atom 12 B row bounds in, 24 B force out, and the
+      forces               - HBM: per edge 4 B skin position of the compact
+        slot, 16 B gradient, 8 B position of the reverse and 16 B gathered
+        reverse gradient; per atom 12 B row bounds in, 24 B force out, and the
         velocity-Verlet work fused into it: species 4 B, E_i 8 B, velocity
         24 B in and out, position 24 B in and out, build snapshot 24 B
     """
@@ -108,7 +108,7 @@ def stage_work(name, spec, n_atoms, n_edges):
         # per-atom kernel: forward and input-gradient products of the MLP
         return "mfma", 4 * (D * F + (nl - 1) * F * F) * n_atoms, "flop"
     if name == "forces":
-        return "hbm", 48 * n_edges + (36 + 132) * n_atoms, "byte"
+        return "hbm", 44 * n_edges + (36 + 132) * n_atoms, "byte"
     return None
 
 

@@ -179,9 +179,8 @@ int ensure_workspace(dpa4c_model* m, int64_t n, int64_t cap) {
   const int64_t nn = n < 1 ? 1 : n, cc = cap < 1 ? 1 : cap;
   DPA4C_TRY(w.ecount.ensure(4 * nn));
   DPA4C_TRY(w.edge.ensure(16 * cc));
-  DPA4C_TRY(w.cidx.ensure(4 * cc));
-  DPA4C_TRY(w.crev.ensure(4 * cc));
-  DPA4C_TRY(w.skin_rev.ensure(4 * cc));
+  DPA4C_TRY(w.cskin.ensure(4 * cc));
+  DPA4C_TRY(w.skin_rev.ensure(8 * cc));
   DPA4C_TRY(w.node.ensure(4 * nn * (m->S + 2)));
   DPA4C_TRY(w.node_grad.ensure(4 * nn * (m->S + 2)));
   DPA4C_TRY(w.epart.ensure(8 * (partial_count(nn) + 8)));
@@ -198,9 +197,8 @@ EvalBufs ws_bufs(Workspace& w) {
   EvalBufs b{};
   b.ecount = w.ecount.as<int32_t>();
   b.edge = w.edge.as<float4>();
-  b.cidx = w.cidx.as<int32_t>();
-  b.crev = w.crev.as<int32_t>();
-  b.skin_rev = w.skin_rev.as<int32_t>();
+  b.cskin = w.cskin.as<int32_t>();
+  b.skin_rev = w.skin_rev.as<int64_t>();
   b.node = w.node.as<float>();
   b.node_grad = w.node_grad.as<float>();
   b.epart = w.epart.as<double>();
@@ -212,8 +210,7 @@ EvalBufs ws_bufs(Workspace& w) {
 
 // the compaction inputs and outputs of a model evaluation
 CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nbr_j,
-                         const int32_t* nbr_shift, const int32_t* skin_rev, int64_t rcq,
-                         int64_t cap, const EvalBufs& w) {
+                         const int32_t* nbr_shift, int64_t rcq, int64_t cap, const EvalBufs& w) {
   CompactArgs ca{};
   ca.pos = pos;
   ca.nbr_j = nbr_j;
@@ -227,9 +224,7 @@ CompactArgs compact_args(const CellGrid& g, const double* pos, const int32_t* nb
   ca.cap = cap;
   ca.ecount = w.ecount;
   ca.edge = w.edge;
-  ca.skin_rev = skin_rev;
-  ca.cidx = w.cidx;
-  ca.crev = w.crev;
+  ca.cskin = w.cskin;
   return ca;
 }
 
@@ -250,7 +245,7 @@ struct NvtConfig {
 // the stages may be timed and the inputs are kept for dpa4c_debug_stages.
 int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, int64_t n,
               const CellGrid& g, const int64_t* row_ptr, const int32_t* nbr_j,
-              const int32_t* nbr_shift, int64_t cap, const int32_t* skin_rev, double* e_atom,
+              const int32_t* nbr_shift, int64_t cap, const int64_t* skin_rev, double* e_atom,
               double* forces, double* e_total, const StepTail* tail, const VirialOut* vir,
               double* virial, const EvalBufs& B, const int32_t* fidx, bool record,
               hipStream_t st) {
@@ -261,7 +256,7 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   Workspace& w = m->ws;
   const int64_t rcq = qfix_host(m->r_c);
   int rc;
-  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, skin_rev, rcq, cap, B);
+  const CompactArgs ca = compact_args(g, pos, nbr_j, nbr_shift, rcq, cap, B);
   {
     StageScope t(m, kStForward, st, record);
     rc = launch_forward(m, n, species, fidx, row_ptr, ca, B.node, st);
@@ -274,14 +269,14 @@ int run_model(const dpa4c_model* mc, const double* pos, const int32_t* species, 
   }
   {
     StageScope t(m, kStBackward, st, record);
-    rc = launch_backward(m, n, species, fidx, row_ptr, B.ecount, B.edge, B.node_grad,
+    rc = launch_backward(m, n, species, fidx, row_ptr, B.ecount, B.edge, B.cskin, B.node_grad,
                          vir ? vir->atom : nullptr, st);
     if (rc) return rc;
   }
   {
     StageScope t(m, kStForces, st, record);
-    // the backward kernel has left dE/dr_ij in the edge records
-    rc = launch_forces(n, row_ptr, B.ecount, B.edge, B.crev, B.cidx, forces, tail, vir, st);
+    // the backward kernel has left dE/dr_ij in the edge array at the skin positions
+    rc = launch_forces(n, row_ptr, B.ecount, B.edge, B.cskin, skin_rev, forces, tail, vir, st);
     if (rc) return rc;
     if (vir && virial) {
       rc = launch_sum_components(vir->part_v, tail_partial_count(n), 9, virial, st);
@@ -356,14 +351,14 @@ void dpa4c_model_destroy(dpa4c_model* m) {
   m->params.release();
   Workspace& w = m->ws;
   DevBuf* bufs[] = {&w.skin_row, &w.skin_j, &w.skin_shift, &w.skin_rev, &w.qbuild, &w.ecount,
-                    &w.edge,     &w.cidx,   &w.node,
+                    &w.edge,     &w.cskin,  &w.node,
                     &w.desc,     &w.node_grad, &w.epart,  &w.flags,      &w.inv_mass, &w.mass,
                     &w.eatom,    &w.tailpart,  &w.backup,  &w.ftab,      &w.fold_map, &w.fold_mask,  &w.fidx,
                     &w.check,
                     &w.nb.qpos,  &w.nb.wrap, &w.nb.cell_of, &w.nb.cell_cnt, &w.nb.cell_start,
                     &w.nb.cell_fill, &w.nb.cell_rec, &w.nb.long_keys, &w.nb.counts,
                     &w.nb.partials,
-                    &w.virpart,  &w.nvt,     &w.crev,     &w.watom,     &w.nb.extent};
+                    &w.virpart,  &w.nvt,     &w.watom,     &w.nb.extent};
   for (DevBuf* b : bufs) b->release();
   for (hipEvent_t e : m->timing.pool) hipEventDestroy(e);
   if (w.host_flags) hipHostFree(w.host_flags);
@@ -454,14 +449,14 @@ int build_neighbors(const double* pos, int64_t N, const double cell[9], const in
 
 namespace dpa4c {
 
-void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[11]) {
+void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[kEvalBufs]) {
   const size_t nn = n < 1 ? 1 : size_t(n), cc = cap < 1 ? 1 : size_t(cap);
   auto r256 = [](size_t b) { return (b + 255) / 256 * 256; };
-  const size_t raw[11] = {4 * nn,       16 * cc,      4 * cc,
-                          4 * cc,       4 * cc,       4 * nn * size_t(ns),
-                          4 * nn * size_t(ns),        8 * (size_t(partial_count(int64_t(nn))) + 8),
-                          4 * nn,       4 * sizeof(uint32_t), 2 * sizeof(int64_t)};
-  for (int k = 0; k < 11; ++k) sizes[k] = r256(raw[k]);
+  const size_t raw[kEvalBufs] = {4 * nn,       16 * cc,      4 * cc,
+                                 8 * cc,       4 * nn * size_t(ns),
+                                 4 * nn * size_t(ns),        8 * (size_t(partial_count(int64_t(nn))) + 8),
+                                 4 * nn,       4 * sizeof(uint32_t), 2 * sizeof(int64_t)};
+  for (int k = 0; k < kEvalBufs; ++k) sizes[k] = r256(raw[k]);
 }
 
 // compute_energy_forces with the optional virial (virial == nullptr: none)
@@ -728,7 +723,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
                        w.edge.as<int32_t>(), st);
     if (r) return r;
     r = launch_skin_rev(w.skin_row.as<int64_t>(), w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(),
-                        N, w.cap, w.edge.as<int32_t>(), true, w.skin_rev.as<int32_t>(), nullptr,
+                        N, w.cap, w.edge.as<int32_t>(), true, w.skin_rev.as<int64_t>(), nullptr,
                         &w.nb, st);
     if (r) return r;
     r = launch_snapshot_q(pos, N, w.qbuild.as<int64_t>(), st);
@@ -819,7 +814,7 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     vo.atom = w.watom.as<double>();
     return run_model(m, pos, species, N, g_cut, w.skin_row.as<int64_t>(),
                      w.skin_j.as<int32_t>(), w.skin_shift.as<int32_t>(), w.cap,
-                     w.skin_rev.as<int32_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
+                     w.skin_rev.as<int64_t>(), w.eatom.as<double>(), forces, nullptr, &tail,
                      nvt ? &vo : nullptr, nullptr, ws_bufs(w), fidx, true, st);
   };
   // the end of a batch: the totals of step ``last`` (NVT: its closing chain
@@ -985,8 +980,7 @@ int dpa4c_debug_stages(const dpa4c_model* m, int64_t N, float* node_state, float
   if (N == 0) return 0;
   // recompute node state and descriptor from the stored compacted edges
   const CompactArgs ca = compact_args(w.last_grid, w.last_pos, w.skin_j_used, w.skin_shift_used,
-                                      w.skin_rev.as<int32_t>(), qfix_host(m->r_c), w.cap_used,
-                                      ws_bufs(w));
+                                      qfix_host(m->r_c), w.cap_used, ws_bufs(w));
   int rc = launch_forward(m, N, w.last_species, w.last_fidx, w.skin_row_used, ca,
                           w.node.as<float>(), st);
   if (rc) return rc;

@@ -189,13 +189,12 @@ __global__ void __launch_bounds__(kBlock) kick_drift_kernel(double* __restrict__
   if ((threadIdx.x & (kWave - 1)) == 0) record_check(c, flags, step);
 }
 
-// Force assembly.  Compact slot s of row b = row_ptr[k] holds the gradient
-// g_e with the bits of j in its fourth component; the reverse edge sits in row
-// j at skin position crev[s], so its gradient is at
-// grad[row_ptr[j] + cidx[row_ptr[j] + crev[s]]] (every edge inside r_c has its
-// reverse inside r_c).  All these indices are row-local, so the list length
-// is not limited by 32-bit indexing.  Sixteen lanes per atom, sixteen atoms
-// per group.
+// Force assembly.  The gradient g_e of compact slot c of row b = row_ptr[k]
+// sits at the skin position of the edge, grad[b + cskin[b + c]], and the
+// gradient of its reverse at the skin position of the reverse,
+// grad[skin_rev[b + cskin[b + c]]] (every edge inside r_c has its reverse
+// inside r_c, by the exact integer predicate), so a reverse takes one
+// gather.  Sixteen lanes per atom, sixteen atoms per group.
 //
 // With TAIL (a velocity-Verlet step) the lane that holds F_k also applies
 // the second half kick v += dt/2 F/m; the group's potential and kinetic
@@ -213,8 +212,8 @@ template <bool TAIL, bool VIR>
 __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t* __restrict__ row_ptr,
                                                         const int32_t* __restrict__ ecount,
                                                         const float4* __restrict__ grad,
-                                                        const int32_t* __restrict__ crev,
-                                                        const int32_t* __restrict__ cidx,
+                                                        const int32_t* __restrict__ cskin,
+                                                        const int64_t* __restrict__ skin_rev,
                                                         double* __restrict__ forces, StepTail tl,
                                                         VirialOut vo) {
   constexpr int APG = kBlock / kLanesPerAtom;
@@ -257,16 +256,11 @@ __global__ void __launch_bounds__(kBlock) forces_kernel(int64_t n, const int64_t
       for (int c = 0; c < 9; ++c) w[c] = vo.atom[9 * k + c];
     if (k < n) {
       const int64_t b = row_ptr[k], e = b + ecount[k];
-      for (int64_t s = b + sub; s < e; s += kLanesPerAtom) {
+      for (int64_t c = b + sub; c < e; c += kLanesPerAtom) {
+        const int64_t s = b + cskin[c];
         const float4 g = grad[s];
-        const int32_t j = __float_as_int(g.w), sr = crev[s];
-        int32_t cr = -1;
-        int64_t jb = 0;
-        if (sr >= 0) {
-          jb = row_ptr[j];
-          cr = cidx[jb + sr];
-        }
-        const float4 r = cr >= 0 ? grad[jb + cr] : g;   // a valid list always has the reverse
+        const int64_t sr = skin_rev[s];
+        const float4 r = sr >= 0 ? grad[sr] : g;   // a valid list always has the reverse
         fx += double(g.x) - double(r.x);
         fy += double(g.y) - double(r.y);
         fz += double(g.z) - double(r.z);
@@ -482,7 +476,7 @@ int blocks_for(int64_t n) {
 }  // namespace
 
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* crev, const int32_t* cidx,
+                  const int32_t* cskin, const int64_t* skin_rev,
                   double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st) {
   const int64_t blocks = tail_partial_count(n);
   const StepTail tl = tail ? *tail : StepTail{};
@@ -491,16 +485,16 @@ int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, cons
   const dim3 grid(static_cast<unsigned>(blocks + (tail ? 1 : 0)));
   if (tail && vir)
     hipLaunchKernelGGL((forces_kernel<true, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, crev, cidx, forces, tl, vo);
+                       grad, cskin, skin_rev, forces, tl, vo);
   else if (tail)
     hipLaunchKernelGGL((forces_kernel<true, false>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, crev, cidx, forces, tl, vo);
+                       grad, cskin, skin_rev, forces, tl, vo);
   else if (vir)
     hipLaunchKernelGGL((forces_kernel<false, true>), grid, dim3(kBlock), 0, st, n, row_ptr, ecount,
-                       grad, crev, cidx, forces, tl, vo);
+                       grad, cskin, skin_rev, forces, tl, vo);
   else
     hipLaunchKernelGGL((forces_kernel<false, false>), grid, dim3(kBlock), 0, st, n, row_ptr,
-                       ecount, grad, crev, cidx, forces, tl, vo);
+                       ecount, grad, cskin, skin_rev, forces, tl, vo);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }

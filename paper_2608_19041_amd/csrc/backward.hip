@@ -27,8 +27,11 @@
 // do not repeat that work per lane; with folded tables a group requests the
 // table entries of its next edge before it evaluates the current one.
 //
-// The gradient of an edge overwrites its record (r_ij, j) in place and keeps
-// j in the fourth component.  With VIR the lane that writes it also adds
+// The gradient of an edge goes to the skin position of the edge (the force
+// assembly finds a reverse gradient there with one lookup), over the
+// compact records, and keeps j in the fourth component.  The passes run
+// from the end of the row to its start: a skin position is never before its
+// compact slot, so a gradient never lands on a record still to be read.  With VIR the lane that writes it also adds
 // -g_e (x) r_e (float64) to its group's slot in LDS; the slots are summed in
 // group order into the atom's term W_i of the virial of Eq. (forces).
 #include <hip/hip_runtime.h>
@@ -56,6 +59,7 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
                                                          const int64_t* __restrict__ row_ptr,
                                                          const int32_t* __restrict__ ecount,
                                                          float4* edge,
+                                                         const int32_t* __restrict__ cskin,
                                                          const float* __restrict__ node_grad,
                                                          double* __restrict__ w_atom) {
   static_assert(P::R == 0 || P::R == 4, "pair modes: 0 or 4");
@@ -64,8 +68,8 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
   // per edge of a pass: (u, 1/rho), (tau, chi, dchi, table row), (j, a_j);
   // the per-edge terms that do not depend on the lane's channel: (chi^2,
   // d chi^2/drho, the S0/S1 term, the degree-three/four part of Q_0), the
-  // gradient of that part, and with folded tables the quintic weights
-  // (e2, e3, f2, f3)
+  // gradient of that part with the edge's skin position (bits), and with
+  // folded tables the quintic weights (e2, e3, f2, f3)
   __shared__ float4 geo_all[kWaves][kWave];
   __shared__ float4 rad_all[kWaves][kWave];
   __shared__ int2 ids_all[kWaves][kWave];
@@ -255,8 +259,8 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
         const float gx = drho * x_ + (dux - udu * x_) * inv_rho;
         const float gy_ = drho * y + (duy - udu * y) * inv_rho;
         const float gz = drho * z + (duz - udu * z) * inv_rho;
-        // in place: every record of the pass was read before its edges run
-        edge[b + c0 + x] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
+        // every record of the pass was read before its edges run
+        edge[b + __float_as_int(cb.w)] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
         if (VIR) {   // LDS adds to the group's own slot: one writer, program order
           const float rho = 1.0f / inv_rho;
           const float ga[3] = {gx, gy_, gz};
@@ -278,14 +282,16 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
     // forms its edge's geometry, envelope and table row into the wave's LDS
     // slice (entries past the row get chi = 0 and table row 0), then the
     // groups take the pass's edges.
-    for (int c0 = 0; c0 < cnt; c0 += kWave) {
+    for (int c0 = ((cnt - 1) / kWave) * kWave; cnt > 0 && c0 >= 0; c0 -= kWave) {
       const int np = cnt - c0 < kWave ? cnt - c0 : kWave;
       {
         float4 ge = make_float4(0.f, 0.f, 0.f, 1.0f), ra = make_float4(0.f, 0.f, 0.f, 0.f);
         float4 sc = make_float4(0.f, 0.f, 0.f, 0.f), cb = sc, wt = sc;
         int2 id = make_int2(0, 0);
+        int sk = 0;
         if (lane < np) {
           const float4 rec = edge[b + c0 + lane];
+          sk = cskin[b + c0 + lane];
           const EdgeGeom g = edge_geom(rec.x, rec.y, rec.z);
           float chi, dchi, tau;
           envelope(g.rho, md.inv_rc, &chi, &dchi);
@@ -319,7 +325,7 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
           float q0 = (1.0f / 3.0f) * (c3[0] * x_ + c3[1] * y + c3[2] * z);
           if constexpr (P::L >= 4) q0 += 0.25f * (c4[0] * x_ + c4[1] * y + c4[2] * z);
           sc = make_float4(chi2, dchi2, gs0 * dchi2 + gs1 * 2.0f * chi2 * dchi2, q0);
-          cb = make_float4(c3[0] + c4[0], c3[1] + c4[1], c3[2] + c4[2], 0.0f);
+          cb = make_float4(c3[0] + c4[0], c3[1] + c4[1], c3[2] + c4[2], __int_as_float(sk));
           if constexpr (FOLD) {
             const float t2 = tau * tau, t3 = t2 * tau;
             wt = make_float4(md.c_inv[0] * t2, md.c_inv[1] * t3, md.c_inv[0] * (2.0f * tau),
@@ -365,8 +371,8 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
 
 template <class P>
 int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
-           const int64_t* row_ptr, const int32_t* ecount, float4* edge, const float* node_grad,
-           double* w_atom, hipStream_t st) {
+           const int64_t* row_ptr, const int32_t* ecount, float4* edge, const int32_t* cskin,
+           const float* node_grad, double* w_atom, hipStream_t st) {
   int64_t blocks = (n + kWaves - 1) / kWaves;   // a wave per centre
   blocks = blocks < 65536 ? blocks : 65536;
   if (blocks < 1) return 0;
@@ -374,16 +380,16 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_
   const dim3 grid(static_cast<unsigned>(blocks)), block(kTeam);
   if (fidx && w_atom)
     hipLaunchKernelGGL((backward_kernel<P, true, true>), grid, block, 0, st, m->dev(), n, typ,
-                       row_ptr, ecount, edge, node_grad, w_atom);
+                       row_ptr, ecount, edge, cskin, node_grad, w_atom);
   else if (fidx)
     hipLaunchKernelGGL((backward_kernel<P, true, false>), grid, block, 0, st, m->dev(), n, typ,
-                       row_ptr, ecount, edge, node_grad, w_atom);
+                       row_ptr, ecount, edge, cskin, node_grad, w_atom);
   else if (w_atom)
     hipLaunchKernelGGL((backward_kernel<P, false, true>), grid, block, 0, st, m->dev(), n, typ,
-                       row_ptr, ecount, edge, node_grad, w_atom);
+                       row_ptr, ecount, edge, cskin, node_grad, w_atom);
   else
     hipLaunchKernelGGL((backward_kernel<P, false, false>), grid, block, 0, st, m->dev(), n, typ,
-                       row_ptr, ecount, edge, node_grad, w_atom);
+                       row_ptr, ecount, edge, cskin, node_grad, w_atom);
   DPA4C_HIP_TRY(hipGetLastError());
   return 0;
 }
@@ -392,9 +398,10 @@ int launch(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_
 
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                     const int64_t* row_ptr, const int32_t* ecount, float4* edge,
-                    const float* node_grad, double* w_atom, hipStream_t st) {
+                    const int32_t* cskin, const float* node_grad, double* w_atom, hipStream_t st) {
   const int rc = with_profile(m->C0, m->L, m->R, m->F, [&](auto p, auto) {
-    return launch<decltype(p)>(m, n, species, fidx, row_ptr, ecount, edge, node_grad, w_atom, st);
+    return launch<decltype(p)>(m, n, species, fidx, row_ptr, ecount, edge, cskin, node_grad,
+                               w_atom, st);
   });
   if (rc == kNoProfile) {
     set_error("backward: profile not compiled");

@@ -20,10 +20,8 @@ struct CompactArgs {
   int64_t cap;                // skin-list capacity
   int32_t* ecount;            // [N] out: edges kept per row
   float4* edge;               // [cap] out: (r_ij, bits of j) at the head of each skin row
-  const int32_t* skin_rev;    // [cap] position of the reverse of each skin edge in row j
-  int32_t* cidx;              // [cap] out: compact slot of each skin edge, or -1, counted
-                              // from the head of its row
-  int32_t* crev;              // [cap] out: skin_rev of the skin edge of each compact slot
+  int32_t* cskin;             // [cap] out: for each compact slot of a row, the position of
+                              // its skin entry in the row (both counted from the row's head)
 };
 
 __device__ inline int64_t qfix_dev(double x) {
@@ -68,9 +66,9 @@ __device__ inline CentreQ centre_q(const CompactArgs& a, int64_t i) {
 // and the entries inside r_c keep canonical order.  ``kept`` edges of the row
 // precede the pass.  A kept lane writes its record r_ij = (r_j + sum_b n_b
 // h_b) - r_i (float64 difference stored as float32) to compact slot kept +
-// *at of the row, the compact slot (or -1) of its skin entry and the reverse
-// position of the slot; it returns the record in *rec and its rank within
-// the pass in *at (-1 for lanes that keep nothing).  Returns the number kept
+// *at of the row, and the position of its skin entry in the row to the same
+// slot of cskin; it returns the record in *rec and its rank within the pass
+// in *at (-1 for lanes that keep nothing).  Returns the number kept
 // by the pass (the same in every lane).
 __device__ inline int compact_pass(const CompactArgs& a, int64_t n, int64_t b, int64_t s0,
                                    int64_t e, int kept, const CentreQ& ci, float4* rec, int* at) {
@@ -122,11 +120,8 @@ __device__ inline int compact_pass(const CompactArgs& a, int64_t n, int64_t b, i
       *rec = make_float4(static_cast<float>(rx), static_cast<float>(ry), static_cast<float>(rz),
                          __int_as_float(j));
       a.edge[b + slot] = *rec;
-      a.cidx[s] = slot;
-      a.crev[b + slot] = a.skin_rev[s];
+      a.cskin[b + slot] = static_cast<int32_t>(s - b);
       *at = pre;
-    } else {
-      a.cidx[s] = -1;
     }
   }
   return __popcll(m);

@@ -29,7 +29,8 @@ int fill_skin_list(NeighborScratch& nb, int64_t n, const CellGrid& g, const int6
 // host6 = [min x, y, z, max x, y, z]; dev6 is device scratch of 6 int64;
 // synchronises ``st``
 int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6, hipStream_t st);
-// skin_rev[s] = position of the reverse of skin edge s within row nbr_j[s], or -1;
+// skin_rev[s] = position in the list of the reverse of skin edge s (in row
+// nbr_j[s]), or -1;
 // jsamp = scratch of cap / 16 + 1 int32: nbr_j at every 16th position of the
 // list, computed here unless ``jsamp_ready`` (fill_skin_list wrote it);
 // with ``paired`` (device int64, zeroed by the caller) also the number of
@@ -38,7 +39,7 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 // taken in the build's spatial bin order
 struct NeighborScratch;
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
+                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int64_t* skin_rev,
                     int64_t* paired, const NeighborScratch* order_of, hipStream_t st);
 // species analysis of a call: builds the pair-folded tables of the species
 // present when they changed (at most kMaxFoldTypes species) and the folded
@@ -59,12 +60,14 @@ int launch_forward(const dpa4c_model* m, int64_t n, const int32_t* species, cons
 // desc_out (float [N][D_out]) receives D when not null
 int launch_atoms(const dpa4c_model* m, int64_t n, const int32_t* species, const float* node,
                  float* node_grad, double* e_atom, float* desc_out, hipStream_t st);
-// the gradients dE/dr_ij overwrite the compact edge records in ``edge``
-// (x, y, z = the gradient, w = the bits of j as before); with w_atom
-// ([N][9]) also the virial terms W_i = -sum_e g_e (x) r_e of every centre
+// the gradient dE/dr_ij of compact slot c of row i goes to the skin position
+// of that edge, edge[row_ptr[i] + cskin[row_ptr[i] + c]] (x, y, z = the
+// gradient, w = the bits of j as before), over the compact records, which
+// it reads first; with w_atom ([N][9]) also the virial terms
+// W_i = -sum_e g_e (x) r_e of every centre
 int launch_backward(const dpa4c_model* m, int64_t n, const int32_t* species, const int32_t* fidx,
                     const int64_t* row_ptr, const int32_t* ecount, float4* edge,
-                    const float* node_grad, double* w_atom, hipStream_t st);
+                    const int32_t* cskin, const float* node_grad, double* w_atom, hipStream_t st);
 struct StepTail;
 // the virial of Eq. (forces): atom = [N][9] per-centre terms W_i written by
 // the backward kernel, part_v = [tail_partial_count(n)][9] block partials of
@@ -76,7 +79,7 @@ struct VirialOut {
 // force assembly; with ``tail`` also the velocity-Verlet work of the step
 // that needs only F_k (see StepTail), with ``vir`` the virial
 int launch_forces(int64_t n, const int64_t* row_ptr, const int32_t* ecount, const float4* grad,
-                  const int32_t* crev, const int32_t* cidx,
+                  const int32_t* cskin, const int64_t* skin_rev,
                   double* forces, const StepTail* tail, const VirialOut* vir, hipStream_t st);
 // out[c] = fixed-order sum over p < np of part[ncomp p + c]
 int launch_sum_components(const double* part, int64_t np, int ncomp, double* out, hipStream_t st);
@@ -170,9 +173,8 @@ int launch_zero_i64(int64_t* p, int64_t n, hipStream_t st);
 struct EvalBufs {
   int32_t* ecount;      // int32 [N]
   float4* edge;         // float4 [cap]
-  int32_t* cidx;        // int32 [cap]
-  int32_t* crev;        // int32 [cap]
-  int32_t* skin_rev;    // int32 [cap]
+  int32_t* cskin;       // int32 [cap]
+  int64_t* skin_rev;    // int64 [cap]
   float* node;          // float [N][S+2]
   float* node_grad;     // float [N][S+2]
   double* epart;        // double [partial_count(N) + 8]
@@ -182,7 +184,8 @@ struct EvalBufs {
 };
 // bytes of each EvalBufs array for N atoms, a list of cap entries and a node
 // state of ns floats per atom, each rounded up to 256 (in struct order)
-void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[11]);
+constexpr int kEvalBufs = 10;
+void eval_buf_sizes(int64_t n, int64_t cap, int ns, size_t sizes[kEvalBufs]);
 // compute_energy_forces(_virial) on the given buffers (null: the model's
 // workspace, grown as needed); ``bufs`` given means no allocation, no timing
 // events and no memset nodes on the stream

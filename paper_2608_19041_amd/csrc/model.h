@@ -68,13 +68,12 @@ struct Workspace {
   DevBuf skin_row;      // int64 [N+1]
   DevBuf skin_j;        // int32 [cap]
   DevBuf skin_shift;    // int32 [cap]
-  DevBuf skin_rev;      // int32 [cap]: position of the reverse edge in row j, or -1
+  DevBuf skin_rev;      // int64 [cap]: position in the list of the reverse edge, or -1
   DevBuf qbuild;        // int64 [N][3] fixed-point positions at the last build
   // compacted (r < r_c) edges, stored in the rows of the skin list
   DevBuf ecount;        // int32 [N]
   DevBuf edge;          // float4 [cap]: r_ij (x, y, z) and j (bits)
-  DevBuf cidx;          // int32 [cap]: compact slot of each skin edge (row-local) or -1
-  DevBuf crev;          // int32 [cap]: skin_rev of the skin edge of each compact slot
+  DevBuf cskin;         // int32 [cap]: skin position of each compact slot (row-local)
   DevBuf watom;         // double [N][9]: per-centre virial terms (when not the caller's)
   // per-atom state
   DevBuf node;          // float [N][NS]

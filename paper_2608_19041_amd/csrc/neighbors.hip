@@ -643,8 +643,8 @@ __global__ void __launch_bounds__(kBlock) fill_kernel(int64_t n, GridDev g,
 }
 
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kBlock) fill_i32_kernel(int32_t* __restrict__ p, int64_t n,
-                                                          int32_t v) {
+__global__ void __launch_bounds__(kBlock) fill_i64_kernel(int64_t* __restrict__ p, int64_t n,
+                                                          int64_t v) {
   for (int64_t i = blockIdx.x * int64_t(kBlock) + threadIdx.x; i < n; i += int64_t(gridDim.x) * kBlock)
     p[i] = v;
 }
@@ -665,8 +665,8 @@ __global__ void __launch_bounds__(kBlock) jsamp_kernel(const int64_t* __restrict
 __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0 && e >= b && e <= cap; }
 
 // The reverse search of entry s = (i -> j, n): the position of the entry
-// (i, -n) within row j, written to rev[s] (row-local) and the position of s
-// within row i to rev of that entry.  Row j is ordered by neighbour index,
+// (i, -n) of row j, written to rev[s], and s to rev of that entry (both
+// positions in the whole list).  Row j is ordered by neighbour index,
 // so the entries (i, m) of row j are consecutive and begin at the first
 // entry with neighbour index >= i: the samples of row j (the neighbour
 // index at every absolute position 16 g inside it) are bisected for the
@@ -679,7 +679,7 @@ __device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s,
                                       const int32_t* __restrict__ nbr_j,
                                       const int32_t* __restrict__ nbr_shift, int64_t cap,
                                       const int32_t* __restrict__ jsamp,
-                                      int32_t* __restrict__ rev) {
+                                      int64_t* __restrict__ rev) {
   const int32_t j = nbr_j[s];
   const int32_t want_sh = negate_shift(nbr_shift[s]);
   if (j < 0 || j >= n) return false;
@@ -718,15 +718,15 @@ __device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s,
   }
   for (int64_t t = p; t < je && nbr_j[t] == i; ++t)
     if (nbr_shift[t] == want_sh) {
-      rev[s] = static_cast<int32_t>(t - jb);
-      rev[t] = static_cast<int32_t>(s - row_ptr[i]);
+      rev[s] = t;
+      rev[t] = s;
       return true;
     }
   return false;
 }
 
-// skin_rev[s] = position of the reverse of entry s (i -> j, n), the key
-// (i, -n), within row j, or -1.  A symmetric list pairs every entry with its
+// skin_rev[s] = position in the list of the reverse of entry s (i -> j, n),
+// the entry (i, -n) of row j, or -1.  A symmetric list pairs every entry with its
 // reverse, so only the canonical entry of a pair, the one with
 // key(j, n) > key(i, -n) (that is j > i, or a periodic self image with the
 // larger shift), searches and writes both indices.  One wave takes rows in
@@ -744,7 +744,7 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
                                                           const int32_t* __restrict__ nbr_shift,
                                                           int64_t cap,
                                                           const int32_t* __restrict__ jsamp,
-                                                          int32_t* __restrict__ rev,
+                                                          int64_t* __restrict__ rev,
                                                           unsigned long long* __restrict__ paired,
                                                           const CellRec* __restrict__ order) {
   __shared__ int64_t qs_all[kWavesPerBlock][2 * kWave];
@@ -1030,7 +1030,7 @@ int position_extent(const double* pos, int64_t n, int64_t* dev6, int64_t* host6,
 }
 
 int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t* nbr_shift,
-                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int32_t* skin_rev,
+                    int64_t n, int64_t cap, int32_t* jsamp, bool jsamp_ready, int64_t* skin_rev,
                     int64_t* paired, const NeighborScratch* order_of, hipStream_t st) {
   const CellRec* order = order_of ? order_of->cell_rec.as<CellRec>() : nullptr;
   if (n <= 0) return 0;
@@ -1042,8 +1042,8 @@ int launch_skin_rev(const int64_t* row_ptr, const int32_t* nbr_j, const int32_t*
     hipLaunchKernelGGL(jsamp_kernel, dim3(static_cast<unsigned>(jb)), dim3(kBlock), 0, st, row_ptr,
                        n, nbr_j, cap, jsamp);
   }
-  hipLaunchKernelGGL(fill_i32_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st,
-                     skin_rev, cap, -1);
+  hipLaunchKernelGGL(fill_i64_kernel, dim3(static_cast<unsigned>(sb)), dim3(kBlock), 0, st,
+                     skin_rev, cap, int64_t(-1));
   // the block compare reads 16-byte groups of nbr_j: a list that is not
   // 16-byte aligned takes one load per entry
   const bool vec = (reinterpret_cast<uintptr_t>(nbr_j) & 15) == 0;

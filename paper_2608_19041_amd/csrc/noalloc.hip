@@ -80,7 +80,7 @@ extern "C" int compute_energy_forces_noalloc(const dpa4c_model* m, const double*
     set_error("compute_energy_forces_noalloc: no scratch on the model's device");
     return DPA4C_ERR_INVALID_ARG;
   }
-  size_t sizes[11];
+  size_t sizes[kEvalBufs];
   eval_buf_sizes(N, n_pairs, m->S + 2, sizes);
   size_t total = 0;
   for (size_t b : sizes) total += b;
@@ -100,15 +100,14 @@ extern "C" int compute_energy_forces_noalloc(const dpa4c_model* m, const double*
   EvalBufs b{};
   b.ecount = reinterpret_cast<int32_t*>(take(0));
   b.edge = reinterpret_cast<float4*>(take(1));
-  b.cidx = reinterpret_cast<int32_t*>(take(2));
-  b.crev = reinterpret_cast<int32_t*>(take(3));
-  b.skin_rev = reinterpret_cast<int32_t*>(take(4));
-  b.node = reinterpret_cast<float*>(take(5));
-  b.node_grad = reinterpret_cast<float*>(take(6));
-  b.epart = reinterpret_cast<double*>(take(7));
-  b.fidx = reinterpret_cast<int32_t*>(take(8));
-  b.fold_mask = reinterpret_cast<uint32_t*>(take(9));
-  b.check = reinterpret_cast<int64_t*>(take(10));
+  b.cskin = reinterpret_cast<int32_t*>(take(2));
+  b.skin_rev = reinterpret_cast<int64_t*>(take(3));
+  b.node = reinterpret_cast<float*>(take(4));
+  b.node_grad = reinterpret_cast<float*>(take(5));
+  b.epart = reinterpret_cast<double*>(take(6));
+  b.fidx = reinterpret_cast<int32_t*>(take(7));
+  b.fold_mask = reinterpret_cast<uint32_t*>(take(8));
+  b.check = reinterpret_cast<int64_t*>(take(9));
   return energy_forces_core(m, pos, species, N, cell, pbc, r_c, row_ptr, nbr_j, nbr_shift, n_pairs,
                             e_atom, forces, e_total, nullptr, nullptr, &b, stream);
 }
