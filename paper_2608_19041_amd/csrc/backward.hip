@@ -259,8 +259,9 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
         const float gx = drho * x_ + (dux - udu * x_) * inv_rho;
         const float gy_ = drho * y + (duy - udu * y) * inv_rho;
         const float gz = drho * z + (duz - udu * z) * inv_rho;
-        // every record of the pass was read before its edges run
-        edge[b + __float_as_int(cb.w)] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
+        // to the entry's LDS slot (its geometry is no longer needed): the
+        // pass's gradients are stored together once every edge has run
+        geo[x] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
         if (VIR) {   // LDS adds to the group's own slot: one writer, program order
           const float rho = 1.0f / inv_rho;
           const float ga[3] = {gx, gy_, gz};
@@ -355,6 +356,9 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
       } else {
         for (int base = 0; base < np; base += G) edge_work(base + grp, c0, nullptr);
       }
+      wave_sync();
+      // every record of the pass was read before its edges ran
+      if (lane < np) edge[b + __float_as_int(cub[lane].w)] = geo[lane];
       wave_sync();   // the LDS entries are rewritten by the next pass
     }
     if (VIR) {
