@@ -789,7 +789,17 @@ int dynamics(const dpa4c_model* m, double* pos, double* vel, const int32_t* spec
     if (!kicked) {
       StageScope t(m, kStIntegrate, st);
       if (nvt) {
-        int r = chain_launch(prev, true);
+        // every step boundary as at the end of a batch or a call: the
+        // closing half step and its velocity scale, then the opening half
+        // step from the kinetic energy of the scaled velocities, so that a
+        // run gives the same bits however it is split into batches and calls
+        if (prev >= 0) {
+          int r = chain_launch(prev, false);
+          if (r) return r;
+          r = launch_scale(vel, N, nvt_state + 2 * nvt->length, st);
+          if (r) return r;
+        }
+        int r = chain_launch(-1, true);
         if (r) return r;
       }
       int r = launch_kick_drift(pos, vel, forces, species, w.inv_mass.as<double>(), T1, N, dt_fs,
