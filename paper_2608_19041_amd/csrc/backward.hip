@@ -29,11 +29,13 @@
 //
 // The gradient of an edge goes to the skin position of the edge (the force
 // assembly finds a reverse gradient there with one lookup), over the
-// compact records, and keeps j in the fourth component.  The passes run
-// from the end of the row to its start: a skin position is never before its
-// compact slot, so a gradient never lands on a record still to be read.  With VIR the lane that writes it also adds
-// -g_e (x) r_e (float64) to its group's slot in LDS; the slots are summed in
-// group order into the atom's term W_i of the virial of Eq. (forces).
+// compact records, and keeps j in the fourth component; a pass's gradients
+// are stored together once its edges have run.  The passes run from the end
+// of the row to its start: a skin position is never before its compact
+// slot, so a gradient never lands on a record still to be read.  With VIR the
+// lane that forms a gradient also adds -g_e (x) r_e (float64) to its group's
+// slot in LDS; the slots are summed in group order into the atom's term W_i
+// of the virial of Eq. (forces).
 #include <hip/hip_runtime.h>
 
 #include "../../include/dpa4c.h"
