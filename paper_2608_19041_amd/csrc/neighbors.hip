@@ -674,14 +674,13 @@ __device__ inline bool row_ok(int64_t b, int64_t e, int64_t cap) { return b >= 0
 // (four 16-byte loads with VEC, one load per entry without), and the entries
 // (i, m) from there are matched on the image.
 template <bool VEC>
-__device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s,
+__device__ inline bool reverse_search(int64_t n, int32_t i, int64_t s, int32_t j, int32_t sh,
                                       const int64_t* __restrict__ row_ptr,
                                       const int32_t* __restrict__ nbr_j,
                                       const int32_t* __restrict__ nbr_shift, int64_t cap,
                                       const int32_t* __restrict__ jsamp,
                                       int64_t* __restrict__ rev) {
-  const int32_t j = nbr_j[s];
-  const int32_t want_sh = negate_shift(nbr_shift[s]);
+  const int32_t want_sh = negate_shift(sh);
   if (j < 0 || j >= n) return false;
   const int64_t jb = row_ptr[j], je = row_ptr[j + 1];
   if (!row_ok(jb, je, cap) || je == jb) return false;
@@ -749,9 +748,13 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
                                                           const CellRec* __restrict__ order) {
   __shared__ int64_t qs_all[kWavesPerBlock][2 * kWave];
   __shared__ int32_t qi_all[kWavesPerBlock][2 * kWave];
+  __shared__ int32_t qj_all[kWavesPerBlock][2 * kWave];   // (j, n) of each queued entry
+  __shared__ int32_t qh_all[kWavesPerBlock][2 * kWave];
   const int w = threadIdx.x / kWave;
   int64_t* qs = qs_all[w];
   int32_t* qi = qi_all[w];
+  int32_t* qj = qj_all[w];
+  int32_t* qh = qh_all[w];
   const int64_t nwaves = int64_t(gridDim.x) * kWavesPerBlock;
   const int lane = lane_id();
   unsigned long long found = 0;
@@ -759,22 +762,27 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
   // runs the first ``count`` (<= 64) queued searches and moves the rest down
   auto run = [&](int count) {
     const bool hit = lane < count &&
-                     reverse_search<VEC>(n, qi[lane], qs[lane], row_ptr, nbr_j, nbr_shift, cap,
+                     reverse_search<VEC>(n, qi[lane], qs[lane], qj[lane], qh[lane], row_ptr, nbr_j,
+                                         nbr_shift, cap,
                                          jsamp, rev);
     found += __popcll(__ballot(hit));
     const int rest = qn - count;
     int64_t ks = 0;
-    int32_t ki = 0;
+    int32_t ki = 0, kj = 0, kh = 0;
     if (lane < rest) {
       ks = qs[count + lane];
       ki = qi[count + lane];
+      kj = qj[count + lane];
+      kh = qh[count + lane];
     }
-    wave_lds_sync();
+    wave_local_sync();
     if (lane < rest) {
       qs[lane] = ks;
       qi[lane] = ki;
+      qj[lane] = kj;
+      qh[lane] = kh;
     }
-    wave_lds_sync();
+    wave_local_sync();
     qn = rest;
   };
   for (int64_t r = xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock + w; r < n; r += nwaves) {
@@ -784,18 +792,22 @@ __global__ void __launch_bounds__(kBlock) skin_rev_kernel(int64_t n, const int64
     for (int64_t s0 = b; s0 < e; s0 += kWave) {
       const int64_t s = s0 + lane;
       bool canon = false;
+      int32_t j = 0, sh = 0;
       if (s < e) {
-        const int32_t sh = nbr_shift[s];
-        canon = entry_key(nbr_j[s], sh) > entry_key(static_cast<int32_t>(i), negate_shift(sh));
+        j = nbr_j[s];
+        sh = nbr_shift[s];
+        canon = entry_key(j, sh) > entry_key(static_cast<int32_t>(i), negate_shift(sh));
       }
       uint64_t m;
       const int pre = ballot_prefix(canon, &m);
       if (canon) {
         qs[qn + pre] = s;
         qi[qn + pre] = static_cast<int32_t>(i);
+        qj[qn + pre] = j;
+        qh[qn + pre] = sh;
       }
       qn += __popcll(m);
-      wave_lds_sync();
+      wave_local_sync();
       if (qn >= kWave) run(kWave);
     }
   }
