@@ -273,7 +273,7 @@ __device__ inline void for_stencil(const GridDev& g, int64_t i, const int64_t* _
     const int vend = wave_inclusive_scan(len);
     sg.vend[lane] = vend;
     const int total = __shfl(vend, kWave - 1);
-    wave_lds_sync();
+    wave_local_sync();
     int seg = 0;   // the run of this lane's candidate (candidates advance, so does the run)
     for (int k0 = 0; k0 < total; k0 += kWave) {
       const int k = k0 + lane;
@@ -294,7 +294,7 @@ __device__ inline void for_stencil(const GridDev& g, int64_t i, const int64_t* _
       }
       f(j, sx, sy, sz, pred);
     }
-    wave_lds_sync();   // the next batch of runs overwrites the table
+    wave_local_sync();   // the next batch of runs overwrites the table
   }
 }
 
