@@ -3,6 +3,7 @@
 Tolerances are the stated targets: neighbour lists bit-identical, E_i within
 1e-5 eV and forces within 1e-4 eV/A (max abs) of the oracle.
 """
+import dataclasses
 import numpy as np
 import pytest
 import torch
@@ -394,3 +395,27 @@ def test_neighbors_long_rows(dev, dp, n, box, r):
     ref = onb.neighbor_list(s.pos, s.cell, s.pbc, r)
     assert e == len(ref[0])
     assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref)
+
+
+def test_shuffled_atom_order(dev, dp):
+    """A crystal with its atoms in random order.  The neighbour indices of a
+    row then spread over the whole index range (in lattice order they come
+    in a few clusters), which changes how the fill's rank pass fills its
+    buckets and where the reverse search looks: the lists stay bit-identical
+    to the oracle's, and E_i and F are those of the ordered crystal, carried
+    by the permutation (only the order of the sums differs)."""
+    s = synth.make_workload("fcc4000_full")[0]
+    perm = np.random.Generator(np.random.PCG64(17)).permutation(s.n)
+    t = dataclasses.replace(s, pos=s.pos[perm].copy(), species=s.species[perm].copy())
+    pos, _ = on_dev(t, dev)
+    for r in (6.0, 7.0):
+        rp, nj, ns, e = dp.build_neighbors(pos, t.cell, t.pbc, r)
+        ref = onb.neighbor_list(t.pos, t.cell, t.pbc, r)
+        assert e == len(ref[0])
+        assert_rows_equal(gpu_rows(rp, nj, ns, dp), ref)
+    model, _, _ = gpu_model(dp, "full")
+    ea0, F0, et0 = evaluate(dp, model, s, dev)
+    ea1, F1, et1 = evaluate(dp, model, t, dev)
+    assert np.abs(ea1 - ea0[perm]).max() < E_TOL
+    assert np.abs(F1 - F0[perm]).max() < F_TOL
+    assert abs(et1 - et0) < E_TOL * s.n
