@@ -6,8 +6,8 @@
 // edges are scanned once; per edge the envelope, the tabulated radial maps
 // g and q, the cached pair coefficients gamma, beta, U, the amplitude psi and
 // the harmonics are formed in registers and accumulated into the node state
-// [sum chi^2, sum chi^4, Y_lmc].  Apart from the compacted edge records, no
-// per-edge quantity is written to memory.
+// [sum chi^2, sum chi^4, Y_lmc].  Apart from the compacted edge records and
+// their skin positions, no per-edge quantity is written to memory.
 // The readout runs in the per-atom kernel.
 //
 // Mapping: one wavefront per centre (four centres per 256-thread

@@ -9,7 +9,7 @@
 // with s_t = SiLU'(pre_t).  Every product runs on v_mfma_f32_16x16x4_f32.
 //
 // Layout: the 16-row activation tile (the A operand) lives in LDS; each of the
-// four waves owns a fixed set of 16-column output tiles, so the SiLU'
+// eight waves owns a fixed set of 16-column output tiles, so the SiLU'
 // factors and the residual carry of every (row, column) stay in the same
 // lane's registers from the forward to the backward pass.  Weights are
 // stored in fragment order: for output tile T and k-block kb (16 inputs) lane
