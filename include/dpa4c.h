@@ -276,7 +276,10 @@ int verlet_step(const dpa4c_model* model, double* pos, double* vel, const int32_
  * masses Q_1 = N_f kT tau^2 and Q_k = kT tau^2 (tau = t_damp_fs), with
  * N_f = 3N - 3.  The virial of Eq. (forces) is assembled at every step.
  * Neighbour list, rebuilds, batches and replay as verlet_step; the chain
- * state is saved with the batch start state.
+ * state is saved with the batch start state.  Between two steps the closing
+ * half step scales the velocities, and the opening one starts from the
+ * kinetic energy of the scaled velocities, as it must at the start of a
+ * call, so a run split over several calls equals one call, bit for bit.
  *
  * temperature      target T (K), > 0
  * t_damp_fs        damping time tau (fs), > 0
