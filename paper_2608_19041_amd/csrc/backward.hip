@@ -265,7 +265,7 @@ __global__ void __launch_bounds__(kTeam, (backward_min_waves<P, VIR>())) backwar
         // pass's gradients are stored together once every edge has run
         geo[x] = make_float4(gx, gy_, gz, __int_as_float(ids[x].x));
         if (VIR) {   // LDS adds to the group's own slot: one writer, program order
-          const float rho = 1.0f / inv_rho;
+          const float rho = __builtin_amdgcn_rcpf(inv_rho);   // hardware reciprocal, 1 ulp
           const float ga[3] = {gx, gy_, gz};
           const float rb[3] = {x_ * rho, y * rho, z * rho};
 #pragma unroll
